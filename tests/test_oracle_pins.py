@@ -1,0 +1,525 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each check below compares the oracle with an independent statement of the
+same quantity: a linear-algebra identity, a torch library routine, a brute
+force over tiny inputs, or a closed form.  The checks are plain functions so
+the mutation tests at the bottom can show that a planted mistake in the
+oracle (a dropped term, a wrong sign or index, a transposed operand) makes at
+least one of them fail.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import decode, prefill, storage
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+# ----------------------------------------------------------------------------
+# small random problems
+# ----------------------------------------------------------------------------
+
+def _orth(rng, n, k):
+    q, r = np.linalg.qr(rng.standard_normal((n, k)))
+    return q * np.sign(np.diag(r))
+
+
+def small_problem(seed=0, B=2, hkv=2, G=2, dh=8, nb=1, rank=6, L=40, s=3, orthonormal=False):
+    rng = np.random.default_rng(seed)
+    Dp = hkv * dh
+    dg = Dp // nb
+    if orthonormal:
+        bk = np.stack([np.stack([_orth(rng, dg, rank) for _ in range(nb)]) for _ in range(B)])
+        bv = np.stack([np.stack([_orth(rng, dg, rank) for _ in range(nb)]) for _ in range(B)])
+    else:
+        bk = rng.standard_normal((B, nb, dg, rank))
+        bv = rng.standard_normal((B, nb, dg, rank))
+    R = nb * rank
+    return {
+        "q": rng.standard_normal((B, hkv * G, dh)),
+        "bases_k": bk, "bases_v": bv,
+        "coef_k": rng.standard_normal((B, L, R)),
+        "coef_v": rng.standard_normal((B, L, R)),
+        "sink_k": rng.standard_normal((B, s, Dp)),
+        "sink_v": rng.standard_normal((B, s, Dp)),
+        "hkv": hkv, "G": G, "dh": dh, "L": L, "s": s, "R": R, "nb": nb,
+    }
+
+
+def cfg_of(p, W=4, k=5, kappa=3, theta=100.0, pool_mode="max", agg="mean"):
+    return dict(n_kv_heads=p["hkv"], window=W, topk=k, pool_kernel=kappa,
+                pool_mode=pool_mode, group_agg=agg, rope_theta=theta, dtype="fp32")
+
+
+def run(p, cfg, **kw):
+    return decode.decode_step(cfg, p["L"], p["q"], p["sink_k"], p["sink_v"], p["bases_k"],
+                              p["bases_v"], p["coef_k"], p["coef_v"], **kw)
+
+
+# ----------------------------------------------------------------------------
+# independent reference pieces (written from the definitions, loop form)
+# ----------------------------------------------------------------------------
+
+def ref_group_query(q, hkv, g):
+    """q_g = concat over kv heads j of query head j*G + g (loop form)."""
+    B, hq, dh = q.shape
+    G = hq // hkv
+    return np.stack([np.concatenate([q[b, j * G + g] for j in range(hkv)]) for b in range(B)])
+
+
+def ref_full_keys(coef, bases):
+    """Every reconstructed key, row by row: sum_r c[r] * basis column r."""
+    B, L, R = coef.shape
+    nb, dg, rank = bases.shape[1:]
+    out = np.zeros((B, L, nb * dg))
+    for b in range(B):
+        for k in range(nb):
+            blk = bases[b if bases.shape[0] > 1 else 0, k]            # [dg, rank]
+            for rr in range(rank):
+                out[b, :, k * dg:(k + 1) * dg] += np.outer(coef[b, :, k * rank + rr], blk[:, rr])
+    return out
+
+
+def ref_rope_complex(x, pos, theta):
+    """RoPE as complex multiplication: (x_i + i x_{i+d/2}) * exp(i pos w_i)."""
+    if theta == 0:          # RoPE switched off
+        return np.array(x, dtype=np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    w = theta ** (-(2.0 * np.arange(half)) / d)
+    z = x[..., :half] + 1j * x[..., half:]
+    z = z * np.exp(1j * np.asarray(pos, dtype=np.float64)[..., None] * w)
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def torch_gqa_attention(q, K, V, pos_k, pos_q, theta, hkv):
+    """Dense GQA attention through torch SDPA (float64) with complex-form RoPE;
+    kv heads are repeated with repeat_interleave (head h reads kv head h // G)."""
+    B, hq, dh = q.shape
+    n = K.shape[1]
+    qr = ref_rope_complex(q, np.broadcast_to(np.asarray(pos_q, float)[:, None], (B, hq)), theta)
+    Kh = K.reshape(B, n, hkv, dh).transpose(0, 2, 1, 3)                # [B, hkv, n, dh]
+    Kr = ref_rope_complex(Kh, np.broadcast_to(np.asarray(pos_k, float)[:, None, :], (B, hkv, n)), theta)
+    Vh = V.reshape(B, n, hkv, dh).transpose(0, 2, 1, 3)
+    G = hq // hkv
+    tq = torch.from_numpy(qr)[:, :, None, :]                          # [B, hq, 1, dh]
+    tk = torch.from_numpy(np.ascontiguousarray(Kr)).repeat_interleave(G, dim=1)
+    tv = torch.from_numpy(np.ascontiguousarray(Vh)).repeat_interleave(G, dim=1)
+    o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+    return o[:, :, 0, :].numpy()
+
+
+# ----------------------------------------------------------------------------
+# pin checks
+# ----------------------------------------------------------------------------
+
+def check_latent_identity(seed=0, nb=1):
+    """(q_g B)(c)^T / sqrt(R) == q_g . (B c) / sqrt(R) for every token (any B)."""
+    p = small_problem(seed, nb=nb, hkv=2 * nb if nb > 1 else 2)
+    Z = decode.latent_logits(decode.query_window(p["q"], None, p["bases_k"], p["hkv"]),
+                             p["coef_k"], p["L"])
+    K = ref_full_keys(p["coef_k"], p["bases_k"])
+    for g in range(p["G"]):
+        qg = ref_group_query(p["q"], p["hkv"], g)
+        ref = np.einsum("bd,bld->bl", qg, K) / np.sqrt(p["R"])
+        if not np.allclose(Z[:, g, 0, :], ref, rtol=1e-11, atol=1e-11):
+            return False
+    return True
+
+
+def check_rotation_invariance(seed=1):
+    """B -> B Q and C -> C Q (Q orthogonal per basis group) change nothing."""
+    p = small_problem(seed, nb=2, hkv=2, rank=5, L=50)
+    cfg = cfg_of(p, W=4, k=7)
+    a = run(p, cfg)
+    rng = np.random.default_rng(seed + 100)
+    p2 = dict(p)
+    bk, bv, ck, cv = (p[x].copy() for x in ("bases_k", "bases_v", "coef_k", "coef_v"))
+    rank = bk.shape[-1]
+    for b in range(bk.shape[0]):
+        for k in range(2):
+            Qk = _orth(rng, rank, rank)
+            Qv = _orth(rng, rank, rank)
+            bk[b, k] = bk[b, k] @ Qk
+            bv[b, k] = bv[b, k] @ Qv
+            ck[b, :, k * rank:(k + 1) * rank] = ck[b, :, k * rank:(k + 1) * rank] @ Qk
+            cv[b, :, k * rank:(k + 1) * rank] = cv[b, :, k * rank:(k + 1) * rank] @ Qv
+    p2.update(bases_k=bk, bases_v=bv, coef_k=ck, coef_v=cv)
+    b_ = run(p2, cfg)
+    return (np.allclose(a["Z"], b_["Z"], rtol=1e-10, atol=1e-12)
+            and np.allclose(a["a_tilde"], b_["a_tilde"], rtol=1e-10, atol=1e-15)
+            and np.array_equal(a["idx"], b_["idx"])
+            and np.allclose(a["out"], b_["out"], rtol=1e-10, atol=1e-12))
+
+
+def check_pool_vs_torch(seed=2):
+    rng = np.random.default_rng(seed)
+    x = rng.random((2, 3, 37))
+    ok = True
+    for kappa in (1, 3, 5, 7, 9):
+        t = torch.from_numpy(x)
+        mx = torch.nn.functional.max_pool1d(t, kappa, stride=1, padding=kappa // 2).numpy()
+        av = torch.nn.functional.avg_pool1d(t, kappa, stride=1, padding=kappa // 2,
+                                            count_include_pad=True).numpy()
+        ok &= np.allclose(decode.pool(x, kappa, "max"), mx, rtol=0, atol=0)
+        ok &= np.allclose(decode.pool(x, kappa, "avg"), av, rtol=1e-14, atol=1e-15)
+    return bool(ok)
+
+
+def check_topk_special_case(seed=3):
+    """W_q = 1, kappa = 1, G = 1: softmax is monotone, so the global picks are
+    the top-k of q . K^ (reconstructed keys), ties to the lower index."""
+    p = small_problem(seed, G=1, hkv=2, L=60)
+    W, k = 5, 9
+    cfg = cfg_of(p, W=W, k=k, kappa=1)
+    r = run(p, cfg)
+    K = ref_full_keys(p["coef_k"], p["bases_k"])
+    qg = ref_group_query(p["q"], p["hkv"], 0)
+    for b in range(p["q"].shape[0]):
+        scores = K[b, :p["L"] - W] @ qg[b]
+        order = sorted(range(p["L"] - W), key=lambda l: (-scores[l], l))[:k]
+        if list(r["idx"][b, :k]) != sorted(order):
+            return False
+    return True
+
+
+def brute_select(a, L, W, k):
+    n_hist = max(L - W, 0)
+    k_eff = min(k, n_hist)
+    out = []
+    for row in a:
+        pairs = sorted(((-row[l], l) for l in range(n_hist)))
+        glob = sorted(l for _, l in pairs[:k_eff])
+        out.append(glob + list(range(n_hist, L)))
+    return np.array(out, dtype=np.int64).reshape(len(a), -1)
+
+
+def check_select_bruteforce(seed=4):
+    rng = np.random.default_rng(seed)
+    for L, W, k in [(20, 4, 5), (20, 4, 0), (20, 4, 16), (20, 4, 40), (3, 5, 2), (1, 1, 3),
+                    (17, 0, 6), (30, 30, 4), (31, 7, 24)]:
+        a = rng.integers(0, 4, size=(3, L)).astype(np.float64)  # many exact ties
+        if not np.array_equal(decode.select(a, L, W, k), brute_select(a, L, W, k)):
+            return False
+        if decode.select(a, L, W, k).shape[1] != decode.num_selected(L, W, k):
+            return False
+    return True
+
+
+def check_full_rank_exact(seed=5):
+    """R = Dp with a square orthonormal basis: reconstruct(project(S)) == S."""
+    rng = np.random.default_rng(seed)
+    Dp = 12
+    S = rng.standard_normal((2, 9, Dp))
+    Bm = np.stack([_orth(rng, Dp, Dp)[None] for _ in range(2)])      # [B, 1, Dp, Dp]
+    C = decode.project(S, Bm)
+    return np.allclose(decode.reconstruct(C, Bm), S, rtol=0, atol=1e-12)
+
+
+def check_full_budget_dense(seed=6, theta=100.0, W=3):
+    """k >= L - W: the step equals dense GQA attention over [sinks; C B^T]."""
+    p = small_problem(seed, hkv=2, G=3, dh=8, L=25, s=2)
+    cfg = cfg_of(p, W=W, k=10 ** 6, kappa=5, theta=theta)
+    r = run(p, cfg)
+    B, L, s = p["q"].shape[0], p["L"], p["s"]
+    K = np.concatenate([p["sink_k"], ref_full_keys(p["coef_k"], p["bases_k"])], axis=1)
+    V = np.concatenate([p["sink_v"], ref_full_keys(p["coef_v"], p["bases_v"])], axis=1)
+    pos_k = np.broadcast_to(np.arange(s + L), (B, s + L))
+    ref = torch_gqa_attention(p["q"], K, V, pos_k, np.full(B, s + L - 1), theta, p["hkv"])
+    return np.allclose(r["out"], ref, rtol=1e-10, atol=1e-12)
+
+
+def check_rope_complex(seed=7):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((3, 5, 16))
+    pos = rng.integers(0, 10 ** 5, size=(3, 5))
+    return np.allclose(decode.rope(x, pos, 500000.0), ref_rope_complex(x, pos, 500000.0),
+                       rtol=1e-10, atol=1e-10)
+
+
+def check_rope_shift_invariance(seed=8):
+    """Shifting every position by the same amount leaves the output unchanged."""
+    rng = np.random.default_rng(seed)
+    B, hq, hkv, dh, n = 2, 4, 2, 8, 11
+    q = rng.standard_normal((B, hq, dh))
+    K = rng.standard_normal((B, n, hkv * dh))
+    V = rng.standard_normal((B, n, hkv * dh))
+    pos_k = np.sort(rng.choice(1000, size=(B, n), replace=False), axis=1)
+    pos_q = np.full(B, 1000)
+    o1 = decode.attend(q, K, V, pos_k, pos_q, 1000.0, hkv)
+    o2 = decode.attend(q, K, V, pos_k + 777, pos_q + 777, 1000.0, hkv)
+    return np.allclose(o1, o2, rtol=1e-9, atol=1e-10)
+
+
+def check_plain_gqa(seed=9, theta=10000.0):
+    """s = 0, L = W and a full-rank basis: ordinary GQA decode attention over S."""
+    rng = np.random.default_rng(seed)
+    B, hkv, G, dh, L = 2, 2, 2, 8, 6
+    Dp = hkv * dh
+    S_k = rng.standard_normal((B, L, Dp))
+    S_v = rng.standard_normal((B, L, Dp))
+    Bk = np.stack([_orth(rng, Dp, Dp)[None] for _ in range(B)])
+    Bv = np.stack([_orth(rng, Dp, Dp)[None] for _ in range(B)])
+    q = rng.standard_normal((B, hkv * G, dh))
+    cfg = dict(n_kv_heads=hkv, window=L, topk=3, pool_kernel=3, rope_theta=theta, dtype="fp32")
+    r = decode.decode_step(cfg, L, q, np.zeros((B, 0, Dp)), np.zeros((B, 0, Dp)), Bk, Bv,
+                           decode.project(S_k, Bk), decode.project(S_v, Bv))
+    ref = torch_gqa_attention(q, S_k, S_v, np.broadcast_to(np.arange(L), (B, L)),
+                              np.full(B, L - 1), theta, hkv)
+    return np.allclose(r["out"], ref, rtol=1e-10, atol=1e-11)
+
+
+def check_causal_window(seed=10):
+    """W_q > 1: row i only sees keys up to its own position, rows are averaged."""
+    p = small_problem(seed, L=30)
+    Wq = 4
+    rng = np.random.default_rng(seed)
+    qprev = rng.standard_normal((p["q"].shape[0], p["G"], Wq - 1, p["R"]))
+    rel = decode.relevance(p["q"], qprev, p["bases_k"], p["coef_k"], p["L"], p["hkv"], 1)
+    cQ = rel["cQ"]
+    L = p["L"]
+    for b in range(cQ.shape[0]):
+        for g in range(cQ.shape[1]):
+            acc = np.zeros(L)
+            for i in range(Wq):
+                pos = L - Wq + i
+                z = np.array([cQ[b, g, i] @ p["coef_k"][b, l] / np.sqrt(p["R"]) for l in range(pos + 1)])
+                e = np.exp(z - z.max())
+                acc[:pos + 1] += e / e.sum()
+            if not np.allclose(rel["AQ"][b, g], acc / Wq, rtol=1e-12, atol=1e-15):
+                return False
+    return True
+
+
+ALL_CHECKS = [check_latent_identity, check_rotation_invariance, check_pool_vs_torch,
+              check_topk_special_case, check_select_bruteforce, check_full_rank_exact,
+              check_full_budget_dense, check_rope_complex, check_rope_shift_invariance,
+              check_plain_gqa, check_causal_window]
+
+
+# ----------------------------------------------------------------------------
+# the pins as tests
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("nb", [1, 2])
+def test_latent_scores_equal_reconstructed_scores(nb):
+    assert check_latent_identity(nb=nb)
+
+
+def test_rotation_invariance():
+    assert check_rotation_invariance()
+
+
+def test_pooling_matches_torch():
+    assert check_pool_vs_torch()
+
+
+def test_single_query_topk_is_plain_topk():
+    assert check_topk_special_case()
+
+
+def test_select_matches_bruteforce():
+    assert check_select_bruteforce()
+
+
+def test_full_rank_reconstruction_exact():
+    assert check_full_rank_exact()
+
+
+@pytest.mark.parametrize("theta,W", [(100.0, 3), (0.0, 3), (500000.0, 0)])
+def test_full_budget_equals_dense_attention(theta, W):
+    assert check_full_budget_dense(theta=theta, W=W)
+
+
+def test_rope_rotate_half_equals_complex_form():
+    assert check_rope_complex()
+
+
+def test_rope_relative_positions():
+    assert check_rope_shift_invariance()
+
+
+def test_plain_gqa_decode_special_case():
+    assert check_plain_gqa()
+
+
+def test_causal_query_window():
+    assert check_causal_window()
+
+
+def test_exact_window_kv_replaces_reconstruction():
+    """With exact window KV equal to the reconstructed window rows the output is
+    unchanged; with different rows only attention changes, never selection."""
+    p = small_problem(11, L=30)
+    W = 5
+    cfg = cfg_of(p, W=W, k=6)
+    a = run(p, cfg)
+    K = ref_full_keys(p["coef_k"], p["bases_k"])
+    V = ref_full_keys(p["coef_v"], p["bases_v"])
+    L = p["L"]
+    same = run(p, cfg, win_k=K[:, L - W:L], win_v=V[:, L - W:L])
+    assert np.allclose(same["out"], a["out"], rtol=1e-12, atol=1e-12)
+    rng = np.random.default_rng(0)
+    other = run(p, cfg, win_k=rng.standard_normal(K[:, L - W:L].shape),
+                win_v=rng.standard_normal(V[:, L - W:L].shape))
+    assert np.array_equal(other["idx"], a["idx"])
+    assert not np.allclose(other["out"], a["out"])
+
+
+def test_append_projects_and_rounds_new_row():
+    p = small_problem(12, L=20)
+    rng = np.random.default_rng(1)
+    Dp = p["hkv"] * p["dh"]
+    kn, vn = rng.standard_normal((2, Dp)), rng.standard_normal((2, Dp))
+    cfg = cfg_of(p)
+    cfg["dtype"] = "bf16"
+    r = run(p, cfg, k_new=kn, v_new=vn)
+    # independent: torch matmul per basis group, torch bf16 cast
+    ref = torch.einsum("bd,bdr->br", torch.from_numpy(kn), torch.from_numpy(p["bases_k"][:, 0]))
+    ref = ref.to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(r["coef_k"][:, p["L"] - 1], ref)
+    assert np.array_equal(r["coef_k"][:, :p["L"] - 1], p["coef_k"][:, :p["L"] - 1])
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(13)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-30, 30, 10000),
+                        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -9, -0.0, 0.0, 65504.0])])
+    ref = torch.from_numpy(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(storage.to_bf16(x), ref)
+
+
+def test_num_selected_formula():
+    for L, W, k in itertools.product([0, 1, 5, 64, 100], [0, 1, 4, 64], [0, 1, 10, 1000]):
+        if L == 0:
+            continue
+        a = np.zeros((1, L))
+        assert decode.select(a, L, W, k).shape[1] == decode.num_selected(L, W, k)
+
+
+# ----------------------------------------------------------------------------
+# mutation tests: a planted mistake in the oracle must trip a pin
+# ----------------------------------------------------------------------------
+
+def _fails(monkeypatch_ctx, target, name, replacement):
+    with monkeypatch_ctx.context() as m:
+        m.setattr(target, name, replacement)
+        return [c.__name__ for c in ALL_CHECKS if not c()]
+
+
+def test_mutation_dropped_scale(monkeypatch):
+    orig = decode.latent_logits
+
+    def bad(cQ, coef_k, L):
+        return orig(cQ, coef_k, L) * np.sqrt(np.asarray(coef_k).shape[-1])
+    assert _fails(monkeypatch, decode, "latent_logits", bad)
+
+
+def test_mutation_wrong_query_grouping(monkeypatch):
+    def bad(q, n_kv_heads):
+        q = np.asarray(q, dtype=np.float64)
+        B, hq, dh = q.shape
+        return q.reshape(B, hq // n_kv_heads, n_kv_heads * dh)   # plain view: wrong heads
+    assert _fails(monkeypatch, decode, "group_queries", bad)
+
+
+def test_mutation_pool_off_by_one(monkeypatch):
+    orig = decode.pool
+
+    def bad(AQ, kappa, mode="max"):
+        return np.roll(orig(AQ, kappa, mode), 1, axis=-1)
+    assert _fails(monkeypatch, decode, "pool", bad)
+
+
+def test_mutation_tie_to_higher_index(monkeypatch):
+    def bad(a_tilde, L, W, k):
+        a = np.asarray(a_tilde, dtype=np.float64)
+        n_hist = max(L - W, 0)
+        k_eff = min(k, n_hist)
+        out = []
+        for row in a:
+            order = np.argsort(-row[:n_hist][::-1], kind="stable")
+            glob = np.sort(n_hist - 1 - order[:k_eff])
+            out.append(np.concatenate([glob, np.arange(n_hist, L)]))
+        return np.array(out, dtype=np.int64)
+    assert "check_select_bruteforce" in _fails(monkeypatch, decode, "select", bad)
+
+
+def test_mutation_rope_sign(monkeypatch):
+    orig = decode.rope
+
+    def bad(x, pos, theta):
+        return orig(x, -np.asarray(pos, dtype=np.float64), theta)
+    assert _fails(monkeypatch, decode, "rope", bad)
+
+
+def test_mutation_transposed_basis(monkeypatch):
+    def bad(coef_rows, bases):
+        bases = np.asarray(bases, dtype=np.float64)
+        c = np.asarray(coef_rows, dtype=np.float64)
+        # uses the basis rows as if they were columns (only shape-valid when square)
+        nb, dg, rank = bases.shape[1:]
+        bt = np.swapaxes(bases, -1, -2) if dg == rank else bases[..., ::-1, :]
+        cb = c.reshape(c.shape[0], c.shape[1], nb, rank)
+        bb = np.broadcast_to(bt, (c.shape[0], nb, dg, rank))
+        return np.einsum("bnkr,bkdr->bnkd", cb, bb).reshape(c.shape[0], c.shape[1], nb * dg)
+    assert _fails(monkeypatch, decode, "reconstruct", bad)
+
+
+def test_mutation_window_mean_drops_row(monkeypatch):
+    def bad(A):
+        return np.mean(A[:, :, 1:, :], axis=2) if A.shape[2] > 1 else np.mean(A, axis=2)
+    assert "check_causal_window" in _fails(monkeypatch, decode, "window_mean", bad)
+
+
+# ----------------------------------------------------------------------------
+# prefill (Section 3.1)
+# ----------------------------------------------------------------------------
+
+def test_prefill_bases_orthonormal_and_exact_on_low_rank():
+    rng = np.random.default_rng(14)
+    B, N, Dp, r_true, s = 2, 200, 16, 5, 4
+    F = rng.standard_normal((B, N, r_true))
+    P = rng.standard_normal((B, r_true, Dp))
+    S = np.einsum("bnr,brd->bnd", F, P)
+    st = prefill.prefill(S, S, s, rank=r_true, sample_idx=np.arange(0, N - s, 3), dtype="fp32")
+    for b in range(B):
+        Bm = st["bases_k"][b, 0]
+        assert np.allclose(Bm.T @ Bm, np.eye(r_true), atol=1e-6)
+    # rank >= true rank: coefficients reconstruct the raw (un-normalised) rows
+    st64 = prefill.prefill(S, S, s, rank=r_true, sample_idx=np.arange(0, N - s, 3), dtype="fp32")
+    rec = decode.reconstruct(st64["coef_k"], st64["bases_k"])
+    assert np.allclose(rec, S[:, s:], rtol=1e-4, atol=1e-4 * np.abs(S).max())
+    assert np.array_equal(st["sink_k"], storage.to_fp32(S[:, :s]))
+
+
+def test_prefill_normalisation_changes_basis_not_projection():
+    """Normalisation only feeds the SVD: the stored coefficients are S B."""
+    rng = np.random.default_rng(15)
+    S = rng.standard_normal((1, 60, 8)) * rng.random((1, 60, 1)) * 50
+    st = prefill.prefill(S, S, 2, rank=3, sample_idx=np.arange(0, 58, 2), dtype="fp32")
+    C_ref = np.einsum("td,dr->tr", S[0, 2:], st["bases_k"][0, 0])
+    assert np.allclose(st["coef_k"][0], C_ref, rtol=1e-6, atol=1e-5)
+    Xn = S[0, 2:][np.arange(0, 58, 2)]
+    Xn = Xn / np.linalg.norm(Xn, axis=1, keepdims=True)
+    v = np.linalg.svd(Xn)[2][:3].T
+    # same subspace as the SVD of the normalised samples
+    assert np.allclose(v @ v.T, st["bases_k"][0, 0] @ st["bases_k"][0, 0].T, atol=1e-5)
+
+
+def test_hybrid_sampler_split():
+    idx = prefill.sample_hybrid(1000, eta=0.2)
+    assert idx.size == 200
+    recent = idx[idx >= 1000 - 140]
+    assert recent.size == 140 and recent.max() == 999
+    assert np.all(np.diff(idx) > 0)
+
+
+def test_oracle_package_exports():
+    for name in ("decode_step", "select", "pool", "rope", "attend", "reconstruct"):
+        assert hasattr(oracle, name)

@@ -1,0 +1,289 @@
+"""Seeded synthetic workloads for the S^4R decode step.
+
+This module only draws random numbers and lays them out in the shapes of the
+paper's long-context workloads (Llama-3.1-8B and Qwen2.5-7B single layers at
+32k/128k context, 4 sinks, ~5x compression).  It holds none of the method's
+arithmetic: no projection onto a learned basis, no scoring, no selection.  It
+is shared by the tests (which turn raw KV into stored state with the oracle's
+prefill) and by the benchmark (which draws the stored state directly in latent
+coordinates).  It imports neither the oracle nor the GPU package.
+
+Two recipes
+-----------
+raw_kv(wl, seed)        raw pre-RoPE keys/values [B, N, Dp] and the query:
+                        low-rank Gaussian (or Student-t) signal + noise, sinks
+                        scaled x10, a few outlier key channels, needles planted
+                        along the group-mean query direction.
+latent_state(wl, seed)  the stored state directly: per-sequence random
+                        orthonormal bases (QR of a Gaussian), coefficient rows
+                        drawn as low-rank latent signal with a decaying
+                        spectrum + noise, needles in latent coordinates, sinks
+                        and a query that lies mostly in the key basis' span.
+
+Seeds come from numpy.random.SeedSequence([workload id, layer, sequence,
+stream tag]) so every sequence and every tensor has its own stream.
+"""
+
+import dataclasses
+
+import numpy as np
+import torch
+
+# stream tags
+_T_KEY, _T_VAL, _T_QRY, _T_NEEDLE, _T_SINK, _T_BASIS_K, _T_BASIS_V, _T_STEP = range(8)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    wid: int                 # numeric id used in seeds
+    batch: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    N: int                   # context length including the sinks
+    n_sink: int
+    rank: int                # rank per basis group
+    basis_groups: int
+    window: int
+    topk: int
+    dtype: str               # "bf16" | "fp32"
+    rope_theta: float
+    r_true: int
+    noise: float
+    n_needles: int
+    outlier_channels: int = 0
+    outlier_scale: float = 1.0
+    heavy_tail: bool = False
+    q_window: int = 1
+    pool_kernel: int = 7
+    pool_mode: str = "max"
+    group_agg: str = "mean"
+    layers: int = 1
+    steps: int = 1
+
+    @property
+    def G(self):
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def Dp(self):
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def R(self):
+        return self.rank * self.basis_groups
+
+    @property
+    def L(self):
+        return self.N - self.n_sink
+
+    def scaled(self, **kw):
+        return dataclasses.replace(self, **kw)
+
+    def describe(self):
+        return (f"{self.name}: B={self.batch} h_q={self.n_q_heads} h_kv={self.n_kv_heads} "
+                f"d_h={self.head_dim} N={self.N} s={self.n_sink} r={self.R} W={self.window} "
+                f"k={self.topk} {self.dtype}")
+
+
+# The five workloads: one tiny fp32 layer, Llama-3.1-8B-shaped layers at 32k
+# and 128k, a Qwen2.5-7B-shaped layer at 128k, and the 32-layer sustained run.
+CONFIGS = {
+    "tiny_fp32": Workload("tiny_fp32", 1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64,
+                          N=4096, n_sink=4, rank=32, basis_groups=2, window=64, topk=128,
+                          dtype="fp32", rope_theta=10000.0, r_true=24, noise=0.05, n_needles=5),
+    "llama8b_32k": Workload("llama8b_32k", 2, batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                            N=32768, n_sink=4, rank=160, basis_groups=1, window=64, topk=1024,
+                            dtype="bf16", rope_theta=500000.0, r_true=128, noise=0.05,
+                            n_needles=32, outlier_channels=4, outlier_scale=8.0),
+    "llama8b_128k": Workload("llama8b_128k", 3, batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                             N=131072, n_sink=4, rank=160, basis_groups=1, window=128, topk=2048,
+                             dtype="bf16", rope_theta=500000.0, r_true=128, noise=0.05,
+                             n_needles=32, outlier_channels=4, outlier_scale=8.0),
+    "qwen7b_128k": Workload("qwen7b_128k", 4, batch=8, n_q_heads=28, n_kv_heads=4, head_dim=128,
+                            N=131072, n_sink=4, rank=96, basis_groups=1, window=64, topk=1024,
+                            dtype="bf16", rope_theta=1000000.0, r_true=80, noise=0.1,
+                            n_needles=32, heavy_tail=True),
+    "llama8b_32L_sustained": Workload("llama8b_32L_sustained", 5, batch=32, n_q_heads=32, n_kv_heads=8,
+                                      head_dim=128, N=32768, n_sink=4, rank=160, basis_groups=1,
+                                      window=64, topk=1024, dtype="bf16", rope_theta=500000.0,
+                                      r_true=128, noise=0.05, n_needles=32, outlier_channels=4,
+                                      outlier_scale=8.0, layers=32, steps=256),
+}
+
+HEADLINE = "llama8b_128k"
+
+
+def _rng(wl, seed, layer, seq, tag):
+    return np.random.default_rng(np.random.SeedSequence([wl.wid, seed, layer, seq, tag]))
+
+
+def round_storage(x, dtype):
+    """Round float64 data to the storage format with torch's own casts
+    (round to nearest even); returns float64 holding representable values."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64)).to(torch.float32)
+    if dtype == "bf16":
+        t = t.to(torch.bfloat16).to(torch.float32)
+    elif dtype != "fp32":
+        raise ValueError(dtype)
+    return t.to(torch.float64).numpy()
+
+
+def _signal(rng, n, r_true, heavy):
+    if heavy:
+        return rng.standard_t(3.0, size=(n, r_true)) / np.sqrt(3.0)
+    return rng.standard_normal((n, r_true))
+
+
+def _needle_positions(rng, wl, count):
+    hi = max(wl.L - wl.window, 1)
+    count = min(count, hi)
+    return np.sort(rng.choice(hi, size=count, replace=False))
+
+
+def _query_heads(q_groups, wl):
+    """[B, G, Dp] group queries -> [B, h_q, d_h] per-head queries (head j*G+g)."""
+    B = q_groups.shape[0]
+    return (q_groups.reshape(B, wl.G, wl.n_kv_heads, wl.head_dim)
+            .transpose(0, 2, 1, 3).reshape(B, wl.n_q_heads, wl.head_dim))
+
+
+def raw_kv(wl, seed=0, layer=0):
+    """Raw prompt keys/values [B, N, Dp] and the query [B, h_q, d_h] (float64).
+
+    Keys and values are F P / sqrt(r_true) + noise * E with a per-sequence
+    mixing matrix P; the first n_sink rows are scaled x10; `outlier_channels`
+    key channels are scaled by `outlier_scale`.  The group queries are 0.9 of
+    a direction in P's row space plus 0.1 noise, scaled so latent logits have
+    a standard deviation of about 1.5.  Needle keys (at positions in
+    [0, L - W), non-sink numbering) get the kv-head slice of the mean group
+    query direction added with a norm that lifts their logits well above the
+    rest.
+    """
+    B, N, Dp = wl.batch, wl.N, wl.Dp
+    S_k = np.empty((B, N, Dp))
+    S_v = np.empty((B, N, Dp))
+    qg = np.empty((B, wl.G, Dp))
+    needles = []
+    for b in range(B):
+        rk, rv, rq = (_rng(wl, seed, layer, b, t) for t in (_T_KEY, _T_VAL, _T_QRY))
+        Pk = rk.standard_normal((wl.r_true, Dp)) / np.sqrt(wl.r_true)
+        Pv = rv.standard_normal((wl.r_true, Dp)) / np.sqrt(wl.r_true)
+        S_k[b] = _signal(rk, N, wl.r_true, wl.heavy_tail) @ Pk + wl.noise * rk.standard_normal((N, Dp))
+        S_v[b] = _signal(rv, N, wl.r_true, wl.heavy_tail) @ Pv + wl.noise * rv.standard_normal((N, Dp))
+        if wl.outlier_channels:
+            ch = rk.choice(Dp, size=wl.outlier_channels, replace=False)
+            S_k[b, :, ch] *= wl.outlier_scale
+        S_k[b, :wl.n_sink] *= 10.0
+        S_v[b, :wl.n_sink] *= 10.0
+        sig = rq.standard_normal((wl.G, wl.r_true)) @ Pk
+        sig /= np.linalg.norm(sig, axis=-1, keepdims=True)
+        noise = rq.standard_normal((wl.G, Dp))
+        noise /= np.linalg.norm(noise, axis=-1, keepdims=True)
+        qdir = 0.9 * sig + 0.1 * noise
+        qdir /= np.linalg.norm(qdir, axis=-1, keepdims=True)
+        qnorm = 1.5 * np.sqrt(wl.R) / (np.linalg.norm(S_k[b, wl.n_sink:], axis=-1).mean() / np.sqrt(wl.r_true))
+        qg[b] = qdir * qnorm
+        rn = _rng(wl, seed, layer, b, _T_NEEDLE)
+        pos = _needle_positions(rn, wl, wl.n_needles)
+        needles.append(pos)
+        mean_dir = qdir.mean(axis=0)
+        for p in pos:
+            lift = (10.0 + 4.0 * rn.random()) * np.sqrt(wl.R) / qnorm
+            for j in range(wl.n_kv_heads):
+                sl = slice(j * wl.head_dim, (j + 1) * wl.head_dim)
+                d = mean_dir[sl]
+                S_k[b, wl.n_sink + p, sl] += lift * d / max(np.linalg.norm(mean_dir), 1e-12)
+    q = round_storage(_query_heads(qg, wl), wl.dtype)
+    return {"S_k": S_k, "S_v": S_v, "q": q, "needles": needles}
+
+
+def _orthonormal(rng, rows, cols):
+    a = rng.standard_normal((rows, cols))
+    qm, rm = np.linalg.qr(a)
+    return qm * np.sign(np.diag(rm))[None, :]
+
+
+def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
+    """Stored decode state drawn directly (already rounded to wl.dtype).
+
+    Returns float64 arrays:
+      bases_k/v [B, nb, Dp/nb, rank] orthonormal columns per group,
+      coef_k/v  [B, capacity, R] (rows >= L are zero),
+      sink_k/v  [B, s, Dp], q [B, h_q, d_h], needles (positions per sequence).
+    Coefficient rows are F M + noise * E with F Gaussian (Student-t nu=3 when
+    heavy_tail) and M a random mixing with a 1/(1 + i/16) column spectrum;
+    row norms are about sqrt(Dp).  The query of group g is B^K u_g (+10%
+    orthogonal noise) scaled for a latent-logit standard deviation of ~1.5.
+    """
+    B, Dp, R, nb = wl.batch, wl.Dp, wl.R, wl.basis_groups
+    dg = Dp // nb
+    L = wl.L if L is None else L
+    cap = L if capacity is None else capacity
+    out = {k: None for k in ("bases_k", "bases_v", "coef_k", "coef_v", "sink_k", "sink_v", "q")}
+    bk = np.empty((B, nb, dg, wl.rank))
+    bv = np.empty((B, nb, dg, wl.rank))
+    ck = np.zeros((B, cap, R))
+    cv = np.zeros((B, cap, R))
+    sk = np.empty((B, wl.n_sink, Dp))
+    sv = np.empty((B, wl.n_sink, Dp))
+    qg = np.empty((B, wl.G, Dp))
+    needles = []
+    spectrum = 1.0 / (1.0 + np.arange(R) / 16.0)
+    for b in range(B):
+        rbk = _rng(wl, seed, layer, b, _T_BASIS_K)
+        rbv = _rng(wl, seed, layer, b, _T_BASIS_V)
+        for g in range(nb):
+            bk[b, g] = _orthonormal(rbk, dg, wl.rank)
+            bv[b, g] = _orthonormal(rbv, dg, wl.rank)
+        rk, rv, rq, rs = (_rng(wl, seed, layer, b, t) for t in (_T_KEY, _T_VAL, _T_QRY, _T_SINK))
+        scale = np.sqrt(Dp) / np.sqrt((spectrum ** 2).sum())
+        Mk = rk.standard_normal((wl.r_true, R)) * spectrum / np.sqrt(wl.r_true) * scale
+        Mv = rv.standard_normal((wl.r_true, R)) * spectrum / np.sqrt(wl.r_true) * scale
+        ck[b, :L] = _signal(rk, L, wl.r_true, wl.heavy_tail) @ Mk + wl.noise * scale * rk.standard_normal((L, R)) * spectrum
+        cv[b, :L] = _signal(rv, L, wl.r_true, wl.heavy_tail) @ Mv + wl.noise * scale * rv.standard_normal((L, R)) * spectrum
+        sk[b] = 10.0 * rs.standard_normal((wl.n_sink, Dp))
+        sv[b] = 10.0 * rs.standard_normal((wl.n_sink, Dp))
+        # query: latent direction u_g in the span of Mk's rows, mapped through B^K
+        u = rq.standard_normal((wl.G, wl.r_true)) @ Mk
+        u /= np.linalg.norm(u, axis=-1, keepdims=True)
+        qlat = np.empty((wl.G, Dp))
+        for g in range(nb):
+            qlat[:, g * dg:(g + 1) * dg] = u[:, g * wl.rank:(g + 1) * wl.rank] @ bk[b, g].T
+        qlat /= np.maximum(np.linalg.norm(qlat, axis=-1, keepdims=True), 1e-12)
+        noise = rq.standard_normal((wl.G, Dp))
+        noise /= np.linalg.norm(noise, axis=-1, keepdims=True)
+        qdir = 0.9 * qlat + 0.1 * noise
+        qdir /= np.linalg.norm(qdir, axis=-1, keepdims=True)
+        # u is aligned with the high-variance latent directions, so the
+        # component of a coefficient row along it is about 2 sqrt(Dp/r_true)
+        qnorm = 1.5 * np.sqrt(R) / (2.0 * np.sqrt(Dp) / np.sqrt(wl.r_true))
+        qg[b] = qdir * qnorm
+        rn = _rng(wl, seed, layer, b, _T_NEEDLE)
+        wl_eff = wl.scaled(N=L + wl.n_sink)
+        pos = _needle_positions(rn, wl_eff, wl.n_needles)
+        needles.append(pos)
+        udir = u.mean(axis=0)
+        udir /= max(np.linalg.norm(udir), 1e-12)
+        for p in pos:
+            lift = (10.0 + 4.0 * rn.random()) * np.sqrt(R) / qnorm
+            ck[b, p] += lift * udir
+    rnd = lambda a: round_storage(a, wl.dtype)  # noqa: E731
+    out.update(bases_k=rnd(bk), bases_v=rnd(bv), coef_k=rnd(ck), coef_v=rnd(cv),
+               sink_k=rnd(sk), sink_v=rnd(sv), q=rnd(_query_heads(qg, wl)), needles=needles)
+    return out
+
+
+def step_inputs(wl, seed, layer, step, state=None):
+    """Per-step inputs of the sustained run: a fresh query and the new token's
+    raw key/value (drawn near the bases' span when a state is given)."""
+    r = _rng(wl, seed, layer, step, _T_STEP)
+    B, Dp = wl.batch, wl.Dp
+    # group-query norm as in latent_state: 1.5 sqrt(R) sqrt(r_true) / sqrt(Dp)
+    qnorm = 1.5 * np.sqrt(wl.R) * np.sqrt(wl.r_true) / np.sqrt(Dp)
+    q = r.standard_normal((B, wl.n_q_heads, wl.head_dim)) * qnorm / np.sqrt(Dp)
+    k_new = r.standard_normal((B, Dp))
+    v_new = r.standard_normal((B, Dp))
+    rnd = lambda a: round_storage(a, wl.dtype)  # noqa: E731
+    return {"q": rnd(q), "k_new": rnd(k_new), "v_new": rnd(v_new)}
