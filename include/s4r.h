@@ -1,0 +1,205 @@
+/*
+ * s4r.h - C ABI of the S^4R decode-step library for AMD MI355X (gfx950).
+ *
+ * S^4R (arxiv 2608.00528) keeps a layer's KV cache as full-precision sink
+ * tokens plus low-rank coefficients of every other token on per-sequence key
+ * and value bases (Section 3.1).  One decode step (Section 3.2) scores every
+ * cached token in the latent space, keeps the local window plus the top-k
+ * tokens, reconstructs only those as coefficients times basis, applies RoPE
+ * at their original positions and runs GQA softmax attention over sinks and
+ * reconstructed tokens.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Array pointers are DEVICE pointers, 16-byte aligned, densely packed in
+ *    the layouts stated below.  The caller owns all memory; the library never
+ *    allocates device memory.  Scratch lives in the caller's workspace, whose
+ *    size s4r_workspace_size() returns; its initial contents do not matter.
+ *  - Every call is asynchronous on the caller's hipStream_t and performs no
+ *    host synchronisation.  Calls that share a workspace must not overlap.
+ *  - Arguments are validated on the host before anything is launched.  On
+ *    error nothing is launched, no output is touched, the status code says
+ *    what class of problem it was and s4r_last_error() (thread-local) says
+ *    which argument.  A failed launch returns S4R_ERR_HIP.
+ *  - Storage dtype (cfg.dtype) applies to q, sinks, window KV, new K/V rows,
+ *    bases and coefficient caches.  Query coefficients and all outputs are
+ *    fp32; indices are int32.
+ *
+ * Notation (paper): B batch, h_q / h_kv query / KV heads, G = h_q / h_kv,
+ * d_h head dim, Dp = h_kv * d_h, R = basis_groups * rank (latent width r of
+ * the paper), s sinks, W local window, W_q query-coefficient rows, k global
+ * budget, L the current non-sink length (the token appended this step
+ * included), m = min(k, max(L - W, 0)) + min(W, L) selected tokens.
+ *
+ * Layouts
+ * -------
+ *  q          [B, h_q, d_h]            pre-RoPE query, head h reads KV head h / G
+ *  sink_k/v   [B, s, Dp]               pre-RoPE sink keys / values (Section 3.1.1)
+ *  win_k/v    [B, W, Dp]               exact KV of positions L-W .. L-1 (optional)
+ *  bases_k/v  [B or 1, basis_groups, Dp / basis_groups, rank], rank fastest.
+ *             Group beta spans KV heads beta*h_kv/basis_groups onward; the
+ *             paper's single basis over Dp is basis_groups = 1 (Eq. svd).
+ *  coef_k/v   per sequence a [capacity, R] matrix in the TILED layout:
+ *             element (t, c) of sequence b is at
+ *               b*capacity*R + (t/16)*16*R + (c/32)*512 + (t%16)*32 + (c%32)
+ *             i.e. 16-token tiles, each split into 32-column blocks of
+ *             16 x 32 elements, token-major inside a block.  capacity % 16 == 0
+ *             and R % 32 == 0.  s4r_pack_coef / s4r_unpack_coef convert from /
+ *             to row-major [B, n, R].
+ *  qwin_prev  [B, G, W_q - 1, R] fp32  older query coefficients, oldest first
+ *  qcoef_out  [B, G, R] fp32           c_t^Q of this step (for the caller's FIFO)
+ *  scores     [B, L] fp32              relevance A~ of every non-sink token
+ *  idx        [B, m] int32             selected non-sink positions: the global
+ *                                      picks ascending, then the window ascending
+ *  k_hat/v_hat[B, m, Dp] fp32          reconstructed pre-RoPE keys / values
+ *  out        [B, h_q, d_h] fp32       attention output O_t
+ */
+#ifndef S4R_H
+#define S4R_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  S4R_OK = 0,
+  S4R_ERR_NULL_ARG = 1,     /* a required pointer is NULL                      */
+  S4R_ERR_BAD_SHAPE = 2,    /* sizes inconsistent (e.g. L > capacity, h_q % h_kv) */
+  S4R_ERR_UNSUPPORTED = 3,  /* valid but outside what the kernels implement     */
+  S4R_ERR_WORKSPACE = 4,    /* workspace smaller than s4r_workspace_size()      */
+  S4R_ERR_MISALIGNED = 5,   /* a pointer is not 16-byte aligned                 */
+  S4R_ERR_HIP = 6           /* a HIP call or kernel launch failed               */
+} s4r_status;
+
+enum { S4R_FP32 = 0, S4R_BF16 = 1 };          /* storage dtype                    */
+enum { S4R_POOL_MAX = 0, S4R_POOL_AVG = 1 };  /* F_P of Section 3.2.3 (default max)  */
+enum { S4R_AGG_MEAN = 0, S4R_AGG_MAX = 1 };   /* F_G of Section 3.2.3 (default mean) */
+
+typedef struct {
+  int32_t batch;         /* B                                                      */
+  int32_t n_q_heads;     /* h_q, a multiple of n_kv_heads                          */
+  int32_t n_kv_heads;    /* h_kv                                                   */
+  int32_t head_dim;      /* d_h: 64 or 128                                         */
+  int32_t basis_groups;  /* 1 = one basis over Dp (paper); must divide n_kv_heads  */
+  int32_t rank;          /* rank per basis group, multiple of 32, <= Dp/basis_groups */
+  int32_t n_sink;        /* s, sink tokens kept at full precision (Section 3.1.1)  */
+  int32_t window;        /* W, local window always kept (Section 3.2.3)            */
+  int32_t q_window;      /* W_q >= 1 query-coefficient rows used for scoring (3.2.2) */
+  int32_t topk;          /* k, global budget; clamped to max(L - W, 0)             */
+  int32_t pool_kernel;   /* kappa, odd, 1 = no pooling                             */
+  int32_t pool_mode;     /* S4R_POOL_MAX | S4R_POOL_AVG                            */
+  int32_t group_agg;     /* S4R_AGG_MEAN | S4R_AGG_MAX                             */
+  int32_t bases_shared;  /* 1: bases have no batch axis (one basis for all sequences) */
+  int64_t capacity;      /* token rows allocated in each coefficient cache, % 16 == 0 */
+  float rope_theta;      /* RoPE base; 0 disables RoPE                             */
+  int32_t dtype;         /* S4R_FP32 | S4R_BF16                                    */
+} s4r_config;
+
+/* Bytes of workspace any call with this config needs (host only, no GPU). */
+s4r_status s4r_workspace_size(const s4r_config* cfg, size_t* bytes);
+
+/* m = min(k, max(L - W, 0)) + min(W, L) (Section 3.3); -1 if cfg or L is invalid. */
+int32_t s4r_num_selected(const s4r_config* cfg, int64_t L);
+
+/* Thread-local description of the last error ("" after success). */
+const char* s4r_last_error(void);
+
+/* Library version string. */
+const char* s4r_version(void);
+
+/*
+ * Latent relevance (Section 3.2.2 and the pooling / group-aggregation
+ * equations of 3.2.3): c_t^Q = s_t^Q B^K per group, C^Q = [qwin_prev; c_t^Q],
+ * Z = C^Q (C^K)^T / sqrt(R) over the L non-sink tokens, causal mask, softmax
+ * over L, mean over the W_q rows, pooling with kernel kappa, aggregation
+ * over G -> scores[b, l].  qwin_prev may be NULL only when W_q == 1;
+ * qcoef_out may be NULL.
+ */
+s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q,
+                            const float* qwin_prev, const void* bases_k,
+                            const void* coef_k, float* scores, float* qcoef_out,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Index selection (Section 3.2.3): I_local = [max(L - W, 0), L),
+ * I_global = the k_eff largest scores[b, 0 : L - W] (equal scores go to the
+ * lower position), idx[b] = sorted(I_global) followed by I_local.  Bit-exact
+ * and deterministic for a given scores array.
+ */
+s4r_status s4r_select_topk(const s4r_config* cfg, int64_t L, const float* scores,
+                           int32_t* idx, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Sparse reconstruction (Section 3.2.3): k_hat[b, n] = C^K[b, idx[b, n]] (B^K)^T,
+ * v_hat likewise, per basis group, pre-RoPE, fp32.  idx entries must lie in
+ * [0, L); m is the number of indices per sequence.
+ */
+s4r_status s4r_reconstruct(const s4r_config* cfg, int64_t L, int32_t m, const int32_t* idx,
+                           const void* bases_k, const void* bases_v, const void* coef_k,
+                           const void* coef_v, float* k_hat, float* v_hat, hipStream_t stream);
+
+/*
+ * Final attention (Section 3.2.3): K* = [sink_k; k_sel], V* = [sink_v; v_sel]
+ * at positions [0 .. s-1, s + idx], query at s + L - 1, RoPE on q and K*,
+ * out[b, h] = softmax(RoPE(q_h) RoPE(K*_j)^T / sqrt(d_h)) V*_j with j = h / G.
+ * k_sel / v_sel are fp32 [B, m, Dp] pre-RoPE rows (e.g. from s4r_reconstruct).
+ */
+s4r_status s4r_sparse_attn(const s4r_config* cfg, int64_t L, int32_t m, const void* q,
+                           const void* sink_k, const void* sink_v, const int32_t* idx,
+                           const float* k_sel, const float* v_sel, float* out,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One fused decode step of one layer (Section 3.2): optional cache update
+ * (k_new / v_new [B, Dp] projected and written into coefficient row L - 1,
+ * Section 3.2.1), latent scoring, selection, reconstruction of the selected
+ * keys and values, RoPE and attention.  Reconstructed keys and values stay
+ * on chip and are never written to memory.  win_k / win_v
+ * may be NULL (the paper: the window is reconstructed like every selected
+ * token); if given they replace the window rows with exact KV.  idx_out
+ * [B, m] and scores_out [B, L] are optional copies of the selection.
+ * coef_k / coef_v are written only when k_new / v_new are given.
+ */
+s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
+                           const float* qwin_prev, const void* sink_k, const void* sink_v,
+                           const void* win_k, const void* win_v, const void* bases_k,
+                           const void* bases_v, void* coef_k, void* coef_v,
+                           const void* k_new, const void* v_new, float* out,
+                           int32_t* idx_out, float* scores_out, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/*
+ * Compressed cache update alone (Section 3.2.1): c^K = k_new B^K and
+ * c^V = v_new B^V, rounded to the storage dtype (fp64 accumulation, then
+ * fp32 and bf16 round-to-nearest-even), written into coefficient row `row`.
+ */
+s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_new,
+                              const void* v_new, const void* bases_k, const void* bases_v,
+                              void* coef_k, void* coef_v, hipStream_t stream);
+
+/* Layout conversion of a coefficient cache: row-major [B, n_rows, R] <-> tiled
+ * [B, capacity, R] (rows 0 .. n_rows-1; other rows of dst are left as they are). */
+s4r_status s4r_pack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_rowmajor,
+                         void* dst_tiled, hipStream_t stream);
+s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_tiled,
+                           void* dst_rowmajor, hipStream_t stream);
+
+/*
+ * Kernel timing for measurement.  While enabled, s4r_decode_step records a
+ * hipEvent pair around its latent-scoring stream kernel on the caller's stream
+ * (up to `max_launches` launches).  s4r_timing_read waits for the recorded
+ * events, returns the summed kernel time and the launch count, and disables
+ * timing.  Host-side event creation happens in s4r_timing_enable only.
+ */
+s4r_status s4r_timing_enable(int32_t max_launches);
+s4r_status s4r_timing_read(double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* S4R_H */

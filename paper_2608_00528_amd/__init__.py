@@ -1,0 +1,31 @@
+"""S^4R decode step (arxiv 2608.00528) for AMD MI355X (gfx950).
+
+The compute path is libs4r.so: hand-written HIP kernels behind the C ABI of
+include/s4r.h.  This package is its Python binding (ctypes + torch device
+memory and streams) and its build script.  Importing it loads the library and
+fails loudly when the library has not been built.
+"""
+
+from . import _lib
+from ._lib import Config, S4RError  # noqa: F401
+
+_lib.load()
+
+from .api import (  # noqa: E402,F401
+    alloc_workspace,
+    decode_step,
+    make_config,
+    num_selected,
+    pack_coef,
+    project_append,
+    reconstruct,
+    score_latent,
+    select_topk,
+    sparse_attn,
+    storage_dtype,
+    timing_enable,
+    timing_read,
+    unpack_coef,
+    version,
+    workspace_size,
+)

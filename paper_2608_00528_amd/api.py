@@ -1,0 +1,190 @@
+"""Python binding of the S^4R C ABI (include/s4r.h).
+
+Thin marshalling only: every function checks tensor placement / dtype /
+contiguity, allocates outputs with torch when the caller passes none, and
+calls the library on torch's current HIP stream.  All arithmetic happens in
+the gfx950 kernels of libs4r.so; there is no CPU path.
+"""
+
+import ctypes
+
+import torch
+
+from . import _lib as L
+
+_DTYPES = {"bf16": (L.S4R_BF16, torch.bfloat16), "fp32": (L.S4R_FP32, torch.float32)}
+_POOL = {"max": L.S4R_POOL_MAX, "avg": L.S4R_POOL_AVG}
+_AGG = {"mean": L.S4R_AGG_MEAN, "max": L.S4R_AGG_MAX}
+
+
+def make_config(*, batch, n_q_heads, n_kv_heads, head_dim, rank, capacity, basis_groups=1, n_sink=4,
+                window=64, q_window=1, topk=1024, pool_kernel=7, pool_mode="max", group_agg="mean",
+                bases_shared=False, rope_theta=0.0, dtype="bf16"):
+    c = L.Config()
+    c.batch, c.n_q_heads, c.n_kv_heads, c.head_dim = batch, n_q_heads, n_kv_heads, head_dim
+    c.basis_groups, c.rank, c.n_sink, c.window = basis_groups, rank, n_sink, window
+    c.q_window, c.topk, c.pool_kernel = q_window, topk, pool_kernel
+    c.pool_mode, c.group_agg = _POOL[pool_mode], _AGG[group_agg]
+    c.bases_shared = int(bool(bases_shared))
+    c.capacity = capacity
+    c.rope_theta = float(rope_theta)
+    c.dtype = _DTYPES[dtype][0]
+    return c
+
+
+def storage_dtype(cfg):
+    return torch.bfloat16 if cfg.dtype == L.S4R_BF16 else torch.float32
+
+
+def _ptr(t, name, dtype=None, required=True):
+    if t is None:
+        if required:
+            raise ValueError(f"{name} is required")
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _cfgp(cfg):
+    return ctypes.byref(cfg)
+
+
+def version():
+    return L.load().s4r_version().decode()
+
+
+def workspace_size(cfg):
+    n = ctypes.c_size_t()
+    L.check(L.load().s4r_workspace_size(_cfgp(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def alloc_workspace(cfg, device="cuda"):
+    return torch.empty(workspace_size(cfg), dtype=torch.uint8, device=device)
+
+
+def num_selected(cfg, length):
+    m = L.load().s4r_num_selected(_cfgp(cfg), length)
+    if m < 0:
+        raise L.S4RError(L.S4R_ERR_BAD_SHAPE, L.load().s4r_last_error().decode())
+    return m
+
+
+def _G(cfg):
+    return cfg.n_q_heads // cfg.n_kv_heads
+
+
+def _R(cfg):
+    return cfg.rank * cfg.basis_groups
+
+
+def score_latent(cfg, length, q, bases_k, coef_k, ws, qwin_prev=None, scores=None, qcoef=None):
+    dt = storage_dtype(cfg)
+    dev = q.device
+    if scores is None:
+        scores = torch.empty((cfg.batch, length), dtype=torch.float32, device=dev)
+    L.check(L.load().s4r_score_latent(
+        _cfgp(cfg), length, _ptr(q, "q", dt), _ptr(qwin_prev, "qwin_prev", torch.float32, False),
+        _ptr(bases_k, "bases_k", dt), _ptr(coef_k, "coef_k", dt), _ptr(scores, "scores", torch.float32),
+        _ptr(qcoef, "qcoef", torch.float32, False), _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+    return scores
+
+
+def select_topk(cfg, length, scores, ws, idx=None):
+    if idx is None:
+        idx = torch.empty((cfg.batch, num_selected(cfg, length)), dtype=torch.int32, device=scores.device)
+    L.check(L.load().s4r_select_topk(_cfgp(cfg), length, _ptr(scores, "scores", torch.float32),
+                                     _ptr(idx, "idx", torch.int32), _ptr(ws, "ws", torch.uint8), ws.numel(),
+                                     _stream()))
+    return idx
+
+
+def reconstruct(cfg, length, idx, bases_k, bases_v, coef_k, coef_v, k_hat=None, v_hat=None):
+    dt = storage_dtype(cfg)
+    m = idx.shape[1]
+    Dp = cfg.n_kv_heads * cfg.head_dim
+    if k_hat is None:
+        k_hat = torch.empty((cfg.batch, m, Dp), dtype=torch.float32, device=idx.device)
+    if v_hat is None:
+        v_hat = torch.empty((cfg.batch, m, Dp), dtype=torch.float32, device=idx.device)
+    L.check(L.load().s4r_reconstruct(_cfgp(cfg), length, m, _ptr(idx, "idx", torch.int32),
+                                     _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt),
+                                     _ptr(coef_k, "coef_k", dt), _ptr(coef_v, "coef_v", dt),
+                                     _ptr(k_hat, "k_hat", torch.float32), _ptr(v_hat, "v_hat", torch.float32),
+                                     _stream()))
+    return k_hat, v_hat
+
+
+def sparse_attn(cfg, length, q, sink_k, sink_v, idx, k_sel, v_sel, ws, out=None):
+    dt = storage_dtype(cfg)
+    m = idx.shape[1] if idx is not None else 0
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    need_sink = cfg.n_sink > 0
+    L.check(L.load().s4r_sparse_attn(_cfgp(cfg), length, m, _ptr(q, "q", dt),
+                                     _ptr(sink_k, "sink_k", dt, need_sink), _ptr(sink_v, "sink_v", dt, need_sink),
+                                     _ptr(idx, "idx", torch.int32, m > 0), _ptr(k_sel, "k_sel", torch.float32, m > 0),
+                                     _ptr(v_sel, "v_sel", torch.float32, m > 0), _ptr(out, "out", torch.float32),
+                                     _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+    return out
+
+
+def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, ws, qwin_prev=None,
+                win_k=None, win_v=None, k_new=None, v_new=None, out=None, idx_out=None, scores_out=None):
+    dt = storage_dtype(cfg)
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    need_sink = cfg.n_sink > 0
+    L.check(L.load().s4r_decode_step(
+        _cfgp(cfg), length, _ptr(q, "q", dt), _ptr(qwin_prev, "qwin_prev", torch.float32, False),
+        _ptr(sink_k, "sink_k", dt, need_sink), _ptr(sink_v, "sink_v", dt, need_sink),
+        _ptr(win_k, "win_k", dt, False), _ptr(win_v, "win_v", dt, False),
+        _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt), _ptr(coef_k, "coef_k", dt),
+        _ptr(coef_v, "coef_v", dt), _ptr(k_new, "k_new", dt, False), _ptr(v_new, "v_new", dt, False),
+        _ptr(out, "out", torch.float32), _ptr(idx_out, "idx_out", torch.int32, False),
+        _ptr(scores_out, "scores_out", torch.float32, False), _ptr(ws, "ws", torch.uint8), ws.numel(),
+        _stream()))
+    return out
+
+
+def project_append(cfg, row, k_new, v_new, bases_k, bases_v, coef_k, coef_v):
+    dt = storage_dtype(cfg)
+    L.check(L.load().s4r_project_append(_cfgp(cfg), row, _ptr(k_new, "k_new", dt), _ptr(v_new, "v_new", dt),
+                                        _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt),
+                                        _ptr(coef_k, "coef_k", dt), _ptr(coef_v, "coef_v", dt), _stream()))
+
+
+def pack_coef(cfg, n_rows, src, dst=None):
+    dt = storage_dtype(cfg)
+    if dst is None:
+        dst = torch.zeros((cfg.batch, cfg.capacity, _R(cfg)), dtype=dt, device=src.device)
+    L.check(L.load().s4r_pack_coef(_cfgp(cfg), n_rows, _ptr(src, "src", dt), _ptr(dst, "dst", dt), _stream()))
+    return dst
+
+
+def unpack_coef(cfg, n_rows, src, dst=None):
+    dt = storage_dtype(cfg)
+    if dst is None:
+        dst = torch.empty((cfg.batch, n_rows, _R(cfg)), dtype=dt, device=src.device)
+    L.check(L.load().s4r_unpack_coef(_cfgp(cfg), n_rows, _ptr(src, "src", dt), _ptr(dst, "dst", dt), _stream()))
+    return dst
+
+
+def timing_enable(max_launches):
+    L.check(L.load().s4r_timing_enable(max_launches))
+
+
+def timing_read():
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    L.check(L.load().s4r_timing_read(ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

@@ -1,0 +1,459 @@
+// C ABI of the S^4R library: argument validation, workspace carving and the
+// launch sequence of each entry point.  All validation happens on the host
+// before anything is launched; see include/s4r.h for the contract.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "s4r_internal.h"
+
+namespace s4r {
+namespace {
+
+thread_local std::string g_err;
+
+s4r_status fail(s4r_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+s4r_status ok() {
+  g_err.clear();
+  return S4R_OK;
+}
+
+constexpr int kMaxExtraTok = 1024 + 64;   // sinks + exact window rows in the combine kernel
+
+s4r_status make_problem(const s4r_config* c, Problem& P) {
+  if (!c) return fail(S4R_ERR_NULL_ARG, "cfg is NULL");
+  if (c->batch < 1) return fail(S4R_ERR_BAD_SHAPE, "batch must be >= 1 (got %d)", c->batch);
+  if (c->n_q_heads < 1 || c->n_kv_heads < 1)
+    return fail(S4R_ERR_BAD_SHAPE, "head counts must be >= 1 (h_q=%d, h_kv=%d)", c->n_q_heads, c->n_kv_heads);
+  if (c->n_q_heads % c->n_kv_heads)
+    return fail(S4R_ERR_BAD_SHAPE, "n_q_heads %d is not a multiple of n_kv_heads %d", c->n_q_heads, c->n_kv_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(S4R_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
+  if (c->basis_groups < 1 || c->n_kv_heads % c->basis_groups)
+    return fail(S4R_ERR_BAD_SHAPE, "basis_groups %d must divide n_kv_heads %d", c->basis_groups, c->n_kv_heads);
+  const int Dp = c->n_kv_heads * c->head_dim;
+  const int Dg = Dp / c->basis_groups;
+  if (c->rank < 1 || c->rank > Dg)
+    return fail(S4R_ERR_BAD_SHAPE, "rank %d must be in [1, Dp/basis_groups = %d]", c->rank, Dg);
+  if (c->rank % 32) return fail(S4R_ERR_UNSUPPORTED, "rank %d must be a multiple of 32", c->rank);
+  const int R = c->rank * c->basis_groups;
+  if (R > 256) return fail(S4R_ERR_UNSUPPORTED, "latent width %d > 256 not supported", R);
+  if (c->n_sink < 0 || c->n_sink > 1024) return fail(S4R_ERR_BAD_SHAPE, "n_sink %d outside [0, 1024]", c->n_sink);
+  if (c->window < 0) return fail(S4R_ERR_BAD_SHAPE, "window %d < 0", c->window);
+  if (c->q_window < 1) return fail(S4R_ERR_BAD_SHAPE, "q_window %d < 1", c->q_window);
+  if (c->topk < 0) return fail(S4R_ERR_BAD_SHAPE, "topk %d < 0", c->topk);
+  if (c->pool_kernel < 1 || c->pool_kernel % 2 == 0)
+    return fail(S4R_ERR_BAD_SHAPE, "pool_kernel %d must be odd and >= 1", c->pool_kernel);
+  if (c->pool_kernel > 65) return fail(S4R_ERR_UNSUPPORTED, "pool_kernel %d > 65", c->pool_kernel);
+  if (c->pool_mode != S4R_POOL_MAX && c->pool_mode != S4R_POOL_AVG)
+    return fail(S4R_ERR_BAD_SHAPE, "pool_mode %d invalid", c->pool_mode);
+  if (c->group_agg != S4R_AGG_MEAN && c->group_agg != S4R_AGG_MAX)
+    return fail(S4R_ERR_BAD_SHAPE, "group_agg %d invalid", c->group_agg);
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if ((int64_t)G * c->q_window > kMaxGW)
+    return fail(S4R_ERR_UNSUPPORTED, "G * q_window = %d > %d not supported", G * c->q_window, kMaxGW);
+  if (c->capacity < 16 || c->capacity % 16)
+    return fail(S4R_ERR_BAD_SHAPE, "capacity %lld must be a positive multiple of 16", (long long)c->capacity);
+  if (c->capacity > ((int64_t)1 << 30))
+    return fail(S4R_ERR_UNSUPPORTED, "capacity %lld > 2^30", (long long)c->capacity);
+  if (!(c->rope_theta >= 0.f) || !std::isfinite(c->rope_theta))
+    return fail(S4R_ERR_BAD_SHAPE, "rope_theta must be finite and >= 0");
+  if (c->dtype != S4R_FP32 && c->dtype != S4R_BF16) return fail(S4R_ERR_BAD_SHAPE, "dtype %d invalid", c->dtype);
+  if (c->bases_shared != 0 && c->bases_shared != 1) return fail(S4R_ERR_BAD_SHAPE, "bases_shared must be 0 or 1");
+
+  P.B = c->batch;
+  P.hq = c->n_q_heads;
+  P.hkv = c->n_kv_heads;
+  P.dh = c->head_dim;
+  P.G = G;
+  P.Dp = Dp;
+  P.nb = c->basis_groups;
+  P.rank = c->rank;
+  P.R = R;
+  P.Dg = Dg;
+  P.s = c->n_sink;
+  P.W = c->window;
+  P.Wq = c->q_window;
+  P.k = c->topk;
+  P.kappa = c->pool_kernel;
+  P.pool_mode = c->pool_mode;
+  P.agg = c->group_agg;
+  P.bases_shared = c->bases_shared;
+  P.dtype = c->dtype;
+  P.cap = c->capacity;
+  P.theta = c->rope_theta;
+  P.GW = G * c->q_window;
+  P.nruns_max = (c->capacity + kRunTok - 1) / kRunTok;
+  P.m_max = std::min<int64_t>(c->topk, std::max<int64_t>(c->capacity - c->window, 0)) +
+            std::min<int64_t>(c->window, c->capacity);
+  return S4R_OK;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
+
+struct Layout {
+  size_t off[14];
+  size_t total;
+};
+
+Layout layout(const Problem& P) {
+  const size_t B = P.B, GW = P.GW, cap = P.cap;
+  const size_t sizes[14] = {
+      B * 3 * GW * P.R * 2,                 // cq_split
+      B * GW * cap * 4,                     // e
+      B * GW * P.nruns_max * 8,             // run_m
+      B * GW * P.nruns_max * 8,             // run_s
+      B * GW * 2 * 8,                       // gstat
+      B * cap * 4,                          // atilde
+      B * kHistBins * 4,                    // hist
+      B * kCounters * 4,                    // counters
+      B * cap * 8,                          // cand
+      B * (cap / 32) * 4,                   // bitmap
+      B * P.m_max * 4,                      // idx
+      B * P.hq * kMaxSplit * 2 * 4,         // part_ml
+      B * P.hq * kMaxSplit * P.dh * 4,      // part_o
+      B * P.hq * (P.s + P.m_max) * 4,       // attn_logits
+  };
+  Layout l;
+  size_t o = 0;
+  for (int i = 0; i < 14; ++i) {
+    l.off[i] = o;
+    o = align256(o + sizes[i]);
+  }
+  l.total = o;
+  return l;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+#define S4R_REQ(ptr)                                                                     \
+  do {                                                                                   \
+    if (!(ptr)) return fail(S4R_ERR_NULL_ARG, "%s is NULL", #ptr);                       \
+    if (!aligned16(ptr)) return fail(S4R_ERR_MISALIGNED, "%s is not 16-byte aligned", #ptr); \
+  } while (0)
+#define S4R_OPT(ptr)                                                                     \
+  do {                                                                                   \
+    if ((ptr) && !aligned16(ptr)) return fail(S4R_ERR_MISALIGNED, "%s is not 16-byte aligned", #ptr); \
+  } while (0)
+
+s4r_status check_ws(const Problem& P, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(S4R_ERR_NULL_ARG, "ws is NULL");
+  if (((uintptr_t)ws & 255) != 0) return fail(S4R_ERR_MISALIGNED, "ws is not 256-byte aligned");
+  const size_t need = layout(P).total;
+  if (ws_bytes < need)
+    return fail(S4R_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, need);
+  return S4R_OK;
+}
+
+s4r_status check_L(const Problem& P, int64_t L) {
+  if (L < 1 || L > P.cap) return fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity = %lld]", (long long)L, (long long)P.cap);
+  if (P.Wq > L) return fail(S4R_ERR_BAD_SHAPE, "q_window %d > L = %lld", P.Wq, (long long)L);
+  return S4R_OK;
+}
+
+s4r_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(S4R_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+// ---- kernel timing ------------------------------------------------------------------
+struct Timing {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+} g_timing;
+
+}  // namespace
+
+Workspace carve_workspace(const Problem& P, void* base) {
+  const Layout l = layout(P);
+  char* b = (char*)base;
+  Workspace w;
+  w.cq_split = (uint16_t*)(b + l.off[0]);
+  w.e = (float*)(b + l.off[1]);
+  w.run_m = (double*)(b + l.off[2]);
+  w.run_s = (double*)(b + l.off[3]);
+  w.gstat = (double*)(b + l.off[4]);
+  w.atilde = (float*)(b + l.off[5]);
+  w.hist = (uint32_t*)(b + l.off[6]);
+  w.counters = (uint32_t*)(b + l.off[7]);
+  w.cand = (uint64_t*)(b + l.off[8]);
+  w.bitmap = (uint32_t*)(b + l.off[9]);
+  w.idx = (int32_t*)(b + l.off[10]);
+  w.part_ml = (float*)(b + l.off[11]);
+  w.part_o = (float*)(b + l.off[12]);
+  w.attn_logits = (float*)(b + l.off[13]);
+  w.total = l.total;
+  return w;
+}
+
+}  // namespace s4r
+
+using namespace s4r;
+
+extern "C" {
+
+const char* s4r_last_error(void) { return g_err.c_str(); }
+
+const char* s4r_version(void) { return "s4r-gfx950 0.1.0"; }
+
+s4r_status s4r_workspace_size(const s4r_config* cfg, size_t* bytes) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (!bytes) return fail(S4R_ERR_NULL_ARG, "bytes is NULL");
+  *bytes = layout(P).total;
+  return ok();
+}
+
+int32_t s4r_num_selected(const s4r_config* cfg, int64_t L) {
+  Problem P;
+  if (make_problem(cfg, P)) return -1;
+  if (L < 1 || L > P.cap) {
+    fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity]", (long long)L);
+    return -1;
+  }
+  ok();
+  return (int32_t)(std::min<int64_t>(P.k, std::max<int64_t>(L - P.W, 0)) + std::min<int64_t>(P.W, L));
+}
+
+s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
+                            const void* bases_k, const void* coef_k, float* scores, float* qcoef_out, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  S4R_REQ(q);
+  S4R_REQ(bases_k);
+  S4R_REQ(coef_k);
+  S4R_REQ(scores);
+  S4R_OPT(qcoef_out);
+  if (P.Wq > 1) S4R_REQ(qwin_prev);
+  else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  hipError_t e = launch_prepare(P, w, L, q, qwin_prev, bases_k, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
+                                qcoef_out, true, true, stream);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+  if (e == hipSuccess) e = launch_relevance(P, w, L, scores, stream);
+  return hip_status(e, "s4r_score_latent launch");
+}
+
+s4r_status s4r_select_topk(const s4r_config* cfg, int64_t L, const float* scores, int32_t* idx, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (L < 1 || L > P.cap) return fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity]", (long long)L);
+  S4R_REQ(scores);
+  S4R_REQ(idx);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  hipError_t e = launch_hist_only(P, w, L, scores, stream);
+  if (e == hipSuccess) e = launch_select(P, w, L, scores, L, idx, nullptr, stream);
+  return hip_status(e, "s4r_select_topk launch");
+}
+
+s4r_status s4r_reconstruct(const s4r_config* cfg, int64_t L, int32_t m, const int32_t* idx, const void* bases_k,
+                           const void* bases_v, const void* coef_k, const void* coef_v, float* k_hat, float* v_hat,
+                           hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (L < 1 || L > P.cap) return fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity]", (long long)L);
+  if (m < 0) return fail(S4R_ERR_BAD_SHAPE, "m = %d < 0", m);
+  if (m == 0) return ok();
+  S4R_REQ(idx);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(coef_k);
+  S4R_REQ(coef_v);
+  S4R_REQ(k_hat);
+  S4R_REQ(v_hat);
+  return hip_status(launch_reconstruct(P, L, m, idx, bases_k, bases_v, coef_k, coef_v, k_hat, v_hat, stream),
+                    "s4r_reconstruct launch");
+}
+
+s4r_status s4r_sparse_attn(const s4r_config* cfg, int64_t L, int32_t m, const void* q, const void* sink_k,
+                           const void* sink_v, const int32_t* idx, const float* k_sel, const float* v_sel, float* out,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (L < 1 || L > P.cap) return fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity]", (long long)L);
+  if (m < 0 || m > P.m_max) return fail(S4R_ERR_BAD_SHAPE, "m = %d outside [0, %lld]", m, (long long)P.m_max);
+  if (m + P.s < 1) return fail(S4R_ERR_BAD_SHAPE, "attention over an empty set (m + n_sink == 0)");
+  S4R_REQ(q);
+  S4R_REQ(out);
+  if (P.s > 0) {
+    S4R_REQ(sink_k);
+    S4R_REQ(sink_v);
+  }
+  if (m > 0) {
+    S4R_REQ(idx);
+    S4R_REQ(k_sel);
+    S4R_REQ(v_sel);
+  }
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  return hip_status(launch_sparse_attn(P, w, L, m, q, sink_k, sink_v, idx, k_sel, v_sel, out, stream),
+                    "s4r_sparse_attn launch");
+}
+
+s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
+                           const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
+                           const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, const void* k_new,
+                           const void* v_new, float* out, int32_t* idx_out, float* scores_out, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  if (!attention_supported(P))
+    return fail(S4R_ERR_UNSUPPORTED, "fused attention not built for G = %d, rank = %d", P.G, P.rank);
+  S4R_REQ(q);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(coef_k);
+  S4R_REQ(coef_v);
+  S4R_REQ(out);
+  S4R_OPT(idx_out);
+  S4R_OPT(scores_out);
+  if (P.s > 0) {
+    S4R_REQ(sink_k);
+    S4R_REQ(sink_v);
+  }
+  if (P.Wq > 1) S4R_REQ(qwin_prev);
+  else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
+  if ((win_k == nullptr) != (win_v == nullptr)) return fail(S4R_ERR_NULL_ARG, "win_k and win_v must both be given or both NULL");
+  if ((k_new == nullptr) != (v_new == nullptr)) return fail(S4R_ERR_NULL_ARG, "k_new and v_new must both be given or both NULL");
+  S4R_OPT(win_k);
+  S4R_OPT(win_v);
+  S4R_OPT(k_new);
+  S4R_OPT(v_new);
+  const int64_t n_hist = std::max<int64_t>(L - P.W, 0);
+  const int k_eff = (int)std::min<int64_t>(P.k, n_hist);
+  const int m = (int)(k_eff + std::min<int64_t>(P.W, L));
+  if (m + P.s < 1) return fail(S4R_ERR_BAD_SHAPE, "attention over an empty set (m + n_sink == 0)");
+  if (win_k && P.s + std::min<int64_t>(P.W, L) > kMaxExtraTok)
+    return fail(S4R_ERR_UNSUPPORTED, "n_sink + window = %lld > %d with exact window KV", (long long)(P.s + P.W), kMaxExtraTok);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+
+  hipError_t e = launch_prepare(P, w, L, q, qwin_prev, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1,
+                                nullptr, true, true, stream);
+  {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    const bool timed = g_timing.enabled && g_timing.used < (int)g_timing.start.size();
+    if (e == hipSuccess && timed) e = hipEventRecord(g_timing.start[g_timing.used], stream);
+    if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+    if (e == hipSuccess && timed) {
+      e = hipEventRecord(g_timing.stop[g_timing.used], stream);
+      g_timing.used++;
+    }
+  }
+  if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);
+  if (e == hipSuccess) e = launch_select(P, w, L, w.atilde, P.cap, w.idx, idx_out, stream);
+  if (e == hipSuccess)
+    e = launch_attention(P, w, L, m, k_eff, q, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, out,
+                         stream, nullptr, nullptr);
+  return hip_status(e, "s4r_decode_step launch");
+}
+
+s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_new, const void* v_new,
+                              const void* bases_k, const void* bases_v, void* coef_k, void* coef_v,
+                              hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (row < 0 || row >= P.cap) return fail(S4R_ERR_BAD_SHAPE, "row %lld outside [0, capacity)", (long long)row);
+  S4R_REQ(k_new);
+  S4R_REQ(v_new);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(coef_k);
+  S4R_REQ(coef_v);
+  Workspace none{};
+  return hip_status(launch_prepare(P, none, row + 1, nullptr, nullptr, bases_k, bases_v, k_new, v_new, coef_k,
+                                   coef_v, row, nullptr, false, false, stream),
+                    "s4r_project_append launch");
+}
+
+static s4r_status pack_common(const s4r_config* cfg, int64_t n_rows, const void* src, void* dst, bool to_tiled,
+                              hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (n_rows < 0 || n_rows > P.cap)
+    return fail(S4R_ERR_BAD_SHAPE, "n_rows %lld outside [0, capacity]", (long long)n_rows);
+  S4R_REQ(src);
+  S4R_REQ(dst);
+  return hip_status(launch_pack(P, n_rows, src, dst, to_tiled, stream), "s4r_pack launch");
+}
+
+s4r_status s4r_pack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_rowmajor, void* dst_tiled,
+                         hipStream_t stream) {
+  return pack_common(cfg, n_rows, src_rowmajor, dst_tiled, true, stream);
+}
+
+s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_tiled, void* dst_rowmajor,
+                           hipStream_t stream) {
+  return pack_common(cfg, n_rows, src_tiled, dst_rowmajor, false, stream);
+}
+
+s4r_status s4r_timing_enable(int32_t max_launches) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (max_launches < 1 || max_launches > 100000) return fail(S4R_ERR_BAD_SHAPE, "max_launches %d outside [1, 100000]", max_launches);
+  for (auto ev : g_timing.start) (void)hipEventDestroy(ev);
+  for (auto ev : g_timing.stop) (void)hipEventDestroy(ev);
+  g_timing.start.assign(max_launches, nullptr);
+  g_timing.stop.assign(max_launches, nullptr);
+  for (int i = 0; i < max_launches; ++i) {
+    if (hipEventCreate(&g_timing.start[i]) != hipSuccess || hipEventCreate(&g_timing.stop[i]) != hipSuccess)
+      return fail(S4R_ERR_HIP, "hipEventCreate failed");
+  }
+  g_timing.used = 0;
+  g_timing.enabled = true;
+  return ok();
+}
+
+s4r_status s4r_timing_read(double* total_ms, int64_t* launches) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (!total_ms || !launches) return fail(S4R_ERR_NULL_ARG, "total_ms / launches is NULL");
+  double sum = 0.0;
+  for (int i = 0; i < g_timing.used; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(g_timing.stop[i]) != hipSuccess ||
+        hipEventElapsedTime(&ms, g_timing.start[i], g_timing.stop[i]) != hipSuccess)
+      return fail(S4R_ERR_HIP, "reading kernel timing events failed");
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = g_timing.used;
+  for (auto ev : g_timing.start) (void)hipEventDestroy(ev);
+  for (auto ev : g_timing.stop) (void)hipEventDestroy(ev);
+  g_timing.start.clear();
+  g_timing.stop.clear();
+  g_timing.used = 0;
+  g_timing.enabled = false;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,126 @@
+// Device-side helpers shared by the gfx950 kernels of the S^4R library:
+// storage-format conversions, the tiled coefficient layout, bf16 MFMA
+// wrappers and wave-level shuffles.  CDNA4 only (wave64, MFMA 16x16x32 bf16).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace s4r {
+
+constexpr int kWave = 64;
+constexpr int kTileTok = 16;   // tokens per coefficient tile
+constexpr int kBlkCol = 32;    // latent columns per coefficient block
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// storage formats
+// ---------------------------------------------------------------------------
+struct BF16 {  // bf16 stored as its 16-bit pattern
+  using storage = uint16_t;
+};
+struct F32 {
+  using storage = float;
+};
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs)
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float load_elem(const uint16_t* p, int64_t i) {
+  return bf16_bits_to_f32(p[i]);
+}
+__device__ __forceinline__ float load_elem(const float* p, int64_t i) { return p[i]; }
+
+__device__ __forceinline__ void store_elem(uint16_t* p, int64_t i, double v) {
+  p[i] = (uint16_t)f32_to_bf16_bits((float)v);
+}
+__device__ __forceinline__ void store_elem(float* p, int64_t i, double v) { p[i] = (float)v; }
+
+// ---------------------------------------------------------------------------
+// tiled coefficient layout: element (t, c) of one sequence's [cap, R] block
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int64_t tiled_offset(int64_t t, int c, int R) {
+  return (t >> 4) * (int64_t)(kTileTok * R) + (int64_t)(c >> 5) * (kTileTok * kBlkCol) +
+         (int64_t)(t & 15) * kBlkCol + (c & 31);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 splits: x ~= hi + mid + lo, each a bf16 value (~24 significant bits)
+// ---------------------------------------------------------------------------
+struct Split3 {
+  uint16_t hi, mid, lo;
+};
+
+__device__ __forceinline__ Split3 split3(double x) {
+  Split3 s;
+  uint32_t h = f32_to_bf16_bits((float)x);
+  double r1 = x - (double)bf16_bits_to_f32(h);
+  uint32_t m = f32_to_bf16_bits((float)r1);
+  double r2 = r1 - (double)bf16_bits_to_f32(m);
+  uint32_t l = f32_to_bf16_bits((float)r2);
+  s.hi = (uint16_t)h;
+  s.mid = (uint16_t)m;
+  s.lo = (uint16_t)l;
+  return s;
+}
+
+// ---------------------------------------------------------------------------
+// MFMA operand packing.  An operand is 8 bf16 values held in 4 VGPRs.
+// ---------------------------------------------------------------------------
+union Op8 {
+  uint4 u;
+  bf16x8 v;
+  uint16_t h[8];
+};
+
+// 8 fp32 values -> three bf16 operands (hi, mid, lo)
+__device__ __forceinline__ void split_f32x8(const float* x, Op8& hi, Op8& mid, Op8& lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    uint32_t h = f32_to_bf16_bits(x[i]);
+    float r1 = x[i] - bf16_bits_to_f32(h);   // exact in fp32
+    uint32_t m = f32_to_bf16_bits(r1);
+    float r2 = r1 - bf16_bits_to_f32(m);     // exact in fp32
+    hi.h[i] = (uint16_t)h;
+    mid.h[i] = (uint16_t)m;
+    lo.h[i] = (uint16_t)f32_to_bf16_bits(r2);
+  }
+}
+
+// D = A * B + C for 16x16x32 bf16 (gfx950).  Lane l supplies row l%16 of A
+// and column l%16 of B for the k-group l/16 (8 values each); it receives
+// D[4*(l/16) + v][l%16], v = 0..3.  The k order inside a group is the same for
+// A and B, so any consistent assignment of contraction indices works.
+__device__ __forceinline__ floatx4 mfma16x16x32(const Op8& a, const Op8& b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// wave shuffles (ds_bpermute based, full 64-lane)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float shfl_xor_f(float v, int mask) {
+  int lane = __lane_id();
+  return __int_as_float(__builtin_amdgcn_ds_bpermute((lane ^ mask) << 2, __float_as_int(v)));
+}
+__device__ __forceinline__ double shfl_xor_d(double v, int mask) {
+  int lane = __lane_id();
+  int lo = __double2loint(v), hi = __double2hiint(v);
+  lo = __builtin_amdgcn_ds_bpermute((lane ^ mask) << 2, lo);
+  hi = __builtin_amdgcn_ds_bpermute((lane ^ mask) << 2, hi);
+  return __hiloint2double(hi, lo);
+}
+
+// order-preserving key of a non-negative fp32 score (sign bit is clear)
+__device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s); }
+
+}  // namespace s4r

@@ -1,0 +1,86 @@
+"""Helpers shared by the GPU parity tests: move oracle-side stored state onto
+the GPU in the library's layouts, and the comparison rules.
+
+Stored state is built on the host (workloads + the oracle's prefill, or the
+workloads' latent recipe), already rounded to the storage format, so the GPU
+and the oracle read exactly the same values."""
+
+import numpy as np
+import torch
+
+import paper_2608_00528_amd as s4r
+import workloads as W
+
+
+def cfg_from_workload(wl, capacity=None, **over):
+    kw = dict(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+              rank=wl.rank, basis_groups=wl.basis_groups, n_sink=wl.n_sink, window=wl.window,
+              q_window=wl.q_window, topk=wl.topk, pool_kernel=wl.pool_kernel, pool_mode=wl.pool_mode,
+              group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype,
+              capacity=capacity if capacity is not None else ((wl.L + 15) // 16) * 16)
+    kw.update(over)
+    return s4r.make_config(**kw)
+
+
+def oracle_cfg(c, pool_mode="max", group_agg="mean"):
+    return dict(n_kv_heads=c.n_kv_heads, window=c.window, topk=c.topk, pool_kernel=c.pool_kernel,
+                pool_mode=pool_mode, group_agg=group_agg, rope_theta=float(np.float32(c.rope_theta)),
+                dtype="bf16" if c.dtype == 1 else "fp32")
+
+
+def dev(x, dtype, device="cuda"):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype)
+
+
+def to_gpu_state(c, st, device="cuda"):
+    """Stored state (float64 numpy, rounded) -> GPU tensors; coefficient caches
+    are uploaded row-major and packed into the tiled layout by the library."""
+    dt = s4r.storage_dtype(c)
+    g = {}
+    for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v"):
+        if k in st and st[k] is not None:
+            g[k] = dev(st[k], dt, device)
+    for k in ("coef_k", "coef_v"):
+        rm = st[k]
+        n = rm.shape[1]
+        full = np.zeros((rm.shape[0], c.capacity, rm.shape[2]))
+        full[:, :n] = rm
+        g[k] = s4r.pack_coef(c, c.capacity, dev(full, dt, device))
+    return g
+
+
+def rel_err_rows(gpu, ref):
+    """max over rows of ||gpu - ref||_inf / ||ref||_inf (rows = last axis)."""
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    num = np.abs(gpu - ref).max(axis=-1)
+    den = np.maximum(np.abs(ref).max(axis=-1), 1e-30)
+    return float((num / den).max())
+
+
+def check_selection(idx_gpu, idx_ref, a_ref, L, W, k, rel_tol=1e-6):
+    """Index sets must be equal except for elements whose oracle score lies
+    within rel_tol of the k-th largest score (near-ties); the window part must
+    match exactly and each row must be strictly ascending per part.
+    Returns the number of tolerated differences."""
+    n_hist = max(L - W, 0)
+    k_eff = min(k, n_hist)
+    flips = 0
+    for b in range(idx_ref.shape[0]):
+        gi, ri = idx_gpu[b], idx_ref[b]
+        assert np.array_equal(gi[k_eff:], ri[k_eff:]), "window part differs"
+        g, r = gi[:k_eff], ri[:k_eff]
+        assert np.all(np.diff(g) > 0), "global part not strictly ascending"
+        assert np.all((g >= 0) & (g < n_hist))
+        diff = np.setxor1d(g, r)
+        if diff.size:
+            srt = np.sort(a_ref[b, :n_hist])[::-1]
+            kth = srt[k_eff - 1]
+            gap = np.abs(a_ref[b, diff] - kth) / max(abs(kth), 1e-300)
+            assert np.all(gap <= rel_tol), f"selection differs beyond ties: gaps {gap.max():.3e}"
+            flips += diff.size // 2
+    return flips
+
+
+def latent_state_np(wl, seed=0, capacity=None, L=None):
+    return W.latent_state(wl, seed=seed, capacity=capacity, L=L)

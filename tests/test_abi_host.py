@@ -1,0 +1,154 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/s4r.h declares, computes sizes, and rejects invalid
+arguments with the documented status codes before launching anything.
+
+Every call with a non-NULL fake pointer here is built to fail validation, so
+nothing is ever launched with it."""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2608_00528_amd as s4r
+from paper_2608_00528_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "s4r.h")
+# fake pointers are only ever passed where validation must reject the call;
+# skip on GPU machines anyway so no fake pointer can reach a kernel there
+pytestmark = pytest.mark.skipif(torch.cuda.is_available(), reason="host-only checks")
+
+FAKE = ctypes.c_void_p(0x10000)        # aligned, never dereferenced
+FAKE_MIS = ctypes.c_void_p(0x10004)    # misaligned
+
+
+def header_functions():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:s4r_status|int32_t|const char\*)\s+(s4r_\w+)\s*\(", txt, re.M)))
+
+
+def cfg(**kw):
+    base = dict(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=64, rank=32, capacity=1024, window=16, topk=32,
+                rope_theta=10000.0, dtype="bf16")
+    base.update(kw)
+    return s4r.make_config(**base)
+
+
+def test_exports_match_header():
+    lib = L.load()
+    funcs = header_functions()
+    assert len(funcs) == len(L.EXPORTS)
+    assert sorted(L.EXPORTS) == funcs
+    for f in funcs:
+        assert hasattr(lib, f)
+
+
+def test_config_struct_layout():
+    assert ctypes.sizeof(L.Config) == 72
+    assert L.Config.capacity.offset == 56 and L.Config.dtype.offset == 68
+
+
+def test_version_and_sizes():
+    assert s4r.version().startswith("s4r-gfx950")
+    c = cfg()
+    ws = s4r.workspace_size(c)
+    assert ws > 0 and ws % 256 == 0
+    assert s4r.num_selected(c, 1000) == 32 + 16
+    assert s4r.num_selected(c, 20) == 4 + 16
+    assert s4r.num_selected(c, 10) == 0 + 10
+    # workspace grows with capacity
+    assert s4r.workspace_size(cfg(capacity=4096)) > ws
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("batch", 0, L.S4R_ERR_BAD_SHAPE),
+    ("n_q_heads", 7, L.S4R_ERR_BAD_SHAPE),
+    ("head_dim", 96, L.S4R_ERR_UNSUPPORTED),
+    ("basis_groups", 3, L.S4R_ERR_BAD_SHAPE),
+    ("rank", 48, L.S4R_ERR_UNSUPPORTED),
+    ("rank", 4096, L.S4R_ERR_BAD_SHAPE),
+    ("pool_kernel", 4, L.S4R_ERR_BAD_SHAPE),
+    ("pool_kernel", 0, L.S4R_ERR_BAD_SHAPE),
+    ("q_window", 0, L.S4R_ERR_BAD_SHAPE),
+    ("q_window", 5, L.S4R_ERR_UNSUPPORTED),      # G * W_q = 20 > 16
+    ("capacity", 1000, L.S4R_ERR_BAD_SHAPE),
+    ("dtype", 7, L.S4R_ERR_BAD_SHAPE),
+    ("topk", -1, L.S4R_ERR_BAD_SHAPE),
+    ("window", -1, L.S4R_ERR_BAD_SHAPE),
+    ("n_sink", -1, L.S4R_ERR_BAD_SHAPE),
+    ("pool_mode", 5, L.S4R_ERR_BAD_SHAPE),
+])
+def test_config_validation(field, value, status):
+    c = cfg()
+    setattr(c, field, value)
+    n = ctypes.c_size_t()
+    st = L.load().s4r_workspace_size(ctypes.byref(c), ctypes.byref(n))
+    assert st == status
+    assert L.load().s4r_last_error().decode()
+
+
+def test_null_config():
+    n = ctypes.c_size_t()
+    assert L.load().s4r_workspace_size(None, ctypes.byref(n)) == L.S4R_ERR_NULL_ARG
+
+
+def _score(c, Lval, q=FAKE, qwin=None, bk=FAKE, ck=FAKE, sc=FAKE, qo=None, ws=FAKE, wsb=1 << 40):
+    return L.load().s4r_score_latent(ctypes.byref(c), Lval, q, qwin, bk, ck, sc, qo, ws, wsb, None)
+
+
+def test_score_latent_argument_errors():
+    c = cfg()
+    assert _score(c, 0) == L.S4R_ERR_BAD_SHAPE                  # L < 1
+    assert _score(c, 2048) == L.S4R_ERR_BAD_SHAPE               # L > capacity
+    assert _score(c, 100, q=None) == L.S4R_ERR_NULL_ARG
+    assert _score(c, 100, ck=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert _score(c, 100, ws=None) == L.S4R_ERR_NULL_ARG
+    assert _score(c, 100, wsb=16) == L.S4R_ERR_WORKSPACE
+    assert _score(c, 100, ws=ctypes.c_void_p(0x10010)) == L.S4R_ERR_MISALIGNED   # ws needs 256 B
+    assert _score(c, 100, qwin=FAKE) == L.S4R_ERR_BAD_SHAPE     # qwin_prev with W_q == 1
+    c2 = cfg(q_window=2)
+    assert _score(c2, 100) == L.S4R_ERR_NULL_ARG                 # qwin_prev missing
+    assert _score(c2, 1, qwin=FAKE) == L.S4R_ERR_BAD_SHAPE       # W_q > L
+
+
+def test_decode_step_argument_errors():
+    c = cfg()
+    lib = L.load()
+
+    def call(Lval=100, k_new=None, v_new=None, win_k=None, win_v=None, sink=FAKE, out=FAKE, wsb=1 << 40, c=c):
+        return lib.s4r_decode_step(ctypes.byref(c), Lval, FAKE, None, sink, sink, win_k, win_v, FAKE, FAKE, FAKE,
+                                   FAKE, k_new, v_new, out, None, None, FAKE, wsb, None)
+    assert call(k_new=FAKE) == L.S4R_ERR_NULL_ARG               # k_new without v_new
+    assert call(win_v=FAKE) == L.S4R_ERR_NULL_ARG               # win_v without win_k
+    assert call(sink=None) == L.S4R_ERR_NULL_ARG                # sinks required when s > 0
+    assert call(out=None) == L.S4R_ERR_NULL_ARG
+    assert call(wsb=0) == L.S4R_ERR_WORKSPACE
+    assert call(Lval=0) == L.S4R_ERR_BAD_SHAPE
+    c3 = cfg(n_q_heads=6, n_kv_heads=2)                          # G = 3: no fused kernel built
+    assert call(c=c3) == L.S4R_ERR_UNSUPPORTED
+    c0 = cfg(n_sink=0, window=0, topk=0)                         # nothing to attend to
+    assert call(c=c0, sink=None) == L.S4R_ERR_BAD_SHAPE
+
+
+def test_other_entry_point_errors():
+    c = cfg()
+    lib = L.load()
+    assert lib.s4r_select_topk(ctypes.byref(c), 100, None, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_select_topk(ctypes.byref(c), 5000, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_reconstruct(ctypes.byref(c), 100, -1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_reconstruct(ctypes.byref(c), 100, 0, None, None, None, None, None, None, None, None) == L.S4R_OK
+    assert lib.s4r_reconstruct(ctypes.byref(c), 100, 8, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == L.S4R_ERR_NULL_ARG
+    big = s4r.num_selected(c, 1024) + 1
+    assert lib.s4r_sparse_attn(ctypes.byref(c), 100, big, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40,
+                               None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_project_append(ctypes.byref(c), 1024, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_project_append(ctypes.byref(c), 3, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_pack_coef(ctypes.byref(c), 2048, FAKE, FAKE, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_unpack_coef(ctypes.byref(c), 10, FAKE_MIS, FAKE, None) == L.S4R_ERR_MISALIGNED
+    assert lib.s4r_timing_enable(0) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_timing_read(None, None) == L.S4R_ERR_NULL_ARG
+    assert s4r.num_selected.__module__   # binding importable
+    assert lib.s4r_num_selected(ctypes.byref(c), 0) == -1
