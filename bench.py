@@ -1,0 +1,241 @@
+"""Benchmark of the fused S^4R decode step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload llama8b_128k] [--gpus 1]
+
+A step is one call of s4r_decode_step: one layer, all heads, the whole batch
+(latent scoring of every cached token, top-k selection, sparse
+reconstruction with RoPE, attention).  The default workload is the
+Llama-3.1-8B-shaped layer at 128k context (B=4, 32/8 heads, d_h=128, rank 160,
+4 sinks, window 128, top-k 2048, bf16 storage), seeded synthetic data drawn in
+latent coordinates (workloads.latent_state), inputs resident in HBM.
+
+Timing: W untimed steps, then K timed steps between two device
+synchronisations, measured with HIP events on the launch stream.  Steps
+rotate over 4 independent copies of the coefficient caches so that no step
+finds its 168 MB key cache in the 256 MB Infinity Cache.  A second pass with
+the library's per-kernel event hook gives the average duration of the
+dominant kernel (the latent-score stream over C^K) for the roofline entry.
+The CPU oracle is timed on a bounded sample (one sequence of the same
+workload, repeated for ~10 s, one thread) for the cpu_baseline entry.
+
+Prints ONE JSON line on stdout.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+N_REPLICAS = 4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic(wl, m):
+    """Bytes the method must move per step and MFMA flops of the reconstruction."""
+    B, L, R, Dp, es = wl.batch, wl.L, wl.R, wl.Dp, (2 if wl.dtype == "bf16" else 4)
+    ck = B * L * R * es                       # C^K streamed once (latent scoring)
+    gather = 2 * B * m * R * es               # selected rows of C^K and C^V
+    bases = 2 * B * Dp * R * es               # B^K and B^V
+    sinks = 2 * B * wl.n_sink * Dp * es
+    q = B * wl.n_q_heads * wl.head_dim * es
+    out = B * wl.n_q_heads * wl.head_dim * 4
+    rec_flops = 2 * 2 * B * m * R * Dp        # K^ and V^ of every selected token
+    return {"step_bytes": ck + gather + bases + sinks + q + out, "stream_bytes": ck, "rec_flops": rec_flops}
+
+
+def traffic_from_profile(kernel_src):
+    """HBM bytes per launch of the stream kernel from the committed rocprofv3
+    counter summary, or None when it is absent or the kernel source changed."""
+    path = os.path.join(ROOT, "profiles", "score_stream_llama8b_128k_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()[:16]
+    if kv.get("kernel_source_sha256_16") != sha:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, st, budget_s=10.0):
+    from threadpoolctl import threadpool_limits
+
+    from oracle import decode
+    cfg = dict(n_kv_heads=wl.n_kv_heads, window=wl.window, topk=wl.topk, pool_kernel=wl.pool_kernel,
+               pool_mode=wl.pool_mode, group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype)
+    one = {k: st[k][:1] for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v", "coef_k", "coef_v")}
+    times = []
+    with threadpool_limits(limits=1):
+        t_end = time.perf_counter() + budget_s
+        while True:
+            t0 = time.perf_counter()
+            decode.decode_step(cfg, wl.L, one["q"], one["sink_k"], one["sink_v"], one["bases_k"], one["bases_v"],
+                               one["coef_k"], one["coef_v"])
+            times.append(time.perf_counter() - t0)
+            if time.perf_counter() > t_end:
+                break
+    per_seq = float(np.median(times))
+    return {"value": per_seq * wl.batch * 1e6, "unit": "us/step", "cores": 1, "kind": "oracle",
+            "sample": (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
+                       f"{len(times)} runs in {sum(times):.1f} s, median x {wl.batch} sequences")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="llama8b_128k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the single-GPU decode step only: this build runs on one GPU "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2608_00528_amd as s4r
+    import workloads as W
+
+    torch.cuda.set_device(0)
+    wl = W.CONFIGS[args.workload]
+    if wl.layers != 1:
+        raise SystemExit(f"{wl.name} is a multi-layer workload; bench.py times single-layer steps")
+    log(f"[bench] generating {wl.describe()}")
+    t0 = time.perf_counter()
+    st = W.latent_state(wl, seed=args.seed)
+    log(f"[bench] generated in {time.perf_counter() - t0:.1f} s")
+
+    cap = ((wl.L + 15) // 16) * 16
+    c = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                        rank=wl.rank, basis_groups=wl.basis_groups, n_sink=wl.n_sink, window=wl.window,
+                        q_window=wl.q_window, topk=wl.topk, pool_kernel=wl.pool_kernel, pool_mode=wl.pool_mode,
+                        group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=cap)
+    dt = s4r.storage_dtype(c)
+
+    def up(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(device="cuda", dtype=dt)
+
+    q, sk, sv, bk, bv = (up(st[k]) for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v"))
+    reps = []
+    for key in ("coef_k", "coef_v"):
+        rm = np.zeros((wl.batch, cap, wl.R))
+        rm[:, :wl.L] = st[key]
+        reps.append(s4r.pack_coef(c, cap, up(rm)))
+    replicas = [(reps[0], reps[1])] + [(reps[0].clone(), reps[1].clone()) for _ in range(N_REPLICAS - 1)]
+    ws = s4r.alloc_workspace(c)
+    out = torch.empty((wl.batch, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+    m = s4r.num_selected(c, wl.L)
+    torch.cuda.synchronize()
+
+    def step(i):
+        ck, cv = replicas[i % N_REPLICAS]
+        s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, ck, cv, ws, out=out)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step * 1e3:.2f} us/step (events), wall {wall / args.steps * 1e6:.2f} us/step")
+
+    # per-kernel pass (events between kernels), same steps again
+    nk = min(args.steps, 200)
+    s4r.timing_enable(nk)
+    for i in range(nk):
+        step(i)
+    torch.cuda.synchronize()
+    kms, nsteps = s4r.timing_read()
+    kus = {k: v / nsteps * 1e3 for k, v in kms.items()}
+    log("[bench] per-kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in kus.items()))
+
+    alg = algorithmic(wl, m)
+    stream_us = kus["score_stream"]
+    achieved = alg["stream_bytes"] / (stream_us * 1e-6) / 1e9
+    traffic = traffic_from_profile(os.path.join(ROOT, "paper_2608_00528_amd", "csrc", "score.hip"))
+    step_gbps = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
+    rec_tflops = alg["rec_flops"] / (kus["attn_split"] * 1e-6) / 1e12
+
+    result = {
+        "metric": "us per decode step (all heads, 1 layer) at 128k ctx; achieved HBM GB/s vs peak",
+        "value": round(ms_step * 1e3, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: Llama-3.1-8B-shaped layer, B={wl.batch}, N={wl.N} (L={wl.L} non-sink), "
+                         f"h_q/h_kv={wl.n_q_heads}/{wl.n_kv_heads}, d_h={wl.head_dim}, rank {wl.R}, "
+                         f"s={wl.n_sink}, W={wl.window}, k={wl.topk}, m={m}, {wl.dtype} storage"),
+            "batch": wl.batch, "context": wl.N, "rank": wl.R, "window": wl.window, "topk": wl.topk,
+            "selected": m, "replicas": N_REPLICAS,
+        },
+        "achieved_step_GBps": round(step_gbps, 1),
+        "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": alg["step_bytes"],
+        "kernels_us": {k: round(v, 3) for k, v in kus.items()},
+        "roofline": {
+            "kernel": "k_score_stream (latent scoring over C^K)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg["stream_bytes"],
+            "avg_launch_us": round(stream_us, 3),
+        },
+        "reconstruction_mfma": {
+            "kernel": "k_attn_split (reconstruction + attention)",
+            "achieved_TFLOPs": round(rec_tflops, 2),
+            "peak_TFLOPs": BF16_PEAK_TFLOPS,
+            "frac": round(rec_tflops / BF16_PEAK_TFLOPS, 5),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(wl, st)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -190,13 +190,18 @@ s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* sr
 
 /*
  * Kernel timing for measurement.  While enabled, s4r_decode_step records a
- * hipEvent pair around its latent-scoring stream kernel on the caller's stream
- * (up to `max_launches` launches).  s4r_timing_read waits for the recorded
- * events, returns the summed kernel time and the launch count, and disables
- * timing.  Host-side event creation happens in s4r_timing_enable only.
+ * hipEvent pair around each of its kernels on the caller's stream, for up to
+ * `max_steps` calls.  Kernels, in launch order (S4R_TIMED_KERNELS of them):
+ *   0 cache update + query projection   1 latent-score stream over C^K
+ *   2 relevance + histogram             3 top-k selection
+ *   4 reconstruction + split attention  5 split combine
+ * s4r_timing_read waits for the recorded events, writes the summed time of
+ * each kernel (ms, array of S4R_TIMED_KERNELS) and the number of timed
+ * steps, and disables timing.  Events are created in s4r_timing_enable only.
  */
-s4r_status s4r_timing_enable(int32_t max_launches);
-s4r_status s4r_timing_read(double* total_ms, int64_t* launches);
+#define S4R_TIMED_KERNELS 6
+s4r_status s4r_timing_enable(int32_t max_steps);
+s4r_status s4r_timing_read(double* total_ms, int64_t* steps);
 
 #ifdef __cplusplus
 }

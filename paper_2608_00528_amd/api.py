@@ -179,12 +179,16 @@ def unpack_coef(cfg, n_rows, src, dst=None):
     return dst
 
 
-def timing_enable(max_launches):
-    L.check(L.load().s4r_timing_enable(max_launches))
+TIMED_KERNELS = ("prepare", "score_stream", "relevance", "select", "attn_split", "attn_combine")
+
+
+def timing_enable(max_steps):
+    L.check(L.load().s4r_timing_enable(max_steps))
 
 
 def timing_read():
-    ms = ctypes.c_double()
+    """-> ({kernel name: summed ms}, timed steps)"""
+    ms = (ctypes.c_double * len(TIMED_KERNELS))()
     n = ctypes.c_int64()
-    L.check(L.load().s4r_timing_read(ctypes.byref(ms), ctypes.byref(n)))
-    return ms.value, n.value
+    L.check(L.load().s4r_timing_read(ms, ctypes.byref(n)))
+    return dict(zip(TIMED_KERNELS, list(ms))), n.value

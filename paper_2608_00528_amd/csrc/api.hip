@@ -67,8 +67,9 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
     return fail(S4R_ERR_UNSUPPORTED, "G * q_window = %d > %d not supported", G * c->q_window, kMaxGW);
   if (c->capacity < 16 || c->capacity % 16)
     return fail(S4R_ERR_BAD_SHAPE, "capacity %lld must be a positive multiple of 16", (long long)c->capacity);
-  if (c->capacity > ((int64_t)1 << 30))
-    return fail(S4R_ERR_UNSUPPORTED, "capacity %lld > 2^30", (long long)c->capacity);
+  if (c->capacity > (int64_t)kMaxSelGroups * kSelChunk)
+    return fail(S4R_ERR_UNSUPPORTED, "capacity %lld > %lld", (long long)c->capacity,
+                (long long)kMaxSelGroups * kSelChunk);
   if (!(c->rope_theta >= 0.f) || !std::isfinite(c->rope_theta))
     return fail(S4R_ERR_BAD_SHAPE, "rope_theta must be finite and >= 0");
   if (c->dtype != S4R_FP32 && c->dtype != S4R_BF16) return fail(S4R_ERR_BAD_SHAPE, "dtype %d invalid", c->dtype);
@@ -97,6 +98,7 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   P.theta = c->rope_theta;
   P.GW = G * c->q_window;
   P.nruns_max = (c->capacity + kRunTok - 1) / kRunTok;
+  P.nwg_max = (P.nruns_max + kScoreWaves - 1) / kScoreWaves;   // runs_per_wave >= 1
   P.m_max = std::min<int64_t>(c->topk, std::max<int64_t>(c->capacity - c->window, 0)) +
             std::min<int64_t>(c->window, c->capacity);
   return S4R_OK;
@@ -106,32 +108,37 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
+constexpr int kRegions = 18;
 struct Layout {
-  size_t off[14];
+  size_t off[kRegions];
   size_t total;
 };
 
 Layout layout(const Problem& P) {
   const size_t B = P.B, GW = P.GW, cap = P.cap;
-  const size_t sizes[14] = {
+  const size_t sizes[kRegions] = {
       B * 3 * GW * P.R * 2,                 // cq_split
       B * GW * cap * 4,                     // e
       B * GW * P.nruns_max * 8,             // run_m
       B * GW * P.nruns_max * 8,             // run_s
-      B * GW * 2 * 8,                       // gstat
+      B * GW * P.nwg_max * 2 * 8,           // wg_stats
       B * cap * 4,                          // atilde
       B * kHistBins * 4,                    // hist
       B * kCounters * 4,                    // counters
-      B * cap * 8,                          // cand
+      B * cand_stride(P) * 8,               // cand
       B * (cap / 32) * 4,                   // bitmap
       B * P.m_max * 4,                      // idx
       B * P.hq * kMaxSplit * 2 * 4,         // part_ml
       B * P.hq * kMaxSplit * P.dh * 4,      // part_o
       B * P.hq * (P.s + P.m_max) * 4,       // attn_logits
+      B * cand_stride(P) * 8,               // cand2
+      B * sel_groups_max(P) * 4,            // cand_count
+      B * rel_groups_max(P) * kHistBins * 4,  // hist_wg
+      B * 2 * (size_t)P.nb * ((P.Dg + 63) / 64) * (kMaxGW + 1) * P.R * 8,   // proj_partial
   };
   Layout l;
   size_t o = 0;
-  for (int i = 0; i < 14; ++i) {
+  for (int i = 0; i < kRegions; ++i) {
     l.off[i] = o;
     o = align256(o + sizes[i]);
   }
@@ -175,7 +182,8 @@ s4r_status hip_status(hipError_t e, const char* what) {
 struct Timing {
   std::mutex mu;
   bool enabled = false;
-  std::vector<hipEvent_t> start, stop;
+  std::vector<hipEvent_t> start, stop;   // [steps][S4R_TIMED_KERNELS]
+  int steps = 0;
   int used = 0;
 } g_timing;
 
@@ -189,7 +197,7 @@ Workspace carve_workspace(const Problem& P, void* base) {
   w.e = (float*)(b + l.off[1]);
   w.run_m = (double*)(b + l.off[2]);
   w.run_s = (double*)(b + l.off[3]);
-  w.gstat = (double*)(b + l.off[4]);
+  w.wg_stats = (double*)(b + l.off[4]);
   w.atilde = (float*)(b + l.off[5]);
   w.hist = (uint32_t*)(b + l.off[6]);
   w.counters = (uint32_t*)(b + l.off[7]);
@@ -199,6 +207,10 @@ Workspace carve_workspace(const Problem& P, void* base) {
   w.part_ml = (float*)(b + l.off[11]);
   w.part_o = (float*)(b + l.off[12]);
   w.attn_logits = (float*)(b + l.off[13]);
+  w.cand2 = (uint64_t*)(b + l.off[14]);
+  w.cand_count = (uint32_t*)(b + l.off[15]);
+  w.hist_wg = (uint32_t*)(b + l.off[16]);
+  w.proj_partial = (double*)(b + l.off[17]);
   w.total = l.total;
   return w;
 }
@@ -249,8 +261,8 @@ s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q, con
   else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
-  hipError_t e = launch_prepare(P, w, L, q, qwin_prev, bases_k, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
-                                qcoef_out, true, true, stream);
+  hipError_t e = launch_project(P, w, q, qwin_prev, bases_k, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
+                                qcoef_out, stream);
   if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores, stream);
   return hip_status(e, "s4r_score_latent launch");
@@ -352,28 +364,38 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
   const int k_eff = (int)std::min<int64_t>(P.k, n_hist);
   const int m = (int)(k_eff + std::min<int64_t>(P.W, L));
   if (m + P.s < 1) return fail(S4R_ERR_BAD_SHAPE, "attention over an empty set (m + n_sink == 0)");
+  if ((int64_t)m > (int64_t)kMaxSplit * kMaxTilesPerSplit * 16)
+    return fail(S4R_ERR_UNSUPPORTED, "m = %d selected tokens exceeds %d", m, kMaxSplit * kMaxTilesPerSplit * 16);
   if (win_k && P.s + std::min<int64_t>(P.W, L) > kMaxExtraTok)
     return fail(S4R_ERR_UNSUPPORTED, "n_sink + window = %lld > %d with exact window KV", (long long)(P.s + P.W), kMaxExtraTok);
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
 
-  hipError_t e = launch_prepare(P, w, L, q, qwin_prev, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1,
-                                nullptr, true, true, stream);
-  {
-    std::lock_guard<std::mutex> lk(g_timing.mu);
-    const bool timed = g_timing.enabled && g_timing.used < (int)g_timing.start.size();
-    if (e == hipSuccess && timed) e = hipEventRecord(g_timing.start[g_timing.used], stream);
-    if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
-    if (e == hipSuccess && timed) {
-      e = hipEventRecord(g_timing.stop[g_timing.used], stream);
-      g_timing.used++;
-    }
-  }
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  const bool timed = g_timing.enabled && g_timing.used < g_timing.steps;
+  const int slot = timed ? g_timing.used * S4R_TIMED_KERNELS : 0;
+  auto mark = [&](hipError_t e, int kernel, bool start) -> hipError_t {
+    if (e != hipSuccess || !timed) return e;
+    return hipEventRecord(start ? g_timing.start[slot + kernel] : g_timing.stop[slot + kernel], stream);
+  };
+  hipError_t e = mark(hipSuccess, 0, true);
+  if (e == hipSuccess)
+    e = launch_project(P, w, q, qwin_prev, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, nullptr, stream);
+  e = mark(e, 0, false);
+  e = mark(e, 1, true);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+  e = mark(e, 1, false);
+  e = mark(e, 2, true);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);
+  e = mark(e, 2, false);
+  e = mark(e, 3, true);
   if (e == hipSuccess) e = launch_select(P, w, L, w.atilde, P.cap, w.idx, idx_out, stream);
+  e = mark(e, 3, false);
   if (e == hipSuccess)
     e = launch_attention(P, w, L, m, k_eff, q, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, out,
-                         stream, nullptr, nullptr);
+                         stream, timed ? &g_timing.start[slot + 4] : nullptr,
+                         timed ? &g_timing.stop[slot + 4] : nullptr);
+  if (timed) g_timing.used++;
   return hip_status(e, "s4r_decode_step launch");
 }
 
@@ -418,39 +440,44 @@ s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* sr
   return pack_common(cfg, n_rows, src_tiled, dst_rowmajor, false, stream);
 }
 
-s4r_status s4r_timing_enable(int32_t max_launches) {
+s4r_status s4r_timing_enable(int32_t max_steps) {
   std::lock_guard<std::mutex> lk(g_timing.mu);
-  if (max_launches < 1 || max_launches > 100000) return fail(S4R_ERR_BAD_SHAPE, "max_launches %d outside [1, 100000]", max_launches);
+  if (max_steps < 1 || max_steps > 10000) return fail(S4R_ERR_BAD_SHAPE, "max_steps %d outside [1, 10000]", max_steps);
   for (auto ev : g_timing.start) (void)hipEventDestroy(ev);
   for (auto ev : g_timing.stop) (void)hipEventDestroy(ev);
-  g_timing.start.assign(max_launches, nullptr);
-  g_timing.stop.assign(max_launches, nullptr);
-  for (int i = 0; i < max_launches; ++i) {
+  const int n = max_steps * S4R_TIMED_KERNELS;
+  g_timing.start.assign(n, nullptr);
+  g_timing.stop.assign(n, nullptr);
+  for (int i = 0; i < n; ++i) {
     if (hipEventCreate(&g_timing.start[i]) != hipSuccess || hipEventCreate(&g_timing.stop[i]) != hipSuccess)
       return fail(S4R_ERR_HIP, "hipEventCreate failed");
   }
+  g_timing.steps = max_steps;
   g_timing.used = 0;
   g_timing.enabled = true;
   return ok();
 }
 
-s4r_status s4r_timing_read(double* total_ms, int64_t* launches) {
+s4r_status s4r_timing_read(double* total_ms, int64_t* steps) {
   std::lock_guard<std::mutex> lk(g_timing.mu);
-  if (!total_ms || !launches) return fail(S4R_ERR_NULL_ARG, "total_ms / launches is NULL");
-  double sum = 0.0;
+  if (!total_ms || !steps) return fail(S4R_ERR_NULL_ARG, "total_ms / steps is NULL");
+  for (int k = 0; k < S4R_TIMED_KERNELS; ++k) total_ms[k] = 0.0;
   for (int i = 0; i < g_timing.used; ++i) {
-    float ms = 0.f;
-    if (hipEventSynchronize(g_timing.stop[i]) != hipSuccess ||
-        hipEventElapsedTime(&ms, g_timing.start[i], g_timing.stop[i]) != hipSuccess)
-      return fail(S4R_ERR_HIP, "reading kernel timing events failed");
-    sum += ms;
+    for (int k = 0; k < S4R_TIMED_KERNELS; ++k) {
+      float ms = 0.f;
+      const int s = i * S4R_TIMED_KERNELS + k;
+      if (hipEventSynchronize(g_timing.stop[s]) != hipSuccess ||
+          hipEventElapsedTime(&ms, g_timing.start[s], g_timing.stop[s]) != hipSuccess)
+        return fail(S4R_ERR_HIP, "reading kernel timing events failed");
+      total_ms[k] += ms;
+    }
   }
-  *total_ms = sum;
-  *launches = g_timing.used;
+  *steps = g_timing.used;
   for (auto ev : g_timing.start) (void)hipEventDestroy(ev);
   for (auto ev : g_timing.stop) (void)hipEventDestroy(ev);
   g_timing.start.clear();
   g_timing.stop.clear();
+  g_timing.steps = 0;
   g_timing.used = 0;
   g_timing.enabled = false;
   return ok();

@@ -1,0 +1,309 @@
+// Device helpers shared by the attention kernels (RoPE, operand parts) and
+// the fused reconstruction + split attention kernel template.
+#pragma once
+
+#include "s4r_device.h"
+#include "s4r_internal.h"
+
+namespace s4r {
+
+// RoPE angle of `pos` at frequency index f: returns cos / sin.  The angle is
+// pos * theta^(-2f/d_h); it is reduced in fp64 revolutions and evaluated
+// with the hardware sine / cosine (argument in revolutions).
+__device__ __forceinline__ double rope_rev_freq(float theta, int f, int dh) {
+  if (theta == 0.f) return 0.0;
+  return exp2(-2.0 * f / dh * log2((double)theta)) * 0.15915494309189535;  // / (2 pi)
+}
+__device__ __forceinline__ void rope_cs(int64_t pos, double rev_freq, float& c, float& s) {
+  double a = (double)pos * rev_freq;
+  a -= floor(a);
+  const float x = (float)a;
+  c = __builtin_amdgcn_cosf(x);
+  s = __builtin_amdgcn_sinf(x);
+}
+
+// operand loaders: 8 consecutive elements -> bf16 parts
+template <typename T>
+struct Parts;
+template <>
+struct Parts<uint16_t> {
+  static constexpr int n = 1;
+  __device__ __forceinline__ static void load(const uint16_t* p, Op8* o) { o[0].u = *reinterpret_cast<const uint4*>(p); }
+};
+template <>
+struct Parts<float> {
+  static constexpr int n = 3;
+  __device__ __forceinline__ static void load(const float* p, Op8* o) {
+    float x[8];
+    *reinterpret_cast<float4*>(&x[0]) = *reinterpret_cast<const float4*>(p);
+    *reinterpret_cast<float4*>(&x[4]) = *reinterpret_cast<const float4*>(p + 4);
+    split_f32x8(x, o[0], o[1], o[2]);
+  }
+};
+
+// accumulate A*B over all part pairs whose combined weight is above ~2^-24
+template <int NA, int NB>
+__device__ __forceinline__ floatx4 mfma_parts(const Op8* a, const Op8* b, floatx4 d) {
+#pragma unroll
+  for (int i = 0; i < NA; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (i + j < 3) d = mfma16x16x32(a[i], b[j], d);
+  return d;
+}
+
+
+template <typename T, int RBH, int DH, int G>
+__global__ __launch_bounds__(DH * 2) void k_attn_split(
+    const T* __restrict__ q, const T* __restrict__ bases_k, const T* __restrict__ bases_v,
+    const T* __restrict__ coef_k, const T* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
+    int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int nsplit,
+    int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap, int bases_shared,
+    float theta) {
+  constexpr int NP = Parts<T>::n;
+  constexpr int NWAVE = DH / 32;          // waves per workgroup
+  constexpr int HALF_MB = DH / 32;        // pair offset in 16-dim blocks
+  const int split = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int slot = lane & 15, kg = lane >> 4;
+  const int Dp = hkv * DH, Dg = Dp / nb;
+  const int grp = j / (hkv / nb);
+  const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
+  const int kb0 = grp * rank / 32;                 // first latent block of the group
+
+  // ---- basis operands (A): rows d = 16*mb + slot, k-group kg ------------------
+  // bf16: the key basis slice of every wave sits in LDS (rows padded by 16
+  // bytes: the 16-byte operand reads of one MFMA hit distinct banks) and the
+  // value basis in registers; fp32 (three bf16 parts each) keeps both in
+  // registers.
+  constexpr bool KB_LDS = (NP == 1);
+  constexpr int KS = RBH * 32 + 8;                 // padded LDS row (elements)
+  __shared__ __align__(16) uint16_t kbase[KB_LDS ? NWAVE : 1][2][16][KB_LDS ? KS : 8];
+  Op8 ak[KB_LDS ? 1 : 2][KB_LDS ? 1 : RBH][NP], av[2][RBH][NP];
+  {
+    const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank;
+    if constexpr (KB_LDS) {
+      // whole workgroup copies the K rows of all waves: [wave][hm][16 rows][RBH*32]
+      const int per_row = RBH * 4;                 // 16-byte pieces per row
+      batched_copy16<(NWAVE * 2 * 16 * RBH * 4 + DH * 2 - 1) / (DH * 2)>(
+          NWAVE * 2 * 16 * per_row,
+          [&](int i) {
+            const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
+            const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
+            const int d = 16 * (ww + hm * HALF_MB) + rem2 / per_row;
+            return reinterpret_cast<const uint4*>(bases_k + boff + (int64_t)(row0 + d) * rank + (rem2 % per_row) * 8);
+          },
+          [&](int i) {
+            const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
+            const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
+            return reinterpret_cast<uint4*>(&kbase[ww][hm][rem2 / per_row][(rem2 % per_row) * 8]);
+          });
+    }
+#pragma unroll
+    for (int hm = 0; hm < 2; ++hm) {
+      const int d = 16 * (w + hm * HALF_MB) + slot;
+#pragma unroll
+      for (int kb = 0; kb < RBH; ++kb) {
+        const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
+        if constexpr (!KB_LDS) Parts<T>::load(bases_k + o, ak[hm][kb]);
+        Parts<T>::load(bases_v + o, av[hm][kb]);
+      }
+    }
+  }
+  auto akop = [&](int hm, int kb) -> const Op8* {
+    if constexpr (KB_LDS) {
+      return reinterpret_cast<const Op8*>(&kbase[w][hm][slot][kb * 32 + kg * 8]);
+    } else {
+      return ak[hm][kb];
+    }
+  };
+  // ---- rotated query for this lane's 8 dims -------------------------------------
+  const int64_t pos_q = s_sink + L - 1;
+  double rf[4];
+  float qr[G][8];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) rf[v] = rope_rev_freq(theta, 16 * w + 4 * kg + v, DH);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    float c, sn;
+    rope_cs(pos_q, rf[v], c, sn);
+    const int dlo = 16 * w + 4 * kg + v, dhi = dlo + DH / 2;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (g < G) {
+        const int64_t qo = ((int64_t)b * hq + (int64_t)j * G + g) * DH;
+        const float xl = load_elem(q, qo + dlo), xh = load_elem(q, qo + dhi);
+        qr[g][v] = xl * c - xh * sn;
+        qr[g][4 + v] = xh * c + xl * sn;
+      }
+    }
+  }
+
+  // ---- split range: indices staged in LDS once ------------------------------------
+  const int ntile = (n_proc + 15) / 16;
+  const int tps = (ntile + nsplit - 1) / nsplit;
+  const int tile0 = split * tps, tile1 = min(ntile, tile0 + tps);
+  const int32_t* idx = idx_all + (int64_t)b * idx_stride;
+  const T* ckb = coef_k + (int64_t)b * cap * R;
+  const T* cvb = coef_v + (int64_t)b * cap * R;
+  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
+
+  extern __shared__ int32_t sidx[];                 // [tps * 16] token positions of the split
+  __shared__ float xlog[2][NWAVE][G][16];
+  batched_copy4<4>(
+      (tile1 - tile0) * 16, [&](int i) -> float { return __int_as_float(idx[min(tile0 * 16 + i, n_proc - 1)]); },
+      [&](int i, float x) { sidx[i] = (tile0 * 16 + i < n_proc) ? __float_as_int(x) : -1; });
+  __syncthreads();
+
+  float mrun[G], lrun[G], oacc[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    mrun[g] = -INFINITY;
+    lrun[g] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) oacc[g][i] = 0.f;
+  }
+
+  // coefficient row offset of this lane's token in a tile (0 for padding slots)
+  auto tok_of = [&](int tile) -> int64_t {
+    const int32_t x = sidx[(tile - tile0) * 16 + slot];
+    return x < 0 ? 0 : (int64_t)x;
+  };
+  auto row_off = [&](int64_t tok) -> int64_t { return (tok >> 4) * 16 * (int64_t)R + (tok & 15) * 32 + kg * 8; };
+  auto issue = [&](const T* base, int64_t tok, Op8 (&dst)[RBH][NP]) {
+    const int64_t co = row_off(tok);
+#pragma unroll
+    for (int kb = 0; kb < RBH; ++kb) Parts<T>::load(base + co + (int64_t)(kb0 + kb) * 512, dst[kb]);
+  };
+
+  // one tile: the key and value gathers of the next tile are issued first
+  // (unconditionally, clamped to the split's last tile, so wait counts are
+  // exact) and stay in flight across the LDS-only barrier of the logit
+  // exchange while this tile's MFMAs, RoPE and softmax run
+  auto process = [&](int tile, Op8 (&bk)[RBH][NP], Op8 (&bv)[RBH][NP], Op8 (&bk_next)[RBH][NP],
+                     Op8 (&bv_next)[RBH][NP]) {
+    const bool valid = sidx[(tile - tile0) * 16 + slot] >= 0;
+    const int64_t tok = tok_of(tile);
+    const int64_t tok_next = tok_of(min(tile + 1, tile1 - 1));
+    issue(ckb, tok_next, bk_next);
+    issue(cvb, tok_next, bv_next);
+    floatx4 dk[2];
+#pragma unroll
+    for (int hm = 0; hm < 2; ++hm) {
+      dk[hm] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < RBH; ++kb) {
+        if constexpr (KB_LDS) {
+          Op8 a0;
+          a0.u = *reinterpret_cast<const uint4*>(akop(hm, kb));
+          dk[hm] = mfma16x16x32(a0, bk[kb][0], dk[hm]);
+        } else {
+          dk[hm] = mfma_parts<NP, NP>(akop(hm, kb), bk[kb], dk[hm]);
+        }
+      }
+    }
+    // RoPE at the token's original position s + idx
+    float kr[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      float c, sn;
+      rope_cs(s_sink + tok, rf[v], c, sn);
+      const float xl = dk[0][v], xh = dk[1][v];
+      kr[v] = xl * c - xh * sn;
+      kr[4 + v] = xh * c + xl * sn;
+    }
+    // partial logits over this lane's 8 dims, then over the k-group lanes
+    float part[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a = fmaf(qr[g][i], kr[i], a);
+      a += shfl_xor_f(a, 16);
+      a += shfl_xor_f(a, 32);
+      part[g] = a;
+    }
+    const int buf = tile & 1;
+    if (kg == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) xlog[buf][w][g][slot] = part[g];
+    }
+    floatx4 dv[2];
+#pragma unroll
+    for (int hm = 0; hm < 2; ++hm) {
+      dv[hm] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < RBH; ++kb) dv[hm] = mfma_parts<NP, NP>(av[hm][kb], bv[kb], dv[hm]);
+    }
+    lds_barrier();   // the next tile's gathers stay in flight
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float sfull = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NWAVE; ++ww) sfull += xlog[buf][ww][g][slot];
+      if (!valid) continue;
+      const float sc = sfull * inv_sqrt_d;
+      const float mn = fmaxf(mrun[g], sc);
+      const float alpha = __expf(mrun[g] - mn);   // 0 when mrun is -inf
+      const float p = __expf(sc - mn);
+      lrun[g] = lrun[g] * alpha + p;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        oacc[g][v] = oacc[g][v] * alpha + p * dv[0][v];
+        oacc[g][4 + v] = oacc[g][4 + v] * alpha + p * dv[1][v];
+      }
+      mrun[g] = mn;
+    }
+  };
+
+  Op8 bka[RBH][NP], bkb[RBH][NP], bva[RBH][NP], bvb[RBH][NP];
+  if (tile0 < tile1) {
+    issue(ckb, tok_of(tile0), bka);
+    issue(cvb, tok_of(tile0), bva);
+  }
+  for (int tile = tile0; tile < tile1; tile += 2) {
+    process(tile, bka, bva, bkb, bvb);
+    if (tile + 1 < tile1) process(tile + 1, bkb, bvb, bka, bva);
+  }
+
+  // ---- merge the 16 token slots (lanes with the same k-group) -----------------------
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    if (g >= G) continue;
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) {
+      const float m2 = shfl_xor_f(mrun[g], msk);
+      const float l2 = shfl_xor_f(lrun[g], msk);
+      const float mn = fmaxf(mrun[g], m2);
+      const float a1 = (mrun[g] == -INFINITY) ? 0.f : __expf(mrun[g] - mn);
+      const float a2 = (m2 == -INFINITY) ? 0.f : __expf(m2 - mn);
+      lrun[g] = lrun[g] * a1 + l2 * a2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float o2 = shfl_xor_f(oacc[g][i], msk);
+        oacc[g][i] = oacc[g][i] * a1 + o2 * a2;
+      }
+      mrun[g] = mn;
+    }
+  }
+  if (slot == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (g >= G) continue;
+      const int h = j * G + g;
+      const int64_t pb = ((int64_t)b * hq + h) * kMaxSplit + split;
+      if (w == 0 && kg == 0) {
+        part_ml[pb * 2 + 0] = mrun[g];
+        part_ml[pb * 2 + 1] = lrun[g];
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int dlo = 16 * w + 4 * kg + v;
+        part_o[pb * DH + dlo] = oacc[g][v];
+        part_o[pb * DH + dlo + DH / 2] = oacc[g][4 + v];
+      }
+    }
+  }
+}
+
+}  // namespace s4r

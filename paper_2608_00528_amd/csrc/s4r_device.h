@@ -120,6 +120,61 @@ __device__ __forceinline__ double shfl_xor_d(double v, int mask) {
   return __hiloint2double(hi, lo);
 }
 
+// Copy n items (16 bytes each) with the whole block: every thread issues PER
+// loads before its first store, so a staging pass costs one memory latency per
+// PER * blockDim items instead of one per item.  src_of(i) / dst_of(i) map an
+// item index to its source and destination.  Loads are never guarded by a
+// condition (out-of-range slots re-read item n - 1): a guarded load makes the
+// compiler wait for it before the branch joins, which serialises the batch.
+template <int PER, typename SrcOf, typename DstOf>
+__device__ __forceinline__ void batched_copy16(int n, SrcOf src_of, DstOf dst_of) {
+  if (n <= 0) return;
+  for (int base = 0; base < n; base += PER * (int)blockDim.x) {
+    uint4 r[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
+      r[k] = *src_of(min(i, n - 1));
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
+      if (i < n) *dst_of(i) = r[k];
+    }
+  }
+}
+
+// same for 4-byte items; src_of(i) must be valid for every i in [0, n)
+template <int PER, typename SrcOf, typename DstOf>
+__device__ __forceinline__ void batched_copy4(int n, SrcOf src_of, DstOf dst_of) {
+  if (n <= 0) return;
+  for (int base = 0; base < n; base += PER * (int)blockDim.x) {
+    float r[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
+      r[k] = src_of(min(i, n - 1));
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
+      if (i < n) dst_of(i, r[k]);
+    }
+  }
+}
+
+// Workgroup barrier for LDS exchange only: waits for this wave's LDS traffic
+// (lgkmcnt) but not for outstanding global loads (vmcnt), so prefetched
+// global data stays in flight across the barrier.  (__syncthreads() waits for
+// every outstanding memory operation.)  The signal fences keep the compiler
+// from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // gfx9 encoding: lgkmcnt(0), vmcnt/expcnt not waited
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // order-preserving key of a non-negative fp32 score (sign bit is clear)
 __device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s); }
 

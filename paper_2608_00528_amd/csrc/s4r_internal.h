@@ -5,19 +5,21 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/s4r.h"
+#include "s4r.h"
 
 namespace s4r {
 
 constexpr int kRunTiles = 4;          // coefficient tiles per softmax run (64 tokens)
 constexpr int kRunTok = kRunTiles * 16;
 constexpr int kScoreWaves = 4;        // waves per scoring workgroup
-constexpr int kHistBins = 4096;       // top-12-bit radix histogram of the scores
-constexpr int kHistShift = 20;
-constexpr int kRelChunk = 1024;       // tokens per relevance workgroup
+constexpr int kHistBins = 2048;       // top-11-bit radix histogram of the scores
+constexpr int kHistShift = 21;
+constexpr int kHistChunk = 2048;      // tokens per histogram workgroup (standalone selection)
 constexpr int kSelChunk = 2048;       // tokens per selection workgroup (multiple of 32)
 constexpr int kCandCap = 4096;        // boundary candidates sorted in LDS
+constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capacity <= 4096 * kSelChunk)
 constexpr int kMaxSplit = 64;         // attention splits per (sequence, kv head)
+constexpr int kMaxTilesPerSplit = 512; // 16-token tiles per split (index list staged in LDS)
 constexpr int kMaxGW = 16;            // G * W_q columns handled by one MFMA block
 constexpr int kCounters = 8;          // per-sequence counters in the workspace
 
@@ -30,19 +32,24 @@ struct Problem {
   float theta;
   int GW;                             // G * Wq
   int64_t nruns_max;                  // softmax runs at L = cap
+  int64_t nwg_max;                    // scoring workgroups per sequence, any L <= cap
   int64_t m_max;                      // selected tokens at L = cap
 };
 
 struct Workspace {
   uint16_t* cq_split;   // [B][3][GW][R] bf16 bits: hi, mid, lo of the query coefficients
+  double* proj_partial; // [B][2][nb * row chunks][kMaxGW + 1][R] projection partial sums
   float* e;             // [B][GW][cap]   exp(z - run max), fp32
   double* run_m;        // [B][GW][nruns] run maxima of z
   double* run_s;        // [B][GW][nruns] run sums of e
-  double* gstat;        // [B][GW][2]     global max M and normaliser S
+  double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   float* atilde;        // [B][cap]       relevance scores
   uint32_t* hist;       // [B][kHistBins]
+  uint32_t* hist_wg;    // [B][rel_groups_max][kHistBins] per relevance workgroup
   uint32_t* counters;   // [B][kCounters]
-  uint64_t* cand;       // [B][cap]       boundary candidates (key << 32 | ~index)
+  uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)
+  uint64_t* cand2;      // [B][cand_stride]  compacted candidates (radix fallback)
+  uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
   uint32_t* bitmap;     // [B][cap / 32]  selected global positions
   int32_t* idx;         // [B][m_max]
   float* part_ml;       // [B][hq][kMaxSplit][2]   split partial (max, sum)
@@ -52,6 +59,14 @@ struct Workspace {
 };
 
 Workspace carve_workspace(const Problem& P, void* base);
+int score_workgroups(const Problem& P, int64_t L);
+inline int64_t sel_groups_max(const Problem& P) { return (P.cap + kSelChunk - 1) / kSelChunk; }
+inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelChunk; }
+int relevance_chunk(int GW);
+inline int64_t rel_groups_max(const Problem& P) {
+  const int c = relevance_chunk(P.GW);
+  return (P.cap + c - 1) / c;
+}
 
 // ---- launchers (each returns hipGetLastError() after its launches) --------
 hipError_t launch_prepare(const Problem& P, const Workspace& ws, int64_t L, const void* q,
@@ -59,12 +74,16 @@ hipError_t launch_prepare(const Problem& P, const Workspace& ws, int64_t L, cons
                           const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                           int64_t append_row, float* qcoef_out, bool do_query, bool clear,
                           hipStream_t st);
+hipError_t launch_project(const Problem& P, const Workspace& ws, const void* q, const float* qwin_prev,
+                          const void* bases_k, const void* bases_v, const void* k_new, const void* v_new,
+                          void* coef_k, void* coef_v, int64_t append_row, float* qcoef_out, hipStream_t st);
 hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L,
                                const void* coef_k, hipStream_t st);
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out,
                             hipStream_t st);
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                             hipStream_t st);
+hipError_t launch_hist_reduce(const Problem& P, const Workspace& ws, int ngroups, hipStream_t st);
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st);
 hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, int m, int k_eff,
