@@ -56,10 +56,21 @@ def algorithmic(wl, m):
     return {"step_bytes": ck + gather + bases + sinks + q + out, "stream_bytes": ck, "rec_flops": rec_flops}
 
 
-def traffic_from_profile(kernel_src):
+STREAM_SOURCES = ("score.hip", "s4r_device.h", "s4r_internal.h")
+
+
+def stream_kernel_sha():
+    """Hash of the sources the latent-score stream kernel is compiled from."""
+    h = hashlib.sha256()
+    for f in STREAM_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2608_00528_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(workload):
     """HBM bytes per launch of the stream kernel from the committed rocprofv3
     counter summary, or None when it is absent or the kernel source changed."""
-    path = os.path.join(ROOT, "profiles", "score_stream_llama8b_128k_traffic.txt")
+    path = os.path.join(ROOT, "profiles", f"score_stream_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -67,8 +78,7 @@ def traffic_from_profile(kernel_src):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()[:16]
-    if kv.get("kernel_source_sha256_16") != sha:
+    if kv.get("kernel_source_sha256_16") != stream_kernel_sha():
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -77,26 +87,42 @@ def traffic_from_profile(kernel_src):
 
 
 def cpu_baseline(wl, st, budget_s=10.0):
-    from threadpoolctl import threadpool_limits
+    """The oracle as it stands (numpy with its default BLAS threads) on one
+    sequence of the workload, repeated for about budget_s seconds."""
+    from threadpoolctl import threadpool_info
 
     from oracle import decode
     cfg = dict(n_kv_heads=wl.n_kv_heads, window=wl.window, topk=wl.topk, pool_kernel=wl.pool_kernel,
                pool_mode=wl.pool_mode, group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype)
     one = {k: st[k][:1] for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v", "coef_k", "coef_v")}
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     times = []
-    with threadpool_limits(limits=1):
-        t_end = time.perf_counter() + budget_s
-        while True:
-            t0 = time.perf_counter()
-            decode.decode_step(cfg, wl.L, one["q"], one["sink_k"], one["sink_v"], one["bases_k"], one["bases_v"],
-                               one["coef_k"], one["coef_v"])
-            times.append(time.perf_counter() - t0)
-            if time.perf_counter() > t_end:
-                break
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        decode.decode_step(cfg, wl.L, one["q"], one["sink_k"], one["sink_v"], one["bases_k"], one["bases_v"],
+                           one["coef_k"], one["coef_v"])
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() > t_end:
+            break
     per_seq = float(np.median(times))
-    return {"value": per_seq * wl.batch * 1e6, "unit": "us/step", "cores": 1, "kind": "oracle",
+    return {"value": round(per_seq * wl.batch * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "host_cpus": os.cpu_count(),
             "sample": (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
-                       f"{len(times)} runs in {sum(times):.1f} s, median x {wl.batch} sequences")}
+                       f"{len(times)} runs in {sum(times):.1f} s, median per sequence x {wl.batch} sequences; "
+                       f"BLAS threads {threads}")}
+
+
+def copy_calibration(nbytes, reps):
+    """A plain elementwise copy of known size (read nbytes, write nbytes), for
+    scaling the FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc run."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes,
+                      "reps": reps, "kernel": "torch.neg (elementwise, float32)"}), flush=True)
 
 
 def main():
@@ -107,6 +133,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain copy of BYTES bytes (counter calibration) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -114,10 +142,14 @@ def main():
               f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
         sys.exit(2)
 
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, 5)
+        return
+
     import paper_2608_00528_amd as s4r
     import workloads as W
 
-    torch.cuda.set_device(0)
     wl = W.CONFIGS[args.workload]
     if wl.layers != 1:
         raise SystemExit(f"{wl.name} is a multi-layer workload; bench.py times single-layer steps")
@@ -185,7 +217,7 @@ def main():
     alg = algorithmic(wl, m)
     stream_us = kus["score_stream"]
     achieved = alg["stream_bytes"] / (stream_us * 1e-6) / 1e9
-    traffic = traffic_from_profile(os.path.join(ROOT, "paper_2608_00528_amd", "csrc", "score.hip"))
+    traffic = traffic_from_profile(wl.name)
     step_gbps = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
     rec_tflops = alg["rec_flops"] / (kus["attn_split"] * 1e-6) / 1e12
 

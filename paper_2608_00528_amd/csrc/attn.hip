@@ -6,7 +6,8 @@
 //                 Per 16-token tile of the index list it gathers the selected
 //                 coefficient rows (64-byte pieces of the tiled cache) as MFMA
 //                 B operands and forms K^T = B^K_j C^T and V^T = B^V_j C^T with
-//                 bf16 MFMA (basis rows as A operands, held in registers), so a
+//                 bf16 MFMA (basis rows as A operands: the key basis staged in LDS,
+//                 the value basis in registers), so a
 //                 lane ends with 8 dims of one token.  RoPE is applied to the
 //                 fp32 accumulators, partial logits are summed over the lane's
 //                 k-group and across the waves through LDS, and each lane runs

@@ -7,11 +7,11 @@
 //                  projection of the new token's K/V into coefficient row L-1.
 //   k_score_stream streams C^K once (the HBM-bound pass), Z = C^Q C^K^T/sqrt(R)
 //                  on bf16 MFMA with per-block fp64 accumulation, writes
-//                  exp(z - run max) and per-run (max, sum); the last
-//                  workgroup of each sequence folds the runs into (M, S).
+//                  exp(z - run max), per-run (max, sum) and per-workgroup
+//                  (max, sum) statistics.
 //   k_relevance    p = e * exp(run max - M) / S, mean over the W_q rows,
 //                  pooling with kernel kappa, aggregation over G -> A~ (fp32),
-//                  plus the 4096-bin radix histogram used by the selection.
+//                  plus the 2048-bin radix histogram used by the selection.
 //   k_pack         row-major <-> tiled coefficient layout.
 #include "s4r_device.h"
 #include "s4r_internal.h"

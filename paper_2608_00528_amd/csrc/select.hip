@@ -5,7 +5,7 @@
 //   idx      = sorted(I_global) ++ I_local
 //
 // Scores are non-negative fp32, so their bit patterns order like the values.
-// A 4096-bin histogram of the top 12 bits (built by the relevance kernel or
+// A 2048-bin histogram of the top 11 bits (built by the relevance kernel or
 // k_hist_scores) fixes the boundary bin.  Then:
 //   - every workgroup owns 2048 consecutive positions (64 bitmap words):
 //     positions above the boundary bin are set in a bitmap, positions inside

@@ -84,3 +84,24 @@ def check_selection(idx_gpu, idx_ref, a_ref, L, W, k, rel_tol=1e-6):
 
 def latent_state_np(wl, seed=0, capacity=None, L=None):
     return W.latent_state(wl, seed=seed, capacity=capacity, L=L)
+
+
+def score_tol(cq, coef_k, L, dtype):
+    """Per-sequence bound on the relative error of the GPU's A~.
+
+    The latent logits are summed by bf16 MFMAs whose 32-product blocks are
+    added in fp32 (products exact, then folded into fp64 per block); the
+    rounding inside a block is bounded by c * 2^-24 * sum_k |cq_k C_lk| (a
+    gfx950 check of random and heavy-tailed blocks measured c <= 4.6; c = 8
+    is used for bf16 storage, 16 for fp32 storage, whose coefficients take
+    several part products).  An absolute logit error dz becomes a relative
+    error dz of exp(z - M); the softmax sum adds at most the largest such
+    error again; fp32 storage of the exp values and of A~ adds ~1e-6.
+    cq: [B, G, W_q, R] query coefficients, coef_k: [B, >=L, R]."""
+    c = 8.0 if dtype == "bf16" else 16.0
+    B, R = cq.shape[0], cq.shape[-1]
+    tol = np.empty(B)
+    for b in range(B):
+        s_abs = np.abs(cq[b].reshape(-1, R)) @ np.abs(coef_k[b, :L]).T
+        tol[b] = 2.0 * c * 2.0 ** -24 * s_abs.max() / np.sqrt(R) + 1e-6
+    return tol
