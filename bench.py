@@ -56,7 +56,7 @@ def algorithmic(wl, m):
     return {"step_bytes": ck + gather + bases + sinks + q + out, "stream_bytes": ck, "rec_flops": rec_flops}
 
 
-STREAM_SOURCES = ("score.hip", "s4r_device.h", "s4r_internal.h")
+STREAM_SOURCES = ("stream.hip", "s4r_device.h", "s4r_internal.h")
 
 
 def stream_kernel_sha():

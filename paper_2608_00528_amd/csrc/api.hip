@@ -9,6 +9,7 @@
 #include <string>
 #include <vector>
 
+#include "s4r_device.h"
 #include "s4r_internal.h"
 
 namespace s4r {
@@ -49,6 +50,8 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   if (c->rank < 1 || c->rank > Dg)
     return fail(S4R_ERR_BAD_SHAPE, "rank %d must be in [1, Dp/basis_groups = %d]", c->rank, Dg);
   if (c->rank % 32) return fail(S4R_ERR_UNSUPPORTED, "rank %d must be a multiple of 32", c->rank);
+  if (Dg > kQMaxChunks * kPChunk)
+    return fail(S4R_ERR_UNSUPPORTED, "Dp / basis_groups = %d > %d not supported", Dg, kQMaxChunks * kPChunk);
   const int R = c->rank * c->basis_groups;
   if (R > 256) return fail(S4R_ERR_UNSUPPORTED, "latent width %d > 256 not supported", R);
   if (c->n_sink < 0 || c->n_sink > 1024) return fail(S4R_ERR_BAD_SHAPE, "n_sink %d outside [0, 1024]", c->n_sink);
@@ -97,8 +100,8 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   P.cap = c->capacity;
   P.theta = c->rope_theta;
   P.GW = G * c->q_window;
-  P.nruns_max = (c->capacity + kRunTok - 1) / kRunTok;
-  P.nwg_max = (P.nruns_max + kScoreWaves - 1) / kScoreWaves;   // runs_per_wave >= 1
+  P.nruns_max = c->capacity / kTileTok;
+  P.nwg_max = (P.nruns_max + kScoreWaves - 1) / kScoreWaves;   // tiles per wave >= 1
   P.m_max = std::min<int64_t>(c->topk, std::max<int64_t>(c->capacity - c->window, 0)) +
             std::min<int64_t>(c->window, c->capacity);
   return S4R_OK;
@@ -108,7 +111,10 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
-constexpr int kRegions = 18;
+enum Region {
+  kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits, kCand2,
+  kCandCount, kHistWg, kRegions
+};
 struct Layout {
   size_t off[kRegions];
   size_t total;
@@ -116,26 +122,22 @@ struct Layout {
 
 Layout layout(const Problem& P) {
   const size_t B = P.B, GW = P.GW, cap = P.cap;
-  const size_t sizes[kRegions] = {
-      B * 3 * GW * P.R * 2,                 // cq_split
-      B * GW * cap * 4,                     // e
-      B * GW * P.nruns_max * 8,             // run_m
-      B * GW * P.nruns_max * 8,             // run_s
-      B * GW * P.nwg_max * 2 * 8,           // wg_stats
-      B * cap * 4,                          // atilde
-      B * kHistBins * 4,                    // hist
-      B * kCounters * 4,                    // counters
-      B * cand_stride(P) * 8,               // cand
-      B * (cap / 32) * 4,                   // bitmap
-      B * P.m_max * 4,                      // idx
-      B * P.hq * kMaxSplit * 2 * 4,         // part_ml
-      B * P.hq * kMaxSplit * P.dh * 4,      // part_o
-      B * P.hq * (P.s + P.m_max) * 4,       // attn_logits
-      B * cand_stride(P) * 8,               // cand2
-      B * sel_groups_max(P) * 4,            // cand_count
-      B * rel_groups_max(P) * kHistBins * 4,  // hist_wg
-      B * 2 * (size_t)P.nb * ((P.Dg + 63) / 64) * (kMaxGW + 1) * P.R * 8,   // proj_partial
-  };
+  size_t sizes[kRegions];
+  sizes[kQpart] = B * project_chunks(P) * P.G * P.R * 8;
+  sizes[kE] = B * GW * cap * 4;
+  sizes[kRunM] = B * GW * P.nruns_max * 8;
+  sizes[kWgStats] = B * GW * P.nwg_max * 2 * 8;
+  sizes[kAtilde] = B * cap * 4;
+  sizes[kHist] = B * kHistBins * 4;
+  sizes[kCand] = B * cand_stride(P) * 8;
+  sizes[kBitmap] = B * (cap / 32) * 4;
+  sizes[kIdx] = B * P.m_max * 4;
+  sizes[kPartMl] = B * P.hq * kMaxSplit * 2 * 4;
+  sizes[kPartO] = B * P.hq * kMaxSplit * P.dh * 4;
+  sizes[kAttnLogits] = B * P.hq * (P.s + P.m_max) * 4;
+  sizes[kCand2] = B * cand_stride(P) * 8;
+  sizes[kCandCount] = B * sel_groups_max(P) * 4;
+  sizes[kHistWg] = B * rel_groups_max(P) * kHistBins * 4;
   Layout l;
   size_t o = 0;
   for (int i = 0; i < kRegions; ++i) {
@@ -193,24 +195,21 @@ Workspace carve_workspace(const Problem& P, void* base) {
   const Layout l = layout(P);
   char* b = (char*)base;
   Workspace w;
-  w.cq_split = (uint16_t*)(b + l.off[0]);
-  w.e = (float*)(b + l.off[1]);
-  w.run_m = (double*)(b + l.off[2]);
-  w.run_s = (double*)(b + l.off[3]);
-  w.wg_stats = (double*)(b + l.off[4]);
-  w.atilde = (float*)(b + l.off[5]);
-  w.hist = (uint32_t*)(b + l.off[6]);
-  w.counters = (uint32_t*)(b + l.off[7]);
-  w.cand = (uint64_t*)(b + l.off[8]);
-  w.bitmap = (uint32_t*)(b + l.off[9]);
-  w.idx = (int32_t*)(b + l.off[10]);
-  w.part_ml = (float*)(b + l.off[11]);
-  w.part_o = (float*)(b + l.off[12]);
-  w.attn_logits = (float*)(b + l.off[13]);
-  w.cand2 = (uint64_t*)(b + l.off[14]);
-  w.cand_count = (uint32_t*)(b + l.off[15]);
-  w.hist_wg = (uint32_t*)(b + l.off[16]);
-  w.proj_partial = (double*)(b + l.off[17]);
+  w.qpart = (double*)(b + l.off[kQpart]);
+  w.e = (float*)(b + l.off[kE]);
+  w.run_m = (double*)(b + l.off[kRunM]);
+  w.wg_stats = (double*)(b + l.off[kWgStats]);
+  w.atilde = (float*)(b + l.off[kAtilde]);
+  w.hist = (uint32_t*)(b + l.off[kHist]);
+  w.cand = (uint64_t*)(b + l.off[kCand]);
+  w.bitmap = (uint32_t*)(b + l.off[kBitmap]);
+  w.idx = (int32_t*)(b + l.off[kIdx]);
+  w.part_ml = (float*)(b + l.off[kPartMl]);
+  w.part_o = (float*)(b + l.off[kPartO]);
+  w.attn_logits = (float*)(b + l.off[kAttnLogits]);
+  w.cand2 = (uint64_t*)(b + l.off[kCand2]);
+  w.cand_count = (uint32_t*)(b + l.off[kCandCount]);
+  w.hist_wg = (uint32_t*)(b + l.off[kHistWg]);
   w.total = l.total;
   return w;
 }
@@ -261,9 +260,8 @@ s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q, con
   else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
-  hipError_t e = launch_project(P, w, q, qwin_prev, bases_k, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
-                                qcoef_out, stream);
-  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+  hipError_t e = launch_project_query(P, w.qpart, q, bases_k, stream);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, qcoef_out, stream);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores, stream);
   return hip_status(e, "s4r_score_latent launch");
 }
@@ -379,11 +377,12 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
     return hipEventRecord(start ? g_timing.start[slot + kernel] : g_timing.stop[slot + kernel], stream);
   };
   hipError_t e = mark(hipSuccess, 0, true);
-  if (e == hipSuccess)
-    e = launch_project(P, w, q, qwin_prev, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, nullptr, stream);
+  if (e == hipSuccess && k_new)   // the new token's rows first: the scoring pass reads row L - 1
+    e = launch_project_rows(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, stream);
+  if (e == hipSuccess) e = launch_project_query(P, w.qpart, q, bases_k, stream);
   e = mark(e, 0, false);
   e = mark(e, 1, true);
-  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, nullptr, stream);
   e = mark(e, 1, false);
   e = mark(e, 2, true);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);
@@ -412,9 +411,7 @@ s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_
   S4R_REQ(bases_v);
   S4R_REQ(coef_k);
   S4R_REQ(coef_v);
-  Workspace none{};
-  return hip_status(launch_prepare(P, none, row + 1, nullptr, nullptr, bases_k, bases_v, k_new, v_new, coef_k,
-                                   coef_v, row, nullptr, false, false, stream),
+  return hip_status(launch_project_rows(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, stream),
                     "s4r_project_append launch");
 }
 

@@ -53,8 +53,16 @@ __device__ __forceinline__ floatx4 mfma_parts(const Op8* a, const Op8* b, floatx
 }
 
 
+// two workgroups per CU (at most 256 registers per lane) where the
+// instantiation fits without spilling: bf16 storage with
+// 24 * (rank / 32) + 19 * (G - 1) <= 186, from the compiled register counts
+template <typename T, int RBH, int G>
+constexpr int attn_split_occupancy() {
+  return (sizeof(T) == 2 && 24 * RBH + 19 * (G - 1) <= 186) ? 2 : 1;
+}
+
 template <typename T, int RBH, int DH, int G>
-__global__ __launch_bounds__(DH * 2) void k_attn_split(
+__global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k_attn_split(
     const T* __restrict__ q, const T* __restrict__ bases_k, const T* __restrict__ bases_v,
     const T* __restrict__ coef_k, const T* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int nsplit,

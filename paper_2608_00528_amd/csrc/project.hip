@@ -1,0 +1,242 @@
+// Section 3.2.1 (compressed cache update) on gfx950: the query coefficients
+// c_t^Q = s_t^Q B^K of every query group and the projection of a new token's
+// key and value into coefficient row L-1 (c_t^K = s_t^K B^K, c_t^V = s_t^V B^V).
+#include "s4r_device.h"
+#include "s4r_internal.h"
+
+namespace s4r {
+
+// ---------------------------------------------------------------------------
+// Both kernels: 256 threads = 4 column groups of 8 latent columns x 64 row
+// groups; a workgroup owns 32 latent columns of one basis group.  A thread
+// holds 4 basis rows (rg + 64 i) of its 8 columns in registers, in storage
+// format; the projected vectors are staged in LDS as fp32 (their exact
+// values).  Products are accumulated in fp64 and reduced over the 64 row
+// groups (DPP within 16-lane rows, shuffles across rows, then the 4 waves
+// through LDS) in a fixed order, so results are deterministic.
+// ---------------------------------------------------------------------------
+constexpr int kPRows = 4;                     // basis rows per thread
+constexpr int kPVec = 4;                      // vectors accumulated per pass
+
+// 8 consecutive basis elements, kept in their storage format until used
+struct Raw8bf16 {
+  uint4 u;
+  __device__ __forceinline__ void load(const uint16_t* p) { u = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ float operator[](int c) const {
+    const uint32_t w = (c >> 1) == 0 ? u.x : (c >> 1) == 1 ? u.y : (c >> 1) == 2 ? u.z : u.w;
+    return (c & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+  }
+};
+struct Raw8f32 {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ float operator[](int c) const {
+    const float4& h = (c < 4) ? a : b;
+    const int k = c & 3;
+    return k == 0 ? h.x : k == 1 ? h.y : k == 2 ? h.z : h.w;
+  }
+};
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<uint16_t> {
+  using type = Raw8bf16;
+};
+template <>
+struct Raw8<float> {
+  using type = Raw8f32;
+};
+
+// fp64 move within 16-lane rows (row_ror)
+template <int CTRL>
+__device__ __forceinline__ double dpp_move_d(double x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+// sum over the 16 lanes of a wave that share (lane & 3)
+__device__ __forceinline__ double wave_sum16(double a) {
+  a += dpp_move_d<0x124>(a);   // row_ror:4
+  a += dpp_move_d<0x128>(a);   // row_ror:8
+  a += shfl_xor_d(a, 16);
+  a += shfl_xor_d(a, 32);
+  return a;
+}
+
+template <int NV, typename RawT>
+__device__ __forceinline__ void accumulate_rows(const RawT (&bw)[kPRows], const float (*xs)[kPChunk], int rg,
+                                                double (&acc)[kPVec][8]) {
+#pragma unroll
+  for (int i = 0; i < kPRows; ++i) {
+    const int r = rg + 64 * i;
+    double xv[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) xv[v] = (double)xs[v][r];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const double bc = (double)bw[i][c];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) acc[v][c] = fma(xv[v], bc, acc[v][c]);
+    }
+  }
+}
+
+// per-thread sums (NV vectors x 8 columns) -> per-wave sums in red[wave][v][32]
+template <int NV>
+__device__ __forceinline__ void reduce_rows(double (&acc)[kPVec][8], double (*red)[kPVec][32], int wave, int lane,
+                                            int cg) {
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[v][c] = wave_sum16(acc[v][c]);
+  if (lane < 4) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) red[wave][v][cg * 8 + c] = acc[v][c];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// query coefficients: grid (R / 32, ceil(Dg / 256) row chunks, B).  Each
+// workgroup writes the partial sums of its 256-row chunk for all G query
+// groups to qpart [B][chunks][G][R] (fp64); the scoring kernel adds the
+// chunks in a fixed order.  Splitting the rows over workgroups keeps every
+// thread's work to one load round trip and a short fp64 dot product.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, const T* __restrict__ bases_k,
+                                                       double* __restrict__ qpart, int hq, int hkv, int dh, int G,
+                                                       int nb, int rank, int R, int bases_shared) {
+  const int cblk = blockIdx.x, ch = blockIdx.y, b = blockIdx.z, nch = gridDim.y;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int cg = t & 3, rg = t >> 2;
+  const int Dp = hkv * dh, Dg = Dp / nb;
+  const int ldh = __builtin_ctz(dh);              // head_dim is a power of two
+  const int c0 = cblk * 32;                       // first latent column of the block
+  const int grp = c0 / rank;                      // its basis group
+  const int r0 = ch * kPChunk;                    // first row of the chunk in the group
+  const int nrow = min(kPChunk, Dg - r0);
+
+  __shared__ float xs[kMaxGW][kPChunk];
+  __shared__ double red[4][kPVec][32];
+  const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + ((int64_t)grp * Dg + r0) * rank +
+                   (c0 - grp * rank) + cg * 8;
+  // basis rows rg + 64 i (addresses clamped; rows past nrow meet x = 0) and
+  // the chunk of every group query, all requested before any is used
+  typename Raw8<T>::type bw[kPRows];
+#pragma unroll
+  for (int i = 0; i < kPRows; ++i) bw[i].load(bases + (int64_t)min(rg + 64 * i, nrow - 1) * rank);
+  batched_copy4<kMaxGW * kPChunk / 256>(
+      G * kPChunk,
+      [&](int i) -> float {
+        const int v = i >> 8, d = grp * Dg + r0 + min(i & (kPChunk - 1), nrow - 1);   // feature index in Dp
+        return load_elem(q, ((int64_t)b * hq + (int64_t)(d >> ldh) * G + v) * dh + (d & (dh - 1)));
+      },
+      [&](int i, float x) { xs[i >> 8][min(i & (kPChunk - 1), nrow - 1)] = x; });
+  if (nrow < kPChunk)
+    for (int i = t; i < G * kPChunk; i += blockDim.x)
+      if ((i & (kPChunk - 1)) >= nrow) xs[i >> 8][i & (kPChunk - 1)] = 0.f;
+  __syncthreads();
+
+  for (int v0 = 0; v0 < G; v0 += kPVec) {
+    const int nv = min(kPVec, G - v0);
+    double acc[kPVec][8];
+#pragma unroll
+    for (int v = 0; v < kPVec; ++v)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[v][c] = 0.0;
+    const float(*xv)[kPChunk] = xs + v0;
+    switch (nv) {
+      case 1: accumulate_rows<1>(bw, xv, rg, acc); reduce_rows<1>(acc, red, wave, lane, cg); break;
+      case 2: accumulate_rows<2>(bw, xv, rg, acc); reduce_rows<2>(acc, red, wave, lane, cg); break;
+      case 3: accumulate_rows<3>(bw, xv, rg, acc); reduce_rows<3>(acc, red, wave, lane, cg); break;
+      default: accumulate_rows<4>(bw, xv, rg, acc); reduce_rows<4>(acc, red, wave, lane, cg); break;
+    }
+    __syncthreads();
+    if (t < nv * 32) {
+      const int v = t >> 5, c = t & 31;
+      const double x = ((red[0][v][c] + red[1][v][c]) + red[2][v][c]) + red[3][v][c];
+      qpart[(((int64_t)b * nch + ch) * G + v0 + v) * R + c0 + c] = x;
+    }
+    __syncthreads();                              // red is reused by the next pass
+  }
+}
+
+// ---------------------------------------------------------------------------
+// new token's coefficient rows: grid (R / 32, B, 2 = {key, value}).  The
+// workgroup loops over 256-row chunks of its basis group and writes the full
+// sums into row append_row of the cache (rounded to the storage format).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
+                                                      const T* __restrict__ k_new, const T* __restrict__ v_new,
+                                                      T* __restrict__ coef_k, T* __restrict__ coef_v,
+                                                      int64_t append_row, int hkv, int dh, int nb, int rank, int R,
+                                                      int bases_shared, int64_t cap) {
+  const int cblk = blockIdx.x, b = blockIdx.y, which = blockIdx.z;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int cg = t & 3, rg = t >> 2;
+  const int Dp = hkv * dh, Dg = Dp / nb;
+  const int c0 = cblk * 32;
+  const int grp = c0 / rank;
+  const T* x_new = which == 0 ? k_new : v_new;
+  T* coef = which == 0 ? coef_k : coef_v;
+
+  __shared__ float xs[1][kPChunk];
+  __shared__ double red[4][kPVec][32];
+  const T* bases = (which == 0 ? bases_k : bases_v) + (bases_shared ? 0 : (int64_t)b * Dp * rank) +
+                   (int64_t)grp * Dg * rank + (c0 - grp * rank) + cg * 8;
+  double acc[kPVec][8];
+#pragma unroll
+  for (int v = 0; v < kPVec; ++v)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[v][c] = 0.0;
+  for (int r0 = 0; r0 < Dg; r0 += kPChunk) {
+    const int nrow = min(kPChunk, Dg - r0);
+    typename Raw8<T>::type bw[kPRows];
+#pragma unroll
+    for (int i = 0; i < kPRows; ++i) bw[i].load(bases + (int64_t)(r0 + min(rg + 64 * i, nrow - 1)) * rank);
+    const float x = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r0 + min(t, nrow - 1));
+    if (r0 > 0) __syncthreads();                  // previous chunk's xs reads are done
+    xs[0][t] = (t < nrow) ? x : 0.f;
+    __syncthreads();
+    accumulate_rows<1>(bw, xs, rg, acc);
+  }
+  reduce_rows<1>(acc, red, wave, lane, cg);
+  __syncthreads();
+  if (t < 32) {
+    const double v = ((red[0][0][t] + red[1][0][t]) + red[2][0][t]) + red[3][0][t];
+    store_elem(coef, (int64_t)b * cap * R + tiled_offset(append_row, c0 + t, R), v);
+  }
+}
+
+hipError_t launch_project_query(const Problem& P, double* qpart, const void* q, const void* bases_k, hipStream_t st) {
+  dim3 grid(P.R / 32, project_chunks(P), P.B);
+  if (P.dtype == S4R_BF16)
+    hipLaunchKernelGGL(k_project_query<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)bases_k, qpart, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
+  else
+    hipLaunchKernelGGL(k_project_query<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k, qpart,
+                       P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
+  return hipGetLastError();
+}
+
+hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
+                               const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
+  dim3 grid(P.R / 32, P.B, 2);
+  if (P.dtype == S4R_BF16)
+    hipLaunchKernelGGL(k_project_rows<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)bases_k,
+                       (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
+                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.bases_shared, P.cap);
+  else
+    hipLaunchKernelGGL(k_project_rows<float>, grid, dim3(256), 0, st, (const float*)bases_k, (const float*)bases_v,
+                       (const float*)k_new, (const float*)v_new, (float*)coef_k, (float*)coef_v, row, P.hkv, P.dh,
+                       P.nb, P.rank, P.R, P.bases_shared, P.cap);
+  return hipGetLastError();
+}
+
+}  // namespace s4r

@@ -123,43 +123,33 @@ __device__ __forceinline__ double shfl_xor_d(double v, int mask) {
 // Copy n items (16 bytes each) with the whole block: every thread issues PER
 // loads before its first store, so a staging pass costs one memory latency per
 // PER * blockDim items instead of one per item.  src_of(i) / dst_of(i) map an
-// item index to its source and destination.  Loads are never guarded by a
-// condition (out-of-range slots re-read item n - 1): a guarded load makes the
-// compiler wait for it before the branch joins, which serialises the batch.
+// item index to its source and destination.  Neither loads nor stores are
+// guarded by a condition: slots past n re-read item n - 1 and write that same
+// value to item n - 1's destination.  (A guarded load makes the compiler wait
+// for it before the branch joins, and a guarded store lets it sink the load
+// into the branch; either serialises the batch.)
 template <int PER, typename SrcOf, typename DstOf>
 __device__ __forceinline__ void batched_copy16(int n, SrcOf src_of, DstOf dst_of) {
   if (n <= 0) return;
   for (int base = 0; base < n; base += PER * (int)blockDim.x) {
     uint4 r[PER];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
-      r[k] = *src_of(min(i, n - 1));
-    }
+    for (int k = 0; k < PER; ++k) r[k] = *src_of(min(base + k * (int)blockDim.x + (int)threadIdx.x, n - 1));
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
-      if (i < n) *dst_of(i) = r[k];
-    }
+    for (int k = 0; k < PER; ++k) *dst_of(min(base + k * (int)blockDim.x + (int)threadIdx.x, n - 1)) = r[k];
   }
 }
 
-// same for 4-byte items; src_of(i) must be valid for every i in [0, n)
+// same for 4-byte items; src_of(i) returns the value, dst_of(i, v) stores it
 template <int PER, typename SrcOf, typename DstOf>
 __device__ __forceinline__ void batched_copy4(int n, SrcOf src_of, DstOf dst_of) {
   if (n <= 0) return;
   for (int base = 0; base < n; base += PER * (int)blockDim.x) {
     float r[PER];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
-      r[k] = src_of(min(i, n - 1));
-    }
+    for (int k = 0; k < PER; ++k) r[k] = src_of(min(base + k * (int)blockDim.x + (int)threadIdx.x, n - 1));
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = base + k * (int)blockDim.x + (int)threadIdx.x;
-      if (i < n) dst_of(i, r[k]);
-    }
+    for (int k = 0; k < PER; ++k) dst_of(min(base + k * (int)blockDim.x + (int)threadIdx.x, n - 1), r[k]);
   }
 }
 
@@ -173,6 +163,25 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_waitcnt(0xC07F);   // gfx9 encoding: lgkmcnt(0), vmcnt/expcnt not waited
   __builtin_amdgcn_s_barrier();
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Wave-aggregated append.  Lanes of one wave that hit the same LDS word in one
+// atomic instruction are serialised by the hardware; this issues one atomic
+// per wave instead.  Every active lane of the wave must make the call
+// (inactive lanes simply do not take part).
+
+// reserves one slot of *counter for every active lane with pred; returns the
+// lane's slot (in lane order within the wave), undefined where pred is false
+__device__ __forceinline__ uint32_t wave_append(uint32_t* counter, bool pred) {
+  const uint64_t m = __ballot(pred);
+  if (m == 0) return 0u;
+  const int leader = __ffsll((unsigned long long)m) - 1;
+  uint32_t base = 0u;
+  if (__lane_id() == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
+  base = (uint32_t)__shfl((int)base, leader);
+  const int lane = __lane_id();
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  return base + (uint32_t)__popcll(m & below);
 }
 
 // order-preserving key of a non-negative fp32 score (sign bit is clear)

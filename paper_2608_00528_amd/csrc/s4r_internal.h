@@ -9,8 +9,6 @@
 
 namespace s4r {
 
-constexpr int kRunTiles = 4;          // coefficient tiles per softmax run (64 tokens)
-constexpr int kRunTok = kRunTiles * 16;
 constexpr int kScoreWaves = 4;        // waves per scoring workgroup
 constexpr int kHistBins = 2048;       // top-11-bit radix histogram of the scores
 constexpr int kHistShift = 21;
@@ -21,7 +19,8 @@ constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capac
 constexpr int kMaxSplit = 64;         // attention splits per (sequence, kv head)
 constexpr int kMaxTilesPerSplit = 512; // 16-token tiles per split (index list staged in LDS)
 constexpr int kMaxGW = 16;            // G * W_q columns handled by one MFMA block
-constexpr int kCounters = 8;          // per-sequence counters in the workspace
+constexpr int kPChunk = 256;          // basis rows per query-projection workgroup
+constexpr int kQMaxChunks = 8;        // row chunks per basis group (Dp / basis_groups <= 2048)
 
 struct Problem {
   int B, hq, hkv, dh, G, Dp;
@@ -31,22 +30,19 @@ struct Problem {
   int64_t cap;
   float theta;
   int GW;                             // G * Wq
-  int64_t nruns_max;                  // softmax runs at L = cap
+  int64_t nruns_max;                  // 16-token tiles at L = cap (one softmax reference each)
   int64_t nwg_max;                    // scoring workgroups per sequence, any L <= cap
   int64_t m_max;                      // selected tokens at L = cap
 };
 
 struct Workspace {
-  uint16_t* cq_split;   // [B][3][GW][R] bf16 bits: hi, mid, lo of the query coefficients
-  double* proj_partial; // [B][2][nb * row chunks][kMaxGW + 1][R] projection partial sums
+  double* qpart;        // [B][row chunks][G][R] partial sums of the query coefficients
   float* e;             // [B][GW][cap]   exp(z - run max), fp32
-  double* run_m;        // [B][GW][nruns] run maxima of z
-  double* run_s;        // [B][GW][nruns] run sums of e
+  double* run_m;        // [B][GW][cap / 16] per-tile softmax reference (running max of z)
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   float* atilde;        // [B][cap]       relevance scores
   uint32_t* hist;       // [B][kHistBins]
   uint32_t* hist_wg;    // [B][rel_groups_max][kHistBins] per relevance workgroup
-  uint32_t* counters;   // [B][kCounters]
   uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)
   uint64_t* cand2;      // [B][cand_stride]  compacted candidates (radix fallback)
   uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
@@ -69,16 +65,16 @@ inline int64_t rel_groups_max(const Problem& P) {
 }
 
 // ---- launchers (each returns hipGetLastError() after its launches) --------
-hipError_t launch_prepare(const Problem& P, const Workspace& ws, int64_t L, const void* q,
-                          const float* qwin_prev, const void* bases_k, const void* bases_v,
-                          const void* k_new, const void* v_new, void* coef_k, void* coef_v,
-                          int64_t append_row, float* qcoef_out, bool do_query, bool clear,
-                          hipStream_t st);
-hipError_t launch_project(const Problem& P, const Workspace& ws, const void* q, const float* qwin_prev,
-                          const void* bases_k, const void* bases_v, const void* k_new, const void* v_new,
-                          void* coef_k, void* coef_v, int64_t append_row, float* qcoef_out, hipStream_t st);
-hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L,
-                               const void* coef_k, hipStream_t st);
+inline int project_chunks(const Problem& P) { return (P.Dg + kPChunk - 1) / kPChunk; }
+
+// coefficient projections of Section 3.2.1: the query groups (row-chunk
+// partial sums into qpart) and a new token's key and value rows (into row
+// `row` of the caches)
+hipError_t launch_project_query(const Problem& P, double* qpart, const void* q, const void* bases_k, hipStream_t st);
+hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
+                               const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st);
+hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
+                               const float* qwin_prev, float* qcoef_out, hipStream_t st);
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out,
                             hipStream_t st);
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores,

@@ -26,7 +26,7 @@ namespace s4r {
 
 constexpr int kSelThreads = 256;
 constexpr int kL3Cap = 1024;     // level-3 candidates ranked by counting
-constexpr int kSegWords = 8192;  // bitmap words staged in LDS per segment
+constexpr int kSegWords = 4096;  // bitmap words staged in LDS per segment (131072 positions)
 
 // block-wide exclusive prefix sum of one value per thread (wave shuffles,
 // then the four wave totals through LDS); returns the block total
@@ -121,15 +121,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
 #pragma unroll
   for (int i = 0; i < per; ++i) {
     const int x = c0 + t * per + i;
-    if (x >= n_hist) break;
     const uint32_t key = score_key(v[i]);
     const int bin = (int)(key >> kHistShift);
-    if (bin > b1) {
-      atomicOr(&words[(t * per + i) >> 5], 1u << ((t * per + i) & 31));
-    } else if (bin == b1) {
-      const uint32_t slot = atomicAdd(&s_count, 1u);
-      cand[slot] = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x);
-    }
+    const bool valid = x < n_hist;
+    if (valid && bin > b1) atomicOr(&words[(t * per + i) >> 5], 1u << ((t * per + i) & 31));
+    const bool is_cand = valid && bin == b1;
+    const uint32_t slot = wave_append(&s_count, is_cand);
+    if (is_cand) cand[slot] = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x);
   }
   __syncthreads();
   if (t < kSelChunk / 32 && c0 + t * 32 < n_hist) bitmap[c0 / 32 + t] = words[t];
@@ -199,6 +197,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   __shared__ uint64_t lcand[kCandCap];           // candidates; chosen ones stacked from the top
   __shared__ uint64_t l3[kL3Cap];
   __shared__ uint32_t segw[kSegWords];
+  __shared__ uint32_t woff[kSegWords];           // bit offset of each non-empty word
+  __shared__ uint32_t wlist[kSegWords];          // index of each non-empty word
   __shared__ uint32_t s_digit, s_rem, s_n3, s_nchosen;
   __shared__ uint32_t s_off[kMaxSelGroups + 1];
 
@@ -229,21 +229,29 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   }
   __syncthreads();
 
-  // source of the i-th candidate in (group, slot) order: binary search of the offsets
-  auto src_of = [&](int i) -> const uint64_t* {
-    int lo = 0, hi = ncw - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_off[mid] <= (uint32_t)i) lo = mid;
-      else hi = mid - 1;
-    }
-    return cand_b + (int64_t)lo * kSelChunk + (i - (int)s_off[lo]);
-  };
+  // candidates in (group, slot) order: the source group of entry i is the
+  // last g with s_off[g] <= i, found by a fixed-step binary search that 16
+  // entries per thread run interleaved (s_off[ncw] = n_cand ends every search)
+  int top = 1;
+  while (top < ncw) top <<= 1;
   auto gather = [&](uint64_t* dst) {
     for (int base = 0; base < (int)n_cand; base += 16 * kSelThreads) {
+      int ii[16], g[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        ii[q] = min(base + q * kSelThreads + t, (int)n_cand - 1);
+        g[q] = 0;
+      }
+      for (int step = top >> 1; step > 0; step >>= 1) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int c = g[q] + step;
+          if (s_off[min(c, ncw)] <= (uint32_t)ii[q]) g[q] = c;
+        }
+      }
       uint64_t r[16];
 #pragma unroll
-      for (int q = 0; q < 16; ++q) r[q] = *src_of(min(base + q * kSelThreads + t, (int)n_cand - 1));
+      for (int q = 0; q < 16; ++q) r[q] = cand_b[(int64_t)g[q] * kSelChunk + (ii[q] - (int)s_off[g[q]])];
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int i = base + q * kSelThreads + t;
@@ -251,9 +259,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
       }
     }
   };
-  auto choose = [&](uint64_t c) {
-    const uint32_t slot = atomicAdd(&s_nchosen, 1u);
-    lcand[kCandCap - 1 - slot] = c;
+  // chosen candidates are stacked into lcand from the top end
+  auto choose = [&](uint64_t c, bool pred) {
+    const uint32_t slot = wave_append(&s_nchosen, pred);
+    if (pred) lcand[kCandCap - 1 - slot] = c;
   };
 
   if (need > 0 && n_cand <= (uint32_t)kCandCap) {
@@ -261,8 +270,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
     // level 2: histogram of the next 11 key bits among the candidates
     for (int i = t; i < kHistBins; i += kSelThreads) h2[i] = 0;
     __syncthreads();
-    for (int i = t; i < (int)n_cand; i += kSelThreads)
-      atomicAdd(&h2[(uint32_t)(lcand[i] >> kSub) & (kHistBins - 1)], 1u);
+    for (int i0 = 0; i0 < (int)n_cand; i0 += kSelThreads) {
+      const int i = i0 + t;
+      if (i < (int)n_cand) atomicAdd(&h2[(uint32_t)(lcand[i] >> kSub) & (kHistBins - 1)], 1u);
+    }
     __syncthreads();
     int b2;
     uint32_t above2;
@@ -281,25 +292,24 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
 #pragma unroll
     for (int q = 0; q < kCandCap / kSelThreads; ++q) {
       const int i = q * kSelThreads + t;
-      if (i >= (int)n_cand) continue;
       const uint64_t c = mine[q];
       const int sb = (int)((uint32_t)(c >> kSub) & (kHistBins - 1));
-      if (sb > b2) {
-        choose(c);
-      } else if (sb == b2) {
-        const uint32_t slot = atomicAdd(&s_n3, 1u);
-        if (slot < (uint32_t)kL3Cap) l3[slot] = c;
-      }
+      const bool valid = i < (int)n_cand;
+      choose(c, valid && sb > b2);
+      const bool lev3 = valid && sb == b2;
+      const uint32_t slot = wave_append(&s_n3, lev3);
+      if (lev3 && slot < (uint32_t)kL3Cap) l3[slot] = c;
     }
     __syncthreads();
     const uint32_t n3 = s_n3;
     if (n3 <= (uint32_t)kL3Cap) {
       // level 3: exact rank of each remaining candidate by counting larger composites
-      for (int i = t; i < (int)n3; i += kSelThreads) {
-        const uint64_t c = l3[i];
+      for (int i0 = 0; i0 < (int)n3; i0 += kSelThreads) {
+        const int i = i0 + t;
+        const uint64_t c = l3[min(i, (int)n3 - 1)];
         uint32_t rank = 0;
         for (uint32_t j = 0; j < n3; ++j) rank += (l3[j] > c) ? 1u : 0u;
-        if (rank < need3) choose(c);
+        choose(c, i < (int)n3 && rank < need3);
       }
     } else {
       // many equal keys in sub-bin b2: exact radix select among them (the
@@ -314,9 +324,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
       const uint64_t fmask = ~kLow52 | (((uint64_t)(kHistBins - 1)) << kSub);
       const uint64_t fval = l3[0] & fmask;
       const uint64_t thr = radix_select52(cand, n_cand, fmask, fval, need3, scratch, &s_digit, &s_rem);
-      for (int i = t; i < (int)n_cand; i += kSelThreads) {
-        const uint64_t c = cand[i];
-        if ((c & fmask) == fval && (c & kLow52) >= thr) choose(c);
+      for (int i0 = 0; i0 < (int)n_cand; i0 += kSelThreads) {
+        const int i = i0 + t;
+        const uint64_t c = cand[min(i, (int)n_cand - 1)];
+        choose(c, i < (int)n_cand && (c & fmask) == fval && (c & kLow52) >= thr);
       }
     }
     __syncthreads();
@@ -337,25 +348,40 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
     __syncthreads();
   }
   const uint32_t nchosen = s_nchosen;
+  // the global bitmap was written by the classify kernel; only the overflow
+  // path above adds to it from this kernel, and then reads it back atomically
+  const bool overflow = need > 0 && n_cand > (uint32_t)kCandCap;
 
   // ---- bitmap (+ chosen positions) -> ascending positions, by segments in LDS -----
+  // Per segment: bit offsets of the words by a block scan of popcounts, the
+  // non-empty words compacted by a second scan, then the non-empty words are
+  // expanded, dealt out round-robin over the threads.  Positions
+  // are staged in LDS (lcand is free once the chosen candidates are merged
+  // into the segment) and written out with coalesced stores when they fit.
   const int nwords = (n_hist + 31) / 32;
+  constexpr int kOutCap = kCandCap * 2;
+  uint32_t* lout = reinterpret_cast<uint32_t*>(lcand);
+  const bool stage = k_eff <= kOutCap && nwords <= kSegWords;
+  constexpr int kWPT = kSegWords / kSelThreads;   // words per thread per segment
   uint32_t base = 0;
   if (k_eff > 0) {
     for (int s0 = 0; s0 < nwords; s0 += kSegWords) {
       const int nw = min(kSegWords, nwords - s0);
       for (int b0 = 0; b0 < nw; b0 += 8 * kSelThreads) {
         uint32_t r[8];
+        if (overflow) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-          r[q] = __hip_atomic_load(&bitmap[s0 + min(b0 + q * kSelThreads + t, nw - 1)], __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+          for (int q = 0; q < 8; ++q)
+            r[q] = __hip_atomic_load(&bitmap[s0 + min(b0 + q * kSelThreads + t, nw - 1)], __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+        } else {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int i = b0 + q * kSelThreads + t;
-          if (i < nw) segw[i] = r[q];
+          for (int q = 0; q < 8; ++q) r[q] = bitmap[s0 + min(b0 + q * kSelThreads + t, nw - 1)];
         }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) segw[min(b0 + q * kSelThreads + t, nw - 1)] = r[q];   // past nw: same value again
       }
+      for (int i = nw + t; i < kSegWords; i += kSelThreads) segw[i] = 0u;
       __syncthreads();
       for (uint32_t i = t; i < nchosen; i += kSelThreads) {
         const uint32_t x = 0xFFFFFFFFu - (uint32_t)(lcand[kCandCap - 1 - i] & 0xFFFFFFFFull);
@@ -363,32 +389,61 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
         if (w >= 0 && w < nw) atomicOr(&segw[w], 1u << (x & 31));
       }
       __syncthreads();
-      for (int w0 = 0; w0 < nw; w0 += kSelThreads * 8) {
-        uint32_t wv[8];
-        uint32_t cnt = 0;
+      // thread t owns words [t * kWPT, (t + 1) * kWPT) of the segment
+      uint32_t cnt = 0, ne = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int w = w0 + t * 8 + i;
-          wv[i] = (w < nw) ? segw[w] : 0u;
-          cnt += __popc(wv[i]);
-        }
-        uint32_t excl;
-        const uint32_t total = block_exclusive_scan(cnt, scratch, excl);
-        uint32_t pos = base + excl;
+      for (int i = 0; i < kWPT; ++i) {
+        const uint32_t v = segw[t * kWPT + i];
+        cnt += __popc(v);
+        ne += v ? 1u : 0u;
+      }
+      uint32_t bexcl, nexcl;
+      const uint32_t total = block_exclusive_scan(cnt, scratch, bexcl);
+      const uint32_t n_ne = block_exclusive_scan(ne, scratch, nexcl);
+      {
+        uint32_t pos = base + bexcl, slot = nexcl;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          uint32_t v = wv[i];
-          const int w = s0 + w0 + t * 8 + i;
-          while (v) {
-            const int bit = __ffs(v) - 1;
-            v &= v - 1;
-            if (idx2) idx2[pos] = w * 32 + bit;
-            idx[pos++] = w * 32 + bit;
+        for (int i = 0; i < kWPT; ++i) {
+          const int w = t * kWPT + i;
+          const uint32_t v = segw[w];
+          if (v) {
+            woff[slot] = pos;
+            wlist[slot] = (uint32_t)w;
+            ++slot;
           }
+          pos += __popc(v);
         }
-        base += total;
       }
       __syncthreads();
+      // expansion: the non-empty words are dealt out round-robin, so every
+      // thread gets words from all over the segment and clustered selections
+      // do not pile up on one thread
+      for (uint32_t j = t; j < n_ne; j += kSelThreads) {
+        const uint32_t w = wlist[j];
+        uint32_t v = segw[w];
+        uint32_t pos = woff[j];
+        while (v) {
+          const int bit = __ffs(v) - 1;
+          v &= v - 1;
+          const int32_t x = (int32_t)((s0 + (int)w) * 32 + bit);
+          if (stage) {
+            lout[pos] = (uint32_t)x;
+          } else {
+            idx[pos] = x;
+            if (idx2) idx2[pos] = x;
+          }
+          ++pos;
+        }
+      }
+      base += total;
+      __syncthreads();
+    }
+  }
+  if (k_eff > 0 && stage) {
+    for (int i = t; i < k_eff; i += kSelThreads) {   // the segment loop ended with a barrier
+      const int32_t v = (int32_t)lout[i];
+      idx[i] = v;
+      if (idx2) idx2[i] = v;
     }
   }
   for (int i = t; i < L - n_hist; i += kSelThreads) {
