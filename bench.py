@@ -204,6 +204,68 @@ def main():
     ms_step = ms_total / args.steps
     log(f"[bench] {args.steps} steps: {ms_step * 1e3:.2f} us/step (events), wall {wall / args.steps * 1e6:.2f} us/step")
 
+    # per-step distribution (an event between consecutive steps)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step(i)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(args.steps)])
+    p10, p50, p90 = (float(np.percentile(per, x)) for x in (10, 50, 90))
+    log(f"[bench] per-step us: p10 {p10:.2f}  median {p50:.2f}  p90 {p90:.2f}")
+
+    # the same steps replayed from a HIP graph (one captured step per cache
+    # replica); the graph's output is checked against an eager step first
+    graph_us = None
+    try:
+        ref_out = []
+        for r in range(N_REPLICAS):
+            step(r)
+            ref_out.append(out.clone())
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for r in range(N_REPLICAS):
+                step(r)
+        g.replay()
+        torch.cuda.synchronize()
+        if torch.equal(out, ref_out[N_REPLICAS - 1]):
+            reps_g = max(1, args.steps // N_REPLICAS)
+            g0 = torch.cuda.Event(enable_timing=True)
+            g1 = torch.cuda.Event(enable_timing=True)
+            g0.record(stream)
+            for _ in range(reps_g):
+                g.replay()
+            g1.record(stream)
+            torch.cuda.synchronize()
+            graph_us = g0.elapsed_time(g1) * 1e3 / (reps_g * N_REPLICAS)
+            log(f"[bench] graph replay: {graph_us:.2f} us/step")
+        else:
+            log("[bench] graph replay output differs from the eager step; graph timing not reported")
+        del g
+    except Exception as exc:   # capture unsupported here: report eager numbers only
+        log(f"[bench] graph capture failed: {exc}")
+
+    # achievable read bandwidth over the same bytes: the library's plain
+    # 16-byte streaming read of one C^K replica per launch, rotating replicas
+    cks = [r[0] for r in replicas]
+    sink = None
+    for r in range(N_REPLICAS):
+        sink = s4r.read_bandwidth(cks[r], sink)
+    torch.cuda.synchronize()
+    r0 = torch.cuda.Event(enable_timing=True)
+    r1 = torch.cuda.Event(enable_timing=True)
+    nrd = 4 * N_REPLICAS
+    r0.record(stream)
+    for i in range(nrd):
+        s4r.read_bandwidth(cks[i % N_REPLICAS], sink)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    read_gbps = cks[0].numel() * cks[0].element_size() * nrd / (r0.elapsed_time(r1) * 1e-3) / 1e9
+    log(f"[bench] read ceiling (plain 16-byte stream over C^K): {read_gbps:.0f} GB/s")
+
     # per-kernel pass (events between kernels), same steps again
     nk = min(args.steps, 200)
     s4r.timing_enable(nk)
@@ -241,7 +303,10 @@ def main():
             "batch": wl.batch, "context": wl.N, "rank": wl.R, "window": wl.window, "topk": wl.topk,
             "selected": m, "replicas": N_REPLICAS,
         },
+        "step_us_p10_median_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
+        "graph_replay_us_per_step": None if graph_us is None else round(graph_us, 3),
         "achieved_step_GBps": round(step_gbps, 1),
+        "read_ceiling_GBps": round(read_gbps, 1),
         "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": alg["step_bytes"],
         "kernels_us": {k: round(v, 3) for k, v in kus.items()},

@@ -203,6 +203,17 @@ s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* sr
 s4r_status s4r_timing_enable(int32_t max_steps);
 s4r_status s4r_timing_read(double* total_ms, int64_t* steps);
 
+/*
+ * Read-bandwidth reference for roofline calibration (not part of the method):
+ * reads `bytes` (a positive multiple of 16) from the device buffer `buf` once,
+ * 16-byte loads, grid-stride over the whole GPU.  `sink` (device, uint32,
+ * s4r_read_bandwidth_sink_len() entries) receives one XOR of the words each
+ * thread read; the XOR of all entries is the XOR of every 32-bit word of
+ * the buffer.  buf must be 16-byte aligned.
+ */
+int64_t s4r_read_bandwidth_sink_len(void);
+s4r_status s4r_read_bandwidth(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,6 +18,7 @@ from .api import (  # noqa: E402,F401
     num_selected,
     pack_coef,
     project_append,
+    read_bandwidth,
     reconstruct,
     score_latent,
     select_topk,

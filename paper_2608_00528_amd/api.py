@@ -192,3 +192,14 @@ def timing_read():
     n = ctypes.c_int64()
     L.check(L.load().s4r_timing_read(ms, ctypes.byref(n)))
     return dict(zip(TIMED_KERNELS, list(ms))), n.value
+
+
+def read_bandwidth(buf, sink=None):
+    """One read pass over the bytes of GPU tensor `buf` (roofline reference).
+    Returns the per-thread XOR sink (uint32 viewed as int32)."""
+    lib = L.load()
+    if sink is None:
+        sink = torch.empty(lib.s4r_read_bandwidth_sink_len(), dtype=torch.int32, device=buf.device)
+    L.check(lib.s4r_read_bandwidth(_ptr(buf, "buf"), buf.numel() * buf.element_size(), _ptr(sink, "sink", torch.int32),
+                                   _stream()))
+    return sink

@@ -27,7 +27,7 @@ CFLAGS = [
     "-fPIC",
     "-Wall",
     "-Wno-unused-function",
-    # packed fp32 instructions stay off (see the DESIGN notes on numerics)
+    # no packed fp32 VALU instructions in the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(HERE, "..", "include"),
 ]

@@ -437,6 +437,16 @@ s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* sr
   return pack_common(cfg, n_rows, src_tiled, dst_rowmajor, false, stream);
 }
 
+int64_t s4r_read_bandwidth_sink_len(void) { return read_bandwidth_threads(); }
+
+s4r_status s4r_read_bandwidth(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream) {
+  S4R_REQ(buf);
+  S4R_REQ(sink);
+  if (bytes <= 0 || bytes % 16) return fail(S4R_ERR_BAD_SHAPE, "bytes %lld must be a positive multiple of 16",
+                                             (long long)bytes);
+  return hip_status(launch_read_all(buf, bytes / 16, sink, stream), "s4r_read_bandwidth launch");
+}
+
 s4r_status s4r_timing_enable(int32_t max_steps) {
   std::lock_guard<std::mutex> lk(g_timing.mu);
   if (max_steps < 1 || max_steps > 10000) return fail(S4R_ERR_BAD_SHAPE, "max_steps %d outside [1, 10000]", max_steps);

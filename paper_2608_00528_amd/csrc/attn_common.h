@@ -53,6 +53,27 @@ __device__ __forceinline__ floatx4 mfma_parts(const Op8* a, const Op8* b, floatx
 }
 
 
+// reductions over the 16 token slots of a wave (lane bits 0..3) with DPP:
+// quad_perm swaps for bits 0 and 1, row rotations by 4 and 8 for bits 2 and 3
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float slot_max16(float x) {
+  x = fmaxf(x, dpp_f<0xB1>(x));    // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp_f<0x4E>(x));    // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp_f<0x124>(x));   // row_ror:4
+  x = fmaxf(x, dpp_f<0x128>(x));   // row_ror:8
+  return x;
+}
+__device__ __forceinline__ float slot_sum16(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x124>(x);
+  x += dpp_f<0x128>(x);
+  return x;
+}
+
 // two workgroups per CU (at most 256 registers per lane) where the
 // instantiation fits without spilling: bf16 storage with
 // 24 * (rank / 32) + 19 * (G - 1) <= 186, from the compiled register counts
@@ -79,45 +100,77 @@ __global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k
   const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
   const int kb0 = grp * rank / 32;                 // first latent block of the group
 
-  // ---- basis operands (A): rows d = 16*mb + slot, k-group kg ------------------
-  // bf16: the key basis slice of every wave sits in LDS (rows padded by 16
-  // bytes: the 16-byte operand reads of one MFMA hit distinct banks) and the
-  // value basis in registers; fp32 (three bf16 parts each) keeps both in
-  // registers.
+  // ---- prologue: every global read of the workgroup's setup is requested
+  // before any is used (value basis and query into registers, the split's
+  // index list and the key basis into LDS), so it costs one round trip.
+  const int ntile = (n_proc + 15) / 16;
+  const int tps = (ntile + nsplit - 1) / nsplit;
+  const int tile0 = split * tps, tile1 = min(ntile, tile0 + tps);
+  const int32_t* idx = idx_all + (int64_t)b * idx_stride;
+  const T* ckb = coef_k + (int64_t)b * cap * R;
+  const T* cvb = coef_v + (int64_t)b * cap * R;
+  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
+  extern __shared__ int32_t sidx[];                 // [tps * 16] token positions of the split
+  __shared__ float xlog[2][NWAVE][G][16];
+
+  // basis operands (A): rows d = 16*mb + slot, k-group kg.  bf16: the key
+  // basis slice of every wave sits in LDS (rows padded by 16 bytes: the
+  // 16-byte operand reads of one MFMA hit distinct banks) and the value basis
+  // in registers; fp32 (three bf16 parts each) keeps both in registers.
   constexpr bool KB_LDS = (NP == 1);
   constexpr int KS = RBH * 32 + 8;                 // padded LDS row (elements)
   __shared__ __align__(16) uint16_t kbase[KB_LDS ? NWAVE : 1][2][16][KB_LDS ? KS : 8];
   Op8 ak[KB_LDS ? 1 : 2][KB_LDS ? 1 : RBH][NP], av[2][RBH][NP];
-  {
-    const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank;
-    if constexpr (KB_LDS) {
-      // whole workgroup copies the K rows of all waves: [wave][hm][16 rows][RBH*32]
-      const int per_row = RBH * 4;                 // 16-byte pieces per row
-      batched_copy16<(NWAVE * 2 * 16 * RBH * 4 + DH * 2 - 1) / (DH * 2)>(
-          NWAVE * 2 * 16 * per_row,
-          [&](int i) {
-            const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
-            const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
-            const int d = 16 * (ww + hm * HALF_MB) + rem2 / per_row;
-            return reinterpret_cast<const uint4*>(bases_k + boff + (int64_t)(row0 + d) * rank + (rem2 % per_row) * 8);
-          },
-          [&](int i) {
-            const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
-            const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
-            return reinterpret_cast<uint4*>(&kbase[ww][hm][rem2 / per_row][(rem2 % per_row) * 8]);
-          });
-    }
+  const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank;
 #pragma unroll
-    for (int hm = 0; hm < 2; ++hm) {
-      const int d = 16 * (w + hm * HALF_MB) + slot;
+  for (int hm = 0; hm < 2; ++hm) {
+    const int d = 16 * (w + hm * HALF_MB) + slot;
 #pragma unroll
-      for (int kb = 0; kb < RBH; ++kb) {
-        const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
-        if constexpr (!KB_LDS) Parts<T>::load(bases_k + o, ak[hm][kb]);
-        Parts<T>::load(bases_v + o, av[hm][kb]);
-      }
+    for (int kb = 0; kb < RBH; ++kb) {
+      const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
+      if constexpr (!KB_LDS) Parts<T>::load(bases_k + o, ak[hm][kb]);
+      Parts<T>::load(bases_v + o, av[hm][kb]);
     }
   }
+  // the query at this lane's 8 dims (rotated below)
+  float qx[G][8];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int dlo = 16 * w + 4 * kg + v, dhi = dlo + DH / 2;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int64_t qo = ((int64_t)b * hq + (int64_t)j * G + g) * DH;
+      qx[g][v] = load_elem(q, qo + dlo);
+      qx[g][4 + v] = load_elem(q, qo + dhi);
+    }
+  }
+  // the split's index list (one item per thread for up to 16 tiles)
+  const int nsi = (tile1 - tile0) * 16;
+  int32_t si0 = 0;
+  if (nsi > 0) si0 = idx[min(tile0 * 16 + min((int)threadIdx.x, nsi - 1), n_proc - 1)];
+  if constexpr (KB_LDS) {
+    // whole workgroup copies the K rows of all waves: [wave][hm][16 rows][RBH*32]
+    const int per_row = RBH * 4;                 // 16-byte pieces per row
+    batched_copy16<(NWAVE * 2 * 16 * RBH * 4 + DH * 2 - 1) / (DH * 2)>(
+        NWAVE * 2 * 16 * per_row,
+        [&](int i) {
+          const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
+          const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
+          const int d = 16 * (ww + hm * HALF_MB) + rem2 / per_row;
+          return reinterpret_cast<const uint4*>(bases_k + boff + (int64_t)(row0 + d) * rank + (rem2 % per_row) * 8);
+        },
+        [&](int i) {
+          const int ww = i / (2 * 16 * per_row), rem = i % (2 * 16 * per_row);
+          const int hm = rem / (16 * per_row), rem2 = rem % (16 * per_row);
+          return reinterpret_cast<uint4*>(&kbase[ww][hm][rem2 / per_row][(rem2 % per_row) * 8]);
+        });
+  }
+  if (nsi > 0) {
+    const int i = min((int)threadIdx.x, nsi - 1);   // threads past nsi rewrite item nsi - 1
+    sidx[i] = (tile0 * 16 + i < n_proc) ? si0 : -1;
+  }
+  for (int i = (int)blockDim.x + (int)threadIdx.x; i < nsi; i += (int)blockDim.x)   // splits over 16 tiles
+    sidx[i] = (tile0 * 16 + i < n_proc) ? idx[tile0 * 16 + i] : -1;
   auto akop = [&](int hm, int kb) -> const Op8* {
     if constexpr (KB_LDS) {
       return reinterpret_cast<const Op8*>(&kbase[w][hm][slot][kb * 32 + kg * 8]);
@@ -135,32 +188,13 @@ __global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k
   for (int v = 0; v < 4; ++v) {
     float c, sn;
     rope_cs(pos_q, rf[v], c, sn);
-    const int dlo = 16 * w + 4 * kg + v, dhi = dlo + DH / 2;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if (g < G) {
-        const int64_t qo = ((int64_t)b * hq + (int64_t)j * G + g) * DH;
-        const float xl = load_elem(q, qo + dlo), xh = load_elem(q, qo + dhi);
-        qr[g][v] = xl * c - xh * sn;
-        qr[g][4 + v] = xh * c + xl * sn;
-      }
+      const float xl = qx[g][v], xh = qx[g][4 + v];
+      qr[g][v] = xl * c - xh * sn;
+      qr[g][4 + v] = xh * c + xl * sn;
     }
   }
-
-  // ---- split range: indices staged in LDS once ------------------------------------
-  const int ntile = (n_proc + 15) / 16;
-  const int tps = (ntile + nsplit - 1) / nsplit;
-  const int tile0 = split * tps, tile1 = min(ntile, tile0 + tps);
-  const int32_t* idx = idx_all + (int64_t)b * idx_stride;
-  const T* ckb = coef_k + (int64_t)b * cap * R;
-  const T* cvb = coef_v + (int64_t)b * cap * R;
-  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
-
-  extern __shared__ int32_t sidx[];                 // [tps * 16] token positions of the split
-  __shared__ float xlog[2][NWAVE][G][16];
-  batched_copy4<4>(
-      (tile1 - tile0) * 16, [&](int i) -> float { return __int_as_float(idx[min(tile0 * 16 + i, n_proc - 1)]); },
-      [&](int i, float x) { sidx[i] = (tile0 * 16 + i < n_proc) ? __float_as_int(x) : -1; });
   __syncthreads();
 
   float mrun[G], lrun[G], oacc[G][8];
@@ -184,17 +218,11 @@ __global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k
     for (int kb = 0; kb < RBH; ++kb) Parts<T>::load(base + co + (int64_t)(kb0 + kb) * 512, dst[kb]);
   };
 
-  // one tile: the key and value gathers of the next tile are issued first
-  // (unconditionally, clamped to the split's last tile, so wait counts are
-  // exact) and stay in flight across the LDS-only barrier of the logit
-  // exchange while this tile's MFMAs, RoPE and softmax run
-  auto process = [&](int tile, Op8 (&bk)[RBH][NP], Op8 (&bv)[RBH][NP], Op8 (&bk_next)[RBH][NP],
-                     Op8 (&bv_next)[RBH][NP]) {
+  // one tile's reconstruction, RoPE, logits and online softmax from gathered
+  // coefficient operands bk / bv (this lane: token slot, k-group kg)
+  auto compute_tile = [&](int tile, const Op8 (&bk)[RBH][NP], const Op8 (&bv)[RBH][NP]) {
     const bool valid = sidx[(tile - tile0) * 16 + slot] >= 0;
     const int64_t tok = tok_of(tile);
-    const int64_t tok_next = tok_of(min(tile + 1, tile1 - 1));
-    issue(ckb, tok_next, bk_next);
-    issue(cvb, tok_next, bv_next);
     floatx4 dk[2];
 #pragma unroll
     for (int hm = 0; hm < 2; ++hm) {
@@ -243,56 +271,63 @@ __global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k
 #pragma unroll
       for (int kb = 0; kb < RBH; ++kb) dv[hm] = mfma_parts<NP, NP>(av[hm][kb], bv[kb], dv[hm]);
     }
-    lds_barrier();   // the next tile's gathers stay in flight
+    lds_barrier();   // logit exchange; gathers in flight stay in flight
+    // online softmax with one running maximum per query head shared by the 16
+    // token slots: the tile's maximum comes from a reduction over the slots,
+    // and the accumulators are rescaled only when it raises the running
+    // maximum (a uniform branch), so most tiles need no rescale
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float sfull = 0.f;
 #pragma unroll
       for (int ww = 0; ww < NWAVE; ++ww) sfull += xlog[buf][ww][g][slot];
-      if (!valid) continue;
-      const float sc = sfull * inv_sqrt_d;
-      const float mn = fmaxf(mrun[g], sc);
-      const float alpha = __expf(mrun[g] - mn);   // 0 when mrun is -inf
-      const float p = __expf(sc - mn);
-      lrun[g] = lrun[g] * alpha + p;
+      const float sc = valid ? sfull * inv_sqrt_d : -INFINITY;
+      const float tmax = slot_max16(sc);
+      if (tmax > mrun[g]) {
+        const float alpha = __expf(mrun[g] - tmax);   // 0 when mrun is -inf
+        lrun[g] *= alpha;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) oacc[g][i] *= alpha;
+        mrun[g] = tmax;
+      }
+      const float p = valid ? __expf(sc - mrun[g]) : 0.f;
+      lrun[g] += p;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        oacc[g][v] = oacc[g][v] * alpha + p * dv[0][v];
-        oacc[g][4 + v] = oacc[g][4 + v] * alpha + p * dv[1][v];
+        oacc[g][v] = fmaf(p, dv[0][v], oacc[g][v]);
+        oacc[g][4 + v] = fmaf(p, dv[1][v], oacc[g][4 + v]);
       }
-      mrun[g] = mn;
     }
   };
 
+  // gathers into registers, the next tile's issued before this tile's compute
+  // and kept in flight across its LDS-only barrier
   Op8 bka[RBH][NP], bkb[RBH][NP], bva[RBH][NP], bvb[RBH][NP];
   if (tile0 < tile1) {
     issue(ckb, tok_of(tile0), bka);
     issue(cvb, tok_of(tile0), bva);
   }
   for (int tile = tile0; tile < tile1; tile += 2) {
-    process(tile, bka, bva, bkb, bvb);
-    if (tile + 1 < tile1) process(tile + 1, bkb, bvb, bka, bva);
+    {
+      const int64_t tn = tok_of(min(tile + 1, tile1 - 1));
+      issue(ckb, tn, bkb);
+      issue(cvb, tn, bvb);
+    }
+    compute_tile(tile, bka, bva);
+    if (tile + 1 < tile1) {
+      const int64_t tn = tok_of(min(tile + 2, tile1 - 1));
+      issue(ckb, tn, bka);
+      issue(cvb, tn, bva);
+      compute_tile(tile + 1, bkb, bvb);
+    }
   }
 
-  // ---- merge the 16 token slots (lanes with the same k-group) -----------------------
+  // ---- merge the 16 token slots (they share the running maximum) ------------------
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    if (g >= G) continue;
+    lrun[g] = slot_sum16(lrun[g]);
 #pragma unroll
-    for (int msk = 1; msk < 16; msk <<= 1) {
-      const float m2 = shfl_xor_f(mrun[g], msk);
-      const float l2 = shfl_xor_f(lrun[g], msk);
-      const float mn = fmaxf(mrun[g], m2);
-      const float a1 = (mrun[g] == -INFINITY) ? 0.f : __expf(mrun[g] - mn);
-      const float a2 = (m2 == -INFINITY) ? 0.f : __expf(m2 - mn);
-      lrun[g] = lrun[g] * a1 + l2 * a2;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float o2 = shfl_xor_f(oacc[g][i], msk);
-        oacc[g][i] = oacc[g][i] * a1 + o2 * a2;
-      }
-      mrun[g] = mn;
-    }
+    for (int i = 0; i < 8; ++i) oacc[g][i] = slot_sum16(oacc[g][i]);
   }
   if (slot == 0) {
 #pragma unroll

@@ -95,6 +95,9 @@ hipError_t launch_sparse_attn(const Problem& P, const Workspace& ws, int64_t L, 
                               const int32_t* idx, const float* k_sel, const float* v_sel,
                               float* out, hipStream_t st);
 bool attention_supported(const Problem& P);
+// read-bandwidth reference: XOR of every word, one value per thread in sink
+int read_bandwidth_threads();
+hipError_t launch_read_all(const void* buf, int64_t n16, uint32_t* sink, hipStream_t st);
 hipError_t launch_pack(const Problem& P, int64_t n_rows, const void* src, void* dst, bool to_tiled,
                        hipStream_t st);
 

@@ -97,11 +97,11 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     // older rows from the caller; with W_q = 1 there are none and the load
     // below re-reads a partial sum (unused) so it needs no branch
     const float* qw = (Wq > 1) ? qwin_prev + (int64_t)b * G * (Wq - 1) * R : reinterpret_cast<const float*>(qp);
-    for (int i0 = 0; i0 < GW * R; i0 += 4 * (int)blockDim.x) {
-      double part[4][kQMaxChunks];
-      float old[4];
+    for (int i0 = 0; i0 < GW * R; i0 += 2 * (int)blockDim.x) {
+      double part[2][kQMaxChunks];
+      float old[2];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int i = min(i0 + u * (int)blockDim.x + t, GW * R - 1);
         const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
 #pragma unroll
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
         old[u] = qw[(Wq > 1) ? ((int64_t)g * (Wq - 1) + min(wi, Wq - 2)) * R + r : 0];
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int i = i0 + u * (int)blockDim.x + t;
         if (i >= GW * R) break;
         const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;

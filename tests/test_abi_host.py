@@ -27,7 +27,7 @@ FAKE_MIS = ctypes.c_void_p(0x10004)    # misaligned
 
 def header_functions():
     txt = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:s4r_status|int32_t|const char\*)\s+(s4r_\w+)\s*\(", txt, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:s4r_status|int32_t|int64_t|const char\*)\s+(s4r_\w+)\s*\(", txt, re.M)))
 
 
 def cfg(**kw):
@@ -152,3 +152,6 @@ def test_other_entry_point_errors():
     assert lib.s4r_timing_read(None, None) == L.S4R_ERR_NULL_ARG
     assert s4r.num_selected.__module__   # binding importable
     assert lib.s4r_num_selected(ctypes.byref(c), 0) == -1
+    assert lib.s4r_read_bandwidth(FAKE, 100, FAKE, None) == L.S4R_ERR_BAD_SHAPE      # not a multiple of 16
+    assert lib.s4r_read_bandwidth(None, 64, FAKE, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_read_bandwidth_sink_len() > 0

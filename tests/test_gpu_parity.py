@@ -320,3 +320,12 @@ def test_exact_window_kv():
                                           st["coef_k"], st["coef_v"], L, wl.n_kv_heads, oracle_cfg(c)["rope_theta"],
                                           win_k=wk, win_v=wv, W=Wn)
     assert rel_err_rows(out.cpu().numpy(), o_ref) <= 2e-2
+
+
+def test_read_bandwidth_reference_reads_every_word():
+    buf = torch.randint(-2**31, 2**31 - 1, (1 << 20,), dtype=torch.int32, device="cuda")
+    sink = s4r.read_bandwidth(buf)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    want = np.bitwise_xor.reduce(buf.cpu().numpy().view(np.uint32))
+    assert got == want
