@@ -113,7 +113,7 @@ size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
 enum Region {
   kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits, kCand2,
-  kCandCount, kHistWg, kRegions
+  kCandCount, kRegions
 };
 struct Layout {
   size_t off[kRegions];
@@ -137,7 +137,6 @@ Layout layout(const Problem& P) {
   sizes[kAttnLogits] = B * P.hq * (P.s + P.m_max) * 4;
   sizes[kCand2] = B * cand_stride(P) * 8;
   sizes[kCandCount] = B * sel_groups_max(P) * 4;
-  sizes[kHistWg] = B * rel_groups_max(P) * kHistBins * 4;
   Layout l;
   size_t o = 0;
   for (int i = 0; i < kRegions; ++i) {
@@ -209,7 +208,6 @@ Workspace carve_workspace(const Problem& P, void* base) {
   w.attn_logits = (float*)(b + l.off[kAttnLogits]);
   w.cand2 = (uint64_t*)(b + l.off[kCand2]);
   w.cand_count = (uint32_t*)(b + l.off[kCandCount]);
-  w.hist_wg = (uint32_t*)(b + l.off[kHistWg]);
   w.total = l.total;
   return w;
 }
@@ -260,7 +258,7 @@ s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q, con
   else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
-  hipError_t e = launch_project_query(P, w.qpart, q, bases_k, stream);
+  hipError_t e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
   if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, qcoef_out, stream);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores, stream);
   return hip_status(e, "s4r_score_latent launch");
@@ -379,7 +377,7 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
   hipError_t e = mark(hipSuccess, 0, true);
   if (e == hipSuccess && k_new)   // the new token's rows first: the scoring pass reads row L - 1
     e = launch_project_rows(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, stream);
-  if (e == hipSuccess) e = launch_project_query(P, w.qpart, q, bases_k, stream);
+  if (e == hipSuccess) e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
   e = mark(e, 0, false);
   e = mark(e, 1, true);
   if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, nullptr, stream);

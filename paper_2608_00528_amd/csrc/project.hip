@@ -109,8 +109,9 @@ __device__ __forceinline__ void reduce_rows(double (&acc)[kPVec][8], double (*re
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, const T* __restrict__ bases_k,
-                                                       double* __restrict__ qpart, int hq, int hkv, int dh, int G,
-                                                       int nb, int rank, int R, int bases_shared) {
+                                                       double* __restrict__ qpart, uint32_t* __restrict__ hist,
+                                                       int hq, int hkv, int dh, int G, int nb, int rank, int R,
+                                                       int bases_shared) {
   const int cblk = blockIdx.x, ch = blockIdx.y, b = blockIdx.z, nch = gridDim.y;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int cg = t & 3, rg = t >> 2;
@@ -120,6 +121,10 @@ __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, 
   const int grp = c0 / rank;                      // its basis group
   const int r0 = ch * kPChunk;                    // first row of the chunk in the group
   const int nrow = min(kPChunk, Dg - r0);
+  // the step's selection histogram starts from zero (the relevance kernel
+  // adds to it later in the step)
+  if (cblk == 0 && ch == 0)
+    for (int i = t; i < kHistBins; i += blockDim.x) hist[(int64_t)b * kHistBins + i] = 0u;
 
   __shared__ float xs[kMaxGW][kPChunk];
   __shared__ double red[4][kPVec][32];
@@ -214,14 +219,16 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
   }
 }
 
-hipError_t launch_project_query(const Problem& P, double* qpart, const void* q, const void* bases_k, hipStream_t st) {
+hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+                                hipStream_t st) {
   dim3 grid(P.R / 32, project_chunks(P), P.B);
   if (P.dtype == S4R_BF16)
     hipLaunchKernelGGL(k_project_query<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)bases_k, qpart, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
+                       (const uint16_t*)bases_k, qpart, hist, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
+                       P.bases_shared);
   else
     hipLaunchKernelGGL(k_project_query<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k, qpart,
-                       P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
+                       hist, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
   return hipGetLastError();
 }
 

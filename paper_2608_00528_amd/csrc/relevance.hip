@@ -1,7 +1,7 @@
 // Section 3.2.2 softmax / window mean and the pooling and group-aggregation
 // equations of Section 3.2.3 on gfx950: k_relevance turns the stream's exp
-// values and statistics into A~ (fp32) plus per-workgroup radix histograms;
-// k_hist_reduce sums them; k_hist_scores builds them for caller-given scores.
+// values and statistics into A~ (fp32) and adds to the sequence's radix
+// histogram; k_hist_scores builds it for caller-given scores.
 #include "s4r_device.h"
 #include "s4r_internal.h"
 
@@ -42,9 +42,9 @@ __device__ __forceinline__ void pool_window(const double* __restrict__ v, int po
 
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const double* __restrict__ run_m, const double* __restrict__ wg_stats,
-    float* __restrict__ atilde, uint32_t* __restrict__ hist_wg, float* __restrict__ scores_out,
+    float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
     int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
-    int chunk, int64_t hist_stride) {
+    int chunk) {
   const int b = blockIdx.y;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int GW = G * Wq;
@@ -206,14 +206,24 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     if (valid && x < n_hist) atomicAdd(&hl[score_key(af) >> kHistShift], 1u);
   }
   __syncthreads();
-  // this workgroup's histogram, written whole (summed by k_hist_reduce)
-  uint32_t* hw = hist_wg + ((int64_t)b * hist_stride + blockIdx.x) * kHistBins;
-  for (int i = t; i < kHistBins; i += blockDim.x) hw[i] = hl[i];
+  // this workgroup's histogram into the sequence's (zeroed by the query
+  // projection earlier in the step): one global atomic per non-empty bin
+  uint32_t* hs = hist + (int64_t)b * kHistBins;
+  for (int i = t; i < kHistBins; i += blockDim.x) {
+    const uint32_t c = hl[i];
+    if (c) atomicAdd(&hs[i], c);
+  }
 }
 
-// histogram of caller-provided scores (standalone selection)
-__global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ scores, uint32_t* __restrict__ hist_wg,
-                                                     int L, int n_hist, int64_t hist_stride) {
+// histogram of caller-provided scores (standalone selection), into a
+// histogram zeroed by k_zero_hist
+__global__ __launch_bounds__(256) void k_zero_hist(uint32_t* __restrict__ hist, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) hist[i] = 0u;
+}
+
+__global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ scores, uint32_t* __restrict__ hist,
+                                                     int L, int n_hist) {
   const int b = blockIdx.y;
   __shared__ uint32_t hl[kHistBins];
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) hl[i] = 0;
@@ -224,27 +234,12 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
     if (x < n_hist) atomicAdd(&hl[score_key(scores[(int64_t)b * L + x]) >> kHistShift], 1u);
   }
   __syncthreads();
-  uint32_t* hw = hist_wg + ((int64_t)b * hist_stride + blockIdx.x) * kHistBins;
-  for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) hw[i] = hl[i];
-}
-
-// per-workgroup histograms -> one histogram per sequence, fixed summation order
-__global__ __launch_bounds__(256) void k_hist_reduce(const uint32_t* __restrict__ hist_wg, uint32_t* __restrict__ hist,
-                                                     int ngroups, int64_t hist_stride) {
-  const int b = blockIdx.y;
-  const int bin = blockIdx.x * blockDim.x + threadIdx.x;
-  const uint32_t* hw = hist_wg + (int64_t)b * hist_stride * kHistBins + bin;
-  uint32_t sum = 0;
-  for (int g0 = 0; g0 < ngroups; g0 += 16) {
-    uint32_t v[16];
-#pragma unroll
-    for (int g = 0; g < 16; ++g) v[g] = hw[(int64_t)min(g0 + g, ngroups - 1) * kHistBins];
-#pragma unroll
-    for (int g = 0; g < 16; ++g) sum += (g0 + g < ngroups) ? v[g] : 0u;
+  uint32_t* hs = hist + (int64_t)b * kHistBins;
+  for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
+    const uint32_t c = hl[i];
+    if (c) atomicAdd(&hs[i], c);
   }
-  hist[(int64_t)b * kHistBins + bin] = sum;
 }
-
 
 int relevance_chunk(int GW) { return GW <= 4 ? 2048 : (GW <= 8 ? 1024 : 512); }   // <= kRelThreads * kRelPerThr
 
@@ -261,25 +256,18 @@ hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, fl
   const int chunk = relevance_chunk(P.GW);
   const size_t lds = relevance_lds(P.G, P.GW, chunk, P.kappa);
   dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
-  hipLaunchKernelGGL(k_relevance, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats, ws.atilde, ws.hist_wg,
+  hipLaunchKernelGGL(k_relevance, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats, ws.atilde, ws.hist,
                      scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), score_workgroups(P, L), chunk, rel_groups_max(P));
-  return launch_hist_reduce(P, ws, (int)grid.x, st);
-}
-
-hipError_t launch_hist_reduce(const Problem& P, const Workspace& ws, int ngroups, hipStream_t st) {
-  hipLaunchKernelGGL(k_hist_reduce, dim3(kHistBins / 256, P.B), dim3(256), 0, st, ws.hist_wg, ws.hist, ngroups,
-                     rel_groups_max(P));
+                     (int)(P.cap / kTileTok), score_workgroups(P, L), chunk);
   return hipGetLastError();
 }
 
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores, hipStream_t st) {
   const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
   const int ng = std::max(1, (n_hist + kHistChunk - 1) / kHistChunk);
-  hipLaunchKernelGGL(k_hist_scores, dim3(ng, P.B), dim3(256), 0, st, scores, ws.hist_wg, (int)L, n_hist,
-                     rel_groups_max(P));
-  return launch_hist_reduce(P, ws, ng, st);
+  hipLaunchKernelGGL(k_zero_hist, dim3((P.B * kHistBins + 255) / 256), dim3(256), 0, st, ws.hist, P.B * kHistBins);
+  hipLaunchKernelGGL(k_hist_scores, dim3(ng, P.B), dim3(256), 0, st, scores, ws.hist, (int)L, n_hist);
+  return hipGetLastError();
 }
-
 
 }  // namespace s4r

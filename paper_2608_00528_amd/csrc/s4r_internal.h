@@ -42,7 +42,6 @@ struct Workspace {
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   float* atilde;        // [B][cap]       relevance scores
   uint32_t* hist;       // [B][kHistBins]
-  uint32_t* hist_wg;    // [B][rel_groups_max][kHistBins] per relevance workgroup
   uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)
   uint64_t* cand2;      // [B][cand_stride]  compacted candidates (radix fallback)
   uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
@@ -70,7 +69,8 @@ inline int project_chunks(const Problem& P) { return (P.Dg + kPChunk - 1) / kPCh
 // coefficient projections of Section 3.2.1: the query groups (row-chunk
 // partial sums into qpart) and a new token's key and value rows (into row
 // `row` of the caches)
-hipError_t launch_project_query(const Problem& P, double* qpart, const void* q, const void* bases_k, hipStream_t st);
+hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+                                hipStream_t st);
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st);
 hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
@@ -79,7 +79,6 @@ hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, fl
                             hipStream_t st);
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                             hipStream_t st);
-hipError_t launch_hist_reduce(const Problem& P, const Workspace& ws, int ngroups, hipStream_t st);
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st);
 hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, int m, int k_eff,
