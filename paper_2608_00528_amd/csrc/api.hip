@@ -124,8 +124,8 @@ Layout layout(const Problem& P) {
   const size_t B = P.B, GW = P.GW, cap = P.cap;
   size_t sizes[kRegions];
   sizes[kQpart] = B * project_chunks(P) * P.G * P.R * 8;
-  sizes[kE] = B * GW * cap * 4;
-  sizes[kRunM] = B * GW * P.nruns_max * 8;
+  sizes[kE] = B * (size_t)gw_padded(P) * cap * 4;
+  sizes[kRunM] = B * (size_t)gw_padded(P) * P.nruns_max * 4;
   sizes[kWgStats] = B * GW * P.nwg_max * 2 * 8;
   sizes[kAtilde] = B * cap * 4;
   sizes[kHist] = B * kHistBins * 4;
@@ -196,7 +196,7 @@ Workspace carve_workspace(const Problem& P, void* base) {
   Workspace w;
   w.qpart = (double*)(b + l.off[kQpart]);
   w.e = (float*)(b + l.off[kE]);
-  w.run_m = (double*)(b + l.off[kRunM]);
+  w.run_m = (float*)(b + l.off[kRunM]);
   w.wg_stats = (double*)(b + l.off[kWgStats]);
   w.atilde = (float*)(b + l.off[kAtilde]);
   w.hist = (uint32_t*)(b + l.off[kHist]);

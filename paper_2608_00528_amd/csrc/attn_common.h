@@ -53,27 +53,6 @@ __device__ __forceinline__ floatx4 mfma_parts(const Op8* a, const Op8* b, floatx
 }
 
 
-// reductions over the 16 token slots of a wave (lane bits 0..3) with DPP:
-// quad_perm swaps for bits 0 and 1, row rotations by 4 and 8 for bits 2 and 3
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float slot_max16(float x) {
-  x = fmaxf(x, dpp_f<0xB1>(x));    // quad_perm [1,0,3,2]
-  x = fmaxf(x, dpp_f<0x4E>(x));    // quad_perm [2,3,0,1]
-  x = fmaxf(x, dpp_f<0x124>(x));   // row_ror:4
-  x = fmaxf(x, dpp_f<0x128>(x));   // row_ror:8
-  return x;
-}
-__device__ __forceinline__ float slot_sum16(float x) {
-  x += dpp_f<0xB1>(x);
-  x += dpp_f<0x4E>(x);
-  x += dpp_f<0x124>(x);
-  x += dpp_f<0x128>(x);
-  return x;
-}
-
 // two workgroups per CU (at most 256 registers per lane) where the
 // instantiation fits without spilling: bf16 storage with
 // 24 * (rank / 32) + 19 * (G - 1) <= 186, from the compiled register counts

@@ -10,206 +10,245 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 // K2: relevance A~ and its radix histogram
 // ---------------------------------------------------------------------------
-// grid (ceil(L / chunk), B), 1024 threads (16 waves, one query row each for
-// the statistics).  One memory latency: the scoring
-// workgroups' statistics of this workgroup's query rows, the per-run maxima
-// of its chunk and the chunk's exp values (plus the pooling halo) are all
-// requested before any of them is used.  Then each wave folds its query rows'
-// statistics into the global (M, S) (the same fixed order in every workgroup,
-// so A~ is deterministic) and the per-run factors exp(run max - M) / S; the
-// window mean of every staged position is formed once; each thread pools and
-// aggregates 2 consecutive outputs from a register window.
+// grid (ceil(L / chunk), B), 256 threads; chunk = 1024 / 512 / 256 tokens for
+// G <= 4 / 8 / 16.  The stream's exp values are stored token-major,
+// e[b][x][c] for query column c = g * W_q + i (GWP = G * W_q rounded up to a
+// multiple of 4, padding columns zero), with one reference per 16-token tile,
+// tref[b][tile][c].  One memory latency: the scoring workgroups' statistics,
+// the chunk's tile references and its exp values (plus the pooling halo) are
+// all requested before any is used.  Then each wave folds query columns'
+// statistics into the global (M, S) in fp64 (the same fixed order in every
+// workgroup, so A~ is deterministic) and the per-tile factors
+// exp(ref - M) / S are formed in fp64.  Per staged position the window mean
+// over the W_q rows is formed once (fp32 products of values exact to about an
+// ulp; the max-pooling that follows is exact), staged in LDS, and every thread
+// pools outputs t, t + 256, ... (consecutive lanes read consecutive words: no
+// bank conflicts) and sums the groups in fp64.
+constexpr int kRelThreads = 256;
+constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk and its halo (h <= 32)
 
-constexpr int kRelThreads = 1024;
-constexpr int kRelStatPer = 4;                // statistics pairs per lane per batch
-constexpr int kRelRunPer = 3;                 // tile references per lane (chunk <= 2048)
-constexpr int kRelPerThr = 2;                 // outputs per thread
+int relevance_chunk(int G) { return G <= 4 ? 1024 : (G <= 8 ? 512 : 256); }
 
-template <int H>
-__device__ __forceinline__ void pool_window(const double* __restrict__ v, int pool_mode, int kappa, double (&p)[kRelPerThr]) {
-  // v points at the window of output 0; outputs j read v[j .. j + 2H]
-  double w[kRelPerThr + 2 * H];
+// Pooling (kappa = 2H + 1, stride 1, same length) and aggregation over the G
+// groups for outputs t, t + 256, ... of a chunk.  With H known at compile time
+// every window value is requested from LDS before any is combined, so the
+// reads overlap; H < 0 is the generic (slower) path for wide kernels.
+template <int H, int TPT, int GMAX>
+__device__ __forceinline__ void pool_aggregate(const float* __restrict__ vs, int span, int t, int G, int kappa,
+                                               int pool_mode, int agg, float (&af)[TPT]) {
+  const int h = (H >= 0) ? H : kappa / 2;
 #pragma unroll
-  for (int i = 0; i < kRelPerThr + 2 * H; ++i) w[i] = v[i];
+  for (int j = 0; j < TPT; ++j) {
+    const int o = t + j * kRelThreads;                     // window of output o: vs[g][o .. o + 2h]
+    double acc = (agg == S4R_AGG_MEAN) ? 0.0 : -INFINITY;
+    if constexpr (H >= 0) {
+      float w[GMAX][2 * (H > 0 ? H : 0) + 1];
 #pragma unroll
-  for (int j = 0; j < kRelPerThr; ++j) {
-    double a = w[j];
+      for (int g = 0; g < GMAX; ++g)
 #pragma unroll
-    for (int o = 1; o <= 2 * H; ++o) a = (pool_mode == S4R_POOL_MAX) ? fmax(a, w[j + o]) : a + w[j + o];
-    p[j] = (pool_mode == S4R_POOL_MAX) ? a : a / kappa;
+        for (int d = 0; d <= 2 * H; ++d) w[g][d] = vs[min(g, G - 1) * span + o + d];   // unguarded: overlapped
+#pragma unroll
+      for (int g = 0; g < GMAX; ++g) {
+        if (g < G) {
+          float a;
+          if (pool_mode == S4R_POOL_MAX) {
+            a = w[g][0];
+#pragma unroll
+            for (int d = 1; d <= 2 * H; ++d) a = fmaxf(a, w[g][d]);
+          } else {
+            double sa = 0.0;
+#pragma unroll
+            for (int d = 0; d <= 2 * H; ++d) sa += (double)w[g][d];
+            a = (float)(sa / kappa);
+          }
+          acc = (agg == S4R_AGG_MEAN) ? acc + (double)a : fmax(acc, (double)a);
+        }
+      }
+    } else {
+      for (int g = 0; g < G; ++g) {
+        const float* v = vs + g * span + o;
+        float a = v[0];
+        double sa = (double)v[0];
+        for (int d = 1; d <= 2 * h; ++d) {
+          a = fmaxf(a, v[d]);
+          sa += (double)v[d];
+        }
+        if (pool_mode != S4R_POOL_MAX) a = (float)(sa / kappa);
+        acc = (agg == S4R_AGG_MEAN) ? acc + (double)a : fmax(acc, (double)a);
+      }
+    }
+    af[j] = (float)((agg == S4R_AGG_MEAN) ? acc / G : acc);
   }
 }
 
+template <int NQ, int TPT, bool WQ1>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
-    const float* __restrict__ e, const double* __restrict__ run_m, const double* __restrict__ wg_stats,
+    const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
-    int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
-    int chunk) {
+    int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg) {
+  constexpr int GWP = 4 * NQ;
+  constexpr int CHUNK = kRelThreads * TPT;
+  constexpr int SPAN_MAX = CHUNK + 64;
+  constexpr int PPT = (SPAN_MAX + kRelThreads - 1) / kRelThreads;   // staged positions per thread
   const int b = blockIdx.y;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int GW = G * Wq;
   const int h = kappa / 2;
-  const int HP = (h + 3) & ~3;                              // halo slot rounded to 16 bytes
-  const int SP = chunk + 2 * HP;                            // staged row stride (floats)
-  const int t0 = blockIdx.x * chunk;
-  const int span = chunk + 2 * h;
-  const int x0 = t0 - h;                                    // first staged position
-  const int r_first = max(x0, 0) / kTileTok;               // tiles with a softmax reference
-  const int r_last = (min(t0 + chunk + h, L) - 1) / kTileTok;
-  const int nr = r_last - r_first + 1;                      // <= chunk / 16 + 2 <= 64 * kRelRunPer
-  const int nrc = chunk / kTileTok + 4;                     // tile slots per query row
+  const int t0 = blockIdx.x * CHUNK;
+  const int x0 = t0 - h;                                   // first staged position
+  const int span = CHUNK + 2 * h;
+  const int tile_lo = max(x0, 0) / kTileTok;
+  const int tile_hi = (min(t0 + CHUNK + h, L) - 1) / kTileTok;
+  const int ntl = tile_hi - tile_lo + 1;                   // <= kRelMaxTiles
 
-  // dynamic LDS: histogram, per-run factors, window means, exp values
-  extern __shared__ __align__(16) unsigned char lds[];
-  uint32_t* hl = reinterpret_cast<uint32_t*>(lds);
-  double* fac = reinterpret_cast<double*>(hl + kHistBins);  // [GW][nrc]: exp(run max - M) / S
-  double* vs = fac + GW * nrc;                              // [G][span]: window mean at x0 + i
-  float* e_s = reinterpret_cast<float*>(vs + G * span);     // [GW][SP]: x at [HP + x - t0]
+  __shared__ uint32_t hl[kHistBins];
+  __shared__ double sM[GWP], sInvS[GWP];
+  __shared__ float fac[kRelMaxTiles][GWP];                 // exp(ref - M) / S per tile and column
+  extern __shared__ float vs[];                            // [G][span]: window mean at x0 + i
 
   // ---- all global reads of this workgroup, issued before any is used ----------
+  // statistics: wave w folds columns w, w + 4, ...; two batches of 64 lanes in flight
+  constexpr int kStatPer = 2;
+  double2 st[NQ][kStatPer];
   const double2* stats = reinterpret_cast<const double2*>(wg_stats) + (int64_t)b * GW * nwg;
-  double2 st[kRelStatPer];
-  double rm[kRelRunPer];
-  {
-    const int gi = min(wave, GW - 1);            // waves >= GW re-read the last row (unused)
 #pragma unroll
-    for (int k = 0; k < kRelStatPer; ++k) st[k] = stats[(int64_t)gi * nwg + min(lane + 64 * k, nwg - 1)];
+  for (int q = 0; q < NQ; ++q) {
+    const int c = min(wave + 4 * q, GW - 1);
 #pragma unroll
-    for (int k = 0; k < kRelRunPer; ++k) rm[k] = run_m[((int64_t)b * GW + gi) * ntiles_cap + min(r_first + lane + 64 * k, r_last)];
+    for (int k = 0; k < kStatPer; ++k) st[q][k] = stats[(int64_t)c * nwg + min(lane + 64 * k, nwg - 1)];
   }
+  // tile references: thread t loads tile tile_lo + t (all columns)
+  float4 rf[NQ];
   {
-    // pooling halo (4-byte items, GW * 2h <= kRelThreads): one per thread,
-    // loaded before the main batch so that batch's wait covers it
-    const int nh = GW * 2 * h;
-    float halo_v = 0.f;
-    int halo_o = 0;
-    if (nh > 0) {
-      const int i = min(t, nh - 1);
-      const int gi = i / (2 * h), k = i % (2 * h);
-      const int x = (k < h) ? t0 - h + k : t0 + chunk + (k - h);
-      halo_v = e[((int64_t)b * GW + gi) * cap + min(max(x, 0), L - 1)];   // out-of-range halo is never used
-      halo_o = gi * SP + ((k < h) ? HP - h + k : HP + chunk + (k - h));
-    }
-    // the chunk itself: 16-byte items, chunk / 4 of them per query row (a power
-    // of two), clamped to the row's valid part (t0 is a multiple of 4;
-    // rounding L - t0 up to 4 stays below the capacity, a multiple of 16)
-    const int lc4 = __builtin_ctz(chunk / 4);
-    const int c4 = (min(chunk, L - t0) + 3) / 4;
-    batched_copy16<2>(
-        GW << lc4,
-        [&](int i) {
-          return reinterpret_cast<const uint4*>(e + ((int64_t)b * GW + (i >> lc4)) * cap + t0) +
-                 min(i & ((1 << lc4) - 1), c4 - 1);
-        },
-        [&](int i) {
-          return reinterpret_cast<uint4*>(e_s + (i >> lc4) * SP + HP) + min(i & ((1 << lc4) - 1), c4 - 1);
-        });
-    if (nh > 0) e_s[halo_o] = halo_v;            // threads past nh rewrite item nh - 1
+    const float4* tp = reinterpret_cast<const float4*>(tref + ((int64_t)b * ntiles_cap + tile_lo + min(t, ntl - 1)) * GWP);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) rf[q] = tp[q];
   }
-  for (int i = t; i < kHistBins; i += blockDim.x) hl[i] = 0;
+  // exp values of the staged positions (clamped into [0, L); masked later)
+  float4 ev[PPT][NQ];
+#pragma unroll
+  for (int k = 0; k < PPT; ++k) {
+    const int x = min(max(x0 + t + k * kRelThreads, 0), L - 1);
+    const float4* ep = reinterpret_cast<const float4*>(e + ((int64_t)b * cap + x) * GWP);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) ev[k][q] = ep[q];
+  }
+  for (int i = t; i < kHistBins; i += kRelThreads) hl[i] = 0;
 
-  // ---- global (M, S) of each query row and the per-run factors (one wave per row)
-  if (wave < GW) {
-    const int gi = wave;
-    const double* srow = wg_stats + ((int64_t)b * GW + gi) * nwg * 2;
-    double M = -INFINITY, S = 0.0;
-    for (int base = 0; base < nwg; base += 64 * kRelStatPer) {
-      double2 s2[kRelStatPer];
-      if (base == 0) {
+  // ---- global (M, S) of each query column ---------------------------------------------
 #pragma unroll
-        for (int k = 0; k < kRelStatPer; ++k) s2[k] = st[k];
-      } else {                                              // more than 256 scoring workgroups: reload
+  for (int q = 0; q < NQ; ++q) {
+    const int c = wave + 4 * q;
+    if (c < GW) {                                          // wave-uniform
+      const double* srow = wg_stats + ((int64_t)b * GW + c) * nwg * 2;
+      double M = -INFINITY, S = 0.0;
+      for (int base = 0; base < nwg; base += 64 * kStatPer) {
+        double2 s2[kStatPer];
 #pragma unroll
-        for (int k = 0; k < kRelStatPer; ++k) {
-          const int w = min(base + lane + 64 * k, nwg - 1);
-          s2[k] = make_double2(srow[2 * w], srow[2 * w + 1]);
+        for (int k = 0; k < kStatPer; ++k) {
+          if (base == 0) {
+            s2[k] = st[q][k];
+          } else {                                         // more than 128 scoring workgroups
+            const int w = min(base + lane + 64 * k, nwg - 1);
+            s2[k] = make_double2(srow[2 * w], srow[2 * w + 1]);
+          }
+        }
+        double m = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < kStatPer; ++k)
+          if (base + lane + 64 * k < nwg) m = fmax(m, s2[k].x);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = fmax(m, shfl_xor_d(m, o));
+        double s = 0.0;
+#pragma unroll
+        for (int k = 0; k < kStatPer; ++k)
+          if (base + lane + 64 * k < nwg && s2[k].x != -INFINITY) s += s2[k].y * exp(s2[k].x - m);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) s += shfl_xor_d(s, o);
+        if (m != -INFINITY) {
+          const double Mn = fmax(M, m);
+          S = ((M == -INFINITY) ? 0.0 : S * exp(M - Mn)) + s * exp(m - Mn);
+          M = Mn;
         }
       }
-      double m = -INFINITY;
-#pragma unroll
-      for (int k = 0; k < kRelStatPer; ++k)
-        if (base + lane + 64 * k < nwg) m = fmax(m, s2[k].x);
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) m = fmax(m, shfl_xor_d(m, o));
-      double s = 0.0;
-#pragma unroll
-      for (int k = 0; k < kRelStatPer; ++k)
-        if (base + lane + 64 * k < nwg && s2[k].x != -INFINITY) s += s2[k].y * exp(s2[k].x - m);
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) s += shfl_xor_d(s, o);
-      if (m != -INFINITY) {                                 // merge this batch into (M, S)
-        const double Mn = fmax(M, m);
-        S = ((M == -INFINITY) ? 0.0 : S * exp(M - Mn)) + s * exp(m - Mn);
-        M = Mn;
+      if (lane == 0) {
+        sM[c] = M;
+        sInvS[c] = 1.0 / S;
       }
     }
-    const double inv_s = 1.0 / S;
-#pragma unroll
-    for (int k = 0; k < kRelRunPer; ++k)
-      if (lane + 64 * k < nr) fac[gi * nrc + lane + 64 * k] = (rm[k] == -INFINITY) ? 0.0 : exp(rm[k] - M) * inv_s;
   }
   __syncthreads();
-
-  // ---- window mean over the W_q rows of every staged position --------------------
-  const double pad = (pool_mode == S4R_POOL_MAX) ? -INFINITY : 0.0;
-  const double inv_wq = 1.0 / Wq;
-  for (int g = 0; g < G; ++g) {
-    for (int i = t; i < span; i += blockDim.x) {
+  // ---- per-tile factors ---------------------------------------------------------------
+  if (t < ntl) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const float r4[4] = {rf[q].x, rf[q].y, rf[q].z, rf[q].w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = 4 * q + u;
+        fac[t][c] = (c < GW && r4[u] != -INFINITY) ? (float)(exp((double)r4[u] - sM[c]) * sInvS[c]) : 0.f;
+      }
+    }
+  }
+  __syncthreads();
+  // ---- window mean over the W_q rows of every staged position -------------------------
+  const float pad = (pool_mode == S4R_POOL_MAX) ? -INFINITY : 0.f;
+  const float inv_wq = 1.f / (float)Wq;
+#pragma unroll
+  for (int k = 0; k < PPT; ++k) {
+    const int i = t + k * kRelThreads;
+    if (i < span) {
       const int x = x0 + i;
-      const int xr = min(max(x, max(x0, 0)), L - 1) / kTileTok - r_first;
-      double sum = 0.0;
-      for (int wi = 0; wi < Wq; ++wi) {
-        const int gi = g * Wq + wi;
-        sum += (double)e_s[gi * SP + HP - h + i] * fac[gi * nrc + xr];
+      const bool in = x >= 0 && x < L;
+      const float* fr = fac[min(max(x, 0), L - 1) / kTileTok - tile_lo];
+      float ex[GWP];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        ex[4 * q] = ev[k][q].x;
+        ex[4 * q + 1] = ev[k][q].y;
+        ex[4 * q + 2] = ev[k][q].z;
+        ex[4 * q + 3] = ev[k][q].w;
       }
-      vs[g * span + i] = (x >= 0 && x < L) ? ((Wq == 1) ? sum : sum * inv_wq) : pad;
+      if constexpr (WQ1) {
+#pragma unroll
+        for (int c = 0; c < GWP; ++c)
+          if (c < G) vs[c * span + i] = in ? ex[c] * fr[c] : pad;
+      } else {
+        for (int g = 0; g < G; ++g) {
+          float sum = 0.f;
+#pragma unroll
+          for (int c = 0; c < GWP; ++c)
+            if (c >= g * Wq && c < (g + 1) * Wq) sum += ex[c] * fr[c];
+          vs[g * span + i] = in ? sum * inv_wq : pad;
+        }
+      }
     }
   }
   __syncthreads();
-
-  // ---- pooling (kappa) and aggregation over G, 2 outputs per thread -----------
-  const int own = t * kRelPerThr;                           // first output (chunk-relative)
-  double acc[kRelPerThr];
-#pragma unroll
-  for (int j = 0; j < kRelPerThr; ++j) acc[j] = (agg == S4R_AGG_MEAN) ? 0.0 : -INFINITY;
-  if (own < chunk) {
-    for (int g = 0; g < G; ++g) {
-      const double* v = vs + g * span + own;                // window of output j: v[j .. j + 2h]
-      double p[kRelPerThr];
-      switch (h) {
-        case 0: pool_window<0>(v, pool_mode, kappa, p); break;
-        case 1: pool_window<1>(v, pool_mode, kappa, p); break;
-        case 2: pool_window<2>(v, pool_mode, kappa, p); break;
-        case 3: pool_window<3>(v, pool_mode, kappa, p); break;
-        case 4: pool_window<4>(v, pool_mode, kappa, p); break;
-        default:
-#pragma unroll
-          for (int j = 0; j < kRelPerThr; ++j) {
-            double a = v[j];
-            for (int o = 1; o < kappa; ++o) a = (pool_mode == S4R_POOL_MAX) ? fmax(a, v[j + o]) : a + v[j + o];
-            p[j] = (pool_mode == S4R_POOL_MAX) ? a : a / kappa;
-          }
-      }
-#pragma unroll
-      for (int j = 0; j < kRelPerThr; ++j) acc[j] = (agg == S4R_AGG_MEAN) ? acc[j] + p[j] : fmax(acc[j], p[j]);
-    }
+  // ---- pooling (kappa, stride 1, same length) and aggregation over G -------------------
+  float af[TPT];
+  switch (h) {
+    case 0: pool_aggregate<0, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 1: pool_aggregate<1, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 2: pool_aggregate<2, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 3: pool_aggregate<3, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 4: pool_aggregate<4, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    default: pool_aggregate<-1, TPT, GWP>(vs, span, t, G, kappa, pool_mode, agg, af); break;
   }
 #pragma unroll
-  for (int j = 0; j < kRelPerThr; ++j) {
-    const int x = t0 + own + j;
-    const bool valid = own < chunk && x < L;
-    const float af = (float)((agg == S4R_AGG_MEAN) ? acc[j] / G : acc[j]);
-    if (valid) {
-      atilde[(int64_t)b * cap + x] = af;
-      if (scores_out) scores_out[(int64_t)b * L + x] = af;
+  for (int j = 0; j < TPT; ++j) {
+    const int x = t0 + t + j * kRelThreads;
+    if (x < L) {
+      atilde[(int64_t)b * cap + x] = af[j];
+      if (scores_out) scores_out[(int64_t)b * L + x] = af[j];
     }
-    if (valid && x < n_hist) atomicAdd(&hl[score_key(af) >> kHistShift], 1u);
+    if (x < n_hist) atomicAdd(&hl[score_key(af[j]) >> kHistShift], 1u);
   }
   __syncthreads();
   // this workgroup's histogram into the sequence's (zeroed by the query
   // projection earlier in the step): one global atomic per non-empty bin
   uint32_t* hs = hist + (int64_t)b * kHistBins;
-  for (int i = t; i < kHistBins; i += blockDim.x) {
+  for (int i = t; i < kHistBins; i += kRelThreads) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
   }
@@ -241,24 +280,34 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
   }
 }
 
-int relevance_chunk(int GW) { return GW <= 4 ? 2048 : (GW <= 8 ? 1024 : 512); }   // <= kRelThreads * kRelPerThr
+template <int NQ, int TPT>
+static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
+  const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
+  constexpr int chunk = kRelThreads * TPT;
+  const size_t lds = (size_t)P.G * (chunk + 2 * (P.kappa / 2)) * sizeof(float);
+  dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
+  auto kern = P.Wq == 1 ? k_relevance<NQ, TPT, true> : k_relevance<NQ, TPT, false>;
+  hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
+                     ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
+                     (int)(P.cap / kTileTok), score_workgroups(P, L));
+}
 
-size_t relevance_lds(int G, int GW, int chunk, int kappa) {
-  const int h = kappa / 2;
-  const int span = chunk + 2 * h;
-  const int SP = chunk + 2 * ((h + 3) & ~3);
-  const int nrc = chunk / kTileTok + 4;
-  return kHistBins * 4 + (size_t)(GW * nrc + (size_t)G * span) * 8 + (size_t)GW * SP * 4 + 16;
+template <int NQ>
+static void launch_rel_nq(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
+  switch (relevance_chunk(P.G)) {
+    case 1024: launch_rel_t<NQ, 4>(P, ws, L, scores_out, st); break;
+    case 512: launch_rel_t<NQ, 2>(P, ws, L, scores_out, st); break;
+    default: launch_rel_t<NQ, 1>(P, ws, L, scores_out, st); break;
+  }
 }
 
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
-  const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
-  const int chunk = relevance_chunk(P.GW);
-  const size_t lds = relevance_lds(P.G, P.GW, chunk, P.kappa);
-  dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
-  hipLaunchKernelGGL(k_relevance, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats, ws.atilde, ws.hist,
-                     scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), score_workgroups(P, L), chunk);
+  switch (gw_padded(P) / 4) {
+    case 1: launch_rel_nq<1>(P, ws, L, scores_out, st); break;
+    case 2: launch_rel_nq<2>(P, ws, L, scores_out, st); break;
+    case 3: launch_rel_nq<3>(P, ws, L, scores_out, st); break;
+    default: launch_rel_nq<4>(P, ws, L, scores_out, st); break;
+  }
   return hipGetLastError();
 }
 

@@ -37,8 +37,8 @@ struct Problem {
 
 struct Workspace {
   double* qpart;        // [B][row chunks][G][R] partial sums of the query coefficients
-  float* e;             // [B][GW][cap]   exp(z - run max), fp32
-  double* run_m;        // [B][GW][cap / 16] per-tile softmax reference (running max of z)
+  float* e;             // [B][cap][GWP]  exp(z - running max), fp32, token-major
+  float* run_m;         // [B][cap / 16][GWP] per-tile softmax reference (running max of z)
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   float* atilde;        // [B][cap]       relevance scores
   uint32_t* hist;       // [B][kHistBins]
@@ -57,11 +57,9 @@ Workspace carve_workspace(const Problem& P, void* base);
 int score_workgroups(const Problem& P, int64_t L);
 inline int64_t sel_groups_max(const Problem& P) { return (P.cap + kSelChunk - 1) / kSelChunk; }
 inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelChunk; }
-int relevance_chunk(int GW);
-inline int64_t rel_groups_max(const Problem& P) {
-  const int c = relevance_chunk(P.GW);
-  return (P.cap + c - 1) / c;
-}
+// query columns G * W_q rounded up to a multiple of 4 (one 16-byte group per
+// MFMA of the scoring kernel): the column stride of the exp values
+inline int gw_padded(const Problem& P) { return (P.GW + 3) / 4 * 4; }
 
 // ---- launchers (each returns hipGetLastError() after its launches) --------
 inline int project_chunks(const Problem& P) { return (P.Dg + kPChunk - 1) / kPChunk; }

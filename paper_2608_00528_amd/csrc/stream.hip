@@ -1,7 +1,8 @@
 // Section 3.2.2 latent logits on gfx950: k_score_stream streams C^K once (the
 // HBM-bound pass), Z = C^Q C^K^T / sqrt(R) on bf16 MFMA with per-block fp64
-// accumulation, and writes exp(z - run max), per-run (max, sum) and
-// per-workgroup (max, sum) statistics of the softmax over the length.
+// accumulation, and writes exp(z - running max) per token, the running max
+// per 16-token tile and per-workgroup (max, sum) statistics of the softmax
+// over the length.
 #include "s4r_device.h"
 #include "s4r_internal.h"
 
@@ -11,88 +12,106 @@ namespace s4r {
 // K1: the coefficient stream
 // ---------------------------------------------------------------------------
 // grid (workgroups per sequence, B), 256 threads = 4 waves.  A wave owns a
-// contiguous range of 16-token tiles; each 16x32 block of C^K is one
-// coalesced 1 KiB wave load that lands directly in MFMA A-operand layout, and
-// four tiles (bf16) are in flight per wave.  The B operand holds the
-// query-coefficient columns (G*W_q <= 16), as hi, mid and lo bf16 parts
-// accumulated into the same fp32 MFMA result, which is folded into fp64
-// after every 32-column block.  Each tile's exp values are taken against the
-// wave's running maximum of z (recorded per tile), so no z outlives its tile.
+// contiguous range of 16-token tiles.  Each 16x32 block of C^K is one
+// coalesced 1 KiB wave load that is used directly as the B operand of a
+// 16x16x32 bf16 MFMA (lane l: token l%16, latent columns 8*(l/16)..+7).  The A
+// operand holds the query-coefficient columns, four per MFMA, each as its
+// hi / mid / lo bf16 parts in rows 4*c + part (row 4*c + 3 is zero), so lane
+// (token t, k-group c) receives the three partial products of query column c
+// against token t.  The MFMA rounds once per instruction, like an fp32 sum
+// aligned to its largest term; the parts of every 32-column block are folded
+// into an fp64 accumulator, so z carries no fp32 accumulation across blocks.
+// Each tile's exp values are taken against the running maximum of z over the
+// wave's tiles (recorded per tile, fp32) with fp64 argument reduction, and
+// the running (max, sum) of every query column is kept per wave.
+
+// exp(x) for x <= 0 given in fp64: 2^(x log2 e) with the integer part split off
+// in fp64, the fraction evaluated by the hardware exp2 (relative error about
+// one fp32 ulp for any x)
+__device__ __forceinline__ float exp_neg_accurate(double x) {
+  const double y = x * 1.4426950408889634;
+  const double n = rint(y);
+  const float f = (float)(y - n);
+  return ldexpf(__builtin_amdgcn_exp2f(f), (int)fmax(n, -300.0));
+}
 
 template <typename T>
-struct ALoad;
+struct BLoad;
 
 template <>
-struct ALoad<uint16_t> {  // 8 bf16 = one 16-byte load
+struct BLoad<uint16_t> {  // 8 bf16 = one 16-byte streaming load
   static constexpr int kParts = 1;
   __device__ __forceinline__ static void load(const uint16_t* p, Op8 (&a)[1]) {
-    a[0].u = *reinterpret_cast<const uint4*>(p);
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    a[0].u = make_uint4(v.x, v.y, v.z, v.w);
   }
 };
 
 template <>
-struct ALoad<float> {  // 8 fp32 = two 16-byte loads, split into 3 bf16 parts
+struct BLoad<float> {  // 8 fp32 = two 16-byte streaming loads, split into 3 bf16 parts
   static constexpr int kParts = 3;
   __device__ __forceinline__ static void load(const float* p, Op8 (&a)[3]) {
-    float x[8];
-    *reinterpret_cast<float4*>(&x[0]) = *reinterpret_cast<const float4*>(p);
-    *reinterpret_cast<float4*>(&x[4]) = *reinterpret_cast<const float4*>(p + 4);
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const f32x4 u = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    const f32x4 w = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
+    const float x[8] = {u.x, u.y, u.z, u.w, w.x, w.y, w.z, w.w};
     split_f32x8(x, a[0], a[1], a[2]);
   }
 };
 
 // Loads are unconditional (the tile index is clamped to the last tile of the
 // sequence) so the compiler can count outstanding loads exactly and keep the
-// prefetched tile in flight while the current one is consumed.
+// prefetched tiles in flight while the current one is consumed.
 template <typename T, int RB>
-__device__ __forceinline__ void load_a_tile(const T* cb, int tile, int ntiles, int col, int kg,
-                                            Op8 (&a)[RB][ALoad<T>::kParts]) {
+__device__ __forceinline__ void load_b_tile(const T* cb, int tile, int ntiles, int slot, int kg,
+                                            Op8 (&a)[RB][BLoad<T>::kParts]) {
   constexpr int R = RB * kBlkCol;
-  const T* tp = cb + (int64_t)min(tile, ntiles - 1) * 16 * R + col * 32 + kg * 8;
+  const T* tp = cb + (int64_t)min(tile, ntiles - 1) * 16 * R + slot * 32 + kg * 8;
 #pragma unroll
-  for (int kb = 0; kb < RB; ++kb) ALoad<T>::load(tp + kb * 512, a[kb]);
+  for (int kb = 0; kb < RB; ++kb) BLoad<T>::load(tp + kb * 512, a[kb]);
 }
 
-template <typename T, int RB>
+template <typename T, int RB, int NM>
 __global__ __launch_bounds__(256, 2) void k_score_stream(
     const T* __restrict__ coef_k, const double* __restrict__ qpart, const float* __restrict__ qwin_prev,
-    float* __restrict__ qcoef_out, float* __restrict__ e_out, double* __restrict__ run_m,
+    float* __restrict__ qcoef_out, float* __restrict__ e_out, float* __restrict__ tref,
     double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int nch, int ntiles_cap, int tiles_per_wave,
     int nwg, double scale) {
   constexpr int R = RB * kBlkCol;
-  constexpr int NP = ALoad<T>::kParts;
+  constexpr int NP = BLoad<T>::kParts;
   const int b = blockIdx.y;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int col = lane & 15, kg = lane >> 4;       // MFMA column / k-group of this lane
+  const int slot = lane & 15, kg = lane >> 4;      // token slot / k-group (= query column within an MFMA)
   const int GW = G * Wq;
   const T* cb = coef_k + (int64_t)b * cap * R;
   const int ntiles = (L + 15) / 16;
 
-  // this wave's tiles; the count is a multiple of the prefetch depth and tiles
-  // past the sequence are computed on a clamped tile and masked.  The first
-  // tiles are requested before the query coefficients are prepared.
-  // tiles in flight per wave, as many as fit in 256 registers without spilling
-  constexpr int PF = (NP == 1) ? (RB <= 6 ? 4 : 2) : (RB <= 3 ? 2 : 1);
+  // tiles in flight per wave and whether the A operands stay in registers:
+  // as much as fits in 256 registers without spilling
+  constexpr bool A_REG = NM * RB * NP <= 10;
+  constexpr int PF = (NP == 1) ? ((NM <= 2 && RB * (A_REG ? 1 + NM / 2 : 1) <= 6) ? 4 : (NM * RB <= 16 ? 2 : 1))
+                                : ((NM <= 2 && RB <= 3) ? 2 : 1);
   const int tile0 = (blockIdx.x * kScoreWaves + wave) * tiles_per_wave;
   const int tile1 = min(tile0 + tiles_per_wave, ntiles);
-  Op8 abuf[PF][RB][NP];
+  Op8 bbuf[PF][RB][NP];
 #pragma unroll
-  for (int p = 0; p < PF; ++p) load_a_tile<T, RB>(cb, min(tile0 + p, tile1 - 1), ntiles, col, kg, abuf[p]);
+  for (int p = 0; p < PF; ++p) load_b_tile<T, RB>(cb, min(tile0 + p, tile1 - 1), ntiles, slot, kg, bbuf[p]);
 
-  // B operands: column gi = g * Wq + i holds query-coefficient row i of group
-  // g (oldest first).  The newest row is the sum of the projection's row-chunk
-  // partials (fixed order); older rows come from the caller.  Each value is
-  // split into hi, mid and lo bf16 parts, staged once per workgroup in LDS;
-  // rows are padded by 16 bytes so the 16-byte reads of one MFMA operand hit
-  // distinct banks.
-  constexpr int RS = R + 8;                        // padded row stride (elements)
-  __shared__ __align__(16) uint16_t bsh[3][16][RS];
+  // A operands: query column gi = g * Wq + i (row i of group g's window, oldest
+  // first) sits in MFMA m = gi / 4, rows 4 * (gi % 4) + part.  The newest row
+  // is the sum of the projection's row-chunk partials (fixed order); older
+  // rows come from the caller.  Staged once per workgroup in LDS (rows padded
+  // by 16 bytes so the 16-byte operand reads of one MFMA hit distinct banks).
+  constexpr int RS = R + 8;
+  __shared__ __align__(16) uint16_t qsh[NM][16][RS];
   {
     constexpr int K8 = R / 8;
-    for (int i = t; i < 3 * 16 * K8; i += blockDim.x) {   // zero columns >= GW
-      const int p = i / (16 * K8), c = (i / K8) % 16;
-      if (c >= GW) *reinterpret_cast<uint4*>(&bsh[p][c][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
+    for (int i = t; i < NM * 16 * K8; i += blockDim.x) {   // zero every row first
+      const int m = i / (16 * K8), r = (i / K8) % 16;
+      *reinterpret_cast<uint4*>(&qsh[m][r][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
     }
+    __syncthreads();
     const double* qp = qpart + (int64_t)b * nch * G * R;
     // older rows from the caller; with W_q = 1 there are none and the load
     // below re-reads a partial sum (unused) so it needs no branch
@@ -119,84 +138,100 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
           if (c < nch) x += part[u][c];
         if (wi < Wq - 1) x = (double)old[u];
         const Split3 sp = split3(x);
-        bsh[0][gi][r] = sp.hi;
-        bsh[1][gi][r] = sp.mid;
-        bsh[2][gi][r] = sp.lo;
+        const int m = gi >> 2, row = 4 * (gi & 3);
+        qsh[m][row + 0][r] = sp.hi;
+        qsh[m][row + 1][r] = sp.mid;
+        qsh[m][row + 2][r] = sp.lo;
         if (qcoef_out && blockIdx.x == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
       }
     }
     __syncthreads();
   }
-  auto bop = [&](int kb, int p) -> Op8 {
-    Op8 o;
-    o.u = *reinterpret_cast<const uint4*>(&bsh[p][col][kb * 32 + kg * 8]);
-    return o;
+  // the A operands stay in registers when they fit, else they are re-read from LDS
+  Op8 areg[A_REG ? NM : 1][A_REG ? RB : 1];
+  if constexpr (A_REG) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int kb = 0; kb < RB; ++kb) areg[m][kb].u = *reinterpret_cast<const uint4*>(&qsh[m][slot][kb * 32 + kg * 8]);
+  }
+  auto aop = [&](int m, int kb) -> Op8 {
+    if constexpr (A_REG) {
+      return areg[m][kb];
+    } else {
+      Op8 o;
+      o.u = *reinterpret_cast<const uint4*>(&qsh[m][slot][kb * 32 + kg * 8]);
+      return o;
+    }
   };
-  // causal limit of this column's query row (Section 3.2.2): keys l <= L - Wq + i
-  const int lim = (col < GW) ? (L - Wq + col % Wq) : -1;
 
-  double Mw = -INFINITY, Sw = 0.0;                 // running (max, sum) of column col over this wave's tiles
+  // per query column of this lane (gi = 4 m + kg): causal limit of its query
+  // row (Section 3.2.2: keys l <= L - Wq + i) and the running (max, sum)
+  int lim[NM];
+  float Mrun[NM];
+  double Srun[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    const int gi = 4 * m + kg;
+    lim[m] = (gi < GW) ? (L - Wq + gi % Wq) : -1;
+    Mrun[m] = -INFINITY;
+    Srun[m] = 0.0;
+  }
+
   for (int tb = tile0; tb < tile1; tb += PF) {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
       const int tile = tb + p;
-      double acc[4] = {0.0, 0.0, 0.0, 0.0};
+      double acc[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) acc[m] = 0.0;
 #pragma unroll
       for (int kb = 0; kb < RB; ++kb) {
-        floatx4 d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int pa = 0; pa < NP; ++pa) {
-          d = mfma16x16x32(abuf[p][kb][pa], bop(kb, 0), d);
-          d = mfma16x16x32(abuf[p][kb][pa], bop(kb, 1), d);
-          d = mfma16x16x32(abuf[p][kb][pa], bop(kb, 2), d);
+        for (int m = 0; m < NM; ++m) {
+          floatx4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int pb = 0; pb < NP; ++pb) d = mfma16x16x32(aop(m, kb), bbuf[p][kb][pb], d);
+          acc[m] += (double)d[0] + (double)(d[1] + d[2]);
         }
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[v] += (double)d[v];
       }
       // prefetch PF tiles ahead into the buffer just consumed (past the end of
       // this wave's range the load is a harmless re-read of its last tile)
-      load_a_tile<T, RB>(cb, min(tile + PF, tile1 - 1), ntiles, col, kg, abuf[p]);
-      double z[4];
-      double m = -INFINITY;
+      load_b_tile<T, RB>(cb, min(tile + PF, tile1 - 1), ntiles, slot, kg, bbuf[p]);
+      const int tok = tile * 16 + slot;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int tok = tile * 16 + kg * 4 + v;
-        z[v] = (tile < tile1 && tok <= lim && tok < L) ? acc[v] * scale : -INFINITY;
-        m = fmax(m, z[v]);
+      for (int m = 0; m < NM; ++m) {
+        const double z = (tile < tile1 && tok <= lim[m] && tok < L) ? acc[m] * scale : -INFINITY;
+        // running maximum over this wave's tiles (all 16 lanes of the row agree)
+        const float ref = fmaxf(slot_max16((float)z), Mrun[m]);
+        const float ev = (z == -INFINITY) ? 0.f : exp_neg_accurate(z - (double)ref);
+        const float ts = slot_sum16(ev);
+        // token-major stores: the wave's tile is one contiguous run of 16 * 4 * NM
+        // values (padding columns hold exp(-inf) = 0)
+        if (tile < tile1) {
+          e_out[((int64_t)b * cap + tok) * (4 * NM) + 4 * m + kg] = ev;
+          if (slot == 0) tref[((int64_t)b * ntiles_cap + tile) * (4 * NM) + 4 * m + kg] = ref;
+        }
+        if (ref > Mrun[m]) {                       // the running maximum grew
+          if (Mrun[m] != -INFINITY) Srun[m] *= (double)exp_neg_accurate((double)Mrun[m] - (double)ref);
+          Mrun[m] = ref;
+        }
+        Srun[m] += (double)ts;
       }
-      // tile maximum of this column (lanes col, col+16, col+32, col+48); the
-      // tile's exp values are taken against the running maximum, which is the
-      // reference recorded for the tile
-      m = fmax(m, shfl_xor_d(m, 16));
-      m = fmax(m, shfl_xor_d(m, 32));
-      const double ref = fmax(Mw, m);
-      float ev[4];
-      double s = 0.0;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        ev[v] = (z[v] == -INFINITY) ? 0.f : expf((float)(z[v] - ref));
-        s += (double)ev[v];
-      }
-      s += shfl_xor_d(s, 16);
-      s += shfl_xor_d(s, 32);
-      if (col < GW && tile < tile1) {
-        float* dst = e_out + ((int64_t)b * GW + col) * cap + (int64_t)tile * 16 + kg * 4;
-        *reinterpret_cast<float4*>(dst) = make_float4(ev[0], ev[1], ev[2], ev[3]);
-        if (kg == 0) run_m[((int64_t)b * GW + col) * ntiles_cap + tile] = ref;
-      }
-      if (ref > Mw && Mw != -INFINITY) Sw *= exp(Mw - ref);   // the running maximum grew
-      Sw += s;
-      Mw = ref;
     }
   }
   // workgroup statistics: the four waves' (max, sum) folded in a fixed order
-  __shared__ double wm[kScoreWaves][16], wsum[kScoreWaves][16];
-  if (kg == 0) {
-    wm[wave][col] = Mw;
-    wsum[wave][col] = Sw;
+  __shared__ double wm[kScoreWaves][kMaxGW], wsum[kScoreWaves][kMaxGW];
+  if (slot == 0) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      wm[wave][4 * m + kg] = (double)Mrun[m];
+      wsum[wave][4 * m + kg] = Srun[m];
+    }
   }
   __syncthreads();
-  if (wave == 0 && kg == 0 && col < GW) {
+  if (t < GW) {
+    const int col = t;
     double M = -INFINITY, S = 0.0;
     for (int w = 0; w < kScoreWaves; ++w) {
       const double mw = wm[w][col];
@@ -228,14 +263,25 @@ int score_workgroups(const Problem& P, int64_t L) {
   return (int)((ntiles + tpw * kScoreWaves - 1) / (tpw * kScoreWaves));
 }
 
+template <typename T, int RB, int NM>
+static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
+                             const float* qwin_prev, float* qcoef_out, hipStream_t st) {
+  const int tpw = tiles_per_wave(P, L);
+  const int nwg = score_workgroups(P, L);
+  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), dim3(nwg, P.B), dim3(256), 0, st, (const T*)coef_k, ws.qpart,
+                     qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
+                     (int)(P.cap / kTileTok), tpw, nwg, 1.0 / sqrt((double)P.R));
+}
+
 template <typename T, int RB>
 static void launch_stream_t(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
                             const float* qwin_prev, float* qcoef_out, hipStream_t st) {
-  const int tpw = tiles_per_wave(P, L);
-  const int nwg = score_workgroups(P, L);
-  hipLaunchKernelGGL((k_score_stream<T, RB>), dim3(nwg, P.B), dim3(256), 0, st, (const T*)coef_k, ws.qpart,
-                     qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
-                     (int)(P.cap / kTileTok), tpw, nwg, 1.0 / sqrt((double)P.R));
+  switch ((P.GW + 3) / 4) {
+    case 1: launch_stream_nm<T, RB, 1>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
+    case 2: launch_stream_nm<T, RB, 2>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
+    case 3: launch_stream_nm<T, RB, 3>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
+    default: launch_stream_nm<T, RB, 4>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
+  }
 }
 
 template <typename T>
