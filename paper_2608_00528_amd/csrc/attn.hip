@@ -305,6 +305,11 @@ bool launch_split_f32_128(const Problem&, const Workspace&, int64_t, int, int, i
 bool launch_split_f32_64(const Problem&, const Workspace&, int64_t, int, int, int, const void*, const void*,
                          const void*, const void*, const void*, hipStream_t);
 
+bool launch_tiles_bf16_128(const Problem&, const Workspace&, int64_t, int, int, const void*, const void*,
+                           const void*, const void*, const void*, hipStream_t, int*);
+bool launch_tiles_bf16_64(const Problem&, const Workspace&, int64_t, int, int, const void*, const void*,
+                          const void*, const void*, const void*, hipStream_t, int*);
+
 // which (G, rank) pairs the fused attention kernel is built for
 bool attention_supported(const Problem& P) {
   const int rb = P.rank / 32;
@@ -318,10 +323,17 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
                             const void* bases_k, const void* bases_v, const void* coef_k, const void* coef_v,
                             float* out, hipStream_t st, hipEvent_t* t0, hipEvent_t* t1) {
   const int n_proc = win_k ? k_eff : m;      // exact window rows go to the combine kernel
-  const int nsplit = choose_splits(P, n_proc);
+  int nsplit = choose_splits(P, n_proc);
   bool ok = true;
   if (t0 && hipEventRecord(t0[0], st) != hipSuccess) return hipErrorUnknown;
-  if (n_proc > 0) {
+  bool tiles = false;                        // bf16: the MFMA kernel when it covers the configuration
+  if (n_proc > 0 && P.dtype == S4R_BF16) {
+    int ns = 0;
+    tiles = P.dh == 128 ? launch_tiles_bf16_128(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns)
+                        : launch_tiles_bf16_64(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns);
+    if (tiles) nsplit = ns;
+  }
+  if (n_proc > 0 && !tiles) {
     if (P.dtype == S4R_BF16)
       ok = P.dh == 128 ? launch_split_bf16_128(P, ws, L, m, n_proc, nsplit, q, bases_k, bases_v, coef_k, coef_v, st)
                        : launch_split_bf16_64(P, ws, L, m, n_proc, nsplit, q, bases_k, bases_v, coef_k, coef_v, st);

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cmath>
+
 #include "s4r.h"
 
 namespace s4r {
@@ -60,6 +62,8 @@ inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelCh
 // query columns G * W_q rounded up to a multiple of 4 (one 16-byte group per
 // MFMA of the scoring kernel): the column stride of the exp values
 inline int gw_padded(const Problem& P) { return (P.GW + 3) / 4 * 4; }
+// RoPE: ratio of consecutive frequencies theta^(-2 / d_h) (0 when RoPE is off)
+inline double rope_ratio(const Problem& P) { return P.theta == 0.f ? 0.0 : pow((double)P.theta, -2.0 / P.dh); }
 
 // ---- launchers (each returns hipGetLastError() after its launches) --------
 inline int project_chunks(const Problem& P) { return (P.Dg + kPChunk - 1) / kPChunk; }
