@@ -112,8 +112,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
 enum Region {
-  kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits, kCand2,
-  kCandCount, kRegions
+  kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits,
+  kCandCount, kAboveCount, kSelInfo, kRegions
 };
 struct Layout {
   size_t off[kRegions];
@@ -128,15 +128,16 @@ Layout layout(const Problem& P) {
   sizes[kRunM] = B * (size_t)gw_padded(P) * P.nruns_max * 4;
   sizes[kWgStats] = B * GW * P.nwg_max * 2 * 8;
   sizes[kAtilde] = B * cap * 4;
-  sizes[kHist] = B * kHistBins * 4;
+  sizes[kHist] = B * 2 * kHistBins * 4;
   sizes[kCand] = B * cand_stride(P) * 8;
   sizes[kBitmap] = B * (cap / 32) * 4;
   sizes[kIdx] = B * P.m_max * 4;
   sizes[kPartMl] = B * P.hq * kMaxSplit * 2 * 4;
   sizes[kPartO] = B * P.hq * kMaxSplit * P.dh * 4;
   sizes[kAttnLogits] = B * P.hq * (P.s + P.m_max) * 4;
-  sizes[kCand2] = B * cand_stride(P) * 8;
   sizes[kCandCount] = B * sel_groups_max(P) * 4;
+  sizes[kAboveCount] = B * sel_groups_max(P) * 4;
+  sizes[kSelInfo] = B * 4 * 4;
   Layout l;
   size_t o = 0;
   for (int i = 0; i < kRegions; ++i) {
@@ -206,8 +207,9 @@ Workspace carve_workspace(const Problem& P, void* base) {
   w.part_ml = (float*)(b + l.off[kPartMl]);
   w.part_o = (float*)(b + l.off[kPartO]);
   w.attn_logits = (float*)(b + l.off[kAttnLogits]);
-  w.cand2 = (uint64_t*)(b + l.off[kCand2]);
   w.cand_count = (uint32_t*)(b + l.off[kCandCount]);
+  w.above_count = (uint32_t*)(b + l.off[kAboveCount]);
+  w.sel_info = (uint32_t*)(b + l.off[kSelInfo]);
   w.total = l.total;
   return w;
 }

@@ -26,14 +26,20 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 // combine: sinks, exact window, splits -> O_t
 // ---------------------------------------------------------------------------
+// One workgroup per (query head, sequence).  Every split's (max, sum, output)
+// is requested up front (thread t holds output dim t % d_h of splits
+// t / d_h, t / d_h + 256 / d_h, ...), the extra full-precision tokens (sinks,
+// optional exact window) are attended on the VALU with the same fixed-point
+// RoPE phases, and the partials are merged with the usual max rescaling.
 constexpr int kMaxExtra = 1024 + 64;   // sinks + exact window rows
+constexpr int kCombPer = kMaxSplit * 128 / 256;   // split outputs per thread
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_combine(
     const T* __restrict__ q, const T* __restrict__ sink_k, const T* __restrict__ sink_v,
     const T* __restrict__ win_k, const T* __restrict__ win_v, const float* __restrict__ part_ml,
     const float* __restrict__ part_o, float* __restrict__ out, int nsplit, int hq, int hkv, int dh,
-    int s_sink, int W, int64_t L, float theta) {
+    int s_sink, int W, int64_t L, double rope_ratio) {
   const int h = blockIdx.x, b = blockIdx.y;
   const int G = hq / hkv, j = h / G;
   const int Dp = hkv * dh;
@@ -42,13 +48,28 @@ __global__ __launch_bounds__(256) void k_attn_combine(
   const int n_win = win_k ? (int)min<int64_t>(W, L) : 0;
   const int n_extra = s_sink + n_win;
   const int half = dh / 2;
+  const int64_t pb = ((int64_t)b * hq + h) * kMaxSplit;
 
   __shared__ float qr[128];
-  __shared__ double rfs[64];
+  __shared__ uint64_t fq[64];
   __shared__ float lg[kMaxExtra];
+  __shared__ float s_as[kMaxSplit], s_ls[kMaxSplit];
   __shared__ float red[256];
-  __shared__ float s_mx, s_sum;
+  __shared__ float s_me, s_le, s_den, s_ae;
 
+  // ---- every load of the split partials and the query, issued together -----------------
+  const int ne = nsplit * dh;
+  float po[kCombPer];
+#pragma unroll
+  for (int i = 0; i < kCombPer; ++i) po[i] = (ne > 0) ? part_o[pb * dh + min(t + 256 * i, ne - 1)] : 0.f;
+  float2 ml = make_float2(-INFINITY, 0.f);
+  if (t < nsplit) ml = reinterpret_cast<const float2*>(part_ml)[pb + t];
+  float xl = 0.f, xh = 0.f;
+  if (t < half) {
+    const int64_t qo = ((int64_t)b * hq + h) * dh;
+    xl = load_elem(q, qo + t);
+    xh = load_elem(q, qo + t + half);
+  }
   auto krow = [&](int e) -> const T* {
     if (e < s_sink) return sink_k + ((int64_t)b * s_sink + e) * Dp + (int64_t)j * dh;
     return win_k + ((int64_t)b * W + (W - n_win) + (e - s_sink)) * Dp + (int64_t)j * dh;
@@ -59,84 +80,85 @@ __global__ __launch_bounds__(256) void k_attn_combine(
   };
   auto kpos = [&](int e) -> int64_t { return e < s_sink ? (int64_t)e : (int64_t)s_sink + (L - n_win) + (e - s_sink); };
 
+  // ---- rotated query ----------------------------------------------------------------------
   if (t < half) {
-    rfs[t] = rope_rev_freq(theta, t, dh);
+    uint64_t F[4];
+    rope_freqs_fixed(rope_ratio, t, F);
+    fq[t] = F[0];
     float c, sn;
-    rope_cs(pos_q, rfs[t], c, sn);
-    const int64_t qo = ((int64_t)b * hq + h) * dh;
-    const float xl = load_elem(q, qo + t), xh = load_elem(q, qo + t + half);
+    rope_cs_fixed(pos_q, F[0], c, sn);
     qr[t] = xl * c - xh * sn;
     qr[t + half] = xh * c + xl * sn;
   }
   __syncthreads();
-  // logits of the full-precision tokens, one wave per token, lane = RoPE pair
-  for (int e = wave; e < n_extra; e += blockDim.x / 64) {
+  // ---- logits of the full-precision tokens: one wave per token, lane = RoPE pair ---------
+  for (int e = wave; e < n_extra; e += 4) {
     float part = 0.f;
     if (lane < half) {
       const T* kp = krow(e);
-      const float xl = load_elem(kp, lane), xh = load_elem(kp, lane + half);
+      const float kl = load_elem(kp, lane), kh = load_elem(kp, lane + half);
       float c, sn;
-      rope_cs(kpos(e), rfs[lane], c, sn);
-      part = qr[lane] * (xl * c - xh * sn) + qr[lane + half] * (xh * c + xl * sn);
+      rope_cs_fixed(kpos(e), fq[lane], c, sn);
+      part = qr[lane] * (kl * c - kh * sn) + qr[lane + half] * (kh * c + kl * sn);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) part += shfl_xor_f(part, o);
     if (lane == 0) lg[e] = part / sqrtf((float)dh);
   }
   __syncthreads();
-  // max / sum of the extra tokens
-  float mx = -INFINITY;
-  for (int e = t; e < n_extra; e += blockDim.x) mx = fmaxf(mx, lg[e]);
-  red[t] = mx;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (t < o) red[t] = fmaxf(red[t], red[t + o]);
-    __syncthreads();
-  }
-  if (t == 0) s_mx = red[0];
-  __syncthreads();
-  const float m_e = s_mx;
-  float sm = 0.f;
-  for (int e = t; e < n_extra; e += blockDim.x) sm += __expf(lg[e] - m_e);
-  red[t] = sm;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (t < o) red[t] += red[t + o];
-    __syncthreads();
-  }
-  if (t == 0) s_sum = red[0];
-  __syncthreads();
-  const float l_e = s_sum;
-
-  // global max over the extra tokens and the splits
-  const int64_t pb = ((int64_t)b * hq + h) * kMaxSplit;
-  __shared__ float sml[kMaxSplit][2];
-  if (t < nsplit) {
-    sml[t][0] = part_ml[(pb + t) * 2];
-    sml[t][1] = part_ml[(pb + t) * 2 + 1];
+  // ---- (max, sum) of the extra tokens, global maximum, split weights (wave 0) ------------
+  if (wave == 0) {
+    float mx = -INFINITY;
+    for (int e = lane; e < n_extra; e += 64) mx = fmaxf(mx, lg[e]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, shfl_xor_f(mx, o));
+    float sm = 0.f;
+    for (int e = lane; e < n_extra; e += 64) sm += __expf(lg[e] - mx);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sm += shfl_xor_f(sm, o);
+    float M = mx;
+    float ms = (lane < nsplit) ? ml.x : -INFINITY;
+    float m2 = ms;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m2 = fmaxf(m2, shfl_xor_f(m2, o));
+    M = fmaxf(M, m2);
+    if (lane == 0) {
+      s_me = mx;
+      s_le = sm;
+      s_ae = (n_extra > 0) ? __expf(mx - M) : 0.f;
+    }
+    const float a = (lane < nsplit && ms != -INFINITY) ? __expf(ms - M) : 0.f;   // empty split: weight 0
+    if (lane < kMaxSplit) {
+      s_as[lane] = a;
+      s_ls[lane] = (lane < nsplit) ? ml.y : 0.f;
+    }
   }
   __syncthreads();
-  float M = m_e;
-  for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, sml[sp][0]);
+  if (t == 0) {
+    float den = s_ae * s_le;
+    for (int sp = 0; sp < nsplit; ++sp) den += s_as[sp] * s_ls[sp];
+    s_den = den;
+  }
+  // ---- weighted split outputs: thread t holds dim t % dh --------------------------------
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < kCombPer; ++i) {
+    const int e = t + 256 * i;
+    if (e < ne) acc += po[i] * s_as[e / dh];
+  }
+  red[t] = acc;
+  __syncthreads();
   if (t < dh) {
-    const int d = t;
-    float num = 0.f, den = 0.f;
+    float num = 0.f;
+    for (int k = t; k < 256; k += dh) num += red[k];
     if (n_extra > 0) {
-      const float a = __expf(m_e - M);
+      const float me = s_me;
       float o = 0.f;
 #pragma unroll 4
-      for (int e = 0; e < n_extra; ++e) o = fmaf(__expf(lg[e] - m_e), load_elem(vrow(e), d), o);
-      num += o * a;
-      den += l_e * a;
+      for (int e = 0; e < n_extra; ++e) o = fmaf(__expf(lg[e] - me), load_elem(vrow(e), t), o);
+      num += o * s_ae;
     }
-#pragma unroll 8
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float ms = sml[sp][0];
-      const float a = (ms == -INFINITY) ? 0.f : __expf(ms - M);   // empty split: weight 0
-      num += part_o[(pb + sp) * dh + d] * a;
-      den += sml[sp][1] * a;
-    }
-    out[((int64_t)b * hq + h) * dh + d] = num / den;
+    out[((int64_t)b * hq + h) * dh + t] = num / s_den;
   }
 }
 
@@ -349,11 +371,11 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
     hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q,
                        (const uint16_t*)sink_k, (const uint16_t*)sink_v, (const uint16_t*)win_k,
                        (const uint16_t*)win_v, ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L,
-                       P.theta);
+                       rope_ratio(P));
   else
     hipLaunchKernelGGL(k_attn_combine<float>, dim3(P.hq, P.B), dim3(256), 0, st, (const float*)q,
                        (const float*)sink_k, (const float*)sink_v, (const float*)win_k, (const float*)win_v,
-                       ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L, P.theta);
+                       ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P));
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && t1) e = hipEventRecord(t1[1], st);
   return e;

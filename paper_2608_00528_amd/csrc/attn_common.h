@@ -22,6 +22,33 @@ __device__ __forceinline__ void rope_cs(int64_t pos, double rev_freq, float& c, 
   s = __builtin_amdgcn_sinf(x);
 }
 
+// RoPE phase of integer position pos at a frequency given as a 0.64
+// fixed-point number of revolutions per position: the fractional revolution
+// pos * F mod 1 is exact in 64-bit integer arithmetic
+__device__ __forceinline__ void rope_cs_fixed(int64_t pos, uint64_t F, float& c, float& s) {
+  const uint64_t frac = (uint64_t)pos * F;
+  const float x = (float)(uint32_t)(frac >> 40) * 5.9604644775390625e-08f;   // 2^-24
+  c = __builtin_amdgcn_cosf(x);
+  s = __builtin_amdgcn_sinf(x);
+}
+// revolutions per position of frequencies f0 .. f0 + 3, as 0.64 fixed point:
+// theta^(-2 f / d_h) / (2 pi) = ratio^f / (2 pi) with ratio = theta^(-2 / d_h)
+// (computed once on the host in fp64; ratio 0 disables RoPE).  ratio^f0 by
+// repeated squaring: about 2^-50 relative, so the phase stays exact to about
+// 2^-32 revolutions for any position below 2^18.
+__device__ __forceinline__ void rope_freqs_fixed(double ratio, int f0, uint64_t (&F)[4]) {
+  double p = 1.0, base = ratio;
+  for (int e = f0; e > 0; e >>= 1) {
+    if (e & 1) p *= base;
+    base *= base;
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    F[v] = (ratio == 0.0) ? 0ull : (uint64_t)(p * 0.15915494309189535 * 18446744073709551616.0);
+    p *= ratio;
+  }
+}
+
 // operand loaders: 8 consecutive elements -> bf16 parts
 template <typename T>
 struct Parts;

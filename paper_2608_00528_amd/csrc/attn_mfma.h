@@ -1,9 +1,10 @@
 // Fused sparse reconstruction + split attention for bf16 storage on gfx950
 // (Section 3.2.3): every contraction on bf16 MFMA, every gather issued up front.
 //
-// One workgroup per (split, KV head j, sequence), NW = d_h / 32 waves, TPW
-// tiles of 16 selected tokens.  The work items are laid out over a 1-D grid
-// so that the KV heads of one (sequence, split) land on the same XCD
+// One workgroup per (split, HPW KV heads, sequence), NW = d_h / 32 waves,
+// TPW tiles of 16 selected tokens; HPW heads of one basis group reuse the
+// gathered rows.  The work items are laid out over a 1-D grid so
+// that the workgroups of one (sequence, split) land on the same XCD
 // (workgroup i runs on XCD i % 8): the gathered coefficient rows are then
 // fetched from HBM once per XCD and re-read from its L2 by the other heads.
 //
@@ -36,33 +37,6 @@
 
 namespace s4r {
 
-// RoPE phase of integer position pos at a frequency given as a 0.64
-// fixed-point number of revolutions per position: the fractional revolution
-// pos * F mod 1 is exact in 64-bit integer arithmetic
-__device__ __forceinline__ void rope_cs_fixed(int64_t pos, uint64_t F, float& c, float& s) {
-  const uint64_t frac = (uint64_t)pos * F;
-  const float x = (float)(uint32_t)(frac >> 40) * 5.9604644775390625e-08f;   // 2^-24
-  c = __builtin_amdgcn_cosf(x);
-  s = __builtin_amdgcn_sinf(x);
-}
-// revolutions per position of frequencies f0 .. f0 + 3, as 0.64 fixed point:
-// theta^(-2 f / d_h) / (2 pi) = ratio^f / (2 pi) with ratio = theta^(-2 / d_h)
-// (computed once on the host in fp64; ratio 0 disables RoPE).  ratio^f0 by
-// repeated squaring: about 2^-50 relative, so the phase stays exact to about
-// 2^-32 revolutions for any position below 2^18.
-__device__ __forceinline__ void rope_freqs_fixed(double ratio, int f0, uint64_t (&F)[4]) {
-  double p = 1.0, base = ratio;
-  for (int e = f0; e > 0; e >>= 1) {
-    if (e & 1) p *= base;
-    base *= base;
-  }
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    F[v] = (ratio == 0.0) ? 0ull : (uint64_t)(p * 0.15915494309189535 * 18446744073709551616.0);
-    p *= ratio;
-  }
-}
-
 // two fp32 values -> packed bf16 (round to nearest even; one v_cvt_pk_bf16_f32)
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -85,8 +59,15 @@ __device__ __forceinline__ void split2_f32x8(const float* x, Op8& hi, Op8& lo) {
   lo.u = make_uint4(pl[0], pl[1], pl[2], pl[3]);
 }
 
-template <int RBH, int NW, int NMH, int TPW>
-__global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
+// occupancy target: three workgroups per CU (at most 168 registers per lane)
+// where the gathered rows of three fit in LDS, else two
+template <int RBH, int TPW>
+constexpr int attn_tiles_waves_per_simd() {
+  return (RBH <= 5 && 3 * 2 * TPW * RBH * 1024 <= 150 * 1024) ? 3 : 2;
+}
+
+template <int RBH, int NW, int NMH, int TPW, int HPW>
+__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) void k_attn_tiles(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ bases_k, const uint16_t* __restrict__ bases_v,
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int nsplit, int ngroups,
@@ -94,19 +75,20 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
     double rope_ratio) {
   constexpr int DH = NW * 32;                      // NMH = ceil(G / 4): 4 heads per MFMA row group
   static_assert(TPW % 2 == 0, "tiles are processed in pairs");
-  // ---- work item: the KV heads of group (sequence, split) share an XCD ----------------
+  // ---- work item: HPW consecutive KV heads of group (sequence, split); the
+  // workgroups of one group share an XCD ---------------------------------------------------
   const int id = blockIdx.x;
+  const int nhp = hkv / HPW;
   const int xcd = id & 7, r8 = id >> 3;
-  const int j = r8 % hkv;
-  const int grp_id = (r8 / hkv) * 8 + xcd;
+  const int hp = r8 % nhp;
+  const int grp_id = (r8 / nhp) * 8 + xcd;
   if (grp_id >= ngroups) return;
   const int b = grp_id / nsplit, split = grp_id % nsplit;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = lane & 15, kg = lane >> 4;
   const int Dp = hkv * DH, Dg = Dp / nb;
-  const int bgrp = j / (hkv / nb);
-  const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
+  const int bgrp = (hp * HPW) / (hkv / nb);        // the HPW heads share one basis group
   const int kb0 = bgrp * rank / 32;                // first latent block of the group
   const int tile0 = split * TPW;
   const int ntile = (n_proc + 15) / 16;
@@ -122,33 +104,13 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
   const int32_t* idx = idx_all + (int64_t)b * idx_stride;
   for (int i = threadIdx.x; i < TPW * 16; i += NW * 64)
     sidx[i] = (tile0 * 16 + i < n_proc) ? idx[tile0 * 16 + i] : -1;
-  // bases (registers, requested while the index list arrives): A operands of
-  // K^ (row = dim) and B operands of V^ (column = dim) read the same 16 bytes
-  const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
-  Op8 bk[2][RBH], bv[2][RBH];
-#pragma unroll
-  for (int m = 0; m < 2; ++m) {
-    const int d = 16 * (w + m * NW) + slot;
-#pragma unroll
-    for (int kb = 0; kb < RBH; ++kb) {
-      const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
-      bk[m][kb].u = *reinterpret_cast<const uint4*>(bases_k + o);
-      bv[m][kb].u = *reinterpret_cast<const uint4*>(bases_v + o);
-    }
-  }
   // the query dims of this lane's k-group: f_v = 16 w + 4 kg + v and f_v + d_h / 2
   const int fq = 16 * w + 4 * kg;
-  uint2 qlo[NMH], qhi[NMH];
-#pragma unroll
-  for (int mh = 0; mh < NMH; ++mh) {
-    const int h = min(4 * mh + (slot >> 2), G - 1);
-    const uint16_t* qp = q + ((int64_t)b * hq + (int64_t)j * G + h) * DH + fq;
-    qlo[mh] = *reinterpret_cast<const uint2*>(qp);
-    qhi[mh] = *reinterpret_cast<const uint2*>(qp + DH / 2);
-  }
   uint64_t Ff[4];
   rope_freqs_fixed(rope_ratio, fq, Ff);
-  lds_barrier();                                   // sidx visible; basis and query loads stay in flight
+  const int64_t pos_q = s_sink + L - 1;
+  const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
+  lds_barrier();                                   // sidx visible
   {
     const uint16_t* ckb = coef_k + (int64_t)b * cap * R;
     const uint16_t* cvb = coef_v + (int64_t)b * cap * R;
@@ -169,8 +131,33 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
       }
     }
   }
+  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
+
+  for (int jj = 0; jj < HPW; ++jj) {
+  const int j = hp * HPW + jj;
+  const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
+  // bases (registers): A operands of K^ (row = dim) and B operands of V^
+  // (column = dim) read the same 16 bytes
+  Op8 bk[2][RBH], bv[2][RBH];
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const int d = 16 * (w + m * NW) + slot;
+#pragma unroll
+    for (int kb = 0; kb < RBH; ++kb) {
+      const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
+      bk[m][kb].u = *reinterpret_cast<const uint4*>(bases_k + o);
+      bv[m][kb].u = *reinterpret_cast<const uint4*>(bases_v + o);
+    }
+  }
+  uint2 qlo[NMH], qhi[NMH];
+#pragma unroll
+  for (int mh = 0; mh < NMH; ++mh) {
+    const int h = min(4 * mh + (slot >> 2), G - 1);
+    const uint16_t* qp = q + ((int64_t)b * hq + (int64_t)j * G + h) * DH + fq;
+    qlo[mh] = *reinterpret_cast<const uint2*>(qp);
+    qhi[mh] = *reinterpret_cast<const uint2*>(qp + DH / 2);
+  }
   // ---- 2. rotated query as the A operand of the logits (overlaps the gathers) ------------
-  const int64_t pos_q = s_sink + L - 1;
   Op8 aq[NMH];
   {
     const int part = slot & 3;
@@ -193,7 +180,6 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
       aq[mh].u = live ? (part == 0 ? hi.u : lo.u) : make_uint4(0, 0, 0, 0);
     }
   }
-  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
   float Mrun[NMH], lrun[NMH];
   floatx4 oacc[NMH][2];
 #pragma unroll
@@ -203,8 +189,10 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
     oacc[mh][0] = floatx4{0.f, 0.f, 0.f, 0.f};
     oacc[mh][1] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
-  __builtin_amdgcn_s_waitcnt(0);                   // this wave's gathers have landed
-  __syncthreads();                                 // everyone's
+  if (jj == 0) {
+    __builtin_amdgcn_s_waitcnt(0);                 // this wave's gathers have landed
+    __syncthreads();                               // everyone's
+  }
 
   // ---- 3-5. tile pairs ----------------------------------------------------------------
   for (int tp = 0; tp < nt; tp += 2) {
@@ -336,6 +324,7 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_tiles(
       for (int m = 0; m < 2; ++m) part_o[pb * DH + 16 * (w + m * NW) + slot] = oacc[mh][m][0] + oacc[mh][m][1];
     }
   }
+  }   // heads of the workgroup
 }
 
 }  // namespace s4r
@@ -345,19 +334,29 @@ namespace s4r {
 // which configurations the MFMA attention kernel covers (bf16 storage)
 inline int attn_tiles_per_wg(int ntile) { return ntile <= kMaxSplit * 4 ? 4 : (ntile <= kMaxSplit * 8 ? 8 : 0); }
 
-template <int RBH, int NW, int NMH, int TPW>
-static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
+template <int RBH, int NW, int NMH, int TPW, int HPW>
+static void launch_tiles_h(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
                            const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
                            int* nsplit_out) {
   const int ntile = (n_proc + 15) / 16;
   const int nsplit = (ntile + TPW - 1) / TPW;
   const int ngroups = P.B * nsplit;
-  const int nwg = 8 * P.hkv * ((ngroups + 7) / 8);
-  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH, TPW>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
+  const int nwg = 8 * (P.hkv / HPW) * ((ngroups + 7) / 8);
+  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH, TPW, HPW>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
                      (const uint16_t*)bk, (const uint16_t*)bv, (const uint16_t*)ck, (const uint16_t*)cv, ws.idx,
                      (int64_t)m, ws.part_ml, ws.part_o, n_proc, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb, P.rank, P.R,
                      P.s, L, P.cap, P.bases_shared, rope_ratio(P));
   *nsplit_out = nsplit;
+}
+
+// one KV head per workgroup: a workgroup that walks two heads over the same
+// gathered rows halves the gather traffic but doubles its critical path, and
+// measured slower on MI355X (the HPW parameter keeps that variant available)
+template <int RBH, int NW, int NMH, int TPW>
+static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
+                           const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
+                           int* nsplit_out) {
+  launch_tiles_h<RBH, NW, NMH, TPW, 1>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, nsplit_out);
 }
 
 template <int NW, int NMH, int TPW>

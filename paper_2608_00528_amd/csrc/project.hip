@@ -121,10 +121,10 @@ __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, 
   const int grp = c0 / rank;                      // its basis group
   const int r0 = ch * kPChunk;                    // first row of the chunk in the group
   const int nrow = min(kPChunk, Dg - r0);
-  // the step's selection histogram starts from zero (the relevance kernel
-  // adds to it later in the step)
+  // the step's two selection histograms start from zero (the relevance and
+  // classify kernels add to them later in the step)
   if (cblk == 0 && ch == 0)
-    for (int i = t; i < kHistBins; i += blockDim.x) hist[(int64_t)b * kHistBins + i] = 0u;
+    for (int i = t; i < 2 * kHistBins; i += blockDim.x) hist[(int64_t)b * 2 * kHistBins + i] = 0u;
 
   __shared__ float xs[kMaxGW][kPChunk];
   __shared__ double red[4][kPVec][32];

@@ -247,7 +247,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   __syncthreads();
   // this workgroup's histogram into the sequence's (zeroed by the query
   // projection earlier in the step): one global atomic per non-empty bin
-  uint32_t* hs = hist + (int64_t)b * kHistBins;
+  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
   for (int i = t; i < kHistBins; i += kRelThreads) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
@@ -273,7 +273,7 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
     if (x < n_hist) atomicAdd(&hl[score_key(scores[(int64_t)b * L + x]) >> kHistShift], 1u);
   }
   __syncthreads();
-  uint32_t* hs = hist + (int64_t)b * kHistBins;
+  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
@@ -314,7 +314,8 @@ hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, fl
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores, hipStream_t st) {
   const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
   const int ng = std::max(1, (n_hist + kHistChunk - 1) / kHistChunk);
-  hipLaunchKernelGGL(k_zero_hist, dim3((P.B * kHistBins + 255) / 256), dim3(256), 0, st, ws.hist, P.B * kHistBins);
+  hipLaunchKernelGGL(k_zero_hist, dim3((P.B * 2 * kHistBins + 255) / 256), dim3(256), 0, st, ws.hist,
+                     P.B * 2 * kHistBins);
   hipLaunchKernelGGL(k_hist_scores, dim3(ng, P.B), dim3(256), 0, st, scores, ws.hist, (int)L, n_hist);
   return hipGetLastError();
 }

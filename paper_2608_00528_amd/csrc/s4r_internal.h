@@ -16,7 +16,6 @@ constexpr int kHistBins = 2048;       // top-11-bit radix histogram of the score
 constexpr int kHistShift = 21;
 constexpr int kHistChunk = 2048;      // tokens per histogram workgroup (standalone selection)
 constexpr int kSelChunk = 2048;       // tokens per selection workgroup (multiple of 32)
-constexpr int kCandCap = 4096;        // boundary candidates sorted in LDS
 constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capacity <= 4096 * kSelChunk)
 constexpr int kMaxSplit = 64;         // attention splits per (sequence, kv head)
 constexpr int kMaxTilesPerSplit = 512; // 16-token tiles per split (index list staged in LDS)
@@ -43,10 +42,11 @@ struct Workspace {
   float* run_m;         // [B][cap / 16][GWP] per-tile softmax reference (running max of z)
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   float* atilde;        // [B][cap]       relevance scores
-  uint32_t* hist;       // [B][kHistBins]
+  uint32_t* hist;       // [B][2][kHistBins]  selection histograms: top 11 key bits, next 11 of the boundary bin
   uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)
-  uint64_t* cand2;      // [B][cand_stride]  compacted candidates (radix fallback)
   uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
+  uint32_t* above_count; // [B][sel_groups_max] positions above the boundary bin per classify workgroup
+  uint32_t* sel_info;   // [B][4] boundary bin and the count above it
   uint32_t* bitmap;     // [B][cap / 32]  selected global positions
   int32_t* idx;         // [B][m_max]
   float* part_ml;       // [B][hq][kMaxSplit][2]   split partial (max, sum)
