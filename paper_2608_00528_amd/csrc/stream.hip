@@ -111,7 +111,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
       const int m = i / (16 * K8), r = (i / K8) % 16;
       *reinterpret_cast<uint4*>(&qsh[m][r][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
     }
-    __syncthreads();
+    lds_barrier();
     const double* qp = qpart + (int64_t)b * nch * G * R;
     // older rows from the caller; with W_q = 1 there are none and the load
     // below re-reads a partial sum (unused) so it needs no branch
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
         if (qcoef_out && blockIdx.x == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
       }
     }
-    __syncthreads();
+    lds_barrier();                                 // the tiles requested above stay in flight
   }
   // the A operands stay in registers when they fit, else they are re-read from LDS
   Op8 areg[A_REG ? NM : 1][A_REG ? RB : 1];
