@@ -248,8 +248,9 @@ def main():
     except Exception as exc:   # capture unsupported here: report eager numbers only
         log(f"[bench] graph capture failed: {exc}")
 
-    # achievable read bandwidth over the same bytes: the library's plain
-    # 16-byte streaming read of one C^K replica per launch, rotating replicas
+    # achievable read bandwidth over the same bytes: the library's read
+    # reference (one contiguous range per workgroup, non-temporal 16-byte
+    # loads) over one C^K replica per launch, rotating replicas
     cks = [r[0] for r in replicas]
     sink = None
     for r in range(N_REPLICAS):
@@ -264,7 +265,7 @@ def main():
     r1.record(stream)
     torch.cuda.synchronize()
     read_gbps = cks[0].numel() * cks[0].element_size() * nrd / (r0.elapsed_time(r1) * 1e-3) / 1e9
-    log(f"[bench] read ceiling (plain 16-byte stream over C^K): {read_gbps:.0f} GB/s")
+    log(f"[bench] read ceiling (contiguous non-temporal 16-byte stream over C^K): {read_gbps:.0f} GB/s")
 
     # per-kernel pass (events between kernels), same steps again
     nk = min(args.steps, 200)
