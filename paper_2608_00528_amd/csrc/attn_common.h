@@ -26,8 +26,11 @@ __device__ __forceinline__ void rope_cs(int64_t pos, double rev_freq, float& c, 
 // fixed-point number of revolutions per position: the fractional revolution
 // pos * F mod 1 is exact in 64-bit integer arithmetic
 __device__ __forceinline__ void rope_cs_fixed(int64_t pos, uint64_t F, float& c, float& s) {
-  const uint64_t frac = (uint64_t)pos * F;
-  const float x = (float)(uint32_t)(frac >> 40) * 5.9604644775390625e-08f;   // 2^-24
+  // high word of the low 64 bits of pos * F (positions are below 2^31): two
+  // 32-bit multiplies and an add
+  const uint32_t p = (uint32_t)pos, flo = (uint32_t)F, fhi = (uint32_t)(F >> 32);
+  const uint32_t hi = (uint32_t)(((uint64_t)p * flo) >> 32) + p * fhi;
+  const float x = (float)(hi >> 8) * 5.9604644775390625e-08f;   // top 24 bits, 2^-24 revolutions
   c = __builtin_amdgcn_cosf(x);
   s = __builtin_amdgcn_sinf(x);
 }

@@ -112,22 +112,27 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
   const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
   lds_barrier();                                   // sidx visible
   {
-    const uint16_t* ckb = coef_k + (int64_t)b * cap * R;
-    const uint16_t* cvb = coef_v + (int64_t)b * cap * R;
-    constexpr int NLOAD = 2 * TPW * RBH;           // wave loads of 1 KiB
+    // wave w gathers tiles w, w + NW, ...: per tile one row offset, then the
+    // 2 x RBH wave loads of 1 KiB at constant distances
+    const uint16_t* ckb = coef_k + (int64_t)b * cap * R + (int64_t)kb0 * 512;
+    const uint16_t* cvb = coef_v + (int64_t)b * cap * R + (int64_t)kb0 * 512;
     const int tq = lane >> 2, quarter = lane & 3;
 #pragma unroll
-    for (int i0 = 0; i0 < NLOAD; i0 += NW) {
-      const int i = i0 + w;
-      if (i < NLOAD) {                             // wave-uniform
-        const int which = i / (TPW * RBH), rem = i % (TPW * RBH);
-        const int t = rem / RBH, kb = rem % RBH;
+    for (int t0 = 0; t0 < TPW; t0 += NW) {
+      const int t = t0 + w;
+      if (t < TPW) {                               // wave-uniform
         const int32_t x = sidx[t * 16 + tq];
-        const int64_t tok = x < 0 ? 0 : (int64_t)x;
-        const int64_t off = (tok >> 4) * 16 * (int64_t)R + (int64_t)(kb0 + kb) * 512 + (tok & 15) * 32 + quarter * 8;
-        const uint16_t* src = (which == 0 ? ckb : cvb) + off;
-        uint16_t* dst = which == 0 ? &gk[t][kb][0] : &gv[t][kb][0];
-        __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+        const uint32_t tok = x < 0 ? 0u : (uint32_t)x;
+        const int64_t off = (int64_t)(tok >> 4) * 16 * R + (tok & 15) * 32 + quarter * 8;
+#pragma unroll
+        for (int kb = 0; kb < RBH; ++kb) {
+          // (destinations through local pointers: the builtin's LDS operand
+          // must be a plain pointer for the host pass to keep the kernel stub)
+          uint16_t* dk = &gk[t][kb][0];
+          uint16_t* dvp = &gv[t][kb][0];
+          __builtin_amdgcn_global_load_lds(ckb + off + kb * 512, dk, 16, 0, 0);
+          __builtin_amdgcn_global_load_lds(cvb + off + kb * 512, dvp, 16, 0, 0);
+        }
       }
     }
   }
