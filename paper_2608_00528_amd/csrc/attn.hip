@@ -27,12 +27,15 @@ namespace s4r {
 // combine: sinks, exact window, splits -> O_t
 // ---------------------------------------------------------------------------
 // One workgroup per (query head, sequence).  Every split's (max, sum, output)
-// is requested up front (thread t holds output dim t % d_h of splits
-// t / d_h, t / d_h + 256 / d_h, ...), the extra full-precision tokens (sinks,
-// optional exact window) are attended on the VALU with the same fixed-point
-// RoPE phases, and the partials are merged with the usual max rescaling.
+// is requested up front (thread t holds float4 t, t + 256, ... of the splits'
+// outputs, i.e. dims 4 t % d_h .. + 3 of several splits), together with the key and value rows
+// of the first kPreTok extra full-precision tokens (the sinks; further rows
+// of an optional exact window are loaded as they are reached).  The extra
+// tokens are attended on the VALU with the same fixed-point RoPE phases, and
+// the partials are merged with the usual max rescaling.
 constexpr int kMaxExtra = 1024 + 64;   // sinks + exact window rows
-constexpr int kCombPer = kMaxSplit * 128 / 256;   // split outputs per thread
+constexpr int kCombVec = kMaxSplit * 128 / (4 * 256);   // float4 of split outputs per thread
+constexpr int kPreTok = 4;             // extra tokens whose rows come with the first loads
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_combine(
@@ -53,15 +56,17 @@ __global__ __launch_bounds__(256) void k_attn_combine(
   __shared__ float qr[128];
   __shared__ uint64_t fq[64];
   __shared__ float lg[kMaxExtra];
-  __shared__ float s_as[kMaxSplit], s_ls[kMaxSplit];
-  __shared__ float red[256];
-  __shared__ float s_me, s_le, s_den, s_ae;
+  __shared__ float s_as[kMaxSplit];
+  __shared__ float red[1024];
+  __shared__ float s_me, s_den, s_ae;
 
   // ---- every load of the split partials and the query, issued together -----------------
-  const int ne = nsplit * dh;
-  float po[kCombPer];
+  const int ne4 = nsplit * dh / 4;                // float4 of split outputs (d_h is a multiple of 4)
+  const int ldh = __builtin_ctz(dh);               // head_dim is a power of two
+  float4 po[kCombVec];
+  const float4* po4 = reinterpret_cast<const float4*>(part_o + pb * dh);
 #pragma unroll
-  for (int i = 0; i < kCombPer; ++i) po[i] = (ne > 0) ? part_o[pb * dh + min(t + 256 * i, ne - 1)] : 0.f;
+  for (int i = 0; i < kCombVec; ++i) po[i] = po4[max(min(t + 256 * i, ne4 - 1), 0)];   // masked below
   float2 ml = make_float2(-INFINITY, 0.f);
   if (t < nsplit) ml = reinterpret_cast<const float2*>(part_ml)[pb + t];
   float xl = 0.f, xh = 0.f;
@@ -79,6 +84,17 @@ __global__ __launch_bounds__(256) void k_attn_combine(
     return win_v + ((int64_t)b * W + (W - n_win) + (e - s_sink)) * Dp + (int64_t)j * dh;
   };
   auto kpos = [&](int e) -> int64_t { return e < s_sink ? (int64_t)e : (int64_t)s_sink + (L - n_win) + (e - s_sink); };
+  // key row of extra token `wave` (lane = RoPE pair) and value rows of the
+  // first kPreTok extra tokens (thread t < d_h = dim t)
+  float pkl = 0.f, pkh = 0.f;
+  if (wave < n_extra && lane < half) {
+    const T* kp = krow(wave);
+    pkl = load_elem(kp, lane);
+    pkh = load_elem(kp, lane + half);
+  }
+  float pv[kPreTok];
+#pragma unroll
+  for (int e = 0; e < kPreTok; ++e) pv[e] = (e < n_extra && t < dh) ? load_elem(vrow(e), t) : 0.f;
 
   // ---- rotated query ----------------------------------------------------------------------
   if (t < half) {
@@ -96,7 +112,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(
     float part = 0.f;
     if (lane < half) {
       const T* kp = krow(e);
-      const float kl = load_elem(kp, lane), kh = load_elem(kp, lane + half);
+      const float kl = (e == wave) ? pkl : load_elem(kp, lane), kh = (e == wave) ? pkh : load_elem(kp, lane + half);
       float c, sn;
       rope_cs_fixed(kpos(e), fq[lane], c, sn);
       part = qr[lane] * (kl * c - kh * sn) + qr[lane + half] * (kh * c + kl * sn);
@@ -122,40 +138,46 @@ __global__ __launch_bounds__(256) void k_attn_combine(
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m2 = fmaxf(m2, shfl_xor_f(m2, o));
     M = fmaxf(M, m2);
+    const float ae = (n_extra > 0) ? __expf(mx - M) : 0.f;
+    const float a = (lane < nsplit && ms != -INFINITY) ? __expf(ms - M) : 0.f;   // empty split: weight 0
+    // denominator: the splits' weighted sums (lane = split) plus the extra tokens'
+    float den = (lane < nsplit) ? a * ml.y : 0.f;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) den += shfl_xor_f(den, o);
     if (lane == 0) {
       s_me = mx;
-      s_le = sm;
-      s_ae = (n_extra > 0) ? __expf(mx - M) : 0.f;
+      s_ae = ae;
+      s_den = den + ae * sm;
     }
-    const float a = (lane < nsplit && ms != -INFINITY) ? __expf(ms - M) : 0.f;   // empty split: weight 0
-    if (lane < kMaxSplit) {
-      s_as[lane] = a;
-      s_ls[lane] = (lane < nsplit) ? ml.y : 0.f;
-    }
+    if (lane < kMaxSplit) s_as[lane] = a;
   }
   __syncthreads();
-  if (t == 0) {
-    float den = s_ae * s_le;
-    for (int sp = 0; sp < nsplit; ++sp) den += s_as[sp] * s_ls[sp];
-    s_den = den;
-  }
-  // ---- weighted split outputs: thread t holds dim t % dh --------------------------------
-  float acc = 0.f;
+  // ---- weighted split outputs: thread t holds dims 4 t % dh .. + 3 -----------------------
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int i = 0; i < kCombPer; ++i) {
-    const int e = t + 256 * i;
-    if (e < ne) acc += po[i] * s_as[e / dh];
+  for (int i = 0; i < kCombVec; ++i) {
+    const int e4 = t + 256 * i;
+    if (e4 < ne4) {
+      const float a = s_as[(4 * e4) >> ldh];
+      acc.x += po[i].x * a;
+      acc.y += po[i].y * a;
+      acc.z += po[i].z * a;
+      acc.w += po[i].w * a;
+    }
   }
-  red[t] = acc;
+  *reinterpret_cast<float4*>(&red[4 * t]) = acc;   // red[e] holds dim e % dh
   __syncthreads();
   if (t < dh) {
     float num = 0.f;
-    for (int k = t; k < 256; k += dh) num += red[k];
+    for (int k = t; k < 1024; k += dh) num += red[k];
     if (n_extra > 0) {
       const float me = s_me;
       float o = 0.f;
+#pragma unroll
+      for (int e = 0; e < kPreTok; ++e)
+        if (e < n_extra) o = fmaf(__expf(lg[e] - me), pv[e], o);
 #pragma unroll 4
-      for (int e = 0; e < n_extra; ++e) o = fmaf(__expf(lg[e] - me), load_elem(vrow(e), t), o);
+      for (int e = kPreTok; e < n_extra; ++e) o = fmaf(__expf(lg[e] - me), load_elem(vrow(e), t), o);
       num += o * s_ae;
     }
     out[((int64_t)b * hq + h) * dh + t] = num / s_den;
@@ -230,7 +252,7 @@ __global__ __launch_bounds__(256) void k_sparse_attn(
   float* lg = logits_all + ((int64_t)b * hq + h) * logit_stride;
   __shared__ float qr[128];
   __shared__ double rfs[64];
-  __shared__ float red[256];
+  __shared__ float red[1024];
   __shared__ float s_mx, s_sum;
   if (t < dh / 2) rfs[t] = rope_rev_freq(theta, t, dh);
   if (t < dh / 2) {

@@ -1,18 +1,20 @@
 // Fused sparse reconstruction + split attention for bf16 storage on gfx950
-// (Section 3.2.3): every contraction on bf16 MFMA, every gather issued up front.
+// (Section 3.2.3): every contraction on bf16 MFMA.
 //
-// One workgroup per (split, HPW KV heads, sequence), NW = d_h / 32 waves,
-// TPW tiles of 16 selected tokens; HPW heads of one basis group reuse the
-// gathered rows.  The work items are laid out over a 1-D grid so
-// that the workgroups of one (sequence, split) land on the same XCD
-// (workgroup i runs on XCD i % 8): the gathered coefficient rows are then
-// fetched from HBM once per XCD and re-read from its L2 by the other heads.
+// One workgroup per (split, KV head, sequence), NW = d_h / 32 waves, tpw
+// tiles of 16 selected tokens (tpw chosen so that all workgroups fit in one
+// round of the chip).  The work items are laid out over a 1-D grid so that the
+// workgroups of one (sequence, split) land on the same XCD (workgroup i runs
+// on XCD i % 8): the gathered coefficient rows are then fetched from HBM once
+// per XCD and re-read from its L2 by the other heads.
 //
-//   1. the split's index list goes to LDS; every selected token's C^K and
-//      C^V row pieces are requested at once with 16-byte global->LDS loads
-//      (lane l of a wave load lands at byte 16 l of the destination, so one
-//      wave load writes one 16-token x 32-column block in MFMA operand
-//      layout);
+//   1. the split's index list goes to LDS; the tiles are gathered in pairs
+//      into two LDS buffers (even pairs in one, odd pairs in the other) with
+//      16-byte global->LDS loads (lane l of a wave load lands at byte 16 l of
+//      the destination, so one wave load writes one 16-token x 32-column block
+//      in MFMA operand layout).  Pairs 0 and 1 are requested up front; pair
+//      p + 2 as soon as every wave has read pair p, so the gathers overlap
+//      the arithmetic of pair p + 1;
 //   2. wave w owns the dimension blocks {w, w + NW} (16 dims each), so each
 //      RoPE pair (i, i + d_h/2) is in one lane; its bases stay in registers;
 //   3. per tile: K^ = B^K_j C^T (D[dim][token]), RoPE at the token's
@@ -32,6 +34,8 @@
 //
 // Each split writes its (max, sum) and unnormalised output per head.
 #pragma once
+
+#include <type_traits>
 
 #include "attn_common.h"
 
@@ -59,90 +63,88 @@ __device__ __forceinline__ void split2_f32x8(const float* x, Op8& hi, Op8& lo) {
   lo.u = make_uint4(pl[0], pl[1], pl[2], pl[3]);
 }
 
-// occupancy target: three workgroups per CU (at most 168 registers per lane)
-// where the gathered rows of three fit in LDS, else two
-template <int RBH, int TPW>
+// occupancy target: three workgroups per CU (at most 168 registers per lane;
+// the four tile slots of a workgroup take 8 * RBH KiB of LDS)
+template <int RBH>
 constexpr int attn_tiles_waves_per_simd() {
-  return (RBH <= 5 && 3 * 2 * TPW * RBH * 1024 <= 150 * 1024) ? 3 : 2;
+  return RBH <= 5 ? 3 : 2;
+}
+constexpr int kTileMax = 16;   // tiles per workgroup (index list in LDS)
+
+// s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt not waited)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int RBH, int NW, int NMH, int TPW, int HPW>
-__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) void k_attn_tiles(
+// one wave's gather of one 16-token tile into slot u of a pair buffer: its RBH
+// 1 KiB blocks of C^K and of C^V as 16-byte global->LDS loads (lane l: token
+// l / 4, quarter l % 4 of the 32 columns; a token past the list reads row 0,
+// never used).  The LDS destinations are named directly (plain LDS pointers
+// for the builtin).
+#define S4R_GATHER_TILE(GK, GV, U, SIDX_TILE)                                               \
+  do {                                                                                       \
+    const int32_t x_ = (SIDX_TILE)[lane >> 2];                                               \
+    const uint32_t tok_ = x_ < 0 ? 0u : (uint32_t)x_;                                        \
+    const int64_t off_ = (int64_t)(tok_ >> 4) * 16 * R + (tok_ & 15) * 32 + (lane & 3) * 8;  \
+    _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb) {                                     \
+      uint16_t* dk_ = &GK[U][kb][0];                                                         \
+      uint16_t* dv_ = &GV[U][kb][0];                                                         \
+      __builtin_amdgcn_global_load_lds(ckb + off_ + kb * 512, dk_, 16, 0, 0);                \
+      __builtin_amdgcn_global_load_lds(cvb + off_ + kb * 512, dv_, 16, 0, 0);                \
+    }                                                                                        \
+  } while (0)
+
+template <int RBH, int NW, int NMH>
+__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k_attn_tiles(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ bases_k, const uint16_t* __restrict__ bases_v,
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
-    int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int nsplit, int ngroups,
-    int G, int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap, int bases_shared,
-    double rope_ratio) {
+    int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int tpw, int nsplit,
+    int ngroups, int G, int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap,
+    int bases_shared, double rope_ratio) {
   constexpr int DH = NW * 32;                      // NMH = ceil(G / 4): 4 heads per MFMA row group
-  static_assert(TPW % 2 == 0, "tiles are processed in pairs");
-  // ---- work item: HPW consecutive KV heads of group (sequence, split); the
-  // workgroups of one group share an XCD ---------------------------------------------------
+  static_assert(NW >= 2, "a tile pair is gathered by two waves");
+  // ---- work item: KV head j of group (sequence, split); the workgroups of
+  // one group share an XCD ------------------------------------------------------------------
   const int id = blockIdx.x;
-  const int nhp = hkv / HPW;
   const int xcd = id & 7, r8 = id >> 3;
-  const int hp = r8 % nhp;
-  const int grp_id = (r8 / nhp) * 8 + xcd;
+  const int j = r8 % hkv;
+  const int grp_id = (r8 / hkv) * 8 + xcd;
   if (grp_id >= ngroups) return;
   const int b = grp_id / nsplit, split = grp_id % nsplit;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = lane & 15, kg = lane >> 4;
   const int Dp = hkv * DH, Dg = Dp / nb;
-  const int bgrp = (hp * HPW) / (hkv / nb);        // the HPW heads share one basis group
-  const int kb0 = bgrp * rank / 32;                // first latent block of the group
-  const int tile0 = split * TPW;
+  const int bgrp = j / (hkv / nb);                 // basis group of head j
+  const int kb0 = bgrp * rank / 32;                // its first latent block
+  const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
+  const int tile0 = split * tpw;
   const int ntile = (n_proc + 15) / 16;
-  const int nt = min(TPW, ntile - tile0);          // >= 1 (nsplit = ceil(ntile / TPW))
+  const int nt = min(tpw, ntile - tile0);          // >= 1 (nsplit = ceil(ntile / tpw))
+  const int npair = (nt + 1) >> 1;
 
-  __shared__ __align__(16) uint16_t gk[TPW][RBH][512];   // gathered C^K blocks: [token slot][32 columns]
-  __shared__ __align__(16) uint16_t gv[TPW][RBH][512];
-  __shared__ int32_t sidx[TPW * 16];
+  // two pair buffers (even pairs in A, odd pairs in B) of gathered C^K / C^V
+  // blocks [tile of pair][block][token slot][32 columns]: separate arrays, so
+  // the loads refilling one buffer never hold up the reads of the other
+  __shared__ __align__(16) uint16_t gkA[2][RBH][512], gvA[2][RBH][512];
+  __shared__ __align__(16) uint16_t gkB[2][RBH][512], gvB[2][RBH][512];
+  __shared__ int32_t sidx[kTileMax * 16];
   __shared__ float xl[2][NW][NMH][4][16];                // partial logits [tile of pair][wave][mh][head][slot]
   __shared__ __align__(16) uint16_t ps[2][NMH][4][2][16]; // P parts [tile of pair][mh][head][hi|lo][slot]
 
-  // ---- 1. index list, then every gather of the workgroup ---------------------------------
+  // ---- 1. index list, bases and query requested; then the first two pairs' gathers ---------
   const int32_t* idx = idx_all + (int64_t)b * idx_stride;
-  for (int i = threadIdx.x; i < TPW * 16; i += NW * 64)
-    sidx[i] = (tile0 * 16 + i < n_proc) ? idx[tile0 * 16 + i] : -1;
-  // the query dims of this lane's k-group: f_v = 16 w + 4 kg + v and f_v + d_h / 2
-  const int fq = 16 * w + 4 * kg;
-  uint64_t Ff[4];
-  rope_freqs_fixed(rope_ratio, fq, Ff);
-  const int64_t pos_q = s_sink + L - 1;
-  const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
-  lds_barrier();                                   // sidx visible
-  {
-    // wave w gathers tiles w, w + NW, ...: per tile one row offset, then the
-    // 2 x RBH wave loads of 1 KiB at constant distances
-    const uint16_t* ckb = coef_k + (int64_t)b * cap * R + (int64_t)kb0 * 512;
-    const uint16_t* cvb = coef_v + (int64_t)b * cap * R + (int64_t)kb0 * 512;
-    const int tq = lane >> 2, quarter = lane & 3;
+  int32_t xi[kTileMax * 16 / (NW * 64)];
 #pragma unroll
-    for (int t0 = 0; t0 < TPW; t0 += NW) {
-      const int t = t0 + w;
-      if (t < TPW) {                               // wave-uniform
-        const int32_t x = sidx[t * 16 + tq];
-        const uint32_t tok = x < 0 ? 0u : (uint32_t)x;
-        const int64_t off = (int64_t)(tok >> 4) * 16 * R + (tok & 15) * 32 + quarter * 8;
-#pragma unroll
-        for (int kb = 0; kb < RBH; ++kb) {
-          // (destinations through local pointers: the builtin's LDS operand
-          // must be a plain pointer for the host pass to keep the kernel stub)
-          uint16_t* dk = &gk[t][kb][0];
-          uint16_t* dvp = &gv[t][kb][0];
-          __builtin_amdgcn_global_load_lds(ckb + off + kb * 512, dk, 16, 0, 0);
-          __builtin_amdgcn_global_load_lds(cvb + off + kb * 512, dvp, 16, 0, 0);
-        }
-      }
-    }
+  for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
+    const int i = threadIdx.x + k * NW * 64;
+    xi[k] = idx[min(tile0 * 16 + i, n_proc - 1)];
   }
-  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
-
-  for (int jj = 0; jj < HPW; ++jj) {
-  const int j = hp * HPW + jj;
-  const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
   // bases (registers): A operands of K^ (row = dim) and B operands of V^
   // (column = dim) read the same 16 bytes
+  const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
   Op8 bk[2][RBH], bv[2][RBH];
 #pragma unroll
   for (int m = 0; m < 2; ++m) {
@@ -154,6 +156,8 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
       bv[m][kb].u = *reinterpret_cast<const uint4*>(bases_v + o);
     }
   }
+  // the query dims of this lane's k-group: f_v = 16 w + 4 kg + v and f_v + d_h / 2
+  const int fq = 16 * w + 4 * kg;
   uint2 qlo[NMH], qhi[NMH];
 #pragma unroll
   for (int mh = 0; mh < NMH; ++mh) {
@@ -162,6 +166,28 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
     qlo[mh] = *reinterpret_cast<const uint2*>(qp);
     qhi[mh] = *reinterpret_cast<const uint2*>(qp + DH / 2);
   }
+#pragma unroll
+  for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
+    const int i = threadIdx.x + k * NW * 64;
+    sidx[i] = (i < nt * 16 && tile0 * 16 + i < n_proc) ? xi[k] : -1;
+  }
+  uint64_t Ff[4];
+  rope_freqs_fixed(rope_ratio, fq, Ff);
+  const int64_t pos_q = s_sink + L - 1;
+  lds_barrier();                                   // sidx visible
+  const uint16_t* ckb = coef_k + (int64_t)b * cap * R + (int64_t)kb0 * 512;
+  const uint16_t* cvb = coef_v + (int64_t)b * cap * R + (int64_t)kb0 * 512;
+  // tile t is gathered by wave t % NW; pairs 0 and 1 now (every wave issues
+  // the same number of loads), pair p + 2 once pair p has been read
+#pragma unroll
+  for (int t0 = 0; t0 < 4; t0 += NW) {
+    const int t = t0 + w;
+    if (t < 2)
+      S4R_GATHER_TILE(gkA, gvA, t, &sidx[t * 16]);
+    else
+      S4R_GATHER_TILE(gkB, gvB, t - 2, &sidx[t * 16]);
+  }
+
   // ---- 2. rotated query as the A operand of the logits (overlaps the gathers) ------------
   Op8 aq[NMH];
   {
@@ -194,20 +220,25 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
     oacc[mh][0] = floatx4{0.f, 0.f, 0.f, 0.f};
     oacc[mh][1] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
-  if (jj == 0) {
-    __builtin_amdgcn_s_waitcnt(0);                 // this wave's gathers have landed
-    __syncthreads();                               // everyone's
-  }
+  const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
 
-  // ---- 3-5. tile pairs ----------------------------------------------------------------
-  for (int tp = 0; tp < nt; tp += 2) {
+  // ---- 3-5. one tile pair from buffer (gk, gv) ---------------------------------------------
+  auto do_pair = [&](const int p, auto buf) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(buf)::value;
+    // this pair's rows have landed: each wave waits for its own loads (those
+    // of the next pair, issued later, may stay in flight), then for the others
+    const bool next_issued = (p == 0) || (p + 1 < npair);
+    if (next_issued && ((2 * p + 2) % NW == w || (2 * p + 3) % NW == w))
+      wait_vmcnt<2 * RBH>();
+    else
+      wait_vmcnt<0>();
+    lds_barrier();
     floatx4 dv[2][2];                              // V^ of the pair: [tile][dim block]
     float sl[2][NMH];
     int32_t tokv[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int t = tp + u;
-      tokv[u] = sidx[t * 16 + slot];
+      tokv[u] = sidx[(2 * p + u) * 16 + slot];
       // K^ for the wave's two dimension blocks: lane (token slot, kg) gets dims 4 kg + v
       floatx4 dk[2];
 #pragma unroll
@@ -216,7 +247,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
 #pragma unroll
         for (int kb = 0; kb < RBH; ++kb) {
           Op8 c;
-          c.u = *reinterpret_cast<const uint4*>(&gk[t][kb][slot * 32 + kg * 8]);
+          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gkA[u][kb][slot * 32 + kg * 8] : &gkB[u][kb][slot * 32 + kg * 8]);
           dk[m] = mfma16x16x32(bk[m][kb], c, dk[m]);
         }
       }
@@ -246,12 +277,24 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
 #pragma unroll
         for (int kb = 0; kb < RBH; ++kb) {
           Op8 c;
-          c.u = *reinterpret_cast<const uint4*>(&gv[t][kb][slot * 32 + kg * 8]);
+          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gvA[u][kb][slot * 32 + kg * 8] : &gvB[u][kb][slot * 32 + kg * 8]);
           dv[u][m] = mfma16x16x32(c, bv[m][kb], dv[u][m]);
         }
       }
     }
-    lds_barrier();                                 // partial logits of every wave
+    lds_barrier();                                 // partial logits of every wave; buffer read
+    if (p + 2 < npair) {                           // refill the buffer with pair p + 2
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int t = 2 * p + 4 + u;
+        if (t % NW == w) {
+          if constexpr (BUF == 0)
+            S4R_GATHER_TILE(gkA, gvA, u, &sidx[t * 16]);
+          else
+            S4R_GATHER_TILE(gkB, gvB, u, &sidx[t * 16]);
+        }
+      }
+    }
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -275,12 +318,12 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const float p = (sl[u][mh] == -INFINITY) ? 0.f : __expf(sl[u][mh] - Mrun[mh]);
-        lrun[mh] += p;
+        const float pr = (sl[u][mh] == -INFINITY) ? 0.f : __expf(sl[u][mh] - Mrun[mh]);
+        lrun[mh] += pr;
         if (w == 0) {                              // one wave stages P for all
-          const uint32_t ph = pack_bf16x2(p, 0.f);
+          const uint32_t ph = pack_bf16x2(pr, 0.f);
           ps[u][mh][kg][0][slot] = (uint16_t)ph;
-          ps[u][mh][kg][1][slot] = (uint16_t)pack_bf16x2(p - __uint_as_float(ph << 16), 0.f);
+          ps[u][mh][kg][1][slot] = (uint16_t)pack_bf16x2(pr - __uint_as_float(ph << 16), 0.f);
         }
       }
     }
@@ -311,7 +354,13 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
         oacc[mh][m] = mfma16x16x32(ap, vlo[m], oacc[mh][m]);
       }
     }
+  };
+  for (int p = 0; p < npair; p += 2) {
+    do_pair(p, std::integral_constant<int, 0>());
+    if (p + 1 < npair) do_pair(p + 1, std::integral_constant<int, 1>());
   }
+  wait_vmcnt<0>();                                 // no gather left in flight (a second pair that
+                                                   // was never used when there is one pair only)
 
   // ---- partial results of the split --------------------------------------------------
 #pragma unroll
@@ -329,53 +378,51 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, TPW>())) v
       for (int m = 0; m < 2; ++m) part_o[pb * DH + 16 * (w + m * NW) + slot] = oacc[mh][m][0] + oacc[mh][m][1];
     }
   }
-  }   // heads of the workgroup
 }
 
 }  // namespace s4r
 
 namespace s4r {
 
-// which configurations the MFMA attention kernel covers (bf16 storage)
-inline int attn_tiles_per_wg(int ntile) { return ntile <= kMaxSplit * 4 ? 4 : (ntile <= kMaxSplit * 8 ? 8 : 0); }
+// tiles per workgroup: the smallest even count whose workgroups fit in one
+// round of the chip (three per CU), at most kMaxSplit splits; 0 when the list
+// needs more than kTileMax tiles per workgroup (the general kernel then runs)
+inline int attn_tiles_per_wg(const Problem& P, int ntile) {
+  const int slots = 256 * 3;
+  const int ns_target = std::max(1, slots / std::max(1, P.B * P.hkv));
+  int tpw = (ntile + ns_target - 1) / ns_target;
+  tpw = std::max(2, (tpw + 1) / 2 * 2);
+  while ((ntile + tpw - 1) / tpw > kMaxSplit) tpw += 2;
+  return tpw <= kTileMax ? tpw : 0;
+}
 
-template <int RBH, int NW, int NMH, int TPW, int HPW>
-static void launch_tiles_h(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
-                           const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
-                           int* nsplit_out) {
+template <int RBH, int NW, int NMH>
+static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
+                           const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
+                           hipStream_t st, int* nsplit_out) {
   const int ntile = (n_proc + 15) / 16;
-  const int nsplit = (ntile + TPW - 1) / TPW;
+  const int nsplit = (ntile + tpw - 1) / tpw;
   const int ngroups = P.B * nsplit;
-  const int nwg = 8 * (P.hkv / HPW) * ((ngroups + 7) / 8);
-  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH, TPW, HPW>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
+  const int nwg = 8 * P.hkv * ((ngroups + 7) / 8);
+  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
                      (const uint16_t*)bk, (const uint16_t*)bv, (const uint16_t*)ck, (const uint16_t*)cv, ws.idx,
-                     (int64_t)m, ws.part_ml, ws.part_o, n_proc, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb, P.rank, P.R,
-                     P.s, L, P.cap, P.bases_shared, rope_ratio(P));
+                     (int64_t)m, ws.part_ml, ws.part_o, n_proc, tpw, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb,
+                     P.rank, P.R, P.s, L, P.cap, P.bases_shared, rope_ratio(P));
   *nsplit_out = nsplit;
 }
 
-// one KV head per workgroup: a workgroup that walks two heads over the same
-// gathered rows halves the gather traffic but doubles its critical path, and
-// measured slower on MI355X (the HPW parameter keeps that variant available)
-template <int RBH, int NW, int NMH, int TPW>
-static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
-                           const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
-                           int* nsplit_out) {
-  launch_tiles_h<RBH, NW, NMH, TPW, 1>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, nsplit_out);
-}
-
-template <int NW, int NMH, int TPW>
-static bool dispatch_tiles_rb(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
-                              const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
-                              int* ns) {
+template <int NW, int NMH>
+static bool dispatch_tiles_rb(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
+                              const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
+                              hipStream_t st, int* ns) {
   switch (P.rank / 32) {
-    case 1: launch_tiles_t<1, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 2: launch_tiles_t<2, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 3: launch_tiles_t<3, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 4: launch_tiles_t<4, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 5: launch_tiles_t<5, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 6: launch_tiles_t<6, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
-    case 8: launch_tiles_t<8, NW, NMH, TPW>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns); return true;
+    case 1: launch_tiles_t<1, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 2: launch_tiles_t<2, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 3: launch_tiles_t<3, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 4: launch_tiles_t<4, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 5: launch_tiles_t<5, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 6: launch_tiles_t<6, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    case 8: launch_tiles_t<8, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
     default: return false;
   }
 }
@@ -386,14 +433,10 @@ template <int NW>
 static bool launch_tiles_dh(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
                             const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
                             int* ns) {
-  const int tpw = attn_tiles_per_wg((n_proc + 15) / 16);
+  const int tpw = attn_tiles_per_wg(P, (n_proc + 15) / 16);
   if (P.G > 8 || tpw == 0) return false;
-  const bool two = P.G > 4;
-  if (tpw == 4)
-    return two ? dispatch_tiles_rb<NW, 2, 4>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns)
-               : dispatch_tiles_rb<NW, 1, 4>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns);
-  return two ? dispatch_tiles_rb<NW, 2, 8>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns)
-             : dispatch_tiles_rb<NW, 1, 8>(P, ws, L, m, n_proc, q, bk, bv, ck, cv, st, ns);
+  return P.G > 4 ? dispatch_tiles_rb<NW, 2>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns)
+                 : dispatch_tiles_rb<NW, 1>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns);
 }
 
 }  // namespace s4r

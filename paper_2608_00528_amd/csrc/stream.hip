@@ -94,15 +94,37 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
                                 : ((NM <= 2 && RB <= 3) ? 2 : 1);
   const int tile0 = (blockIdx.x * kScoreWaves + wave) * tiles_per_wave;
   const int tile1 = min(tile0 + tiles_per_wave, ntiles);
-  Op8 bbuf[PF][RB][NP];
-#pragma unroll
-  for (int p = 0; p < PF; ++p) load_b_tile<T, RB>(cb, min(tile0 + p, tile1 - 1), ntiles, slot, kg, bbuf[p]);
 
   // A operands: query column gi = g * Wq + i (row i of group g's window, oldest
   // first) sits in MFMA m = gi / 4, rows 4 * (gi % 4) + part.  The newest row
   // is the sum of the projection's row-chunk partials (fixed order); older
   // rows come from the caller.  Staged once per workgroup in LDS (rows padded
   // by 16 bytes so the 16-byte operand reads of one MFMA hit distinct banks).
+  // The values of the first kQPre * 256 query elements are requested before
+  // the coefficient tiles, so they do not queue behind the streaming loads.
+  constexpr int kQPre = 4;
+  const double* qp = qpart + (int64_t)b * nch * G * R;
+  // older rows from the caller; with W_q = 1 there are none and the load
+  // below re-reads a partial sum (unused) so it needs no branch
+  const float* qw = (Wq > 1) ? qwin_prev + (int64_t)b * G * (Wq - 1) * R : reinterpret_cast<const float*>(qp);
+  double part[kQPre][kQMaxChunks];
+  float old[kQPre];
+  auto load_q = [&](int i0, int u) {
+    const int i = min(i0 + u * (int)blockDim.x + t, GW * R - 1);
+    const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
+#pragma unroll
+    for (int c = 0; c < kQMaxChunks; ++c) part[u][c] = qp[((int64_t)min(c, nch - 1) * G + g) * R + r];
+    old[u] = qw[(Wq > 1) ? ((int64_t)g * (Wq - 1) + min(wi, Wq - 2)) * R + r : 0];
+  };
+#pragma unroll
+  for (int u = 0; u < kQPre; ++u) load_q(0, u);
+
+  // the first tile now, the rest of the prefetch once the query is staged: the
+  // two workgroups of a CU then start streaming together (a full prefetch here
+  // would queue the second workgroup's first tiles behind the first's)
+  Op8 bbuf[PF][RB][NP];
+  load_b_tile<T, RB>(cb, min(tile0, tile1 - 1), ntiles, slot, kg, bbuf[0]);
+
   constexpr int RS = R + 8;
   __shared__ __align__(16) uint16_t qsh[NM][16][RS];
   {
@@ -112,23 +134,13 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
       *reinterpret_cast<uint4*>(&qsh[m][r][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
     }
     lds_barrier();
-    const double* qp = qpart + (int64_t)b * nch * G * R;
-    // older rows from the caller; with W_q = 1 there are none and the load
-    // below re-reads a partial sum (unused) so it needs no branch
-    const float* qw = (Wq > 1) ? qwin_prev + (int64_t)b * G * (Wq - 1) * R : reinterpret_cast<const float*>(qp);
-    for (int i0 = 0; i0 < GW * R; i0 += 2 * (int)blockDim.x) {
-      double part[2][kQMaxChunks];
-      float old[2];
+    for (int i0 = 0; i0 < GW * R; i0 += kQPre * (int)blockDim.x) {
+      if (i0 > 0) {                                // more than kQPre * 256 elements
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int i = min(i0 + u * (int)blockDim.x + t, GW * R - 1);
-        const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
-#pragma unroll
-        for (int c = 0; c < kQMaxChunks; ++c) part[u][c] = qp[((int64_t)min(c, nch - 1) * G + g) * R + r];
-        old[u] = qw[(Wq > 1) ? ((int64_t)g * (Wq - 1) + min(wi, Wq - 2)) * R + r : 0];
+        for (int u = 0; u < kQPre; ++u) load_q(i0, u);
       }
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < kQPre; ++u) {
         const int i = i0 + u * (int)blockDim.x + t;
         if (i >= GW * R) break;
         const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
@@ -145,8 +157,10 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
         if (qcoef_out && blockIdx.x == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
       }
     }
-    lds_barrier();                                 // the tiles requested above stay in flight
+    lds_barrier();                                 // the tile requested above stays in flight
   }
+#pragma unroll
+  for (int p = 1; p < PF; ++p) load_b_tile<T, RB>(cb, min(tile0 + p, tile1 - 1), ntiles, slot, kg, bbuf[p]);
   // the A operands stay in registers when they fit, else they are re-read from LDS
   Op8 areg[A_REG ? NM : 1][A_REG ? RB : 1];
   if constexpr (A_REG) {
