@@ -152,7 +152,8 @@ def main():
 
     wl = W.CONFIGS[args.workload]
     if wl.layers != 1:
-        raise SystemExit(f"{wl.name} is a multi-layer workload; bench.py times single-layer steps")
+        bench_sustained(args, wl)
+        return
     log(f"[bench] generating {wl.describe()}")
     t0 = time.perf_counter()
     st = W.latent_state(wl, seed=args.seed)
@@ -333,6 +334,158 @@ def main():
         log("[bench] timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(wl, st)
     print(json.dumps(result), flush=True)
+
+
+def bench_sustained(args, wl, kernel_steps=8):
+    """Sustained multi-layer decode: every step runs all layers one after the
+    other, each layer appending the new token's key/value coefficients (row
+    L - 1) before scoring, so the context grows by one token per step.  Steps
+    W..W+K-1 are timed as a whole; a further `kernel_steps` steps run with the
+    per-kernel event hook for the roofline entry."""
+    import paper_2608_00528_amd as s4r
+    import workloads as W
+
+    warmup, steps = args.warmup, args.steps
+    total = warmup + steps + kernel_steps
+    L0 = wl.L - 1                       # the first step appends row L0 and runs at L = wl.L
+    cap = ((L0 + total + 15) // 16) * 16
+    c = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                        rank=wl.rank, basis_groups=wl.basis_groups, n_sink=wl.n_sink, window=wl.window,
+                        q_window=wl.q_window, topk=wl.topk, pool_kernel=wl.pool_kernel, pool_mode=wl.pool_mode,
+                        group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=cap)
+    log(f"[bench] generating {wl.describe()}: {wl.layers} layers, {total} steps, capacity {cap}")
+    t0 = time.perf_counter()
+    layers, host0 = [], None
+    for layer in range(wl.layers):
+        st = W.sustained_layer(wl, args.seed, layer, L0, cap, total)
+        if layer == 0:
+            host0 = {k: st[k][:1].float().cpu().numpy().astype(np.float64)
+                     for k in ("sink_k", "sink_v", "bases_k", "bases_v")}
+            host0["coef_k"] = st["coef_k"][:1, :L0].float().cpu().numpy().astype(np.float64)
+            host0["coef_v"] = st["coef_v"][:1, :L0].float().cpu().numpy().astype(np.float64)
+            host0["q"] = st["q"][0, :1].float().cpu().numpy().astype(np.float64)
+            host0["k_new"] = st["k_new"][0, :1].float().cpu().numpy().astype(np.float64)
+            host0["v_new"] = st["v_new"][0, :1].float().cpu().numpy().astype(np.float64)
+        for key in ("coef_k", "coef_v"):
+            st[key] = s4r.pack_coef(c, cap, st[key])
+        torch.cuda.synchronize()
+        layers.append(st)
+        if layer % 8 == 7:
+            log(f"[bench] layer {layer + 1}/{wl.layers} resident ({time.perf_counter() - t0:.1f} s)")
+    ws = s4r.alloc_workspace(c)
+    outs = [torch.empty((wl.batch, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+            for _ in range(wl.layers)]
+    coef_bytes = sum(st[k].numel() * st[k].element_size() for st in layers for k in ("coef_k", "coef_v"))
+    log(f"[bench] {coef_bytes / 1e9:.1f} GB of coefficients resident")
+
+    def step(t):
+        for layer, st in enumerate(layers):
+            s4r.decode_step(c, L0 + t + 1, st["q"][t], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                            st["coef_k"], st["coef_v"], ws, k_new=st["k_new"][t], v_new=st["v_new"][t],
+                            out=outs[layer])
+
+    for t in range(warmup):
+        step(t)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({warmup} steps)")
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for t in range(warmup, warmup + steps):
+        step(t)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / steps
+    log(f"[bench] {steps} steps x {wl.layers} layers: {ms_step:.3f} ms/step, {1e3 / ms_step:.1f} steps/s")
+
+    s4r.timing_enable(kernel_steps * wl.layers)
+    for t in range(warmup + steps, total):
+        step(t)
+    torch.cuda.synchronize()
+    kms, ncalls = s4r.timing_read()
+    kus = {k: v / ncalls * 1e3 for k, v in kms.items()}
+    log("[bench] per-layer kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in kus.items()))
+
+    m = s4r.num_selected(c, wl.L)
+    es = 2 if wl.dtype == "bf16" else 4
+    L_mid = L0 + warmup + steps + kernel_steps // 2 + 1
+    stream_bytes = wl.batch * L_mid * wl.R * es
+    achieved = stream_bytes / (kus["score_stream"] * 1e-6) / 1e9
+    layer_bytes = (stream_bytes + 2 * wl.batch * m * wl.R * es + 2 * wl.batch * wl.Dp * wl.R * es
+                   + 2 * wl.batch * wl.n_sink * wl.Dp * es + wl.batch * wl.n_q_heads * wl.head_dim * (es + 4)
+                   + 2 * wl.batch * wl.Dp * es + 2 * wl.batch * wl.R * es)
+    step_gbps = layer_bytes * wl.layers / (ms_step * 1e-3) / 1e9
+    result = {
+        "metric": f"decode steps/s, {wl.layers} layers, sustained over {steps} steps",
+        "value": round(1e3 / ms_step, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: {wl.layers} Llama-3.1-8B-shaped layers, B={wl.batch}, N={wl.N} at the first "
+                         f"timed step and +1 token per step, h_q/h_kv={wl.n_q_heads}/{wl.n_kv_heads}, "
+                         f"d_h={wl.head_dim}, rank {wl.R}, s={wl.n_sink}, W={wl.window}, k={wl.topk}, "
+                         f"{wl.dtype} storage, new token projected and appended in every layer of every step"),
+            "batch": wl.batch, "context": wl.N, "layers": wl.layers, "rank": wl.R, "window": wl.window,
+            "topk": wl.topk, "selected": m, "coefficient_GB": round(coef_bytes / 1e9, 2),
+        },
+        "achieved_step_GBps": round(step_gbps, 1),
+        "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "kernels_us_per_layer": {k: round(v, 3) for k, v in kus.items()},
+        "roofline": {
+            "kernel": "k_score_stream (latent scoring over C^K)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "algorithmic_bytes_per_launch": stream_bytes,
+            "avg_launch_us": round(kus["score_stream"], 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline_sustained(wl, host0, L0 + 1)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline_sustained(wl, one, L, budget_s=10.0):
+    """The oracle on one sequence of one layer (append + decode step),
+    repeated for about budget_s seconds, extrapolated to the whole step."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import decode
+    cfg = dict(n_kv_heads=wl.n_kv_heads, window=wl.window, topk=wl.topk, pool_kernel=wl.pool_kernel,
+               pool_mode=wl.pool_mode, group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype)
+    ck = np.zeros((1, L, wl.R))
+    cv = np.zeros((1, L, wl.R))
+    ck[:, :L - 1], cv[:, :L - 1] = one["coef_k"], one["coef_v"]
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        decode.decode_step(cfg, L, one["q"], one["sink_k"], one["sink_v"], one["bases_k"], one["bases_v"], ck, cv,
+                           k_new=one["k_new"], v_new=one["v_new"])
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() > t_end:
+            break
+    per_seq = float(np.median(times))
+    step_s = per_seq * wl.batch * wl.layers
+    return {"value": round(1.0 / step_s, 5), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "host_cpus": os.cpu_count(),
+            "sample": (f"float64 numpy oracle, sequence 0 of layer 0 at L={L} (append + decode step), {len(times)} "
+                       f"runs in {sum(times):.1f} s, median per sequence extrapolated x {wl.batch} sequences x "
+                       f"{wl.layers} layers; BLAS threads {threads}")}
 
 
 if __name__ == "__main__":

@@ -61,3 +61,92 @@ def test_full_size_decode_step(name):
     assert err <= OUT_TOL[wl.dtype], f"output rel err {err:.3e} (tie flips {flips})"
     for b in range(wl.batch):
         assert err_s[b].max() <= tol_s[b], f"sequence {b}: score rel err {err_s[b].max():.3e} > {tol_s[b]:.3e}"
+
+
+def test_sustained_32_layers():
+    """The 32-layer sustained run at full size, as bench.py runs it: every step
+    runs all layers in turn, each appending its new token (row L - 1) before
+    scoring, 16 + 256 steps.  Sampled (layer, step) pairs are checked against
+    the oracle replaying the same appends on the stored state of two sampled
+    sequences; the appended rows of those sequences must equal the oracle's."""
+    wl = W.CONFIGS["llama8b_32L_sustained"]
+    T = 16 + 256
+    L0 = wl.L - 1
+    cap = ((L0 + T + 15) // 16) * 16
+    c = cfg_from_workload(wl, capacity=cap)
+    seqs = [0, wl.batch - 1]
+    checks = {(0, 0), (13, 100), (wl.layers - 1, T - 1)}
+    check_layers = sorted({l for l, _ in checks})
+    print(f"[sustained] {wl.describe()}, {wl.layers} layers, {T} steps, capacity {cap}", flush=True)
+    layers, host = [], {}
+    for layer in range(wl.layers):
+        st = W.sustained_layer(wl, 0, layer, L0, cap, T)
+        if layer in check_layers:
+            h = {k: st[k][seqs].float().cpu().numpy().astype(np.float64)
+                 for k in ("sink_k", "sink_v", "bases_k", "bases_v")}
+            for k in ("coef_k", "coef_v"):
+                h[k] = st[k][seqs, :L0].float().cpu().numpy().astype(np.float64)
+            for k in ("q", "k_new", "v_new"):
+                h[k] = st[k][:, seqs].float().cpu().numpy().astype(np.float64)
+            host[layer] = h
+        for k in ("coef_k", "coef_v"):
+            st[k] = s4r.pack_coef(c, cap, st[k])
+        torch.cuda.synchronize()
+        layers.append(st)
+    ws = s4r.alloc_workspace(c)
+    m_max = s4r.num_selected(c, L0 + T)
+    got = {}
+    for t in range(T):
+        L = L0 + t + 1
+        for layer, st in enumerate(layers):
+            args = (c, L, st["q"][t], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"], st["coef_k"],
+                    st["coef_v"], ws)
+            kw = dict(k_new=st["k_new"][t], v_new=st["v_new"][t])
+            if (layer, t) in checks:
+                m = s4r.num_selected(c, L)
+                idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
+                scores = torch.empty((wl.batch, L), dtype=torch.float32, device="cuda")
+                out_chk = s4r.decode_step(*args, idx_out=idx, scores_out=scores, **kw)
+                out = s4r.decode_step(*args, **kw)      # the timed form; re-appending the same row is idempotent
+                torch.cuda.synchronize()
+                assert torch.equal(out, out_chk), "the timed launch differs from the checked one"
+                got[(layer, t)] = (out[seqs].cpu().numpy(), idx[seqs].cpu().numpy().astype(np.int64),
+                                   scores[seqs].cpu().numpy().astype(np.float64))
+            else:
+                s4r.decode_step(*args, **kw)
+    torch.cuda.synchronize()
+    assert m_max == s4r.num_selected(c, L0 + T)
+    oc = oracle_cfg(c, wl.pool_mode, wl.group_agg)
+    for layer in check_layers:
+        h = host[layer]
+        # the oracle's own appends, step by step
+        ck = np.zeros((len(seqs), L0 + T, wl.R))
+        cv = np.zeros((len(seqs), L0 + T, wl.R))
+        ck[:, :L0], cv[:, :L0] = h["coef_k"], h["coef_v"]
+        for t in range(T):
+            ck[:, L0 + t], cv[:, L0 + t] = decode.project_append(h["k_new"][t], h["v_new"][t], h["bases_k"],
+                                                                 h["bases_v"], oc["dtype"])
+        rows_k = s4r.unpack_coef(c, L0 + T, layers[layer]["coef_k"])[seqs, L0:].float().cpu().numpy()
+        rows_v = s4r.unpack_coef(c, L0 + T, layers[layer]["coef_v"])[seqs, L0:].float().cpu().numpy()
+        assert np.array_equal(rows_k, ck[:, L0:]) and np.array_equal(rows_v, cv[:, L0:]), \
+            f"layer {layer}: appended rows differ from the oracle's projection"
+        for (l2, t) in sorted(checks):
+            if l2 != layer:
+                continue
+            L = L0 + t + 1
+            ref = decode.decode_step(oc, L, h["q"][t], h["sink_k"], h["sink_v"], h["bases_k"], h["bases_v"],
+                                     ck[:, :L], cv[:, :L])
+            out, idx_np, sc = got[(layer, t)]
+            flips = check_selection(idx_np, ref["idx"], ref["a_tilde"], L, wl.window, wl.topk)
+            assert np.array_equal(idx_np, decode.select(sc, L, wl.window, wl.topk))
+            err_s = np.abs(sc - ref["a_tilde"]) / np.maximum(np.abs(ref["a_tilde"]), 1e-30)
+            tol_s = score_tol(ref["cQ"], ck, L, wl.dtype)
+            o_ref, _, _ = decode.sparse_attention(h["q"][t], idx_np, h["sink_k"], h["sink_v"], h["bases_k"],
+                                                  h["bases_v"], ck[:, :L], cv[:, :L], L, wl.n_kv_heads,
+                                                  oc["rope_theta"])
+            err = rel_err_rows(out, o_ref)
+            print(f"[sustained] layer {layer} step {t} (L={L}): score err {err_s.max():.2e}, tie flips {flips}, "
+                  f"out err {err:.2e}", flush=True)
+            assert err <= OUT_TOL[wl.dtype]
+            for i in range(len(seqs)):
+                assert err_s[i].max() <= tol_s[i], f"sequence {seqs[i]}: score rel err {err_s[i].max():.3e}"

@@ -6,6 +6,7 @@ import os
 
 import numpy as np
 import pytest
+import torch
 
 import workloads as W
 from oracle import decode, prefill
@@ -69,3 +70,22 @@ def test_needles_are_recalled(name):
     r = decode.decode_step(cfg, wl.L, raw["q"], st["sink_k"], st["sink_v"], st["bases_k"],
                            st["bases_v"], st["coef_k"], st["coef_v"])
     assert np.isin(raw["needles"][0], r["idx"][0]).mean() >= 0.9
+
+
+def test_sustained_layer_recipe():
+    wl = W.CONFIGS["llama8b_32L_sustained"].scaled(batch=2, N=1024 + 4)
+    L0, cap, T = wl.L - 1, 1040, 3
+    a = W.sustained_layer(wl, 0, 5, L0, cap, T, device="cpu")
+    b = W.sustained_layer(wl, 0, 5, L0, cap, T, device="cpu")
+    other = W.sustained_layer(wl, 0, 6, L0, cap, T, device="cpu")
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    assert not torch.equal(a["coef_k"], other["coef_k"])
+    assert a["coef_k"].shape == (2, cap, wl.R) and a["q"].shape == (T, 2, wl.n_q_heads, wl.head_dim)
+    assert a["k_new"].shape == (T, 2, wl.Dp) and a["bases_v"].shape == (2, 1, wl.Dp, wl.rank)
+    assert torch.count_nonzero(a["coef_k"][:, L0:]) == 0
+    bk = a["bases_k"][0, 0].double()
+    assert (bk.T @ bk - torch.eye(wl.rank, dtype=torch.float64)).abs().max() < 2e-2   # orthonormal up to bf16
+    assert not torch.equal(a["bases_k"][0], a["bases_k"][1])                          # per-sequence bases
+    norms = a["coef_k"][:, :L0].double().norm(dim=-1)
+    assert 0.8 * np.sqrt(wl.Dp) < norms.mean() < 1.2 * np.sqrt(wl.Dp)

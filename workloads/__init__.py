@@ -287,3 +287,58 @@ def step_inputs(wl, seed, layer, step, state=None):
     v_new = r.standard_normal((B, Dp))
     rnd = lambda a: round_storage(a, wl.dtype)  # noqa: E731
     return {"q": rnd(q), "k_new": rnd(k_new), "v_new": rnd(v_new)}
+
+
+def _torch_seed(wl, seed, layer, tag):
+    return int(np.random.SeedSequence([wl.wid, seed, layer, tag]).generate_state(1, dtype=np.uint64)[0] >> 1)
+
+
+def sustained_layer(wl, seed, layer, L0, capacity, steps, device="cuda"):
+    """One layer of the sustained multi-layer run, drawn on `device`.
+
+    The stored state is drawn directly in latent coordinates (valid because
+    the bases are orthonormal): coefficient rows F M + noise with F Gaussian
+    [L0, r_true] and M a random mixing with a 1/(1 + i/16) column spectrum, row
+    norms about sqrt(Dp), rows >= L0 zero; per-sequence orthonormal bases by a
+    seeded float32 QR on the host; sinks 10x Gaussian.  Per step s (0-based)
+    it draws a fresh query, Gaussian per head with a group norm of 1.5 sqrt(R)
+    (latent logits of standard deviation about 1.5), and the new token's raw
+    key/value, Gaussian.  Everything is rounded once to the storage type.
+
+    Returns a dict of device tensors: bases_k/v [B, nb, Dp/nb, rank],
+    coef_k/v row-major [B, capacity, R], sink_k/v [B, s, Dp], and per step
+    q [steps, B, h_q, d_h], k_new/v_new [steps, B, Dp].
+    """
+    if wl.basis_groups != 1:
+        raise ValueError("the sustained recipe draws one joint basis per sequence")
+    B, Dp, R = wl.batch, wl.Dp, wl.R
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    gh = torch.Generator(device="cpu")
+    out = {}
+    for key, tag in (("bases_k", _T_BASIS_K), ("bases_v", _T_BASIS_V)):
+        gh.manual_seed(_torch_seed(wl, seed, layer, tag))
+        a = torch.randn((B, Dp, R), generator=gh, dtype=torch.float32)
+        qm, rm = torch.linalg.qr(a)
+        qm = qm * torch.sign(torch.diagonal(rm, dim1=-2, dim2=-1))[:, None, :]
+        out[key] = qm.reshape(B, 1, Dp, R).to(device=device, dtype=dt).contiguous()
+    gd = torch.Generator(device=device)
+    spectrum = 1.0 / (1.0 + torch.arange(R, dtype=torch.float32, device=device) / 16.0)
+    scale = float(np.sqrt(Dp) / np.sqrt(float((spectrum.double() ** 2).sum())))
+    for key, tag in (("coef_k", _T_KEY), ("coef_v", _T_VAL)):
+        gd.manual_seed(_torch_seed(wl, seed, layer, tag))
+        mix = torch.randn((B, wl.r_true, R), generator=gd, device=device) * (spectrum * (scale / np.sqrt(wl.r_true)))
+        c = torch.zeros((B, capacity, R), dtype=dt, device=device)
+        for b in range(B):   # one sequence at a time bounds the float32 temporaries
+            f = torch.randn((L0, wl.r_true), generator=gd, device=device)
+            e = torch.randn((L0, R), generator=gd, device=device)
+            c[b, :L0] = (torch.mm(f, mix[b].contiguous()) + e * (spectrum * (wl.noise * scale))).to(dt)
+        out[key] = c
+    gd.manual_seed(_torch_seed(wl, seed, layer, _T_SINK))
+    out["sink_k"] = (10.0 * torch.randn((B, wl.n_sink, Dp), generator=gd, device=device)).to(dt)
+    out["sink_v"] = (10.0 * torch.randn((B, wl.n_sink, Dp), generator=gd, device=device)).to(dt)
+    gd.manual_seed(_torch_seed(wl, seed, layer, _T_STEP))
+    q_std = 1.5 * np.sqrt(R) / np.sqrt(Dp)
+    out["q"] = (q_std * torch.randn((steps, B, wl.n_q_heads, wl.head_dim), generator=gd, device=device)).to(dt)
+    out["k_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
+    out["v_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
+    return out
