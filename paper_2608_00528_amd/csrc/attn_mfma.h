@@ -69,7 +69,7 @@ template <int RBH>
 constexpr int attn_tiles_waves_per_simd() {
   return RBH <= 5 ? 3 : 2;
 }
-constexpr int kTileMax = 16;   // tiles per workgroup (index list in LDS)
+constexpr int kTileMax = 32;   // tiles per workgroup (index list in LDS)
 
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt not waited)
 template <int N>

@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 OUT_TOL = {"bf16": 2e-2, "fp32": 1e-4}
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k", "qwen7b_128k"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k", "qwen7b_128k", "qwen3_4b_120k"])
 def test_full_size_decode_step(name):
     wl = W.CONFIGS[name]
     print(f"[full-size] {wl.describe()}", flush=True)
@@ -33,16 +33,17 @@ def test_full_size_decode_step(name):
     m = s4r.num_selected(c, wl.L)
     idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
     scores = torch.empty((wl.batch, wl.L), dtype=torch.float32, device="cuda")
+    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
     out = s4r.decode_step(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
-                          g["coef_v"], ws, idx_out=idx, scores_out=scores)
+                          g["coef_v"], ws, qwin_prev=qwin, idx_out=idx, scores_out=scores)
     out_bench = s4r.decode_step(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"],
-                                g["coef_k"], g["coef_v"], ws)
+                                g["coef_k"], g["coef_v"], ws, qwin_prev=qwin)
     torch.cuda.synchronize()
     assert torch.equal(out, out_bench), "the timed launch differs from the checked one"
 
     oc = oracle_cfg(c, wl.pool_mode, wl.group_agg)
     ref = decode.decode_step(oc, wl.L, st["q"], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
-                             st["coef_k"], st["coef_v"])
+                             st["coef_k"], st["coef_v"], qwin_prev=st["qwin_prev"])
     a = ref["a_tilde"]
     got = scores.cpu().numpy().astype(np.float64)
     err_s = np.abs(got - a) / np.maximum(np.abs(a), 1e-30)

@@ -137,6 +137,8 @@ def _select_case(scores, L, W_, k, capacity=None):
     (5000, 64, 256, "pooled"), (5000, 64, 0, "pooled"), (5000, 64, 10_000, "pooled"),
     (40, 64, 10, "pooled"), (1, 1, 5, "pooled"), (9000, 128, 1000, "ints"),
     (20000, 16, 700, "equal"), (7001, 7, 6000, "equal"), (33000, 100, 2048, "tiny_range"),
+    (263000, 900, 4000, "ints"),        # the most positions one selection workgroup takes
+    (270000, 100, 3000, "pooled"),      # beyond it: the multi-workgroup selection
 ])
 def test_select_topk_bit_exact(L, W_, k, kind):
     rng = np.random.default_rng(L + k)

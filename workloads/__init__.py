@@ -30,7 +30,7 @@ import numpy as np
 import torch
 
 # stream tags
-_T_KEY, _T_VAL, _T_QRY, _T_NEEDLE, _T_SINK, _T_BASIS_K, _T_BASIS_V, _T_STEP = range(8)
+_T_KEY, _T_VAL, _T_QRY, _T_NEEDLE, _T_SINK, _T_BASIS_K, _T_BASIS_V, _T_STEP, _T_QWIN = range(9)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -87,8 +87,13 @@ class Workload:
                 f"k={self.topk} {self.dtype}")
 
 
-# The five workloads: one tiny fp32 layer, Llama-3.1-8B-shaped layers at 32k
-# and 128k, a Qwen2.5-7B-shaped layer at 128k, and the 32-layer sustained run.
+# The workloads: one tiny fp32 layer, Llama-3.1-8B-shaped layers at 32k and
+# 128k, a Qwen2.5-7B-shaped layer at 128k, the 32-layer sustained run, and
+# the paper's own efficiency setting (Section 4.2 / Appendix B.4): a
+# Qwen3-4B-shaped layer (32/8 heads, d_h = 128, D' = 1024) at a 120k context,
+# query window tied to the local window W = 4, reconstruction ratio 0.2 so
+# k = floor(0.2 L) - W, rank 192 (the paper's 204 rounded down to the
+# coefficient layout's 32-column blocks).
 CONFIGS = {
     "tiny_fp32": Workload("tiny_fp32", 1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64,
                           N=4096, n_sink=4, rank=32, basis_groups=2, window=64, topk=128,
@@ -110,6 +115,10 @@ CONFIGS = {
                                       window=64, topk=1024, dtype="bf16", rope_theta=500000.0,
                                       r_true=128, noise=0.05, n_needles=32, outlier_channels=4,
                                       outlier_scale=8.0, layers=32, steps=256),
+    "qwen3_4b_120k": Workload("qwen3_4b_120k", 6, batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                              N=120_004, n_sink=4, rank=192, basis_groups=1, window=4,
+                              topk=int(0.2 * 120_000) - 4, dtype="bf16", rope_theta=1000000.0, r_true=160,
+                              noise=0.05, n_needles=32, q_window=4),
 }
 
 HEADLINE = "llama8b_128k"
@@ -211,7 +220,9 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
     Returns float64 arrays:
       bases_k/v [B, nb, Dp/nb, rank] orthonormal columns per group,
       coef_k/v  [B, capacity, R] (rows >= L are zero),
-      sink_k/v  [B, s, Dp], q [B, h_q, d_h], needles (positions per sequence).
+      sink_k/v  [B, s, Dp], q [B, h_q, d_h], needles (positions per sequence),
+      qwin_prev [B, G, W_q - 1, R] fp32 latent coefficients of the window's
+                earlier queries (None when W_q = 1).
     Coefficient rows are F M + noise * E with F Gaussian (Student-t nu=3 when
     heavy_tail) and M a random mixing with a 1/(1 + i/16) column spectrum;
     row norms are about sqrt(Dp).  The query of group g is B^K u_g (+10%
@@ -221,7 +232,7 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
     dg = Dp // nb
     L = wl.L if L is None else L
     cap = L if capacity is None else capacity
-    out = {k: None for k in ("bases_k", "bases_v", "coef_k", "coef_v", "sink_k", "sink_v", "q")}
+    out = {k: None for k in ("bases_k", "bases_v", "coef_k", "coef_v", "sink_k", "sink_v", "q", "qwin_prev")}
     bk = np.empty((B, nb, dg, wl.rank))
     bv = np.empty((B, nb, dg, wl.rank))
     ck = np.zeros((B, cap, R))
@@ -229,6 +240,7 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
     sk = np.empty((B, wl.n_sink, Dp))
     sv = np.empty((B, wl.n_sink, Dp))
     qg = np.empty((B, wl.G, Dp))
+    qwin = np.empty((B, wl.G, wl.q_window - 1, R))
     needles = []
     spectrum = 1.0 / (1.0 + np.arange(R) / 16.0)
     for b in range(B):
@@ -260,6 +272,16 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
         # component of a coefficient row along it is about 2 sqrt(Dp/r_true)
         qnorm = 1.5 * np.sqrt(R) / (2.0 * np.sqrt(Dp) / np.sqrt(wl.r_true))
         qg[b] = qdir * qnorm
+        if wl.q_window > 1:
+            # the earlier queries of the window, drawn directly as latent query
+            # coefficients of the same scale (their own latent directions plus 10% noise)
+            rw = _rng(wl, seed, layer, b, _T_QWIN)
+            for i in range(wl.q_window - 1):
+                uw = rw.standard_normal((wl.G, wl.r_true)) @ Mk
+                uw /= np.linalg.norm(uw, axis=-1, keepdims=True)
+                nw = rw.standard_normal((wl.G, R))
+                nw /= np.linalg.norm(nw, axis=-1, keepdims=True)
+                qwin[b, :, i] = (0.9 * uw + 0.1 * nw) * qnorm
         rn = _rng(wl, seed, layer, b, _T_NEEDLE)
         wl_eff = wl.scaled(N=L + wl.n_sink)
         pos = _needle_positions(rn, wl_eff, wl.n_needles)
@@ -271,7 +293,8 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
             ck[b, p] += lift * udir
     rnd = lambda a: round_storage(a, wl.dtype)  # noqa: E731
     out.update(bases_k=rnd(bk), bases_v=rnd(bv), coef_k=rnd(ck), coef_v=rnd(cv),
-               sink_k=rnd(sk), sink_v=rnd(sv), q=rnd(_query_heads(qg, wl)), needles=needles)
+               sink_k=rnd(sk), sink_v=rnd(sv), q=rnd(_query_heads(qg, wl)), needles=needles,
+               qwin_prev=round_storage(qwin, "fp32") if wl.q_window > 1 else None)
     return out
 
 
