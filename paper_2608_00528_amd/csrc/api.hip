@@ -113,7 +113,7 @@ size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
 enum Region {
   kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits,
-  kCandCount, kAboveCount, kSelInfo, kRegions
+  kCandCount, kAboveCount, kSelInfo, kColStats, kRegions
 };
 struct Layout {
   size_t off[kRegions];
@@ -138,6 +138,7 @@ Layout layout(const Problem& P) {
   sizes[kCandCount] = B * sel_groups_max(P) * 4;
   sizes[kAboveCount] = B * sel_groups_max(P) * 4;
   sizes[kSelInfo] = B * 4 * 4;
+  sizes[kColStats] = B * GW * 2 * 8;
   Layout l;
   size_t o = 0;
   for (int i = 0; i < kRegions; ++i) {
@@ -210,6 +211,7 @@ Workspace carve_workspace(const Problem& P, void* base) {
   w.cand_count = (uint32_t*)(b + l.off[kCandCount]);
   w.above_count = (uint32_t*)(b + l.off[kAboveCount]);
   w.sel_info = (uint32_t*)(b + l.off[kSelInfo]);
+  w.col_stats = (double*)(b + l.off[kColStats]);
   w.total = l.total;
   return w;
 }

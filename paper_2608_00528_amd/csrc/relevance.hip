@@ -17,17 +17,27 @@ namespace s4r {
 // tref[b][tile][c].  One memory latency: the scoring workgroups' statistics,
 // the chunk's tile references and its exp values (plus the pooling halo) are
 // all requested before any is used.  Then each wave folds query columns'
-// statistics into the global (M, S) in fp64 (the same fixed order in every
-// workgroup, so A~ is deterministic) and the per-tile factors
-// exp(ref - M) / S are formed in fp64.  Per staged position the window mean
+// statistics into the global (M, S), sums in fp64 (the same fixed order in
+// every workgroup, so A~ is deterministic), and the per-tile factors
+// exp(ref - M) / S; every exponential there takes its fp64 argument through
+// exp_neg_accurate (fp64 range reduction, hardware exp2 of the fraction: about
+// one fp32 ulp), far cheaper than an fp64 exp per scoring workgroup and
+// column in every workgroup.  Per staged position the window mean
 // over the W_q rows is formed once (fp32 products of values exact to about an
 // ulp; the max-pooling that follows is exact), staged in LDS, and every thread
 // pools outputs t, t + 256, ... (consecutive lanes read consecutive words: no
 // bank conflicts) and sums the groups in fp64.
 constexpr int kRelThreads = 256;
+constexpr int kRelStatPer = 2;   // scoring-workgroup statistics per lane folded inside the relevance kernel
 constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk and its halo (h <= 32)
 
-int relevance_chunk(int G) { return G <= 4 ? 1024 : (G <= 8 ? 512 : 256); }
+// tokens per workgroup: 1024 (G <= 4), 512 (G <= 8) or 256, halved while the
+// grid would give fewer than two workgroups per CU (small batches)
+int relevance_chunk(const Problem& P, int64_t L) {
+  int c = P.G <= 4 ? 1024 : (P.G <= 8 ? 512 : 256);
+  while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < 512) c >>= 1;
+  return c;
+}
 
 // Pooling (kappa = 2H + 1, stride 1, same length) and aggregation over the G
 // groups for outputs t, t + 256, ... of a chunk.  With H known at compile time
@@ -84,7 +94,7 @@ __device__ __forceinline__ void pool_aggregate(const float* __restrict__ vs, int
 template <int NQ, int TPT, bool WQ1>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
-    float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
+    const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
     int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg) {
   constexpr int GWP = 4 * NQ;
   constexpr int CHUNK = kRelThreads * TPT;
@@ -108,14 +118,19 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
 
   // ---- all global reads of this workgroup, issued before any is used ----------
   // statistics: wave w folds columns w, w + 4, ...; two batches of 64 lanes in flight
-  constexpr int kStatPer = 2;
-  double2 st[NQ][kStatPer];
+  // (or, with many scoring workgroups, the global statistics k_fold_stats formed)
+  double2 st[NQ][kRelStatPer];
   const double2* stats = reinterpret_cast<const double2*>(wg_stats) + (int64_t)b * GW * nwg;
+  double2 cs = make_double2(0.0, 0.0);
+  if (col_stats) {
+    cs = reinterpret_cast<const double2*>(col_stats)[(int64_t)b * GW + min(t, GW - 1)];
+  } else {
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int c = min(wave + 4 * q, GW - 1);
+    for (int q = 0; q < NQ; ++q) {
+      const int c = min(wave + 4 * q, GW - 1);
 #pragma unroll
-    for (int k = 0; k < kStatPer; ++k) st[q][k] = stats[(int64_t)c * nwg + min(lane + 64 * k, nwg - 1)];
+      for (int k = 0; k < kRelStatPer; ++k) st[q][k] = stats[(int64_t)c * nwg + min(lane + 64 * k, nwg - 1)];
+    }
   }
   // tile references: thread t loads tile tile_lo + t (all columns)
   float4 rf[NQ];
@@ -136,16 +151,22 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   for (int i = t; i < kHistBins; i += kRelThreads) hl[i] = 0;
 
   // ---- global (M, S) of each query column ---------------------------------------------
+  if (col_stats) {
+    if (t < GW) {
+      sM[t] = cs.x;
+      sInvS[t] = cs.y;
+    }
+  }
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int c = wave + 4 * q;
-    if (c < GW) {                                          // wave-uniform
+    if (!col_stats && c < GW) {                            // wave-uniform
       const double* srow = wg_stats + ((int64_t)b * GW + c) * nwg * 2;
       double M = -INFINITY, S = 0.0;
-      for (int base = 0; base < nwg; base += 64 * kStatPer) {
-        double2 s2[kStatPer];
+      for (int base = 0; base < nwg; base += 64 * kRelStatPer) {
+        double2 s2[kRelStatPer];
 #pragma unroll
-        for (int k = 0; k < kStatPer; ++k) {
+        for (int k = 0; k < kRelStatPer; ++k) {
           if (base == 0) {
             s2[k] = st[q][k];
           } else {                                         // more than 128 scoring workgroups
@@ -155,19 +176,19 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
         }
         double m = -INFINITY;
 #pragma unroll
-        for (int k = 0; k < kStatPer; ++k)
+        for (int k = 0; k < kRelStatPer; ++k)
           if (base + lane + 64 * k < nwg) m = fmax(m, s2[k].x);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) m = fmax(m, shfl_xor_d(m, o));
         double s = 0.0;
 #pragma unroll
-        for (int k = 0; k < kStatPer; ++k)
-          if (base + lane + 64 * k < nwg && s2[k].x != -INFINITY) s += s2[k].y * exp(s2[k].x - m);
+        for (int k = 0; k < kRelStatPer; ++k)
+          if (base + lane + 64 * k < nwg && s2[k].x != -INFINITY) s += s2[k].y * (double)exp_neg_accurate(s2[k].x - m);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) s += shfl_xor_d(s, o);
         if (m != -INFINITY) {
           const double Mn = fmax(M, m);
-          S = ((M == -INFINITY) ? 0.0 : S * exp(M - Mn)) + s * exp(m - Mn);
+          S = ((M == -INFINITY) ? 0.0 : S * (double)exp_neg_accurate(M - Mn)) + s * (double)exp_neg_accurate(m - Mn);
           M = Mn;
         }
       }
@@ -186,7 +207,8 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = 4 * q + u;
-        fac[t][c] = (c < GW && r4[u] != -INFINITY) ? (float)(exp((double)r4[u] - sM[c]) * sInvS[c]) : 0.f;
+        fac[t][c] = (c < GW && r4[u] != -INFINITY)
+                        ? (float)((double)exp_neg_accurate((double)r4[u] - sM[c]) * sInvS[c]) : 0.f;
       }
     }
   }
@@ -280,6 +302,46 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
   }
 }
 
+// Global (max, 1 / sum) of every query column's softmax over the length,
+// folded once from the scoring workgroups' (max, sum) pairs when there are
+// more than the relevance kernel folds itself (64 * kRelStatPer): grid (GW,
+// B), thread t folds pairs t, t + 256, ... in order, then a fixed-order tree
+// across the threads (deterministic).
+__global__ __launch_bounds__(256) void k_fold_stats(const double* __restrict__ wg_stats, double* __restrict__ col_stats,
+                                                    int GW, int nwg) {
+  const int c = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  const double2* row = reinterpret_cast<const double2*>(wg_stats) + ((int64_t)b * GW + c) * nwg;
+  __shared__ double sm[256], ss[256];
+  auto merge = [](double& M, double& S, double m, double s) {
+    if (m == -INFINITY) return;
+    const double Mn = fmax(M, m);
+    S = ((M == -INFINITY) ? 0.0 : S * (double)exp_neg_accurate(M - Mn)) + s * (double)exp_neg_accurate(m - Mn);
+    M = Mn;
+  };
+  double M = -INFINITY, S = 0.0;
+  for (int w0 = 0; w0 < nwg; w0 += 4 * 256) {
+    double2 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = row[min(w0 + k * 256 + t, nwg - 1)];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (w0 + k * 256 + t < nwg) merge(M, S, v[k].x, v[k].y);
+  }
+  sm[t] = M;
+  ss[t] = S;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) {
+      double M2 = sm[t], S2 = ss[t];
+      merge(M2, S2, sm[t + o], ss[t + o]);
+      sm[t] = M2;
+      ss[t] = S2;
+    }
+    __syncthreads();
+  }
+  if (t == 0) reinterpret_cast<double2*>(col_stats)[(int64_t)b * GW + c] = make_double2(sm[0], 1.0 / ss[0]);
+}
+
 template <int NQ, int TPT>
 static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
   const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
@@ -287,14 +349,17 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   const size_t lds = (size_t)P.G * (chunk + 2 * (P.kappa / 2)) * sizeof(float);
   dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
   auto kern = P.Wq == 1 ? k_relevance<NQ, TPT, true> : k_relevance<NQ, TPT, false>;
+  const int nwg = score_workgroups(P, L);
+  const bool fold = nwg > 64 * kRelStatPer;
+  if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
-                     ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), score_workgroups(P, L));
+                     fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
+                     (int)(P.cap / kTileTok), nwg);
 }
 
 template <int NQ>
 static void launch_rel_nq(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
-  switch (relevance_chunk(P.G)) {
+  switch (relevance_chunk(P, L)) {
     case 1024: launch_rel_t<NQ, 4>(P, ws, L, scores_out, st); break;
     case 512: launch_rel_t<NQ, 2>(P, ws, L, scores_out, st); break;
     default: launch_rel_t<NQ, 1>(P, ws, L, scores_out, st); break;

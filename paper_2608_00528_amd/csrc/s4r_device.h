@@ -205,6 +205,16 @@ __device__ __forceinline__ uint32_t wave_append(uint32_t* counter, bool pred) {
   return base + (uint32_t)__popcll(m & below);
 }
 
+// exp(x) for x <= 0 given in fp64: 2^(x log2 e) with the integer part split off
+// in fp64, the fraction evaluated by the hardware exp2 (relative error about
+// one fp32 ulp for any x)
+__device__ __forceinline__ float exp_neg_accurate(double x) {
+  const double y = x * 1.4426950408889634;
+  const double n = rint(y);
+  const float f = (float)(y - n);
+  return ldexpf(__builtin_amdgcn_exp2f(f), (int)fmax(n, -300.0));
+}
+
 // order-preserving key of a non-negative fp32 score (sign bit is clear)
 __device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s); }
 

@@ -41,6 +41,7 @@ struct Workspace {
   float* e;             // [B][cap][GWP]  exp(z - running max), fp32, token-major
   float* run_m;         // [B][cap / 16][GWP] per-tile softmax reference (running max of z)
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
+  double* col_stats;    // [B][GW][2]     global (max, 1 / sum) per query column, when folded by k_fold_stats
   float* atilde;        // [B][cap]       relevance scores
   uint32_t* hist;       // [B][2][kHistBins]  selection histograms: top 11 key bits, next 11 of the boundary bin
   uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)

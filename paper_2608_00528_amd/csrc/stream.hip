@@ -25,16 +25,6 @@ namespace s4r {
 // wave's tiles (recorded per tile, fp32) with fp64 argument reduction, and
 // the running (max, sum) of every query column is kept per wave.
 
-// exp(x) for x <= 0 given in fp64: 2^(x log2 e) with the integer part split off
-// in fp64, the fraction evaluated by the hardware exp2 (relative error about
-// one fp32 ulp for any x)
-__device__ __forceinline__ float exp_neg_accurate(double x) {
-  const double y = x * 1.4426950408889634;
-  const double n = rint(y);
-  const float f = (float)(y - n);
-  return ldexpf(__builtin_amdgcn_exp2f(f), (int)fmax(n, -300.0));
-}
-
 template <typename T>
 struct BLoad;
 
