@@ -137,6 +137,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama8b_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-comparator", action="store_true",
+                    help="skip the dense Full-KV comparator (uncompressed bf16 KV of the same shape)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (counter calibration) and exit")
@@ -274,6 +276,47 @@ def main():
     read_gbps = cks[0].numel() * cks[0].element_size() * nrd / (r0.elapsed_time(r1) * 1e-3) / 1e9
     log(f"[bench] read ceiling (contiguous non-temporal 16-byte stream over C^K): {read_gbps:.0f} GB/s")
 
+    # comparator: dense GQA decode over the uncompressed bf16 KV cache of the
+    # same shape (the paper's "Full KV" baseline), on the same GPU
+    comparator = None
+    if not args.no_comparator and wl.dtype == "bf16" and wl.head_dim == 128:
+        dc = W.dense_cache(wl, seed=args.seed)
+        cd = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads,
+                             head_dim=wl.head_dim, rank=wl.rank, n_sink=wl.n_sink, window=wl.window, topk=wl.topk,
+                             rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=((wl.N + 15) // 16) * 16)
+        dk = torch.zeros((wl.batch, cd.capacity, wl.Dp), dtype=torch.bfloat16, device="cuda")
+        dv = torch.zeros_like(dk)
+        dk[:, :wl.N], dv[:, :wl.N] = dc["k"], dc["v"]
+        del dc["k"], dc["v"]
+        wsd = s4r.alloc_workspace(cd)
+        outd = torch.empty_like(out)
+        for _ in range(3):
+            s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
+        torch.cuda.synchronize()
+        nd = 20
+        d0 = torch.cuda.Event(enable_timing=True)
+        d1 = torch.cuda.Event(enable_timing=True)
+        d0.record(stream)
+        for _ in range(nd):
+            s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
+        d1.record(stream)
+        torch.cuda.synchronize()
+        dense_us = d0.elapsed_time(d1) * 1e3 / nd
+        dense_bytes = 2 * wl.batch * wl.N * wl.Dp * 2
+        comparator = {
+            "what": "dense GQA decode over the uncompressed bf16 KV cache of the same shape (Full KV), "
+                    "s4r_dense_decode: k_dense_decode + k_attn_combine",
+            "us_per_step": round(dense_us, 2),
+            "kv_bytes_per_step": dense_bytes,
+            "achieved_GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
+            "frac_of_hbm_peak": round(dense_bytes / (dense_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "s4r_step_speedup": round(dense_us / (ms_step * 1e3), 2),
+        }
+        log(f"[bench] dense Full-KV comparator: {dense_us:.1f} us/step "
+            f"({comparator['achieved_GBps']:.0f} GB/s), S4R step {comparator['s4r_step_speedup']:.2f}x faster")
+        del dk, dv, wsd
+        torch.cuda.synchronize()
+
     # per-kernel pass (events between kernels), same steps again
     nk = min(args.steps, 200)
     s4r.timing_enable(nk)
@@ -340,6 +383,8 @@ def main():
             "frac": round(rec_tflops / BF16_PEAK_TFLOPS, 5),
         },
     }
+    if comparator is not None:
+        result["comparator_full_kv"] = comparator
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(wl, st)

@@ -173,6 +173,24 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
                            hipStream_t stream);
 
 /*
+ * Comparator: dense GQA decode attention over an uncompressed KV cache, the
+ * "Full KV" baseline of the efficiency comparison (Section 4.2, Table
+ * "efficiency"; the full-attention term of Appendix B.1).  Not part of the
+ * S^4R step; it exists so the method and the full cache are measured on the
+ * same GPU.  k_cache / v_cache: [B, capacity, Dp] bf16, row n of sequence b
+ * holding token n (keys already rotated by RoPE at position n, as a plain KV
+ * cache stores them); the N tokens 0..N-1 are attended, the query q
+ * [B, h_q, d_h] (pre-RoPE) is rotated at position N - 1.
+ * out[b, h] = softmax(RoPE(q_h) K_j^T / sqrt(d_h)) V_j with j = h / G, fp32.
+ * Uses cfg's batch, head counts, head_dim, capacity, rope_theta and dtype only;
+ * bf16, head_dim 128 and G <= 8 (otherwise S4R_ERR_UNSUPPORTED); the workspace
+ * is the same as for s4r_decode_step.
+ */
+s4r_status s4r_dense_decode(const s4r_config* cfg, int64_t N, const void* q, const void* k_cache,
+                            const void* v_cache, float* out, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/*
  * Compressed cache update alone (Section 3.2.1): c^K = k_new B^K and
  * c^V = v_new B^V, rounded to the storage dtype (fp64 accumulation, then
  * fp32 and bf16 round-to-nearest-even), written into coefficient row `row`.

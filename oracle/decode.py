@@ -234,6 +234,28 @@ def attend(q, kstar, vstar, pos_k, pos_q, theta, n_kv_heads):
 # The whole step
 # ----------------------------------------------------------------------------
 
+def dense_decode(q, k_cache, v_cache, n_kv_heads, theta):
+    """Comparator, not part of S^4R: the "Full KV" decode attention of the
+    efficiency comparison (Section 4.2; the full attention term of Appendix
+    B.1).  The cache holds the N = k_cache.shape[1] tokens uncompressed, keys
+    already rotated by RoPE at their positions 0..N-1 (as a plain KV cache
+    stores them); the query is rotated at position N - 1.  Head h reads KV
+    head h // G (R1).  Returns [B, h_q, d_h]."""
+    q = _f64(q)
+    K = _f64(k_cache)
+    V = _f64(v_cache)
+    B, hq, dh = q.shape
+    N = K.shape[1]
+    G = hq // n_kv_heads
+    qr = rope(q, np.full((B, hq), float(N - 1)), theta)
+    out = np.empty((B, hq, dh))
+    for h in range(hq):
+        j = h // G
+        logits = np.einsum("bd,bnd->bn", qr[:, h], K[:, :, j * dh:(j + 1) * dh]) / np.sqrt(dh)
+        out[:, h] = np.einsum("bn,bnd->bd", softmax_over_length(logits), V[:, :, j * dh:(j + 1) * dh])
+    return out
+
+
 def relevance(q, qwin_prev, bases_k, coef_k, L, n_kv_heads, pool_kernel=7,
               pool_mode="max", group_agg="mean"):
     """Latent relevance A~ of every non-sink token (3.2.2 and the first two

@@ -156,6 +156,18 @@ def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v
     return out
 
 
+def dense_decode(cfg, n_tokens, q, k_cache, v_cache, ws, out=None):
+    """Comparator: dense GQA decode over an uncompressed bf16 KV cache
+    [B, capacity, Dp] (keys stored after RoPE) for tokens 0..n_tokens-1."""
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    dt = storage_dtype(cfg)
+    L.check(L.load().s4r_dense_decode(_cfgp(cfg), n_tokens, _ptr(q, "q", dt), _ptr(k_cache, "k_cache", dt),
+                                      _ptr(v_cache, "v_cache", dt), _ptr(out, "out", torch.float32),
+                                      _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+    return out
+
+
 def project_append(cfg, row, k_new, v_new, bases_k, bases_v, coef_k, coef_v):
     dt = storage_dtype(cfg)
     L.check(L.load().s4r_project_append(_cfgp(cfg), row, _ptr(k_new, "k_new", dt), _ptr(v_new, "v_new", dt),

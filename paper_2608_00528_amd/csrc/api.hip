@@ -329,6 +329,25 @@ s4r_status s4r_sparse_attn(const s4r_config* cfg, int64_t L, int32_t m, const vo
                     "s4r_sparse_attn launch");
 }
 
+s4r_status s4r_dense_decode(const s4r_config* cfg, int64_t N, const void* q, const void* k_cache,
+                            const void* v_cache, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (P.dtype != S4R_BF16) return fail(S4R_ERR_UNSUPPORTED, "the dense comparator is built for bf16 caches only");
+  if (P.dh != 128) return fail(S4R_ERR_UNSUPPORTED, "the dense comparator is built for head_dim 128 only");
+  if (P.G > 8) return fail(S4R_ERR_UNSUPPORTED, "the dense comparator is built for G <= 8");
+  if (N < 1 || N > P.cap) return fail(S4R_ERR_BAD_SHAPE, "N = %lld outside [1, capacity = %lld]", (long long)N,
+                                      (long long)P.cap);
+  S4R_REQ(q);
+  S4R_REQ(k_cache);
+  S4R_REQ(v_cache);
+  S4R_REQ(out);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  return hip_status(launch_dense_decode(P, w, N, q, k_cache, v_cache, out, stream), "s4r_dense_decode launch");
+}
+
 s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
                            const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
                            const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, const void* k_new,

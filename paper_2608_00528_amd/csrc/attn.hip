@@ -403,6 +403,16 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
   return e;
 }
 
+// the split merge alone (no extra full-precision tokens), for kernels that
+// leave split partials in the workspace
+hipError_t launch_combine_only(const Problem& P, const Workspace& ws, int64_t L, int nsplit, const void* q, float* out,
+                               hipStream_t st) {
+  hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q, nullptr,
+                     nullptr, nullptr, nullptr, ws.part_ml, ws.part_o, out, nsplit, P.hq, P.hkv, P.dh, 0, 0, L,
+                     rope_ratio(P));
+  return hipGetLastError();
+}
+
 template <typename T, int RBH>
 static void launch_rec_t(const Problem& P, int64_t L, int m, const int32_t* idx, const void* bk, const void* bv,
                          const void* ck, const void* cv, float* kh, float* vh, hipStream_t st) {

@@ -41,28 +41,6 @@
 
 namespace s4r {
 
-// two fp32 values -> packed bf16 (round to nearest even; one v_cvt_pk_bf16_f32)
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  const f32x2_t v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
-}
-
-// 8 fp32 values -> bf16 hi and lo parts (x ~= hi + lo to about 2^-17)
-__device__ __forceinline__ void split2_f32x8(const float* x, Op8& hi, Op8& lo) {
-  uint32_t ph[4], pl[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ph[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
-    const float r0 = x[2 * i] - __uint_as_float(ph[i] << 16);
-    const float r1 = x[2 * i + 1] - __uint_as_float(ph[i] & 0xFFFF0000u);
-    pl[i] = pack_bf16x2(r0, r1);
-  }
-  hi.u = make_uint4(ph[0], ph[1], ph[2], ph[3]);
-  lo.u = make_uint4(pl[0], pl[1], pl[2], pl[3]);
-}
-
 // occupancy target: three workgroups per CU (at most 168 registers per lane;
 // the four tile slots of a workgroup take 8 * RBH KiB of LDS)
 template <int RBH>

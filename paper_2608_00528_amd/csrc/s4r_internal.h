@@ -84,6 +84,8 @@ hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, co
                             hipStream_t st);
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st);
+hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
+                               const void* v_cache, float* out, hipStream_t st);
 hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, int m, int k_eff,
                             const void* q, const void* sink_k, const void* sink_v,
                             const void* win_k, const void* win_v, const void* bases_k,

@@ -151,3 +151,23 @@ def test_sustained_32_layers():
             assert err <= OUT_TOL[wl.dtype]
             for i in range(len(seqs)):
                 assert err_s[i].max() <= tol_s[i], f"sequence {seqs[i]}: score rel err {err_s[i].max():.3e}"
+
+
+def test_dense_comparator_full_size():
+    """The dense comparator at the headline shape (B=4, N=131072, 32/8 heads),
+    in the launch configuration bench.py times; sequences 0 and 3 compared in
+    full against the oracle."""
+    wl = W.CONFIGS["llama8b_128k"]
+    print(f"[full-size] dense comparator, {wl.describe()}", flush=True)
+    dc = W.dense_cache(wl, seed=0)
+    c = cfg_from_workload(wl, capacity=wl.N)
+    ws = s4r.alloc_workspace(c)
+    out = s4r.dense_decode(c, wl.N, dc["q"], dc["k"], dc["v"], ws)
+    torch.cuda.synchronize()
+    oc = oracle_cfg(c)
+    for b in (0, wl.batch - 1):
+        f64 = lambda t: t[b:b + 1].float().cpu().numpy().astype(np.float64)  # noqa: E731
+        ref = decode.dense_decode(f64(dc["q"]), f64(dc["k"]), f64(dc["v"]), wl.n_kv_heads, oc["rope_theta"])
+        err = rel_err_rows(out[b:b + 1].cpu().numpy(), ref)
+        print(f"[full-size] dense comparator sequence {b}: out err {err:.2e}", flush=True)
+        assert err <= 1e-4

@@ -331,3 +331,22 @@ def test_read_bandwidth_reference_reads_every_word():
     got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     want = np.bitwise_xor.reduce(buf.cpu().numpy().view(np.uint32))
     assert got == want
+
+
+@pytest.mark.parametrize("shape,N", [("llama8b_32k", 3001), ("llama8b_32k", 17), ("llama8b_32k", 1),
+                                     ("qwen7b_128k", 2000)])
+def test_dense_comparator(shape, N):
+    """The dense Full-KV comparator against the oracle's dense attention."""
+    wl = W.CONFIGS[shape].scaled(batch=2)
+    cap = ((N + 15) // 16) * 16 + 16                  # rows past N exist and are never read
+    dc = W.dense_cache(wl, seed=N, n_tokens=cap)
+    for key in ("k", "v"):
+        dc[key][:, N:] = float("nan")
+    c = cfg_from_workload(wl, capacity=cap)
+    ws = s4r.alloc_workspace(c)
+    out = s4r.dense_decode(c, N, dc["q"], dc["k"], dc["v"], ws)
+    torch.cuda.synchronize()
+    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    ref = decode.dense_decode(f64(dc["q"]), f64(dc["k"][:, :N]), f64(dc["v"][:, :N]), wl.n_kv_heads,
+                              oracle_cfg(c)["rope_theta"])
+    assert rel_err_rows(out.cpu().numpy(), ref) <= 1e-4

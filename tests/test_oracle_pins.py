@@ -296,10 +296,26 @@ def check_causal_window(seed=10):
     return True
 
 
+def check_dense_comparator(seed=11):
+    """The dense comparator (keys stored after RoPE) equals torch SDPA with
+    complex-form RoPE applied to pre-RoPE keys at positions 0..N-1."""
+    rng = np.random.default_rng(seed)
+    B, hq, hkv, dh, N = 2, 8, 2, 16, 37
+    q = rng.standard_normal((B, hq, dh))
+    K = rng.standard_normal((B, N, hkv * dh))
+    V = rng.standard_normal((B, N, hkv * dh))
+    theta = 10000.0
+    pos = np.broadcast_to(np.arange(N, dtype=float), (B, N))
+    Kst = np.concatenate([ref_rope_complex(K[:, :, j * dh:(j + 1) * dh], pos, theta) for j in range(hkv)], axis=-1)
+    got = decode.dense_decode(q, Kst, V, hkv, theta)
+    want = torch_gqa_attention(q, K, V, pos, np.full(B, N - 1.0), theta, hkv)
+    return np.allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
 ALL_CHECKS = [check_latent_identity, check_rotation_invariance, check_pool_vs_torch,
               check_topk_special_case, check_select_bruteforce, check_full_rank_exact,
               check_full_budget_dense, check_rope_complex, check_rope_shift_invariance,
-              check_plain_gqa, check_causal_window]
+              check_plain_gqa, check_causal_window, check_dense_comparator]
 
 
 # ----------------------------------------------------------------------------
@@ -334,6 +350,10 @@ def test_full_rank_reconstruction_exact():
 @pytest.mark.parametrize("theta,W", [(100.0, 3), (0.0, 3), (500000.0, 0)])
 def test_full_budget_equals_dense_attention(theta, W):
     assert check_full_budget_dense(theta=theta, W=W)
+
+
+def test_dense_comparator_matches_torch_sdpa():
+    assert check_dense_comparator()
 
 
 def test_rope_rotate_half_equals_complex_form():

@@ -365,3 +365,20 @@ def sustained_layer(wl, seed, layer, L0, capacity, steps, device="cuda"):
     out["k_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
     out["v_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
     return out
+
+
+def dense_cache(wl, seed=0, device="cuda", n_tokens=None):
+    """An uncompressed KV cache of the workload's shape for the dense
+    comparator, drawn on `device`: keys and values [B, N, Dp] Gaussian (keys
+    taken as already stored after RoPE: a random vector is as good a rotated
+    key as any), a Gaussian query [B, h_q, d_h] with logits of standard
+    deviation about 1.5, everything rounded once to bf16."""
+    N = wl.N if n_tokens is None else n_tokens
+    g = torch.Generator(device=device)
+    g.manual_seed(_torch_seed(wl, seed, 0, _T_KEY))
+    k = torch.randn((wl.batch, N, wl.Dp), generator=g, device=device).to(torch.bfloat16)
+    g.manual_seed(_torch_seed(wl, seed, 0, _T_VAL))
+    v = torch.randn((wl.batch, N, wl.Dp), generator=g, device=device).to(torch.bfloat16)
+    g.manual_seed(_torch_seed(wl, seed, 0, _T_QRY))
+    q = (1.5 * torch.randn((wl.batch, wl.n_q_heads, wl.head_dim), generator=g, device=device)).to(torch.bfloat16)
+    return {"k": k, "v": v, "q": q}
