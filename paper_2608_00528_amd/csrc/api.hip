@@ -398,9 +398,10 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
     return hipEventRecord(start ? g_timing.start[slot + kernel] : g_timing.stop[slot + kernel], stream);
   };
   hipError_t e = mark(hipSuccess, 0, true);
-  if (e == hipSuccess && k_new)   // the new token's rows first: the scoring pass reads row L - 1
-    e = launch_project_rows(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, stream);
-  if (e == hipSuccess) e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
+  if (e == hipSuccess && k_new)   // the new token's rows with the query coefficients: the scoring pass reads row L - 1
+    e = launch_project_step(P, w.qpart, w.hist, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, stream);
+  else if (e == hipSuccess)
+    e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
   e = mark(e, 0, false);
   e = mark(e, 1, true);
   if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, nullptr, stream);

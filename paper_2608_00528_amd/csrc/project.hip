@@ -108,11 +108,10 @@ __device__ __forceinline__ void reduce_rows(double (&acc)[kPVec][8], double (*re
 // thread's work to one load round trip and a short fp64 dot product.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, const T* __restrict__ bases_k,
-                                                       double* __restrict__ qpart, uint32_t* __restrict__ hist,
-                                                       int hq, int hkv, int dh, int G, int nb, int rank, int R,
-                                                       int bases_shared) {
-  const int cblk = blockIdx.x, ch = blockIdx.y, b = blockIdx.z, nch = gridDim.y;
+__device__ __forceinline__ void project_query_body(const T* __restrict__ q, const T* __restrict__ bases_k,
+                                                   double* __restrict__ qpart, uint32_t* __restrict__ hist, int hq,
+                                                   int hkv, int dh, int G, int nb, int rank, int R, int bases_shared,
+                                                   int cblk, int ch, int b, int nch) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int cg = t & 3, rg = t >> 2;
   const int Dp = hkv * dh, Dg = Dp / nb;
@@ -171,18 +170,26 @@ __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, 
   }
 }
 
+template <typename T>
+__global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, const T* __restrict__ bases_k,
+                                                       double* __restrict__ qpart, uint32_t* __restrict__ hist,
+                                                       int hq, int hkv, int dh, int G, int nb, int rank, int R,
+                                                       int bases_shared) {
+  project_query_body<T>(q, bases_k, qpart, hist, hq, hkv, dh, G, nb, rank, R, bases_shared, blockIdx.x, blockIdx.y,
+                        blockIdx.z, gridDim.y);
+}
+
 // ---------------------------------------------------------------------------
 // new token's coefficient rows: grid (R / 32, B, 2 = {key, value}).  The
 // workgroup loops over 256-row chunks of its basis group and writes the full
 // sums into row append_row of the cache (rounded to the storage format).
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
-                                                      const T* __restrict__ k_new, const T* __restrict__ v_new,
-                                                      T* __restrict__ coef_k, T* __restrict__ coef_v,
-                                                      int64_t append_row, int hkv, int dh, int nb, int rank, int R,
-                                                      int bases_shared, int64_t cap) {
-  const int cblk = blockIdx.x, b = blockIdx.y, which = blockIdx.z;
+__device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
+                                                  const T* __restrict__ k_new, const T* __restrict__ v_new,
+                                                  T* __restrict__ coef_k, T* __restrict__ coef_v, int64_t append_row,
+                                                  int hkv, int dh, int nb, int rank, int R, int bases_shared,
+                                                  int64_t cap, int cblk, int b, int which) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int cg = t & 3, rg = t >> 2;
   const int Dp = hkv * dh, Dg = Dp / nb;
@@ -219,6 +226,42 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
   }
 }
 
+template <typename T>
+__global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
+                                                      const T* __restrict__ k_new, const T* __restrict__ v_new,
+                                                      T* __restrict__ coef_k, T* __restrict__ coef_v,
+                                                      int64_t append_row, int hkv, int dh, int nb, int rank, int R,
+                                                      int bases_shared, int64_t cap) {
+  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, append_row, hkv, dh, nb, rank, R,
+                       bases_shared, cap, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// both projections of a step that appends a token, in one launch: blocks
+// [0, nq) are the query-coefficient workgroups (R / 32 x chunks x B, in that
+// order), the rest the new rows' (R / 32 x B x 2).  They touch disjoint
+// memory, and one launch saves a dispatch and a first-read latency.
+template <typename T>
+__global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, const T* __restrict__ bases_k,
+                                                      const T* __restrict__ bases_v, const T* __restrict__ k_new,
+                                                      const T* __restrict__ v_new, T* __restrict__ coef_k,
+                                                      T* __restrict__ coef_v, double* __restrict__ qpart,
+                                                      uint32_t* __restrict__ hist, int64_t append_row, int hq,
+                                                      int hkv, int dh, int G, int nb, int rank, int R,
+                                                      int bases_shared, int64_t cap, int B, int nch) {
+  const int ncb = R / 32;
+  const int nq = ncb * nch * B;
+  int id = blockIdx.x;
+  if (id < nq) {
+    const int cblk = id % ncb, ch = (id / ncb) % nch, b = id / (ncb * nch);
+    project_query_body<T>(q, bases_k, qpart, hist, hq, hkv, dh, G, nb, rank, R, bases_shared, cblk, ch, b, nch);
+  } else {
+    id -= nq;
+    const int cblk = id % ncb, b = (id / ncb) % B, which = id / (ncb * B);
+    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, append_row, hkv, dh, nb, rank, R,
+                         bases_shared, cap, cblk, b, which);
+  }
+}
+
 hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
                                 hipStream_t st) {
   dim3 grid(P.R / 32, project_chunks(P), P.B);
@@ -243,6 +286,24 @@ hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void
     hipLaunchKernelGGL(k_project_rows<float>, grid, dim3(256), 0, st, (const float*)bases_k, (const float*)bases_v,
                        (const float*)k_new, (const float*)v_new, (float*)coef_k, (float*)coef_v, row, P.hkv, P.dh,
                        P.nb, P.rank, P.R, P.bases_shared, P.cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+                               const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
+                               int64_t row, hipStream_t st) {
+  const int nch = project_chunks(P);
+  dim3 grid((P.R / 32) * nch * P.B + (P.R / 32) * P.B * 2);
+  if (P.dtype == S4R_BF16)
+    hipLaunchKernelGGL(k_project_step<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q, (const uint16_t*)bases_k,
+                       (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
+                       (uint16_t*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
+                       P.bases_shared, P.cap, P.B, nch);
+  else
+    hipLaunchKernelGGL(k_project_step<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k,
+                       (const float*)bases_v, (const float*)k_new, (const float*)v_new, (float*)coef_k,
+                       (float*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared,
+                       P.cap, P.B, nch);
   return hipGetLastError();
 }
 

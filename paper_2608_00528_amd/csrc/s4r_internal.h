@@ -86,6 +86,9 @@ hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st);
 hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
                                const void* v_cache, float* out, hipStream_t st);
+hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+                               const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
+                               int64_t row, hipStream_t st);
 hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, int m, int k_eff,
                             const void* q, const void* sink_k, const void* sink_v,
                             const void* win_k, const void* win_v, const void* bases_k,
