@@ -111,11 +111,25 @@ def cpu_baseline(wl, st, budget_s=10.0):
         if time.perf_counter() > t_end:
             break
     per_seq = float(np.median(times))
+    # the same sample with one BLAS thread, for about half the budget
+    from threadpoolctl import threadpool_limits
+    times1 = []
+    with threadpool_limits(limits=1):
+        t_end = time.perf_counter() + budget_s / 2
+        while True:
+            t0 = time.perf_counter()
+            decode.decode_step(cfg, wl.L, one["q"], one["sink_k"], one["sink_v"], one["bases_k"], one["bases_v"],
+                               one["coef_k"], one["coef_v"], qwin_prev=qwin)
+            times1.append(time.perf_counter() - t0)
+            if time.perf_counter() > t_end:
+                break
+    per_seq1 = float(np.median(times1))
     return {"value": round(per_seq * wl.batch * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
-            "host_cpus": os.cpu_count(),
+            "host_cpus": os.cpu_count(), "value_1_thread": round(per_seq1 * wl.batch * 1e6, 1),
             "sample": (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
                        f"{len(times)} runs in {sum(times):.1f} s, median per sequence x {wl.batch} sequences; "
-                       f"BLAS threads {threads}")}
+                       f"BLAS threads {threads}; value_1_thread: the same with one BLAS thread, "
+                       f"{len(times1)} runs in {sum(times1):.1f} s")}
 
 
 def copy_calibration(nbytes, reps):

@@ -155,3 +155,19 @@ def test_other_entry_point_errors():
     assert lib.s4r_read_bandwidth(FAKE, 100, FAKE, None) == L.S4R_ERR_BAD_SHAPE      # not a multiple of 16
     assert lib.s4r_read_bandwidth(None, 64, FAKE, None) == L.S4R_ERR_NULL_ARG
     assert lib.s4r_read_bandwidth_sink_len() > 0
+
+
+def test_dense_comparator_argument_errors():
+    lib = L.load()
+
+    def call(c, n=100, q=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, wsb=1 << 40):
+        return lib.s4r_dense_decode(ctypes.byref(c), n, q, k, v, out, ws, wsb, None)
+    c = cfg(head_dim=128)
+    assert call(c, n=0) == L.S4R_ERR_BAD_SHAPE                      # N < 1
+    assert call(c, n=1025) == L.S4R_ERR_BAD_SHAPE                   # N > capacity
+    assert call(c, k=None) == L.S4R_ERR_NULL_ARG
+    assert call(c, v=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert call(c, wsb=16) == L.S4R_ERR_WORKSPACE
+    assert call(cfg()) == L.S4R_ERR_UNSUPPORTED                     # head_dim 64
+    assert call(cfg(head_dim=128, dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
+    assert call(cfg(head_dim=128, n_q_heads=32, n_kv_heads=2)) == L.S4R_ERR_UNSUPPORTED   # G = 16
