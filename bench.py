@@ -328,7 +328,34 @@ def main():
         }
         log(f"[bench] dense Full-KV comparator: {dense_us:.1f} us/step "
             f"({comparator['achieved_GBps']:.0f} GB/s), S4R step {comparator['s4r_step_speedup']:.2f}x faster")
-        del dk, dv, wsd
+        # the prefill's bulk projection C = S B of the same prompt (those rows as S)
+        n_pf = cd.capacity
+        cpf = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads,
+                              head_dim=wl.head_dim, rank=wl.rank, n_sink=wl.n_sink, window=wl.window,
+                              topk=wl.topk, rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=n_pf)
+        pk = torch.empty((wl.batch, n_pf, wl.R), dtype=torch.bfloat16, device="cuda")
+        pv = torch.empty_like(pk)
+        wspf = s4r.alloc_workspace(cpf)
+        s4r.prefill_project(cpf, n_pf, dk, dv, bk, bv, pk, pv, wspf)
+        torch.cuda.synchronize()
+        p0 = torch.cuda.Event(enable_timing=True)
+        p1 = torch.cuda.Event(enable_timing=True)
+        npf = 5
+        p0.record(stream)
+        for _ in range(npf):
+            s4r.prefill_project(cpf, n_pf, dk, dv, bk, bv, pk, pv, wspf)
+        p1.record(stream)
+        torch.cuda.synchronize()
+        pf_us = p0.elapsed_time(p1) * 1e3 / npf
+        pf_bytes = 2 * wl.batch * n_pf * (wl.Dp + wl.R) * 2
+        comparator["prefill_projection"] = {
+            "what": f"s4r_prefill_project: C = S B for K and V of {wl.batch} x {n_pf} prompt rows (Section 3.1)",
+            "us": round(pf_us, 1), "bytes": pf_bytes,
+            "achieved_GBps": round(pf_bytes / (pf_us * 1e-6) / 1e9, 1),
+            "frac_of_hbm_peak": round(pf_bytes / (pf_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        }
+        log(f"[bench] prefill bulk projection: {pf_us:.1f} us ({comparator['prefill_projection']['achieved_GBps']:.0f} GB/s)")
+        del dk, dv, wsd, pk, pv, wspf
         torch.cuda.synchronize()
 
     # per-kernel pass (events between kernels), same steps again

@@ -173,6 +173,27 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
                            hipStream_t stream);
 
 /*
+ * Bulk projection of the prefill stage (Section 3.1, the coefficient
+ * equation): C^K = S^K B^K and C^V = S^V B^V per basis group for the prompt's
+ * non-sink rows, written into rows [0, n_rows) of the tiled coefficient caches
+ * (other rows untouched).  s_k / s_v: [B, n_rows, Dp] raw pre-RoPE rows, row
+ * t = non-sink token t, row-major, storage dtype; bases as in
+ * s4r_score_latent.  Products of the bf16 inputs are exact, sums are fp32 on
+ * the matrix cores, rounded once to bf16 (a coefficient can differ by one
+ * bf16 ulp from the fp64-rounded value where the fp32 sum lies next to a
+ * rounding boundary).  bf16 storage and rank 32..192 only (otherwise
+ * S4R_ERR_UNSUPPORTED).  ws / ws_bytes: the workspace of s4r_decode_step
+ * (s4r_workspace_size); its first B * 2 * Dp * rank * 2 bytes hold the bases
+ * transposed while the call runs.  The bases themselves come from a truncated
+ * SVD of sampled, normalised rows (Section 3.1), which this library does not
+ * compute.
+ */
+s4r_status s4r_prefill_project(const s4r_config* cfg, int64_t n_rows, const void* s_k,
+                               const void* s_v, const void* bases_k, const void* bases_v,
+                               void* coef_k, void* coef_v, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
  * Comparator: dense GQA decode attention over an uncompressed KV cache, the
  * "Full KV" baseline of the efficiency comparison (Section 4.2, Table
  * "efficiency"; the full-attention term of Appendix B.1).  Not part of the

@@ -18,6 +18,7 @@ from .api import (  # noqa: E402,F401
     make_config,
     num_selected,
     pack_coef,
+    prefill_project,
     project_append,
     read_bandwidth,
     reconstruct,

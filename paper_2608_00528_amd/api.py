@@ -156,6 +156,17 @@ def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v
     return out
 
 
+def prefill_project(cfg, n_rows, s_k, s_v, bases_k, bases_v, coef_k, coef_v, ws):
+    """Bulk projection of a prompt's non-sink raw K/V rows [B, n_rows, Dp]
+    into rows [0, n_rows) of the tiled coefficient caches (ws: the decode
+    workspace)."""
+    dt = storage_dtype(cfg)
+    L.check(L.load().s4r_prefill_project(_cfgp(cfg), n_rows, _ptr(s_k, "s_k", dt), _ptr(s_v, "s_v", dt),
+                                         _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt),
+                                         _ptr(coef_k, "coef_k", dt), _ptr(coef_v, "coef_v", dt),
+                                         _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+
+
 def dense_decode(cfg, n_tokens, q, k_cache, v_cache, ws, out=None):
     """Comparator: dense GQA decode over an uncompressed bf16 KV cache
     [B, capacity, Dp] (keys stored after RoPE) for tokens 0..n_tokens-1."""

@@ -329,6 +329,32 @@ s4r_status s4r_sparse_attn(const s4r_config* cfg, int64_t L, int32_t m, const vo
                     "s4r_sparse_attn launch");
 }
 
+s4r_status s4r_prefill_project(const s4r_config* cfg, int64_t n_rows, const void* s_k, const void* s_v,
+                               const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (P.dtype != S4R_BF16) return fail(S4R_ERR_UNSUPPORTED, "the bulk projection is built for bf16 storage only");
+  if (P.rank / 32 < 1 || P.rank / 32 > 6)
+    return fail(S4R_ERR_UNSUPPORTED, "the bulk projection is built for rank 32 .. 192 (rank %d)", P.rank);
+  if ((P.hkv * P.dh / P.nb) % 32)
+    return fail(S4R_ERR_UNSUPPORTED, "basis group width %d is not a multiple of 32", P.hkv * P.dh / P.nb);
+  if (n_rows < 1 || n_rows > P.cap)
+    return fail(S4R_ERR_BAD_SHAPE, "n_rows = %lld outside [1, capacity = %lld]", (long long)n_rows,
+                (long long)P.cap);
+  S4R_REQ(s_k);
+  S4R_REQ(s_v);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(coef_k);
+  S4R_REQ(coef_v);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;     // the transposed bases use its first bytes
+  if (prefill_ws_bytes(P) > layout(P).total) return fail(S4R_ERR_WORKSPACE, "workspace too small for the bases");
+  return hip_status(launch_prefill_project(P, n_rows, s_k, s_v, bases_k, bases_v, coef_k, coef_v, ws, stream),
+                    "s4r_prefill_project launch");
+}
+
 s4r_status s4r_dense_decode(const s4r_config* cfg, int64_t N, const void* q, const void* k_cache,
                             const void* v_cache, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   Problem P;

@@ -89,6 +89,10 @@ hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N,
 hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
                                const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                                int64_t row, hipStream_t st);
+size_t prefill_ws_bytes(const Problem& P);
+hipError_t launch_prefill_project(const Problem& P, int64_t n_rows, const void* s_k, const void* s_v,
+                                  const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, void* ws,
+                                  hipStream_t st);
 hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, int m, int k_eff,
                             const void* q, const void* sink_k, const void* sink_v,
                             const void* win_k, const void* win_v, const void* bases_k,

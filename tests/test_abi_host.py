@@ -171,3 +171,18 @@ def test_dense_comparator_argument_errors():
     assert call(cfg()) == L.S4R_ERR_UNSUPPORTED                     # head_dim 64
     assert call(cfg(head_dim=128, dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
     assert call(cfg(head_dim=128, n_q_heads=32, n_kv_heads=2)) == L.S4R_ERR_UNSUPPORTED   # G = 16
+
+
+def test_prefill_projection_argument_errors():
+    lib = L.load()
+
+    def call(c, n=100, s=FAKE, cv=FAKE, wsb=1 << 40):
+        return lib.s4r_prefill_project(ctypes.byref(c), n, s, FAKE, FAKE, FAKE, FAKE, cv, FAKE, wsb, None)
+    c = cfg()
+    assert call(c, n=0) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, n=1025) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, s=None) == L.S4R_ERR_NULL_ARG
+    assert call(c, cv=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert call(c, wsb=16) == L.S4R_ERR_WORKSPACE
+    assert call(cfg(dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
+    assert call(cfg(head_dim=128, rank=256)) == L.S4R_ERR_UNSUPPORTED      # rank > 192

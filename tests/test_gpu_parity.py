@@ -350,3 +350,41 @@ def test_dense_comparator(shape, N):
     ref = decode.dense_decode(f64(dc["q"]), f64(dc["k"][:, :N]), f64(dc["v"][:, :N]), wl.n_kv_heads,
                               oracle_cfg(c)["rope_theta"])
     assert rel_err_rows(out.cpu().numpy(), ref) <= 1e-4
+
+
+@pytest.mark.parametrize("n_rows,nb,rank", [(1000, 1, 160), (300, 8, 32), (16, 1, 96), (700, 2, 64)])
+def test_prefill_projection(n_rows, nb, rank):
+    """Bulk projection C = S B (Section 3.1) against the oracle's projection
+    rounded once to bf16.  The GPU sums exact bf16 products in fp32 over 32
+    chained MFMAs of 32 products, so its sum differs from the exact one by at
+    most about 64 * 2^-24 * sum_d |S_d B_d| (absolute); after both round to
+    bf16 the two values differ by at most that plus one bf16 ulp.  Almost all
+    coefficients must be bit-equal."""
+    from oracle import prefill, storage
+    wl = W.CONFIGS["llama8b_32k"].scaled(batch=2, N=n_rows + 4, rank=rank, basis_groups=nb)
+    st = W.latent_state(wl, seed=n_rows)
+    cap = ((n_rows + 15) // 16) * 16 + 16
+    c = cfg_from_workload(wl, capacity=cap)
+    rng = np.random.default_rng(n_rows)
+    S_k = W.round_storage(rng.standard_normal((wl.batch, n_rows, wl.Dp)), "bf16")
+    S_v = W.round_storage(3.0 * rng.standard_normal((wl.batch, n_rows, wl.Dp)), "bf16")
+    dt = torch.bfloat16
+    ck = torch.full((wl.batch, cap, wl.R), float("nan"), dtype=dt, device="cuda")
+    cv = torch.full_like(ck, float("nan"))
+    ws = s4r.alloc_workspace(c)
+    s4r.prefill_project(c, n_rows, dev(S_k, dt), dev(S_v, dt), dev(st["bases_k"], dt), dev(st["bases_v"], dt), ck, cv,
+                        ws)
+    torch.cuda.synchronize()
+    for S, cc, bases in ((S_k, ck, st["bases_k"]), (S_v, cv, st["bases_v"])):
+        ref = storage.round_to(prefill.project_tokens(S, bases), "bf16")
+        got = s4r.unpack_coef(c, cap, cc)
+        assert torch.isnan(got[:, n_rows:].float()).all(), "rows past n_rows were written"
+        g = got[:, :n_rows].float().cpu().numpy().astype(np.float64)
+        gb = torch.from_numpy(g.astype(np.float32)).view(torch.int32).numpy()
+        rb = torch.from_numpy(ref.astype(np.float32)).view(torch.int32).numpy()
+        exact = (gb == rb).mean()
+        absum = prefill.project_tokens(np.abs(S), np.abs(bases))
+        ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.maximum(np.abs(g), np.abs(ref)), 1e-30))) - 7)
+        bound = 64 * 2.0 ** -24 * absum + ulp
+        assert np.all(np.abs(g - ref) <= bound), f"max excess {np.max(np.abs(g - ref) / bound):.3f} of the bound"
+        assert exact > 0.999, f"bit-equal fraction {exact:.5f}"
