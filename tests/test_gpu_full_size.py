@@ -171,3 +171,38 @@ def test_dense_comparator_full_size():
         err = rel_err_rows(out[b:b + 1].cpu().numpy(), ref)
         print(f"[full-size] dense comparator sequence {b}: out err {err:.2e}", flush=True)
         assert err <= 1e-4
+
+
+def test_prefill_projection_full_size():
+    """The bulk projection at the headline shape as bench.py times it (B=4,
+    131072 rows of K and V, rank 160): 64 sampled rows of every sequence (the
+    first, the last and 62 seeded ones) against the oracle's projection,
+    within the fp32 summation bound of the parity test, almost all
+    bit-equal."""
+    from oracle import prefill, storage
+    wl = W.CONFIGS["llama8b_128k"]
+    n = wl.N
+    c = cfg_from_workload(wl, capacity=n)
+    st = W.latent_state(wl.scaled(N=2048 + 4), seed=3)          # bases only (per sequence)
+    dc = W.dense_cache(wl, seed=3)                               # raw rows [B, N, Dp]
+    dt = torch.bfloat16
+    bk = torch.from_numpy(st["bases_k"]).to("cuda", dt)
+    bv = torch.from_numpy(st["bases_v"]).to("cuda", dt)
+    ck = torch.empty((wl.batch, n, wl.R), dtype=dt, device="cuda")
+    cv = torch.empty_like(ck)
+    ws = s4r.alloc_workspace(c)
+    s4r.prefill_project(c, n, dc["k"], dc["v"], bk, bv, ck, cv, ws)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, n - 1], np.random.default_rng(3).integers(0, n, 62)]))
+    exact = []
+    for S, cc, bases in ((dc["k"], ck, st["bases_k"]), (dc["v"], cv, st["bases_v"])):
+        got = s4r.unpack_coef(c, n, cc)[:, rows].float().cpu().numpy().astype(np.float64)
+        Ss = S[:, rows].float().cpu().numpy().astype(np.float64)
+        ref = storage.round_to(prefill.project_tokens(Ss, bases), "bf16")
+        absum = prefill.project_tokens(np.abs(Ss), np.abs(bases))
+        ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.maximum(np.abs(got), np.abs(ref)), 1e-30))) - 7)
+        assert np.all(np.abs(got - ref) <= 64 * 2.0 ** -24 * absum + ulp)
+        exact.append((got == ref).mean())
+    print(f"[full-size] prefill projection: bit-equal fraction {min(exact):.5f} on {len(rows)} rows x {wl.batch}",
+          flush=True)
+    assert min(exact) > 0.999
