@@ -173,6 +173,28 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
                            hipStream_t stream);
 
 /*
+ * The fused decode step over a ragged batch (Section 3.2, each sequence at
+ * its own length): lengths[b] (host memory, B entries, read before the call
+ * returns) is sequence b's L, counted with the appended token when k_new /
+ * v_new are given, each in [q_window, capacity].  Every other argument is as
+ * for s4r_decode_step with L = max_b lengths[b]: coefficient rows past
+ * lengths[b] are never read, the new token goes into row lengths[b] - 1 of
+ * its sequence, the query sits at position n_sink + lengths[b] - 1,
+ * idx_out is [B, m] and scores_out [B, max L] (row b written up to
+ * lengths[b]).  Every sequence must select the same number of tokens
+ * m = min(topk, L_b - window) + min(window, L_b) (true whenever every
+ * L_b >= window + topk), else S4R_ERR_BAD_SHAPE; B <= 64, else
+ * S4R_ERR_UNSUPPORTED.
+ */
+s4r_status s4r_decode_step_ragged(const s4r_config* cfg, const int64_t* lengths, const void* q,
+                                  const float* qwin_prev, const void* sink_k, const void* sink_v,
+                                  const void* win_k, const void* win_v, const void* bases_k,
+                                  const void* bases_v, void* coef_k, void* coef_v,
+                                  const void* k_new, const void* v_new, float* out,
+                                  int32_t* idx_out, float* scores_out, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
+
+/*
  * Bulk projection of the prefill stage (Section 3.1, the coefficient
  * equation): C^K = S^K B^K and C^V = S^V B^V per basis group for the prompt's
  * non-sink rows, written into rows [0, n_rows) of the tiled coefficient caches

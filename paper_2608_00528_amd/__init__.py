@@ -14,6 +14,7 @@ _lib.load()
 from .api import (  # noqa: E402,F401
     alloc_workspace,
     decode_step,
+    decode_step_ragged,
     dense_decode,
     make_config,
     num_selected,

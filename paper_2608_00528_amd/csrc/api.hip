@@ -102,6 +102,7 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   P.GW = G * c->q_window;
   P.nruns_max = c->capacity / kTileTok;
   P.nwg_max = (P.nruns_max + kScoreWaves - 1) / kScoreWaves;   // tiles per wave >= 1
+  P.lens.n = 0;
   P.m_max = std::min<int64_t>(c->topk, std::max<int64_t>(c->capacity - c->window, 0)) +
             std::min<int64_t>(c->window, c->capacity);
   return S4R_OK;
@@ -130,7 +131,7 @@ Layout layout(const Problem& P) {
   sizes[kAtilde] = B * cap * 4;
   sizes[kHist] = B * 2 * kHistBins * 4;
   sizes[kCand] = B * cand_stride(P) * 8;
-  sizes[kBitmap] = B * (cap / 32) * 4;
+  sizes[kBitmap] = B * bitmap_words(cap) * 4;
   sizes[kIdx] = B * P.m_max * 4;
   sizes[kPartMl] = B * P.hq * kMaxSplit * 2 * 4;
   sizes[kPartO] = B * P.hq * kMaxSplit * P.dh * 4;
@@ -374,15 +375,14 @@ s4r_status s4r_dense_decode(const s4r_config* cfg, int64_t N, const void* q, con
   return hip_status(launch_dense_decode(P, w, N, q, k_cache, v_cache, out, stream), "s4r_dense_decode launch");
 }
 
-s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
-                           const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
-                           const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, const void* k_new,
-                           const void* v_new, float* out, int32_t* idx_out, float* scores_out, void* ws,
-                           size_t ws_bytes, hipStream_t stream) {
-  Problem P;
-  s4r_status st = make_problem(cfg, P);
-  if (st) return st;
-  if ((st = check_L(P, L))) return st;
+// the fused step for a uniform (P.lens.n == 0) or ragged batch; L is the
+// largest length, already checked against the capacity
+static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, const float* qwin_prev,
+                                   const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
+                                   const void* bases_k, const void* bases_v, void* coef_k, void* coef_v,
+                                   const void* k_new, const void* v_new, float* out, int32_t* idx_out,
+                                   float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  s4r_status st = S4R_OK;
   if (!attention_supported(P))
     return fail(S4R_ERR_UNSUPPORTED, "fused attention not built for G = %d, rank = %d", P.G, P.rank);
   S4R_REQ(q);
@@ -444,6 +444,47 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
                          timed ? &g_timing.stop[slot + 4] : nullptr);
   if (timed) g_timing.used++;
   return hip_status(e, "s4r_decode_step launch");
+}
+
+s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
+                           const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
+                           const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, const void* k_new,
+                           const void* v_new, float* out, int32_t* idx_out, float* scores_out, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  return decode_step_impl(P, L, q, qwin_prev, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
+                          v_new, out, idx_out, scores_out, ws, ws_bytes, stream);
+}
+
+s4r_status s4r_decode_step_ragged(const s4r_config* cfg, const int64_t* lengths, const void* q,
+                                  const float* qwin_prev, const void* sink_k, const void* sink_v, const void* win_k,
+                                  const void* win_v, const void* bases_k, const void* bases_v, void* coef_k,
+                                  void* coef_v, const void* k_new, const void* v_new, float* out, int32_t* idx_out,
+                                  float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (!lengths) return fail(S4R_ERR_NULL_ARG, "lengths is NULL");
+  if (P.B > kMaxRaggedB) return fail(S4R_ERR_UNSUPPORTED, "ragged batch of %d sequences exceeds %d", P.B, kMaxRaggedB);
+  int64_t L = 0, m0 = -1;
+  P.lens.n = P.B;
+  for (int b = 0; b < P.B; ++b) {
+    const int64_t Lb = lengths[b];
+    if ((st = check_L(P, Lb))) return st;
+    // every sequence selects the same number of tokens (the index rows share a stride)
+    const int64_t mb = std::min<int64_t>(P.k, std::max<int64_t>(Lb - P.W, 0)) + std::min<int64_t>(P.W, Lb);
+    if (m0 >= 0 && mb != m0)
+      return fail(S4R_ERR_BAD_SHAPE, "ragged lengths must give every sequence the same selected count (%lld vs %lld at b = %d)",
+                  (long long)m0, (long long)mb, b);
+    m0 = mb;
+    L = std::max(L, Lb);
+    P.lens.v[b] = (int32_t)Lb;
+  }
+  return decode_step_impl(P, L, q, qwin_prev, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
+                          v_new, out, idx_out, scores_out, ws, ws_bytes, stream);
 }
 
 s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_new, const void* v_new,

@@ -42,8 +42,9 @@ __global__ __launch_bounds__(256) void k_attn_combine(
     const T* __restrict__ q, const T* __restrict__ sink_k, const T* __restrict__ sink_v,
     const T* __restrict__ win_k, const T* __restrict__ win_v, const float* __restrict__ part_ml,
     const float* __restrict__ part_o, float* __restrict__ out, int nsplit, int hq, int hkv, int dh,
-    int s_sink, int W, int64_t L, double rope_ratio) {
+    int s_sink, int W, int64_t L, double rope_ratio, Lens lens) {
   const int h = blockIdx.x, b = blockIdx.y;
+  L = len_of(lens, b, L);
   const int G = hq / hkv, j = h / G;
   const int Dp = hkv * dh;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -393,11 +394,12 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
     hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q,
                        (const uint16_t*)sink_k, (const uint16_t*)sink_v, (const uint16_t*)win_k,
                        (const uint16_t*)win_v, ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L,
-                       rope_ratio(P));
+                       rope_ratio(P), P.lens);
   else
     hipLaunchKernelGGL(k_attn_combine<float>, dim3(P.hq, P.B), dim3(256), 0, st, (const float*)q,
                        (const float*)sink_k, (const float*)sink_v, (const float*)win_k, (const float*)win_v,
-                       ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P));
+                       ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P),
+                       P.lens);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && t1) e = hipEventRecord(t1[1], st);
   return e;
@@ -409,7 +411,7 @@ hipError_t launch_combine_only(const Problem& P, const Workspace& ws, int64_t L,
                                hipStream_t st) {
   hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q, nullptr,
                      nullptr, nullptr, nullptr, ws.part_ml, ws.part_o, out, nsplit, P.hq, P.hkv, P.dh, 0, 0, L,
-                     rope_ratio(P));
+                     rope_ratio(P), P.lens);
   return hipGetLastError();
 }
 

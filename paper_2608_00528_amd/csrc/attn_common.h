@@ -97,11 +97,12 @@ __global__ __launch_bounds__(DH * 2, (attn_split_occupancy<T, RBH, G>())) void k
     const T* __restrict__ coef_k, const T* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int nsplit,
     int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap, int bases_shared,
-    float theta) {
+    float theta, Lens lens) {
   constexpr int NP = Parts<T>::n;
   constexpr int NWAVE = DH / 32;          // waves per workgroup
   constexpr int HALF_MB = DH / 32;        // pair offset in 16-dim blocks
   const int split = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  L = len_of(lens, b, L);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = lane & 15, kg = lane >> 4;
   const int Dp = hkv * DH, Dg = Dp / nb;

@@ -80,7 +80,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int tpw, int nsplit,
     int ngroups, int G, int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap,
-    int bases_shared, double rope_ratio) {
+    int bases_shared, double rope_ratio, Lens lens) {
   constexpr int DH = NW * 32;                      // NMH = ceil(G / 4): 4 heads per MFMA row group
   static_assert(NW >= 2, "a tile pair is gathered by two waves");
   // ---- work item: KV head j of group (sequence, split); the workgroups of
@@ -91,6 +91,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   const int grp_id = (r8 / hkv) * 8 + xcd;
   if (grp_id >= ngroups) return;
   const int b = grp_id / nsplit, split = grp_id % nsplit;
+  L = len_of(lens, b, L);
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = lane & 15, kg = lane >> 4;
@@ -385,7 +386,7 @@ static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int
   hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
                      (const uint16_t*)bk, (const uint16_t*)bv, (const uint16_t*)ck, (const uint16_t*)cv, ws.idx,
                      (int64_t)m, ws.part_ml, ws.part_o, n_proc, tpw, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb,
-                     P.rank, P.R, P.s, L, P.cap, P.bases_shared, rope_ratio(P));
+                     P.rank, P.R, P.s, L, P.cap, P.bases_shared, rope_ratio(P), P.lens);
   *nsplit_out = nsplit;
 }
 

@@ -15,7 +15,7 @@ static void launch_split_t(const Problem& P, const Workspace& ws, int64_t L, int
   hipLaunchKernelGGL((k_attn_split<T, RBH, DH, G>), dim3(nsplit, P.hkv, P.B), dim3(DH * 2), lds, st, (const T*)q,
                      (const T*)bases_k, (const T*)bases_v, (const T*)coef_k, (const T*)coef_v, ws.idx,
                      (int64_t)m, ws.part_ml, ws.part_o, n_proc, nsplit, P.hq, P.hkv, P.nb, P.rank, P.R,
-                     P.s, L, P.cap, P.bases_shared, P.theta);
+                     P.s, L, P.cap, P.bases_shared, P.theta, P.lens);
 }
 
 #define S4R_SPLIT_ARGS P, ws, L, m, n_proc, nsplit, q, bk, bv, ck, cv, st

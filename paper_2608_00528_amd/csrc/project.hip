@@ -231,8 +231,10 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
                                                       const T* __restrict__ k_new, const T* __restrict__ v_new,
                                                       T* __restrict__ coef_k, T* __restrict__ coef_v,
                                                       int64_t append_row, int hkv, int dh, int nb, int rank, int R,
-                                                      int bases_shared, int64_t cap) {
-  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, append_row, hkv, dh, nb, rank, R,
+                                                      int bases_shared, int64_t cap, Lens lens) {
+  // a ragged batch appends at each sequence's own last row
+  const int64_t row = lens.n ? (int64_t)lens.v[blockIdx.y] - 1 : append_row;
+  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, rank, R,
                        bases_shared, cap, blockIdx.x, blockIdx.y, blockIdx.z);
 }
 
@@ -247,7 +249,7 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
                                                       T* __restrict__ coef_v, double* __restrict__ qpart,
                                                       uint32_t* __restrict__ hist, int64_t append_row, int hq,
                                                       int hkv, int dh, int G, int nb, int rank, int R,
-                                                      int bases_shared, int64_t cap, int B, int nch) {
+                                                      int bases_shared, int64_t cap, int B, int nch, Lens lens) {
   const int ncb = R / 32;
   const int nq = ncb * nch * B;
   int id = blockIdx.x;
@@ -257,7 +259,8 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
   } else {
     id -= nq;
     const int cblk = id % ncb, b = (id / ncb) % B, which = id / (ncb * B);
-    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, append_row, hkv, dh, nb, rank, R,
+    const int64_t row = lens.n ? (int64_t)lens.v[b] - 1 : append_row;
+    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, rank, R,
                          bases_shared, cap, cblk, b, which);
   }
 }
@@ -281,11 +284,11 @@ hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void
   if (P.dtype == S4R_BF16)
     hipLaunchKernelGGL(k_project_rows<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)bases_k,
                        (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
-                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.bases_shared, P.cap);
+                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.bases_shared, P.cap, P.lens);
   else
     hipLaunchKernelGGL(k_project_rows<float>, grid, dim3(256), 0, st, (const float*)bases_k, (const float*)bases_v,
                        (const float*)k_new, (const float*)v_new, (float*)coef_k, (float*)coef_v, row, P.hkv, P.dh,
-                       P.nb, P.rank, P.R, P.bases_shared, P.cap);
+                       P.nb, P.rank, P.R, P.bases_shared, P.cap, P.lens);
   return hipGetLastError();
 }
 
@@ -298,12 +301,12 @@ hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, 
     hipLaunchKernelGGL(k_project_step<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q, (const uint16_t*)bases_k,
                        (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
                        (uint16_t*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
-                       P.bases_shared, P.cap, P.B, nch);
+                       P.bases_shared, P.cap, P.B, nch, P.lens);
   else
     hipLaunchKernelGGL(k_project_step<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k,
                        (const float*)bases_v, (const float*)k_new, (const float*)v_new, (float*)coef_k,
                        (float*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared,
-                       P.cap, P.B, nch);
+                       P.cap, P.B, nch, P.lens);
   return hipGetLastError();
 }
 

@@ -95,12 +95,20 @@ template <int NQ, int TPT, bool WQ1>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
-    int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg) {
+    int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
+    Lens lens) {
   constexpr int GWP = 4 * NQ;
   constexpr int CHUNK = kRelThreads * TPT;
   constexpr int SPAN_MAX = CHUNK + 64;
   constexpr int PPT = (SPAN_MAX + kRelThreads - 1) / kRelThreads;   // staged positions per thread
   const int b = blockIdx.y;
+  const int score_stride = L;                      // scores_out rows are [B, L] with the call's (largest) L
+  {                                                // this sequence's length (ragged batch: n_hist shifts with it)
+    const int Lb = (int)len_of(lens, b, L);
+    n_hist += Lb - L;
+    L = Lb;
+  }
+  if ((int)blockIdx.x * kRelThreads * TPT >= L) return;   // past this sequence's end
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int GW = G * Wq;
   const int h = kappa / 2;
@@ -262,7 +270,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const int x = t0 + t + j * kRelThreads;
     if (x < L) {
       atilde[(int64_t)b * cap + x] = af[j];
-      if (scores_out) scores_out[(int64_t)b * L + x] = af[j];
+      if (scores_out) scores_out[(int64_t)b * score_stride + x] = af[j];
     }
     if (x < n_hist) atomicAdd(&hl[score_key(af[j]) >> kHistShift], 1u);
   }
@@ -354,7 +362,7 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), nwg);
+                     (int)(P.cap / kTileTok), nwg, P.lens);
 }
 
 template <int NQ>

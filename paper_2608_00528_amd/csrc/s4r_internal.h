@@ -23,6 +23,15 @@ constexpr int kMaxGW = 16;            // G * W_q columns handled by one MFMA blo
 constexpr int kPChunk = 256;          // basis rows per query-projection workgroup
 constexpr int kQMaxChunks = 8;        // row chunks per basis group (Dp / basis_groups <= 2048)
 
+// per-sequence lengths of a ragged batch, passed to the kernels by value
+// (n = 0: every sequence has the call's L)
+constexpr int kMaxRaggedB = 64;
+struct Lens {
+  int32_t n;
+  int32_t v[kMaxRaggedB];
+};
+__host__ __device__ inline int64_t len_of(const Lens& l, int b, int64_t L) { return l.n ? (int64_t)l.v[b] : L; }
+
 struct Problem {
   int B, hq, hkv, dh, G, Dp;
   int nb, rank, R, Dg;                // basis groups, rank per group, R = nb*rank, Dg = Dp/nb
@@ -34,6 +43,7 @@ struct Problem {
   int64_t nruns_max;                  // 16-token tiles at L = cap (one softmax reference each)
   int64_t nwg_max;                    // scoring workgroups per sequence, any L <= cap
   int64_t m_max;                      // selected tokens at L = cap
+  Lens lens;                          // ragged batch (n = 0: uniform)
 };
 
 struct Workspace {
@@ -48,7 +58,7 @@ struct Workspace {
   uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
   uint32_t* above_count; // [B][sel_groups_max] positions above the boundary bin per classify workgroup
   uint32_t* sel_info;   // [B][4] boundary bin and the count above it
-  uint32_t* bitmap;     // [B][cap / 32]  selected global positions
+  uint32_t* bitmap;     // [B][bitmap_words(cap)]  selected global positions
   int32_t* idx;         // [B][m_max]
   float* part_ml;       // [B][hq][kMaxSplit][2]   split partial (max, sum)
   float* part_o;        // [B][hq][kMaxSplit][dh]  split partial outputs
@@ -58,6 +68,9 @@ struct Workspace {
 
 Workspace carve_workspace(const Problem& P, void* base);
 int score_workgroups(const Problem& P, int64_t L);
+// bitmap words of one sequence (rounded up: a capacity that is an odd
+// multiple of 16 ends in half a word)
+__host__ __device__ inline int64_t bitmap_words(int64_t cap) { return (cap + 31) / 32; }
 inline int64_t sel_groups_max(const Problem& P) { return (P.cap + kSelChunk - 1) / kSelChunk; }
 inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelChunk; }
 // query columns G * W_q rounded up to a multiple of 4 (one 16-byte group per

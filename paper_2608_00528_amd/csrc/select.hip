@@ -99,12 +99,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
     const float* __restrict__ scores, int64_t score_stride, uint32_t* __restrict__ hist_all,
     uint64_t* __restrict__ cand_all, uint32_t* __restrict__ bitmap_all, uint32_t* __restrict__ cand_count,
     uint32_t* __restrict__ above_count, uint32_t* __restrict__ sel_info, int64_t cand_stride, int64_t cnt_stride,
-    int64_t cap, int L, int W, int k) {
+    int64_t cap, int L, int W, int k, Lens lens) {
   const int b = blockIdx.y, c = blockIdx.x;
+  L = (int)len_of(lens, b, L);
   const int t = threadIdx.x, lane = t & 63;
   const int n_hist = max(L - W, 0);
   const int k_eff = min(k, n_hist);
-  if (k_eff == 0) return;
+  if (k_eff == 0 || c * kSelChunk >= n_hist) return;   // (a shorter sequence of a ragged batch)
   uint32_t* hist1 = hist_all + (int64_t)b * 2 * kHistBins;
   uint32_t* hist2 = hist1 + kHistBins;
   uint64_t* cand = cand_all + (int64_t)b * cand_stride + (int64_t)c * kSelChunk;
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
                  m3 = (uint32_t)__shfl_down((int)mask8, 3);
   const uint32_t word = mask8 | (m1 << 8) | (m2 << 16) | (m3 << 24);
   const int wi = t >> 2;                                // word index within the chunk
-  if ((lane & 3) == 0 && c0 + wi * 32 < n_hist) bitmap_all[(int64_t)b * (cap / 32) + c0 / 32 + wi] = word;
+  if ((lane & 3) == 0 && c0 + wi * 32 < n_hist) bitmap_all[b * bitmap_words(cap) + c0 / 32 + wi] = word;
   uint32_t excl;
   const uint32_t n_above = block_exclusive_scan((uint32_t)__popc(mask8), scratch, excl);
   __syncthreads();                                      // s_count and h2 complete
@@ -183,9 +184,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
     const uint32_t* __restrict__ bitmap_all, const uint32_t* __restrict__ cand_count,
     const uint32_t* __restrict__ above_count, const uint32_t* __restrict__ sel_info, int32_t* __restrict__ idx_all,
     int32_t* __restrict__ idx_copy, int64_t idx_stride, int64_t cand_stride, int64_t cnt_stride, int64_t cap, int L,
-    int W, int k) {
+    int W, int k, Lens lens) {
   constexpr uint64_t kLow42 = (1ull << 42) - 1;          // low 10 key bits + position bits
   const int b = blockIdx.y, c = blockIdx.x;
+  L = (int)len_of(lens, b, L);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n_hist = max(L - W, 0);
   const int k_eff = min(k, n_hist);
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
       if (idx2) idx2[k_eff + i] = n_hist + i;
     }
   }
-  if (k_eff == 0) return;
+  if (k_eff == 0 || c >= max(nch, 1)) return;          // (a shorter sequence of a ragged batch)
   const uint32_t* hist2 = hist_all + (int64_t)b * 2 * kHistBins + kHistBins;
   const uint64_t* cand_b = cand_all + (int64_t)b * cand_stride;
 
@@ -223,7 +225,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   const int wbase = c * (kSelChunk / 32);
   const int nwords = (n_hist + 31) / 32;
   uint32_t myword = 0u;
-  if (t < kSelChunk / 32) myword = bitmap_all[(int64_t)b * (cap / 32) + min(wbase + t, nwords - 1)];
+  if (t < kSelChunk / 32) myword = bitmap_all[b * bitmap_words(cap) + min(wbase + t, nwords - 1)];
   const uint32_t need = (uint32_t)k_eff - above1;        // >= 1
   int b2;
   uint32_t above2;
@@ -399,11 +401,11 @@ hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const
   if (std::min<int64_t>(P.k, n_hist) > 0) {
     hipLaunchKernelGGL(k_select_classify, dim3(nch, P.B), dim3(kSelThreads), 0, st, scores, score_stride, ws.hist,
                        ws.cand, ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P),
-                       sel_groups_max(P), P.cap, (int)L, P.W, P.k);
+                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens);
   }
   hipLaunchKernelGGL(k_select_finish, dim3(std::max(nch, 1), P.B), dim3(kSelThreads), 0, st, ws.hist, ws.cand,
                      ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, idx, idx_copy, (int64_t)m,
-                     cand_stride(P), sel_groups_max(P), P.cap, (int)L, P.W, P.k);
+                     cand_stride(P), sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens);
   return hipGetLastError();
 }
 

@@ -67,10 +67,11 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     const T* __restrict__ coef_k, const double* __restrict__ qpart, const float* __restrict__ qwin_prev,
     float* __restrict__ qcoef_out, float* __restrict__ e_out, float* __restrict__ tref,
     double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int nch, int ntiles_cap, int tiles_per_wave,
-    int nwg, double scale) {
+    int nwg, double scale, Lens lens) {
   constexpr int R = RB * kBlkCol;
   constexpr int NP = BLoad<T>::kParts;
   const int b = blockIdx.y;
+  L = (int)len_of(lens, b, L);                     // this sequence's length (ragged batch)
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int slot = lane & 15, kg = lane >> 4;      // token slot / k-group (= query column within an MFMA)
   const int GW = G * Wq;
@@ -274,7 +275,7 @@ static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, c
   const int nwg = score_workgroups(P, L);
   hipLaunchKernelGGL((k_score_stream<T, RB, NM>), dim3(nwg, P.B), dim3(256), 0, st, (const T*)coef_k, ws.qpart,
                      qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
-                     (int)(P.cap / kTileTok), tpw, nwg, 1.0 / sqrt((double)P.R));
+                     (int)(P.cap / kTileTok), tpw, nwg, 1.0 / sqrt((double)P.R), P.lens);
 }
 
 template <typename T, int RB>

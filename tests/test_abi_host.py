@@ -133,6 +133,25 @@ def test_decode_step_argument_errors():
     assert call(c=c0, sink=None) == L.S4R_ERR_BAD_SHAPE
 
 
+def test_ragged_decode_step_argument_errors():
+    lib = L.load()
+
+    def call(lens, c=None, out=FAKE, wsb=1 << 40):
+        c = c or cfg()
+        arr = None if lens is None else (ctypes.c_int64 * len(lens))(*lens)
+        return lib.s4r_decode_step_ragged(ctypes.byref(c), arr, FAKE, None, FAKE, FAKE, None, None, FAKE, FAKE,
+                                          FAKE, FAKE, None, None, out, None, None, FAKE, wsb, None)
+    assert call(None) == L.S4R_ERR_NULL_ARG                      # no lengths
+    assert call([100, 0]) == L.S4R_ERR_BAD_SHAPE                 # a length below 1
+    assert call([100, 1025]) == L.S4R_ERR_BAD_SHAPE              # a length past the capacity
+    # window 16 + topk 32: a sequence of 40 selects 40, one of 100 selects 48
+    assert call([100, 40]) == L.S4R_ERR_BAD_SHAPE
+    assert call([100, 48], wsb=0) == L.S4R_ERR_WORKSPACE         # equal counts pass on to the workspace check
+    assert call([100, 48], out=None) == L.S4R_ERR_NULL_ARG
+    c65 = cfg(batch=65)
+    assert call([100] * 65, c=c65) == L.S4R_ERR_UNSUPPORTED      # more sequences than the length table holds
+
+
 def test_other_entry_point_errors():
     c = cfg()
     lib = L.load()

@@ -267,6 +267,34 @@ def test_decode_edge_cases(L, W_, k, s):
     assert rel_err_rows(o, o_ref) <= 2e-2
 
 
+def test_decode_step_capacity_odd_multiple_of_16():
+    """Capacity 3024 = 189 x 16 and a window of 4 (the paper's setting): the
+    non-window part, 3020 positions, spans 95 bitmap words while the capacity
+    holds 94.5; each sequence's selection must stay in its own row."""
+    L = 3024
+    wl = W.CONFIGS["qwen3_4b_120k"].scaled(N=L + 4, batch=3, topk=200, n_needles=3)
+    st = W.latent_state(wl, seed=14)
+    c = cfg_from_workload(wl)
+    assert c.capacity == L and c.window == 4
+    g = to_gpu_state(c, st)
+    qwin = torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    ws = s4r.alloc_workspace(c)
+    m = s4r.num_selected(c, L)
+    idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
+    scores = torch.empty((wl.batch, L), dtype=torch.float32, device="cuda")
+    out = s4r.decode_step(c, L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
+                          g["coef_v"], ws, qwin_prev=qwin, idx_out=idx, scores_out=scores)
+    torch.cuda.synchronize()
+    ref = decode.decode_step(oracle_cfg(c, wl.pool_mode, wl.group_agg), L, st["q"], st["sink_k"], st["sink_v"],
+                             st["bases_k"], st["bases_v"], st["coef_k"], st["coef_v"], qwin_prev=st["qwin_prev"])
+    idx_np = idx.cpu().numpy().astype(np.int64)
+    check_selection(idx_np, ref["idx"], ref["a_tilde"], L, wl.window, wl.topk)
+    assert np.array_equal(idx_np, decode.select(scores.cpu().numpy().astype(np.float64), L, wl.window, wl.topk))
+    o_ref, _, _ = decode.sparse_attention(st["q"], idx_np, st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                                          st["coef_k"], st["coef_v"], L, wl.n_kv_heads, oracle_cfg(c)["rope_theta"])
+    assert rel_err_rows(out.cpu().numpy(), o_ref) <= OUT_TOL["bf16"]
+
+
 def test_append_then_step():
     wl = W.CONFIGS["llama8b_32k"].scaled(N=4000 + 4, batch=2, topk=128)
     L = wl.L
@@ -388,3 +416,113 @@ def test_prefill_projection(n_rows, nb, rank):
         bound = 64 * 2.0 ** -24 * absum + ulp
         assert np.all(np.abs(g - ref) <= bound), f"max excess {np.max(np.abs(g - ref) / bound):.3f} of the bound"
         assert exact > 0.999, f"bit-equal fraction {exact:.5f}"
+
+
+def _slice_state(st, b, L_b):
+    """Sequence b of a batch state, coefficient rows cut at L_b."""
+    one = {}
+    for key, x in st.items():
+        if key == "needles" or x is None or not isinstance(x, np.ndarray):
+            one[key] = x
+            continue
+        one[key] = x[b:b + 1]
+    one["coef_k"], one["coef_v"] = st["coef_k"][b:b + 1, :L_b], st["coef_v"][b:b + 1, :L_b]
+    return one
+
+
+@pytest.mark.parametrize("shape,lengths,append", [
+    ("llama8b_32k", (6000, 3001, 1777), False),
+    ("llama8b_32k", (2900, 6004, 4097), True),
+    ("qwen3_4b_120k", (5000, 2222, 4999, 700), True),
+])
+def test_ragged_decode_step(shape, lengths, append):
+    """Each sequence at its own length in one launch equals the oracle's step
+    on that sequence alone (Section 3.2 per sequence); rows past a sequence's
+    end hold NaN and must never be read."""
+    B, Lmax = len(lengths), max(lengths)
+    base = W.CONFIGS[shape]
+    wl = base.scaled(N=Lmax + base.n_sink, batch=B, topk=min(base.topk, 300), n_needles=4)
+    st = W.latent_state(wl, seed=11)
+    c = cfg_from_workload(wl)
+    st_gpu = dict(st)
+    for key in ("coef_k", "coef_v"):
+        x = st[key].copy()
+        for b, L_b in enumerate(lengths):
+            x[b, L_b - (1 if append else 0):] = np.nan
+        st_gpu[key] = x
+    g = to_gpu_state(c, st_gpu)
+    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    kw = {}
+    if append:
+        rng = np.random.default_rng(12)
+        kn = W.round_storage(rng.standard_normal((B, wl.Dp)), "bf16")
+        vn = W.round_storage(rng.standard_normal((B, wl.Dp)), "bf16")
+        kw = dict(k_new=dev(kn, torch.bfloat16), v_new=dev(vn, torch.bfloat16))
+    ws = s4r.alloc_workspace(c)
+    m = s4r.num_selected(c, min(lengths))
+    assert m == s4r.num_selected(c, Lmax)
+    idx = torch.empty((B, m), dtype=torch.int32, device="cuda")
+    scores = torch.full((B, Lmax), -7.0, dtype=torch.float32, device="cuda")
+    out = s4r.decode_step_ragged(c, lengths, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"],
+                                 g["coef_k"], g["coef_v"], ws, qwin_prev=qwin, idx_out=idx, scores_out=scores,
+                                 **kw)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert np.isfinite(o).all()
+    idx_np = idx.cpu().numpy().astype(np.int64)
+    sc = scores.cpu().numpy()
+    rows_k = s4r.unpack_coef(c, Lmax, g["coef_k"]).float().cpu().numpy().astype(np.float64)
+    rows_v = s4r.unpack_coef(c, Lmax, g["coef_v"]).float().cpu().numpy().astype(np.float64)
+    theta = oracle_cfg(c)["rope_theta"]
+    for b, L_b in enumerate(lengths):
+        one = _slice_state(st, b, L_b)
+        if append:
+            # the new rows went to row L_b - 1 of this sequence only: equal to the
+            # oracle's projection up to one bf16 rounding step ...
+            ck, cv = decode.project_append(kn[b:b + 1], vn[b:b + 1], one["bases_k"], one["bases_v"],
+                                           oracle_cfg(c)["dtype"])
+            assert np.abs(rows_k[b, L_b - 1] - ck[0]).max() <= 2 ** -7 * np.abs(ck).max()
+            assert (rows_k[b, L_b - 1] == ck[0]).mean() > 0.99
+            assert (rows_v[b, L_b - 1] == cv[0]).mean() > 0.99
+            assert np.isnan(rows_k[b, L_b:]).all()
+            # ... and the step is checked on the stored rows the GPU read
+            one["coef_k"], one["coef_v"] = rows_k[b:b + 1, :L_b], rows_v[b:b + 1, :L_b]
+        ref = decode.decode_step(oracle_cfg(c, wl.pool_mode, wl.group_agg), L_b, one["q"], one["sink_k"],
+                                 one["sink_v"], one["bases_k"], one["bases_v"], one["coef_k"], one["coef_v"],
+                                 qwin_prev=one["qwin_prev"])
+        # scores: row b written up to L_b, untouched after
+        a_ref = ref["a_tilde"][0]
+        err = np.abs(sc[b, :L_b] - a_ref) / np.maximum(np.abs(a_ref), 1e-30)
+        assert err.max() <= SCORE_TOL, f"sequence {b} (L = {L_b}): score rel err {err.max():.3e}"
+        assert (sc[b, L_b:] == -7.0).all()
+        check_selection(idx_np[b:b + 1], ref["idx"], ref["a_tilde"], L_b, wl.window, wl.topk)
+        assert np.array_equal(idx_np[b:b + 1], decode.select(sc[b:b + 1, :L_b].astype(np.float64), L_b,
+                                                             wl.window, wl.topk))
+        o_ref, _, _ = decode.sparse_attention(one["q"], idx_np[b:b + 1], one["sink_k"], one["sink_v"],
+                                              one["bases_k"], one["bases_v"], rows_k[b:b + 1, :L_b],
+                                              rows_v[b:b + 1, :L_b], L_b, wl.n_kv_heads, theta)
+        err = rel_err_rows(o[b:b + 1], o_ref)
+        assert err <= OUT_TOL["bf16"], f"sequence {b} (L = {L_b}): output rel err {err:.3e}"
+
+
+def test_ragged_equal_lengths_match_uniform_step():
+    """A ragged call whose lengths are all equal is the uniform step, bit for bit."""
+    wl = W.CONFIGS["llama8b_32k"].scaled(N=5000 + 4, batch=3, topk=256)
+    st = W.latent_state(wl, seed=13)
+    c = cfg_from_workload(wl)
+    g = to_gpu_state(c, st)
+    ws = s4r.alloc_workspace(c)
+    m = s4r.num_selected(c, wl.L)
+    outs, idxs = [], []
+    for ragged in (False, True):
+        idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
+        args = (g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"], g["coef_v"], ws)
+        if ragged:
+            o = s4r.decode_step_ragged(c, [wl.L] * wl.batch, *args, idx_out=idx)
+        else:
+            o = s4r.decode_step(c, wl.L, *args, idx_out=idx)
+        torch.cuda.synchronize()
+        outs.append(o.cpu())
+        idxs.append(idx.cpu())
+    assert torch.equal(idxs[0], idxs[1])
+    assert torch.equal(outs[0], outs[1])
