@@ -357,6 +357,36 @@ def main():
         log(f"[bench] prefill bulk projection: {pf_us:.1f} us ({comparator['prefill_projection']['achieved_GBps']:.0f} GB/s)")
         del dk, dv, wsd, pk, pv, wspf
         torch.cuda.synchronize()
+        # full-reconstruction low-rank decoding (Appendix B.1) over the same
+        # coefficient caches: every one of the L tokens reconstructed
+        ck0, cv0 = replicas[0]
+        outf = torch.empty_like(out)
+        for _ in range(2):
+            s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
+        torch.cuda.synchronize()
+        f0 = torch.cuda.Event(enable_timing=True)
+        f1 = torch.cuda.Event(enable_timing=True)
+        nfr = 10
+        f0.record(stream)
+        for _ in range(nfr):
+            s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        fr_us = f0.elapsed_time(f1) * 1e3 / nfr
+        fr_flops = 2 * 2 * wl.batch * wl.L * wl.R * wl.Dp
+        comparator["full_reconstruction"] = {
+            "what": "full-reconstruction low-rank decoding (Appendix B.1): s4r_full_recon_decode, every non-sink "
+                    "token reconstructed on the matrix cores (k_attn_tiles over all tokens + k_attn_combine)",
+            "us_per_step": round(fr_us, 2),
+            "reconstruction_flops": fr_flops,
+            "achieved_TFLOPs": round(fr_flops / (fr_us * 1e-6) / 1e12, 1),
+            "frac_of_bf16_peak": round(fr_flops / (fr_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "s4r_step_speedup": round(fr_us / (ms_step * 1e3), 2),
+        }
+        log(f"[bench] full-reconstruction comparator: {fr_us:.1f} us/step "
+            f"({comparator['full_reconstruction']['achieved_TFLOPs']:.0f} TFLOP/s), "
+            f"S4R step {comparator['full_reconstruction']['s4r_step_speedup']:.2f}x faster")
+        del outf
 
     # per-kernel pass (events between kernels), same steps again
     nk = min(args.steps, 200)

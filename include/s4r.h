@@ -195,6 +195,23 @@ s4r_status s4r_decode_step_ragged(const s4r_config* cfg, const int64_t* lengths,
                                   hipStream_t stream);
 
 /*
+ * Comparator (Appendix B.1, "full reconstruction"; not the method): the
+ * cache is stored as coefficients like S^4R's, but every one of the L
+ * non-sink tokens is reconstructed, K^ = C^K (B^K)^T and V^ = C^V (B^V)^T,
+ * and attention runs over the sinks and all of them: out[b, h] =
+ * softmax(RoPE(q_h) RoPE(K*_j)^T / sqrt(d_h)) V*_j, K* = [sink_k; K^],
+ * j = h / G, query at position n_sink + L - 1.  The reconstructed rows stay
+ * on chip (the MFMA kernel of s4r_decode_step over every token, no index
+ * list).  Arguments as for s4r_decode_step; out [B, h_q, d_h] fp32.  bf16
+ * storage, head_dim 64 or 128, G <= 8 and the fused kernel's ranks only
+ * (otherwise S4R_ERR_UNSUPPORTED).
+ */
+s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q, const void* sink_k,
+                                 const void* sink_v, const void* bases_k, const void* bases_v,
+                                 const void* coef_k, const void* coef_v, float* out, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
+/*
  * Bulk projection of the prefill stage (Section 3.1, the coefficient
  * equation): C^K = S^K B^K and C^V = S^V B^V per basis group for the prompt's
  * non-sink rows, written into rows [0, n_rows) of the tiled coefficient caches

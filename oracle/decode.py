@@ -256,6 +256,24 @@ def dense_decode(q, k_cache, v_cache, n_kv_heads, theta):
     return out
 
 
+def full_reconstruction_decode(q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, L, n_kv_heads, theta):
+    """Comparator, not S^4R: full-reconstruction low-rank decoding (Appendix
+    B.1).  Every cached non-sink token is reconstructed, K = C^K (B^K)^T and
+    V = C^V (B^V)^T (rows 0..L-1), the result is laid out as a plain KV cache
+    (sinks at positions 0..s-1, token l at s + l, keys rotated at their
+    positions, R6) and attended to as in the Full-KV decode, the query at
+    s + L - 1.  Returns [B, h_q, d_h]."""
+    k_hat = reconstruct(_f64(coef_k)[:, :L], bases_k)
+    v_hat = reconstruct(_f64(coef_v)[:, :L], bases_v)
+    k_all = np.concatenate([_f64(sink_k), k_hat], axis=1)
+    v_all = np.concatenate([_f64(sink_v), v_hat], axis=1)
+    B, N, Dp = k_all.shape
+    dh = q.shape[2]
+    pos = np.broadcast_to(np.arange(N, dtype=np.float64)[None, :, None], (B, N, Dp // dh))
+    k_rot = rope(k_all.reshape(B, N, Dp // dh, dh), pos, theta).reshape(B, N, Dp)
+    return dense_decode(q, k_rot, v_all, n_kv_heads, theta)
+
+
 def relevance(q, qwin_prev, bases_k, coef_k, L, n_kv_heads, pool_kernel=7,
               pool_mode="max", group_agg="mean"):
     """Latent relevance A~ of every non-sink token (3.2.2 and the first two

@@ -16,6 +16,7 @@ from .api import (  # noqa: E402,F401
     decode_step,
     decode_step_ragged,
     dense_decode,
+    full_recon_decode,
     make_config,
     num_selected,
     pack_coef,

@@ -20,6 +20,7 @@ EXPORTS = (
     "s4r_decode_step", "s4r_project_append", "s4r_pack_coef", "s4r_unpack_coef",
     "s4r_timing_enable", "s4r_timing_read", "s4r_read_bandwidth_sink_len", "s4r_read_bandwidth",
     "s4r_dense_decode", "s4r_prefill_project", "s4r_decode_step_ragged",
+    "s4r_full_recon_decode",
 )
 
 
@@ -71,6 +72,7 @@ _SIGS = {
     "s4r_read_bandwidth": (_I32, [_P, _I64, _P, _P]),
     "s4r_dense_decode": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "s4r_prefill_project": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "s4r_full_recon_decode": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "s4r_decode_step_ragged": (_I32, [_CFG, ctypes.POINTER(_I64), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       _P, _P, _P, _P, _P, _SZ, _P]),
 }

@@ -190,6 +190,21 @@ def prefill_project(cfg, n_rows, s_k, s_v, bases_k, bases_v, coef_k, coef_v, ws)
                                          _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
 
 
+def full_recon_decode(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, ws, out=None):
+    """Comparator (Appendix B.1): attention over the sinks and every one of
+    the `length` tokens reconstructed from the coefficient caches."""
+    dt = storage_dtype(cfg)
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    need_sink = cfg.n_sink > 0
+    L.check(L.load().s4r_full_recon_decode(
+        _cfgp(cfg), length, _ptr(q, "q", dt), _ptr(sink_k, "sink_k", dt, need_sink),
+        _ptr(sink_v, "sink_v", dt, need_sink), _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt),
+        _ptr(coef_k, "coef_k", dt), _ptr(coef_v, "coef_v", dt), _ptr(out, "out", torch.float32),
+        _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+    return out
+
+
 def dense_decode(cfg, n_tokens, q, k_cache, v_cache, ws, out=None):
     """Comparator: dense GQA decode over an uncompressed bf16 KV cache
     [B, capacity, Dp] (keys stored after RoPE) for tokens 0..n_tokens-1."""

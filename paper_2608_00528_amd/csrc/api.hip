@@ -375,6 +375,32 @@ s4r_status s4r_dense_decode(const s4r_config* cfg, int64_t N, const void* q, con
   return hip_status(launch_dense_decode(P, w, N, q, k_cache, v_cache, out, stream), "s4r_dense_decode launch");
 }
 
+s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q, const void* sink_k,
+                                 const void* sink_v, const void* bases_k, const void* bases_v, const void* coef_k,
+                                 const void* coef_v, float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  if (P.dtype != S4R_BF16 || (P.dh != 64 && P.dh != 128) || P.G > 8 || !attention_supported(P))
+    return fail(S4R_ERR_UNSUPPORTED, "full reconstruction is built for bf16 storage, head_dim 64 or 128, G <= 8 and "
+                                     "the ranks of the fused attention kernel");
+  S4R_REQ(q);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(coef_k);
+  S4R_REQ(coef_v);
+  S4R_REQ(out);
+  if (P.s > 0) {
+    S4R_REQ(sink_k);
+    S4R_REQ(sink_v);
+  }
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  return hip_status(launch_full_recon(P, w, L, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, out, stream),
+                    "s4r_full_recon_decode launch");
+}
+
 // the fused step for a uniform (P.lens.n == 0) or ragged batch; L is the
 // largest length, already checked against the capacity
 static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, const float* qwin_prev,

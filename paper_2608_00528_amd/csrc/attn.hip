@@ -351,9 +351,9 @@ bool launch_split_f32_64(const Problem&, const Workspace&, int64_t, int, int, in
                          const void*, const void*, const void*, hipStream_t);
 
 bool launch_tiles_bf16_128(const Problem&, const Workspace&, int64_t, int, int, const void*, const void*,
-                           const void*, const void*, const void*, hipStream_t, int*);
+                           const void*, const void*, const void*, hipStream_t, int*, bool);
 bool launch_tiles_bf16_64(const Problem&, const Workspace&, int64_t, int, int, const void*, const void*,
-                          const void*, const void*, const void*, hipStream_t, int*);
+                          const void*, const void*, const void*, hipStream_t, int*, bool);
 
 // which (G, rank) pairs the fused attention kernel is built for
 bool attention_supported(const Problem& P) {
@@ -374,8 +374,9 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
   bool tiles = false;                        // bf16: the MFMA kernel when it covers the configuration
   if (n_proc > 0 && P.dtype == S4R_BF16) {
     int ns = 0;
-    tiles = P.dh == 128 ? launch_tiles_bf16_128(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns)
-                        : launch_tiles_bf16_64(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns);
+    tiles = P.dh == 128
+                ? launch_tiles_bf16_128(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns, false)
+                : launch_tiles_bf16_64(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns, false);
     if (tiles) nsplit = ns;
   }
   if (n_proc > 0 && !tiles) {
@@ -403,6 +404,24 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && t1) e = hipEventRecord(t1[1], st);
   return e;
+}
+
+// full reconstruction (Appendix B.1): attention over the sinks and all L
+// tokens, each reconstructed from its coefficients: the bf16 MFMA kernel in
+// its every-token mode, then the split merge with the sinks
+hipError_t launch_full_recon(const Problem& P, const Workspace& ws, int64_t L, const void* q, const void* sink_k,
+                             const void* sink_v, const void* bases_k, const void* bases_v, const void* coef_k,
+                             const void* coef_v, float* out, hipStream_t st) {
+  int ns = 0;
+  const bool ok =
+      P.dh == 128
+          ? launch_tiles_bf16_128(P, ws, L, (int)L, (int)L, q, bases_k, bases_v, coef_k, coef_v, st, &ns, true)
+          : launch_tiles_bf16_64(P, ws, L, (int)L, (int)L, q, bases_k, bases_v, coef_k, coef_v, st, &ns, true);
+  if (!ok) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q,
+                     (const uint16_t*)sink_k, (const uint16_t*)sink_v, nullptr, nullptr, ws.part_ml, ws.part_o, out,
+                     ns, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P), P.lens);
+  return hipGetLastError();
 }
 
 // the split merge alone (no extra full-precision tokens), for kernels that

@@ -59,11 +59,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 // one wave's gather of one 16-token tile into slot u of a pair buffer: its RBH
 // 1 KiB blocks of C^K and of C^V as 16-byte global->LDS loads (lane l: token
 // l / 4, quarter l % 4 of the 32 columns; a token past the list reads row 0,
-// never used).  The LDS destinations are named directly (plain LDS pointers
-// for the builtin).
-#define S4R_GATHER_TILE(GK, GV, U, SIDX_TILE)                                               \
+// never used).  T is the tile's number within the workgroup.  The LDS
+// destinations are named directly (plain LDS pointers for the builtin).
+#define S4R_GATHER_TILE(GK, GV, U, T)                                                       \
   do {                                                                                       \
-    const int32_t x_ = (SIDX_TILE)[lane >> 2];                                               \
+    const int32_t x_ = tok_at((T) * 16 + (lane >> 2));                                       \
     const uint32_t tok_ = x_ < 0 ? 0u : (uint32_t)x_;                                        \
     const int64_t off_ = (int64_t)(tok_ >> 4) * 16 * R + (tok_ & 15) * 32 + (lane & 3) * 8;  \
     _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb) {                                     \
@@ -74,7 +74,10 @@ __device__ __forceinline__ void wait_vmcnt() {
     }                                                                                        \
   } while (0)
 
-template <int RBH, int NW, int NMH>
+// IDENT: every token of the sequence in order (full reconstruction,
+// Appendix B.1): token i of the workgroup's tiles is tile0 * 16 + i, no index
+// list is read and the tiles per workgroup are not bounded by its LDS slot.
+template <int RBH, int NW, int NMH, bool IDENT>
 __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k_attn_tiles(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ bases_k, const uint16_t* __restrict__ bases_v,
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
@@ -114,13 +117,24 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   __shared__ __align__(16) uint16_t ps[2][NMH][4][2][16]; // P parts [tile of pair][mh][head][hi|lo][slot]
 
   // ---- 1. index list, bases and query requested; then the first two pairs' gathers ---------
-  const int32_t* idx = idx_all + (int64_t)b * idx_stride;
   int32_t xi[kTileMax * 16 / (NW * 64)];
+  if constexpr (!IDENT) {
+    const int32_t* idx = idx_all + (int64_t)b * idx_stride;
 #pragma unroll
-  for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
-    const int i = threadIdx.x + k * NW * 64;
-    xi[k] = idx[min(tile0 * 16 + i, n_proc - 1)];
+    for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
+      const int i = threadIdx.x + k * NW * 64;
+      xi[k] = idx[min(tile0 * 16 + i, n_proc - 1)];
+    }
   }
+  // token of slot i of this workgroup's tiles (-1: past the list)
+  auto tok_at = [&](int i) __attribute__((always_inline)) -> int32_t {
+    if constexpr (IDENT) {
+      const int x = tile0 * 16 + i;
+      return (i < nt * 16 && x < n_proc) ? x : -1;
+    } else {
+      return sidx[i];
+    }
+  };
   // bases (registers): A operands of K^ (row = dim) and B operands of V^
   // (column = dim) read the same 16 bytes
   const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
@@ -145,10 +159,12 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
     qlo[mh] = *reinterpret_cast<const uint2*>(qp);
     qhi[mh] = *reinterpret_cast<const uint2*>(qp + DH / 2);
   }
+  if constexpr (!IDENT) {
 #pragma unroll
-  for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
-    const int i = threadIdx.x + k * NW * 64;
-    sidx[i] = (i < nt * 16 && tile0 * 16 + i < n_proc) ? xi[k] : -1;
+    for (int k = 0; k < kTileMax * 16 / (NW * 64); ++k) {
+      const int i = threadIdx.x + k * NW * 64;
+      sidx[i] = (i < nt * 16 && tile0 * 16 + i < n_proc) ? xi[k] : -1;
+    }
   }
   uint64_t Ff[4];
   rope_freqs_fixed(rope_ratio, fq, Ff);
@@ -162,9 +178,9 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   for (int t0 = 0; t0 < 4; t0 += NW) {
     const int t = t0 + w;
     if (t < 2)
-      S4R_GATHER_TILE(gkA, gvA, t, &sidx[t * 16]);
+      S4R_GATHER_TILE(gkA, gvA, t, t);
     else
-      S4R_GATHER_TILE(gkB, gvB, t - 2, &sidx[t * 16]);
+      S4R_GATHER_TILE(gkB, gvB, t - 2, t);
   }
 
   // ---- 2. rotated query as the A operand of the logits (overlaps the gathers) ------------
@@ -217,7 +233,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
     int32_t tokv[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      tokv[u] = sidx[(2 * p + u) * 16 + slot];
+      tokv[u] = tok_at((2 * p + u) * 16 + slot);
       // K^ for the wave's two dimension blocks: lane (token slot, kg) gets dims 4 kg + v
       floatx4 dk[2];
 #pragma unroll
@@ -268,9 +284,9 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
         const int t = 2 * p + 4 + u;
         if (t % NW == w) {
           if constexpr (BUF == 0)
-            S4R_GATHER_TILE(gkA, gvA, u, &sidx[t * 16]);
+            S4R_GATHER_TILE(gkA, gvA, u, t);
           else
-            S4R_GATHER_TILE(gkB, gvB, u, &sidx[t * 16]);
+            S4R_GATHER_TILE(gkB, gvB, u, t);
         }
       }
     }
@@ -364,18 +380,19 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
 namespace s4r {
 
 // tiles per workgroup: the smallest even count whose workgroups fit in one
-// round of the chip (three per CU), at most kMaxSplit splits; 0 when the list
-// needs more than kTileMax tiles per workgroup (the general kernel then runs)
-inline int attn_tiles_per_wg(const Problem& P, int ntile) {
+// round of the chip (three per CU), at most kMaxSplit splits; with an index
+// list, 0 when the list needs more than kTileMax tiles per workgroup (the
+// general kernel then runs)
+inline int attn_tiles_per_wg(const Problem& P, int ntile, bool ident) {
   const int slots = 256 * 3;
   const int ns_target = std::max(1, slots / std::max(1, P.B * P.hkv));
   int tpw = (ntile + ns_target - 1) / ns_target;
   tpw = std::max(2, (tpw + 1) / 2 * 2);
   while ((ntile + tpw - 1) / tpw > kMaxSplit) tpw += 2;
-  return tpw <= kTileMax ? tpw : 0;
+  return (ident || tpw <= kTileMax) ? tpw : 0;
 }
 
-template <int RBH, int NW, int NMH>
+template <int RBH, int NW, int NMH, bool IDENT>
 static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
                            const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
                            hipStream_t st, int* nsplit_out) {
@@ -383,39 +400,46 @@ static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int
   const int nsplit = (ntile + tpw - 1) / tpw;
   const int ngroups = P.B * nsplit;
   const int nwg = 8 * P.hkv * ((ngroups + 7) / 8);
-  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
+  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH, IDENT>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
                      (const uint16_t*)bk, (const uint16_t*)bv, (const uint16_t*)ck, (const uint16_t*)cv, ws.idx,
                      (int64_t)m, ws.part_ml, ws.part_o, n_proc, tpw, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb,
                      P.rank, P.R, P.s, L, P.cap, P.bases_shared, rope_ratio(P), P.lens);
   *nsplit_out = nsplit;
 }
 
-template <int NW, int NMH>
+template <int NW, int NMH, bool IDENT>
 static bool dispatch_tiles_rb(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
                               const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
                               hipStream_t st, int* ns) {
+#define S4R_TILES_CASE(RB)                                                                           \
+  case RB: launch_tiles_t<RB, NW, NMH, IDENT>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
   switch (P.rank / 32) {
-    case 1: launch_tiles_t<1, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 2: launch_tiles_t<2, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 3: launch_tiles_t<3, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 4: launch_tiles_t<4, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 5: launch_tiles_t<5, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 6: launch_tiles_t<6, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-    case 8: launch_tiles_t<8, NW, NMH>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
+    S4R_TILES_CASE(1)
+    S4R_TILES_CASE(2)
+    S4R_TILES_CASE(3)
+    S4R_TILES_CASE(4)
+    S4R_TILES_CASE(5)
+    S4R_TILES_CASE(6)
+    S4R_TILES_CASE(8)
     default: return false;
   }
+#undef S4R_TILES_CASE
 }
 
-// launches the split kernel for head dim 32 * NW; returns false when the
-// configuration is not covered (the caller then uses the general kernel)
+// launches the split kernel for head dim 32 * NW over the index list in the
+// workspace (ident: over every token); returns false when the configuration
+// is not covered (the caller then uses the general kernel)
 template <int NW>
 static bool launch_tiles_dh(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, const void* q,
                             const void* bk, const void* bv, const void* ck, const void* cv, hipStream_t st,
-                            int* ns) {
-  const int tpw = attn_tiles_per_wg(P, (n_proc + 15) / 16);
+                            int* ns, bool ident) {
+  const int tpw = attn_tiles_per_wg(P, (n_proc + 15) / 16, ident);
   if (P.G > 8 || tpw == 0) return false;
-  return P.G > 4 ? dispatch_tiles_rb<NW, 2>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns)
-                 : dispatch_tiles_rb<NW, 1>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns);
+  if (ident)
+    return P.G > 4 ? dispatch_tiles_rb<NW, 2, true>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns)
+                   : dispatch_tiles_rb<NW, 1, true>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns);
+  return P.G > 4 ? dispatch_tiles_rb<NW, 2, false>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns)
+                 : dispatch_tiles_rb<NW, 1, false>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns);
 }
 
 }  // namespace s4r

@@ -97,6 +97,9 @@ hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, co
                             hipStream_t st);
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st);
+hipError_t launch_full_recon(const Problem& P, const Workspace& ws, int64_t L, const void* q, const void* sink_k,
+                             const void* sink_v, const void* bases_k, const void* bases_v, const void* coef_k,
+                             const void* coef_v, float* out, hipStream_t st);
 hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
                                const void* v_cache, float* out, hipStream_t st);
 hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,

@@ -192,6 +192,25 @@ def test_dense_comparator_argument_errors():
     assert call(cfg(head_dim=128, n_q_heads=32, n_kv_heads=2)) == L.S4R_ERR_UNSUPPORTED   # G = 16
 
 
+def test_full_recon_argument_errors():
+    lib = L.load()
+
+    def call(c, n=100, q=FAKE, ck=FAKE, sink=FAKE, out=FAKE, wsb=1 << 40):
+        return lib.s4r_full_recon_decode(ctypes.byref(c), n, q, sink, sink, FAKE, FAKE, ck, FAKE, out, FAKE, wsb,
+                                         None)
+    c = cfg()
+    assert call(c, n=0) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, n=1025) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, q=None) == L.S4R_ERR_NULL_ARG
+    assert call(c, sink=None) == L.S4R_ERR_NULL_ARG               # sinks required when s > 0
+    assert call(c, out=None) == L.S4R_ERR_NULL_ARG
+    assert call(c, ck=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert call(c, wsb=16) == L.S4R_ERR_WORKSPACE
+    assert call(cfg(dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
+    assert call(cfg(n_q_heads=6, n_kv_heads=2)) == L.S4R_ERR_UNSUPPORTED     # G = 3
+    assert call(cfg(head_dim=32)) == L.S4R_ERR_UNSUPPORTED
+
+
 def test_prefill_projection_argument_errors():
     lib = L.load()
 

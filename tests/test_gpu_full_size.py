@@ -173,6 +173,30 @@ def test_dense_comparator_full_size():
         assert err <= 1e-4
 
 
+def test_full_reconstruction_full_size():
+    """The full-reconstruction comparator (Appendix B.1) at the headline shape
+    (B=4, L=131068, rank 160), in the launch configuration bench.py times;
+    sequences 0 and 3 compared in full against the oracle."""
+    wl = W.CONFIGS["llama8b_128k"]
+    print(f"[full-size] full reconstruction, {wl.describe()}", flush=True)
+    st = W.latent_state(wl, seed=1)
+    c = cfg_from_workload(wl)
+    g = to_gpu_state(c, st)
+    ws = s4r.alloc_workspace(c)
+    out = s4r.full_recon_decode(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
+                                g["coef_v"], ws)
+    torch.cuda.synchronize()
+    oc = oracle_cfg(c)
+    for b in (0, wl.batch - 1):
+        sl = lambda x: x[b:b + 1]  # noqa: E731
+        ref = decode.full_reconstruction_decode(sl(st["q"]), sl(st["sink_k"]), sl(st["sink_v"]), sl(st["bases_k"]),
+                                                sl(st["bases_v"]), sl(st["coef_k"])[:, :wl.L],
+                                                sl(st["coef_v"])[:, :wl.L], wl.L, wl.n_kv_heads, oc["rope_theta"])
+        err = rel_err_rows(out[b:b + 1].cpu().numpy(), ref)
+        print(f"[full-size] full reconstruction sequence {b}: out err {err:.2e}", flush=True)
+        assert err <= OUT_TOL[wl.dtype]
+
+
 def test_prefill_projection_full_size():
     """The bulk projection at the headline shape as bench.py times it (B=4,
     131072 rows of K and V, rank 160): 64 sampled rows of every sequence (the

@@ -526,3 +526,33 @@ def test_ragged_equal_lengths_match_uniform_step():
         idxs.append(idx.cpu())
     assert torch.equal(idxs[0], idxs[1])
     assert torch.equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("shape,L,B,dh", [("llama8b_32k", 3001, 2, 128), ("qwen3_4b_120k", 1000, 3, 128),
+                                         ("llama8b_32k", 700, 2, 64), ("llama8b_32k", 17, 1, 128),
+                                         ("llama8b_32k", 1, 2, 128)])
+def test_full_reconstruction(shape, L, B, dh):
+    """Full-reconstruction decoding (Appendix B.1) against the oracle; rows
+    past L hold NaN and must never be read."""
+    base = W.CONFIGS[shape]
+    wl = base.scaled(N=L + base.n_sink, batch=B, head_dim=dh, topk=16, n_needles=1)
+    cap = ((L + 15) // 16) * 16 + 32
+    st = W.latent_state(wl, seed=L, capacity=cap, L=L)
+    c = cfg_from_workload(wl, capacity=cap)
+    st_gpu = dict(st)
+    for key in ("coef_k", "coef_v"):
+        x = st[key].copy()
+        x[:, L:] = np.nan
+        st_gpu[key] = x
+    g = to_gpu_state(c, st_gpu)
+    ws = s4r.alloc_workspace(c)
+    out = s4r.full_recon_decode(c, L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
+                                g["coef_v"], ws)
+    torch.cuda.synchronize()
+    ref = decode.full_reconstruction_decode(st["q"], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                                            st["coef_k"][:, :L], st["coef_v"][:, :L], L, wl.n_kv_heads,
+                                            oracle_cfg(c)["rope_theta"])
+    o = out.cpu().numpy()
+    assert np.isfinite(o).all()
+    err = rel_err_rows(o, ref)
+    assert err <= OUT_TOL["bf16"], f"output rel err {err:.3e}"

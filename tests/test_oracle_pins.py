@@ -312,10 +312,40 @@ def check_dense_comparator(seed=11):
     return np.allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
+def check_full_reconstruction(seed=12, nb=1):
+    """Full-reconstruction decoding (Appendix B.1) equals torch SDPA over the
+    cache rebuilt with torch matrix products, C B^T per basis group, sinks
+    first, complex-form RoPE at positions 0..s+L-1."""
+    rng = np.random.default_rng(seed)
+    B, hq, hkv, dh, L, s, rank = 2, 8, 2, 16, 23, 3, 5
+    Dp = hkv * dh
+    Dg = Dp // nb
+    q = rng.standard_normal((B, hq, dh))
+    bases_k = rng.standard_normal((B, nb, Dg, rank))
+    bases_v = rng.standard_normal((B, nb, Dg, rank))
+    ck = rng.standard_normal((B, L + 4, nb * rank))           # rows past L are never used
+    cv = rng.standard_normal((B, L + 4, nb * rank))
+    sk = rng.standard_normal((B, s, Dp))
+    sv = rng.standard_normal((B, s, Dp))
+    theta = 10000.0
+
+    def rebuild(c, bases):
+        tc = torch.from_numpy(c[:, :L])
+        tb = torch.from_numpy(bases)
+        parts = [tc[:, :, g * rank:(g + 1) * rank] @ tb[:, g].transpose(1, 2) for g in range(nb)]
+        return torch.cat(parts, dim=2).numpy()
+    K = np.concatenate([sk, rebuild(ck, bases_k)], axis=1)
+    V = np.concatenate([sv, rebuild(cv, bases_v)], axis=1)
+    pos = np.broadcast_to(np.arange(s + L, dtype=float), (B, s + L))
+    want = torch_gqa_attention(q, K, V, pos, np.full(B, s + L - 1.0), theta, hkv)
+    got = decode.full_reconstruction_decode(q, sk, sv, bases_k, bases_v, ck, cv, L, hkv, theta)
+    return np.allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
 ALL_CHECKS = [check_latent_identity, check_rotation_invariance, check_pool_vs_torch,
               check_topk_special_case, check_select_bruteforce, check_full_rank_exact,
               check_full_budget_dense, check_rope_complex, check_rope_shift_invariance,
-              check_plain_gqa, check_causal_window, check_dense_comparator]
+              check_plain_gqa, check_causal_window, check_dense_comparator, check_full_reconstruction]
 
 
 # ----------------------------------------------------------------------------
@@ -354,6 +384,27 @@ def test_full_budget_equals_dense_attention(theta, W):
 
 def test_dense_comparator_matches_torch_sdpa():
     assert check_dense_comparator()
+
+
+@pytest.mark.parametrize("nb", [1, 2])
+def test_full_reconstruction_matches_torch_sdpa(nb):
+    assert check_full_reconstruction(nb=nb)
+
+
+def test_full_reconstruction_over_every_index_is_sparse_attention():
+    """With every token selected, S^4R's sparse attention is full
+    reconstruction (Section 3.2.3 against Appendix B.1)."""
+    rng = np.random.default_rng(13)
+    B, hq, hkv, dh, L, s, rank = 2, 4, 2, 8, 19, 2, 4
+    Dp = hkv * dh
+    args = dict(sink_k=rng.standard_normal((B, s, Dp)), sink_v=rng.standard_normal((B, s, Dp)),
+                bases_k=rng.standard_normal((1, 1, Dp, rank)), bases_v=rng.standard_normal((1, 1, Dp, rank)),
+                coef_k=rng.standard_normal((B, L, rank)), coef_v=rng.standard_normal((B, L, rank)))
+    q = rng.standard_normal((B, hq, dh))
+    full = decode.full_reconstruction_decode(q, L=L, n_kv_heads=hkv, theta=500.0, **args)
+    idx = np.broadcast_to(np.arange(L), (B, L))
+    sparse, _, _ = decode.sparse_attention(q, idx, L=L, n_kv_heads=hkv, rope_theta=500.0, **args)
+    assert np.allclose(full, sparse, rtol=1e-12, atol=1e-12)
 
 
 def test_rope_rotate_half_equals_complex_form():
