@@ -36,10 +36,12 @@
  *  q          [B, h_q, d_h]            pre-RoPE query, head h reads KV head h / G
  *  sink_k/v   [B, s, Dp]               pre-RoPE sink keys / values (Section 3.1.1)
  *  win_k/v    [B, W, Dp]               exact KV of positions L-W .. L-1 (optional)
- *  bases_k/v  [B or 1, basis_groups, Dp / basis_groups, rank], rank fastest.
+ *  bases_k/v  [B or 1, basis_groups, Dp / basis_groups, rank], rank fastest
+ *             (bases_v: rank_v when set).
  *             Group beta spans KV heads beta*h_kv/basis_groups onward; the
  *             paper's single basis over Dp is basis_groups = 1 (Eq. svd).
- *  coef_k/v   per sequence a [capacity, R] matrix in the TILED layout:
+ *  coef_k/v   per sequence a [capacity, R] matrix (the value cache
+ *             [capacity, R_V] when rank_v is set) in the TILED layout:
  *             element (t, c) of sequence b is at
  *               b*capacity*R + (t/16)*16*R + (c/32)*512 + (t%16)*32 + (c%32)
  *             i.e. 16-token tiles, each split into 32-column blocks of
@@ -85,7 +87,8 @@ typedef struct {
   int32_t n_kv_heads;    /* h_kv                                                   */
   int32_t head_dim;      /* d_h: 64 or 128                                         */
   int32_t basis_groups;  /* 1 = one basis over Dp (paper); must divide n_kv_heads  */
-  int32_t rank;          /* rank per basis group, multiple of 32, <= Dp/basis_groups */
+  int32_t rank;          /* rank per basis group, multiple of 32, <= Dp/basis_groups;
+                            the key rank r^K when rank_v is set                    */
   int32_t n_sink;        /* s, sink tokens kept at full precision (Section 3.1.1)  */
   int32_t window;        /* W, local window always kept (Section 3.2.3)            */
   int32_t q_window;      /* W_q >= 1 query-coefficient rows used for scoring (3.2.2) */
@@ -97,6 +100,12 @@ typedef struct {
   int64_t capacity;      /* token rows allocated in each coefficient cache, % 16 == 0 */
   float rope_theta;      /* RoPE base; 0 disables RoPE                             */
   int32_t dtype;         /* S4R_FP32 | S4R_BF16                                    */
+  int32_t rank_v;        /* 0: values share `rank`; else the value rank r^V per basis
+                            group (Appendix D.2: r^K <= r^V), a multiple of 32 <=
+                            Dp/basis_groups.  The value cache and basis are then
+                            [.., R_V = basis_groups * rank_v] wide; asymmetric
+                            ranks run on the bf16 matrix-core path for the rank
+                            pairs s4r_decode_step lists                            */
 } s4r_config;
 
 /* Bytes of workspace any call with this config needs (host only, no GPU). */
@@ -136,7 +145,8 @@ s4r_status s4r_select_topk(const s4r_config* cfg, int64_t L, const float* scores
 /*
  * Sparse reconstruction (Section 3.2.3): k_hat[b, n] = C^K[b, idx[b, n]] (B^K)^T,
  * v_hat likewise, per basis group, pre-RoPE, fp32.  idx entries must lie in
- * [0, L); m is the number of indices per sequence.
+ * [0, L); m is the number of indices per sequence.  Equal key and value ranks
+ * only (rank_v set to another rank: S4R_ERR_UNSUPPORTED).
  */
 s4r_status s4r_reconstruct(const s4r_config* cfg, int64_t L, int32_t m, const int32_t* idx,
                            const void* bases_k, const void* bases_v, const void* coef_k,
@@ -163,6 +173,10 @@ s4r_status s4r_sparse_attn(const s4r_config* cfg, int64_t L, int32_t m, const vo
  * token); if given they replace the window rows with exact KV.  idx_out
  * [B, m] and scores_out [B, L] are optional copies of the selection.
  * coef_k / coef_v are written only when k_new / v_new are given.
+ * Asymmetric ranks (rank_v set, Appendix D.2) run for bf16 storage, head_dim
+ * 64 or 128, G <= 8, m <= 32768 and the (rank, rank_v) pairs (96, 160),
+ * (64, 192), (128, 192), (96, 224), (160, 224), (128, 256); other settings
+ * return S4R_ERR_UNSUPPORTED.
  */
 s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
                            const float* qwin_prev, const void* sink_k, const void* sink_v,
@@ -220,9 +234,9 @@ s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q
  * s4r_score_latent.  Products of the bf16 inputs are exact, sums are fp32 on
  * the matrix cores, rounded once to bf16 (a coefficient can differ by one
  * bf16 ulp from the fp64-rounded value where the fp32 sum lies next to a
- * rounding boundary).  bf16 storage and rank 32..192 only (otherwise
- * S4R_ERR_UNSUPPORTED).  ws / ws_bytes: the workspace of s4r_decode_step
- * (s4r_workspace_size); its first B * 2 * Dp * rank * 2 bytes hold the bases
+ * rounding boundary).  bf16 storage, rank 32..192 and equal key and value
+ * ranks only (otherwise S4R_ERR_UNSUPPORTED).  ws / ws_bytes: the workspace
+ * of s4r_decode_step (s4r_workspace_size); its first B * 2 * Dp * rank * 2 bytes hold the bases
  * transposed while the call runs.  The bases themselves come from a truncated
  * SVD of sampled, normalised rows (Section 3.1), which this library does not
  * compute.
@@ -260,7 +274,9 @@ s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_
                               void* coef_k, void* coef_v, hipStream_t stream);
 
 /* Layout conversion of a coefficient cache: row-major [B, n_rows, R] <-> tiled
- * [B, capacity, R] (rows 0 .. n_rows-1; other rows of dst are left as they are). */
+ * [B, capacity, R] (rows 0 .. n_rows-1; other rows of dst are left as they are).
+ * The width is R = basis_groups * rank: convert a value cache of rank_v with a
+ * configuration whose rank is rank_v. */
 s4r_status s4r_pack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_rowmajor,
                          void* dst_tiled, hipStream_t stream);
 s4r_status s4r_unpack_coef(const s4r_config* cfg, int64_t n_rows, const void* src_tiled,

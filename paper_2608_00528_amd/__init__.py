@@ -31,6 +31,7 @@ from .api import (  # noqa: E402,F401
     timing_enable,
     timing_read,
     unpack_coef,
+    value_config,
     version,
     workspace_size,
 )

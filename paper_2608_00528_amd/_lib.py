@@ -43,6 +43,7 @@ class Config(ctypes.Structure):
         ("capacity", ctypes.c_int64),
         ("rope_theta", ctypes.c_float),
         ("dtype", ctypes.c_int32),
+        ("rank_v", ctypes.c_int32),
     ]
 
 

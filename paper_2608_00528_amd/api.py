@@ -19,7 +19,7 @@ _AGG = {"mean": L.S4R_AGG_MEAN, "max": L.S4R_AGG_MAX}
 
 def make_config(*, batch, n_q_heads, n_kv_heads, head_dim, rank, capacity, basis_groups=1, n_sink=4,
                 window=64, q_window=1, topk=1024, pool_kernel=7, pool_mode="max", group_agg="mean",
-                bases_shared=False, rope_theta=0.0, dtype="bf16"):
+                bases_shared=False, rope_theta=0.0, dtype="bf16", rank_v=0):
     c = L.Config()
     c.batch, c.n_q_heads, c.n_kv_heads, c.head_dim = batch, n_q_heads, n_kv_heads, head_dim
     c.basis_groups, c.rank, c.n_sink, c.window = basis_groups, rank, n_sink, window
@@ -29,6 +29,18 @@ def make_config(*, batch, n_q_heads, n_kv_heads, head_dim, rank, capacity, basis
     c.capacity = capacity
     c.rope_theta = float(rope_theta)
     c.dtype = _DTYPES[dtype][0]
+    c.rank_v = rank_v
+    return c
+
+
+def value_config(cfg):
+    """The configuration whose `rank` is the value rank: the layout helpers
+    (pack_coef / unpack_coef) take a cache's width from `rank`, so a value
+    cache of an asymmetric configuration is converted with this one."""
+    c = L.Config()
+    ctypes.pointer(c)[0] = cfg
+    if cfg.rank_v:
+        c.rank, c.rank_v = cfg.rank_v, 0
     return c
 
 

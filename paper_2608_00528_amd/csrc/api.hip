@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
+#include <cstddef>
 #include <cstdio>
 #include <mutex>
 #include <string>
@@ -11,6 +12,10 @@
 
 #include "s4r_device.h"
 #include "s4r_internal.h"
+
+static_assert(sizeof(s4r_config) == 80 && offsetof(s4r_config, capacity) == 56 &&
+                  offsetof(s4r_config, rank_v) == 72,
+              "s4r_config layout is part of the ABI");
 
 namespace s4r {
 namespace {
@@ -54,6 +59,12 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
     return fail(S4R_ERR_UNSUPPORTED, "Dp / basis_groups = %d > %d not supported", Dg, kQMaxChunks * kPChunk);
   const int R = c->rank * c->basis_groups;
   if (R > 256) return fail(S4R_ERR_UNSUPPORTED, "latent width %d > 256 not supported", R);
+  const int rank_v = c->rank_v ? c->rank_v : c->rank;
+  if (rank_v < 1 || rank_v > Dg)
+    return fail(S4R_ERR_BAD_SHAPE, "rank_v %d must be 0 or in [1, Dp/basis_groups = %d]", c->rank_v, Dg);
+  if (rank_v % 32) return fail(S4R_ERR_UNSUPPORTED, "rank_v %d must be a multiple of 32", rank_v);
+  if (rank_v * c->basis_groups > 256)
+    return fail(S4R_ERR_UNSUPPORTED, "value latent width %d > 256 not supported", rank_v * c->basis_groups);
   if (c->n_sink < 0 || c->n_sink > 1024) return fail(S4R_ERR_BAD_SHAPE, "n_sink %d outside [0, 1024]", c->n_sink);
   if (c->window < 0) return fail(S4R_ERR_BAD_SHAPE, "window %d < 0", c->window);
   if (c->q_window < 1) return fail(S4R_ERR_BAD_SHAPE, "q_window %d < 1", c->q_window);
@@ -87,6 +98,8 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   P.nb = c->basis_groups;
   P.rank = c->rank;
   P.R = R;
+  P.rank_v = rank_v;
+  P.Rv = rank_v * c->basis_groups;
   P.Dg = Dg;
   P.s = c->n_sink;
   P.W = c->window;
@@ -292,6 +305,8 @@ s4r_status s4r_reconstruct(const s4r_config* cfg, int64_t L, int32_t m, const in
   if (st) return st;
   if (L < 1 || L > P.cap) return fail(S4R_ERR_BAD_SHAPE, "L = %lld outside [1, capacity]", (long long)L);
   if (m < 0) return fail(S4R_ERR_BAD_SHAPE, "m = %d < 0", m);
+  if (P.rank_v != P.rank)
+    return fail(S4R_ERR_UNSUPPORTED, "explicit reconstruction is built for equal key and value ranks");
   if (m == 0) return ok();
   S4R_REQ(idx);
   S4R_REQ(bases_k);
@@ -337,6 +352,8 @@ s4r_status s4r_prefill_project(const s4r_config* cfg, int64_t n_rows, const void
   s4r_status st = make_problem(cfg, P);
   if (st) return st;
   if (P.dtype != S4R_BF16) return fail(S4R_ERR_UNSUPPORTED, "the bulk projection is built for bf16 storage only");
+  if (P.rank_v != P.rank)
+    return fail(S4R_ERR_UNSUPPORTED, "the bulk projection is built for equal key and value ranks");
   if (P.rank / 32 < 1 || P.rank / 32 > 6)
     return fail(S4R_ERR_UNSUPPORTED, "the bulk projection is built for rank 32 .. 192 (rank %d)", P.rank);
   if ((P.hkv * P.dh / P.nb) % 32)
@@ -437,6 +454,9 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
   if (m + P.s < 1) return fail(S4R_ERR_BAD_SHAPE, "attention over an empty set (m + n_sink == 0)");
   if ((int64_t)m > (int64_t)kMaxSplit * kMaxTilesPerSplit * 16)
     return fail(S4R_ERR_UNSUPPORTED, "m = %d selected tokens exceeds %d", m, kMaxSplit * kMaxTilesPerSplit * 16);
+  if (P.rank_v != P.rank && (int64_t)m > (int64_t)kMaxSplit * kTileMax * 16)
+    return fail(S4R_ERR_UNSUPPORTED, "m = %d selected tokens exceeds %d with asymmetric ranks", m,
+                kMaxSplit * kTileMax * 16);
   if (win_k && P.s + std::min<int64_t>(P.W, L) > kMaxExtraTok)
     return fail(S4R_ERR_UNSUPPORTED, "n_sink + window = %lld > %d with exact window KV", (long long)(P.s + P.W), kMaxExtraTok);
   if ((st = check_ws(P, ws, ws_bytes))) return st;

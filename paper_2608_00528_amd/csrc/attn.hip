@@ -355,8 +355,12 @@ bool launch_tiles_bf16_128(const Problem&, const Workspace&, int64_t, int, int, 
 bool launch_tiles_bf16_64(const Problem&, const Workspace&, int64_t, int, int, const void*, const void*,
                           const void*, const void*, const void*, hipStream_t, int*, bool);
 
-// which (G, rank) pairs the fused attention kernel is built for
+// which (G, rank) pairs the fused attention kernel is built for (asymmetric
+// key / value ranks: the bf16 MFMA kernel only)
 bool attention_supported(const Problem& P) {
+  if (P.rank_v != P.rank)
+    return P.dtype == S4R_BF16 && (P.dh == 64 || P.dh == 128) && P.G <= 8 &&
+           tiles_rank_pair(P.rank / 32, P.rank_v / 32);
   const int rb = P.rank / 32;
   const bool g_ok = P.G == 1 || P.G == 2 || P.G == 4 || P.G == 7 || P.G == 8;
   const bool rb_ok = (rb >= 1 && rb <= 6) || rb == 8;
@@ -379,6 +383,7 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
                 : launch_tiles_bf16_64(P, ws, L, m, n_proc, q, bases_k, bases_v, coef_k, coef_v, st, &ns, false);
     if (tiles) nsplit = ns;
   }
+  if (n_proc > 0 && !tiles && P.rank_v != P.rank) return hipErrorInvalidValue;   // MFMA kernel only
   if (n_proc > 0 && !tiles) {
     if (P.dtype == S4R_BF16)
       ok = P.dh == 128 ? launch_split_bf16_128(P, ws, L, m, n_proc, nsplit, q, bases_k, bases_v, coef_k, coef_v, st)

@@ -42,12 +42,11 @@
 namespace s4r {
 
 // occupancy target: three workgroups per CU (at most 168 registers per lane;
-// the four tile slots of a workgroup take 8 * RBH KiB of LDS)
-template <int RBH>
+// the four tile slots of a workgroup take 4 * (RBH + RBV) KiB of LDS)
+template <int RBH, int RBV>
 constexpr int attn_tiles_waves_per_simd() {
-  return RBH <= 5 ? 3 : 2;
+  return RBH + RBV <= 10 ? 3 : 2;
 }
-constexpr int kTileMax = 32;   // tiles per workgroup (index list in LDS)
 
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt not waited)
 template <int N>
@@ -57,7 +56,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // one wave's gather of one 16-token tile into slot u of a pair buffer: its RBH
-// 1 KiB blocks of C^K and of C^V as 16-byte global->LDS loads (lane l: token
+// 1 KiB blocks of C^K and RBV of C^V as 16-byte global->LDS loads (lane l: token
 // l / 4, quarter l % 4 of the 32 columns; a token past the list reads row 0,
 // never used).  T is the tile's number within the workgroup.  The LDS
 // destinations are named directly (plain LDS pointers for the builtin).
@@ -65,24 +64,31 @@ __device__ __forceinline__ void wait_vmcnt() {
   do {                                                                                       \
     const int32_t x_ = tok_at((T) * 16 + (lane >> 2));                                       \
     const uint32_t tok_ = x_ < 0 ? 0u : (uint32_t)x_;                                        \
-    const int64_t off_ = (int64_t)(tok_ >> 4) * 16 * R + (tok_ & 15) * 32 + (lane & 3) * 8;  \
+    const int64_t in_ = (tok_ & 15) * 32 + (lane & 3) * 8;                                   \
+    const int64_t offk_ = (int64_t)(tok_ >> 4) * 16 * R + in_;                               \
+    const int64_t offv_ = (int64_t)(tok_ >> 4) * 16 * Rv + in_;                              \
     _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb) {                                     \
       uint16_t* dk_ = &GK[U][kb][0];                                                         \
+      __builtin_amdgcn_global_load_lds(ckb + offk_ + kb * 512, dk_, 16, 0, 0);               \
+    }                                                                                        \
+    _Pragma("unroll") for (int kb = 0; kb < RBV; ++kb) {                                     \
       uint16_t* dv_ = &GV[U][kb][0];                                                         \
-      __builtin_amdgcn_global_load_lds(ckb + off_ + kb * 512, dk_, 16, 0, 0);                \
-      __builtin_amdgcn_global_load_lds(cvb + off_ + kb * 512, dv_, 16, 0, 0);                \
+      __builtin_amdgcn_global_load_lds(cvb + offv_ + kb * 512, dv_, 16, 0, 0);               \
     }                                                                                        \
   } while (0)
 
 // IDENT: every token of the sequence in order (full reconstruction,
 // Appendix B.1): token i of the workgroup's tiles is tile0 * 16 + i, no index
 // list is read and the tiles per workgroup are not bounded by its LDS slot.
-template <int RBH, int NW, int NMH, bool IDENT>
-__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k_attn_tiles(
+// RBH / RBV: 32-column blocks of one head's key / value basis group (they
+// differ when the ranks are asymmetric, Appendix D.2).
+template <int RBH, int RBV, int NW, int NMH, bool IDENT>
+__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) void k_attn_tiles(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ bases_k, const uint16_t* __restrict__ bases_v,
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int tpw, int nsplit,
-    int ngroups, int G, int hq, int hkv, int nb, int rank, int R, int s_sink, int64_t L, int64_t cap,
+    int ngroups, int G, int hq, int hkv, int nb, int rank, int R, int rank_v, int Rv, int s_sink, int64_t L,
+    int64_t cap,
     int bases_shared, double rope_ratio, Lens lens) {
   constexpr int DH = NW * 32;                      // NMH = ceil(G / 4): 4 heads per MFMA row group
   static_assert(NW >= 2, "a tile pair is gathered by two waves");
@@ -100,7 +106,8 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   const int slot = lane & 15, kg = lane >> 4;
   const int Dp = hkv * DH, Dg = Dp / nb;
   const int bgrp = j / (hkv / nb);                 // basis group of head j
-  const int kb0 = bgrp * rank / 32;                // its first latent block
+  const int kb0 = bgrp * rank / 32;                // its first latent block (keys)
+  const int kbv0 = bgrp * rank_v / 32;             // (values)
   const int row0 = (j % (hkv / nb)) * DH;          // first basis row of head j in its group
   const int tile0 = split * tpw;
   const int ntile = (n_proc + 15) / 16;
@@ -110,8 +117,8 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   // two pair buffers (even pairs in A, odd pairs in B) of gathered C^K / C^V
   // blocks [tile of pair][block][token slot][32 columns]: separate arrays, so
   // the loads refilling one buffer never hold up the reads of the other
-  __shared__ __align__(16) uint16_t gkA[2][RBH][512], gvA[2][RBH][512];
-  __shared__ __align__(16) uint16_t gkB[2][RBH][512], gvB[2][RBH][512];
+  __shared__ __align__(16) uint16_t gkA[2][RBH][512], gvA[2][RBV][512];
+  __shared__ __align__(16) uint16_t gkB[2][RBH][512], gvB[2][RBV][512];
   __shared__ int32_t sidx[kTileMax * 16];
   __shared__ float xl[2][NW][NMH][4][16];                // partial logits [tile of pair][wave][mh][head][slot]
   __shared__ __align__(16) uint16_t ps[2][NMH][4][2][16]; // P parts [tile of pair][mh][head][hi|lo][slot]
@@ -136,18 +143,20 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
     }
   };
   // bases (registers): A operands of K^ (row = dim) and B operands of V^
-  // (column = dim) read the same 16 bytes
+  // (column = dim) read the same 16-byte pattern of their basis
   const int64_t boff = (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)bgrp * Dg * rank;
-  Op8 bk[2][RBH], bv[2][RBH];
+  const int64_t boffv = (bases_shared ? 0 : (int64_t)b * Dp * rank_v) + (int64_t)bgrp * Dg * rank_v;
+  Op8 bk[2][RBH], bv[2][RBV];
 #pragma unroll
   for (int m = 0; m < 2; ++m) {
     const int d = 16 * (w + m * NW) + slot;
 #pragma unroll
-    for (int kb = 0; kb < RBH; ++kb) {
-      const int64_t o = boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8;
-      bk[m][kb].u = *reinterpret_cast<const uint4*>(bases_k + o);
-      bv[m][kb].u = *reinterpret_cast<const uint4*>(bases_v + o);
-    }
+    for (int kb = 0; kb < RBH; ++kb)
+      bk[m][kb].u = *reinterpret_cast<const uint4*>(bases_k + boff + (int64_t)(row0 + d) * rank + kb * 32 + kg * 8);
+#pragma unroll
+    for (int kb = 0; kb < RBV; ++kb)
+      bv[m][kb].u =
+          *reinterpret_cast<const uint4*>(bases_v + boffv + (int64_t)(row0 + d) * rank_v + kb * 32 + kg * 8);
   }
   // the query dims of this lane's k-group: f_v = 16 w + 4 kg + v and f_v + d_h / 2
   const int fq = 16 * w + 4 * kg;
@@ -171,7 +180,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
   const int64_t pos_q = s_sink + L - 1;
   lds_barrier();                                   // sidx visible
   const uint16_t* ckb = coef_k + (int64_t)b * cap * R + (int64_t)kb0 * 512;
-  const uint16_t* cvb = coef_v + (int64_t)b * cap * R + (int64_t)kb0 * 512;
+  const uint16_t* cvb = coef_v + (int64_t)b * cap * Rv + (int64_t)kbv0 * 512;
   // tile t is gathered by wave t % NW; pairs 0 and 1 now (every wave issues
   // the same number of loads), pair p + 2 once pair p has been read
 #pragma unroll
@@ -224,7 +233,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
     // of the next pair, issued later, may stay in flight), then for the others
     const bool next_issued = (p == 0) || (p + 1 < npair);
     if (next_issued && ((2 * p + 2) % NW == w || (2 * p + 3) % NW == w))
-      wait_vmcnt<2 * RBH>();
+      wait_vmcnt<RBH + RBV>();                   // one tile's gathers
     else
       wait_vmcnt<0>();
     lds_barrier();
@@ -270,7 +279,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH>())) void k
       for (int m = 0; m < 2; ++m) {
         dv[u][m] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kb = 0; kb < RBH; ++kb) {
+        for (int kb = 0; kb < RBV; ++kb) {
           Op8 c;
           c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gvA[u][kb][slot * 32 + kg * 8] : &gvB[u][kb][slot * 32 + kg * 8]);
           dv[u][m] = mfma16x16x32(c, bv[m][kb], dv[u][m]);
@@ -392,7 +401,7 @@ inline int attn_tiles_per_wg(const Problem& P, int ntile, bool ident) {
   return (ident || tpw <= kTileMax) ? tpw : 0;
 }
 
-template <int RBH, int NW, int NMH, bool IDENT>
+template <int RBH, int RBV, int NW, int NMH, bool IDENT>
 static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
                            const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
                            hipStream_t st, int* nsplit_out) {
@@ -400,10 +409,10 @@ static void launch_tiles_t(const Problem& P, const Workspace& ws, int64_t L, int
   const int nsplit = (ntile + tpw - 1) / tpw;
   const int ngroups = P.B * nsplit;
   const int nwg = 8 * P.hkv * ((ngroups + 7) / 8);
-  hipLaunchKernelGGL((k_attn_tiles<RBH, NW, NMH, IDENT>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
+  hipLaunchKernelGGL((k_attn_tiles<RBH, RBV, NW, NMH, IDENT>), dim3(nwg), dim3(NW * 64), 0, st, (const uint16_t*)q,
                      (const uint16_t*)bk, (const uint16_t*)bv, (const uint16_t*)ck, (const uint16_t*)cv, ws.idx,
                      (int64_t)m, ws.part_ml, ws.part_o, n_proc, tpw, nsplit, ngroups, P.G, P.hq, P.hkv, P.nb,
-                     P.rank, P.R, P.s, L, P.cap, P.bases_shared, rope_ratio(P), P.lens);
+                     P.rank, P.R, P.rank_v, P.Rv, P.s, L, P.cap, P.bases_shared, rope_ratio(P), P.lens);
   *nsplit_out = nsplit;
 }
 
@@ -411,19 +420,27 @@ template <int NW, int NMH, bool IDENT>
 static bool dispatch_tiles_rb(const Problem& P, const Workspace& ws, int64_t L, int m, int n_proc, int tpw,
                               const void* q, const void* bk, const void* bv, const void* ck, const void* cv,
                               hipStream_t st, int* ns) {
-#define S4R_TILES_CASE(RB)                                                                           \
-  case RB: launch_tiles_t<RB, NW, NMH, IDENT>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns); return true;
-  switch (P.rank / 32) {
-    S4R_TILES_CASE(1)
-    S4R_TILES_CASE(2)
-    S4R_TILES_CASE(3)
-    S4R_TILES_CASE(4)
-    S4R_TILES_CASE(5)
-    S4R_TILES_CASE(6)
-    S4R_TILES_CASE(8)
-    default: return false;
+#define S4R_TILES_CASE(RK, RV)                                                                         \
+  if (P.rank / 32 == RK && P.rank_v / 32 == RV) {                                                     \
+    static_assert(tiles_rank_pair(RK, RV), "pair not in the list");                                  \
+    launch_tiles_t<RK, RV, NW, NMH, IDENT>(P, ws, L, m, n_proc, tpw, q, bk, bv, ck, cv, st, ns);       \
+    return true;                                                                                      \
   }
+  S4R_TILES_CASE(1, 1)
+  S4R_TILES_CASE(2, 2)
+  S4R_TILES_CASE(3, 3)
+  S4R_TILES_CASE(4, 4)
+  S4R_TILES_CASE(5, 5)
+  S4R_TILES_CASE(6, 6)
+  S4R_TILES_CASE(8, 8)
+  S4R_TILES_CASE(3, 5)
+  S4R_TILES_CASE(2, 6)
+  S4R_TILES_CASE(4, 6)
+  S4R_TILES_CASE(3, 7)
+  S4R_TILES_CASE(5, 7)
+  S4R_TILES_CASE(4, 8)
 #undef S4R_TILES_CASE
+  return false;
 }
 
 // launches the split kernel for head dim 32 * NW over the index list in the

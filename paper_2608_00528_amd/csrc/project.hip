@@ -231,16 +231,19 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
                                                       const T* __restrict__ k_new, const T* __restrict__ v_new,
                                                       T* __restrict__ coef_k, T* __restrict__ coef_v,
                                                       int64_t append_row, int hkv, int dh, int nb, int rank, int R,
-                                                      int bases_shared, int64_t cap, Lens lens) {
+                                                      int rank_v, int Rv, int bases_shared, int64_t cap, Lens lens) {
+  // the value side has its own width when the ranks are asymmetric
+  const int which = blockIdx.z;
+  if ((int)blockIdx.x * 32 >= (which ? Rv : R)) return;
   // a ragged batch appends at each sequence's own last row
   const int64_t row = lens.n ? (int64_t)lens.v[blockIdx.y] - 1 : append_row;
-  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, rank, R,
-                       bases_shared, cap, blockIdx.x, blockIdx.y, blockIdx.z);
+  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
+                       which ? Rv : R, bases_shared, cap, blockIdx.x, blockIdx.y, which);
 }
 
 // both projections of a step that appends a token, in one launch: blocks
 // [0, nq) are the query-coefficient workgroups (R / 32 x chunks x B, in that
-// order), the rest the new rows' (R / 32 x B x 2).  They touch disjoint
+// order), the rest the new rows' (max(R, R_V) / 32 x B x 2).  They touch disjoint
 // memory, and one launch saves a dispatch and a first-read latency.
 template <typename T>
 __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, const T* __restrict__ bases_k,
@@ -249,7 +252,8 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
                                                       T* __restrict__ coef_v, double* __restrict__ qpart,
                                                       uint32_t* __restrict__ hist, int64_t append_row, int hq,
                                                       int hkv, int dh, int G, int nb, int rank, int R,
-                                                      int bases_shared, int64_t cap, int B, int nch, Lens lens) {
+                                                      int rank_v, int Rv, int bases_shared, int64_t cap, int B,
+                                                      int nch, Lens lens) {
   const int ncb = R / 32;
   const int nq = ncb * nch * B;
   int id = blockIdx.x;
@@ -258,9 +262,12 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
     project_query_body<T>(q, bases_k, qpart, hist, hq, hkv, dh, G, nb, rank, R, bases_shared, cblk, ch, b, nch);
   } else {
     id -= nq;
-    const int cblk = id % ncb, b = (id / ncb) % B, which = id / (ncb * B);
+    const int ncr = max(R, Rv) / 32;               // row blocks per (sequence, side)
+    const int cblk = id % ncr, b = (id / ncr) % B, which = id / (ncr * B);
+    if (cblk * 32 >= (which ? Rv : R)) return;
     const int64_t row = lens.n ? (int64_t)lens.v[b] - 1 : append_row;
-    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, rank, R,
+    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
+                         which ? Rv : R,
                          bases_shared, cap, cblk, b, which);
   }
 }
@@ -280,15 +287,16 @@ hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist,
 
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
-  dim3 grid(P.R / 32, P.B, 2);
+  dim3 grid(std::max(P.R, P.Rv) / 32, P.B, 2);
   if (P.dtype == S4R_BF16)
     hipLaunchKernelGGL(k_project_rows<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)bases_k,
                        (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
-                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.bases_shared, P.cap, P.lens);
+                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap,
+                       P.lens);
   else
     hipLaunchKernelGGL(k_project_rows<float>, grid, dim3(256), 0, st, (const float*)bases_k, (const float*)bases_v,
                        (const float*)k_new, (const float*)v_new, (float*)coef_k, (float*)coef_v, row, P.hkv, P.dh,
-                       P.nb, P.rank, P.R, P.bases_shared, P.cap, P.lens);
+                       P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap, P.lens);
   return hipGetLastError();
 }
 
@@ -296,17 +304,17 @@ hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, 
                                const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                                int64_t row, hipStream_t st) {
   const int nch = project_chunks(P);
-  dim3 grid((P.R / 32) * nch * P.B + (P.R / 32) * P.B * 2);
+  dim3 grid((P.R / 32) * nch * P.B + (std::max(P.R, P.Rv) / 32) * P.B * 2);
   if (P.dtype == S4R_BF16)
     hipLaunchKernelGGL(k_project_step<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q, (const uint16_t*)bases_k,
                        (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
                        (uint16_t*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
-                       P.bases_shared, P.cap, P.B, nch, P.lens);
+                       P.rank_v, P.Rv, P.bases_shared, P.cap, P.B, nch, P.lens);
   else
     hipLaunchKernelGGL(k_project_step<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k,
                        (const float*)bases_v, (const float*)k_new, (const float*)v_new, (float*)coef_k,
-                       (float*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared,
-                       P.cap, P.B, nch, P.lens);
+                       (float*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.rank_v, P.Rv,
+                       P.bases_shared, P.cap, P.B, nch, P.lens);
   return hipGetLastError();
 }
 

@@ -19,6 +19,7 @@ constexpr int kSelChunk = 2048;       // tokens per selection workgroup (multipl
 constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capacity <= 4096 * kSelChunk)
 constexpr int kMaxSplit = 64;         // attention splits per (sequence, kv head)
 constexpr int kMaxTilesPerSplit = 512; // 16-token tiles per split (index list staged in LDS)
+constexpr int kTileMax = 32;          // tiles per workgroup of the MFMA attention kernel (index list in LDS)
 constexpr int kMaxGW = 16;            // G * W_q columns handled by one MFMA block
 constexpr int kPChunk = 256;          // basis rows per query-projection workgroup
 constexpr int kQMaxChunks = 8;        // row chunks per basis group (Dp / basis_groups <= 2048)
@@ -32,9 +33,19 @@ struct Lens {
 };
 __host__ __device__ inline int64_t len_of(const Lens& l, int b, int64_t L) { return l.n ? (int64_t)l.v[b] : L; }
 
+// the (key, value) rank pairs the kernel is built for, in 32-column blocks:
+// equal ranks 32 .. 192 and 256, and the value-heavy pairs near 1:1.5 and
+// 1:2 of Appendix D.2 for the totals 2 r = 256, 320 and 384
+constexpr bool tiles_rank_pair(int rbk, int rbv) {
+  return (rbk == rbv && ((rbk >= 1 && rbk <= 6) || rbk == 8)) || (rbk == 3 && rbv == 5) ||
+         (rbk == 2 && rbv == 6) || (rbk == 4 && rbv == 6) || (rbk == 3 && rbv == 7) || (rbk == 5 && rbv == 7) ||
+         (rbk == 4 && rbv == 8);
+}
+
 struct Problem {
   int B, hq, hkv, dh, G, Dp;
   int nb, rank, R, Dg;                // basis groups, rank per group, R = nb*rank, Dg = Dp/nb
+  int rank_v, Rv;                     // the value side's (= rank, R unless asymmetric)
   int s, W, Wq, k, kappa, pool_mode, agg;
   int bases_shared, dtype;
   int64_t cap;

@@ -16,7 +16,7 @@ def cfg_from_workload(wl, capacity=None, **over):
     kw = dict(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
               rank=wl.rank, basis_groups=wl.basis_groups, n_sink=wl.n_sink, window=wl.window,
               q_window=wl.q_window, topk=wl.topk, pool_kernel=wl.pool_kernel, pool_mode=wl.pool_mode,
-              group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype,
+              group_agg=wl.group_agg, rope_theta=wl.rope_theta, dtype=wl.dtype, rank_v=wl.rank_v,
               capacity=capacity if capacity is not None else ((wl.L + 15) // 16) * 16)
     kw.update(over)
     return s4r.make_config(**kw)
@@ -45,7 +45,8 @@ def to_gpu_state(c, st, device="cuda"):
         n = rm.shape[1]
         full = np.zeros((rm.shape[0], c.capacity, rm.shape[2]))
         full[:, :n] = rm
-        g[k] = s4r.pack_coef(c, c.capacity, dev(full, dt, device))
+        ck = c if k == "coef_k" else s4r.value_config(c)       # the value cache has its own width
+        g[k] = s4r.pack_coef(ck, c.capacity, dev(full, dt, device))
     return g
 
 

@@ -47,8 +47,8 @@ def test_exports_match_header():
 
 
 def test_config_struct_layout():
-    assert ctypes.sizeof(L.Config) == 72
-    assert L.Config.capacity.offset == 56 and L.Config.dtype.offset == 68
+    assert ctypes.sizeof(L.Config) == 80
+    assert L.Config.capacity.offset == 56 and L.Config.dtype.offset == 68 and L.Config.rank_v.offset == 72
 
 
 def test_version_and_sizes():
@@ -88,6 +88,33 @@ def test_config_validation(field, value, status):
     st = L.load().s4r_workspace_size(ctypes.byref(c), ctypes.byref(n))
     assert st == status
     assert L.load().s4r_last_error().decode()
+
+
+@pytest.mark.parametrize("rank_v,status", [(16, L.S4R_ERR_UNSUPPORTED), (-32, L.S4R_ERR_BAD_SHAPE),
+                                           (160, L.S4R_ERR_BAD_SHAPE)])
+def test_value_rank_validation(rank_v, status):
+    """rank_v: 0 (= rank) or a multiple of 32 within Dp / basis_groups = 128."""
+    lib = L.load()
+    sz = ctypes.c_size_t()
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank_v=rank_v)), ctypes.byref(sz)) == status
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank_v=96)), ctypes.byref(sz)) == L.S4R_OK
+
+
+def test_asymmetric_ranks_support():
+    """Asymmetric ranks run on the bf16 matrix-core path for the listed pairs;
+    other settings are refused before any launch."""
+    lib = L.load()
+
+    def step(c):
+        return lib.s4r_decode_step(ctypes.byref(c), 100, FAKE, None, FAKE, FAKE, None, None, FAKE, FAKE, FAKE,
+                                   FAKE, None, None, FAKE, None, None, FAKE, 0, None)
+    assert step(cfg(rank=32, rank_v=96)) == L.S4R_ERR_UNSUPPORTED             # pair (32, 96) not built
+    assert step(cfg(rank=64, rank_v=96, dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
+    assert step(cfg(head_dim=128, rank=96, rank_v=160)) == L.S4R_ERR_WORKSPACE  # built: fails on ws only
+    assert lib.s4r_reconstruct(ctypes.byref(cfg(head_dim=128, rank=96, rank_v=160)), 100, 4, FAKE, FAKE, FAKE,
+                               FAKE, FAKE, FAKE, FAKE, None) == L.S4R_ERR_UNSUPPORTED
+    assert lib.s4r_prefill_project(ctypes.byref(cfg(head_dim=128, rank=96, rank_v=160)), 100, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_UNSUPPORTED
 
 
 def test_null_config():

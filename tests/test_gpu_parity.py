@@ -556,3 +556,71 @@ def test_full_reconstruction(shape, L, B, dh):
     assert np.isfinite(o).all()
     err = rel_err_rows(o, ref)
     assert err <= OUT_TOL["bf16"], f"output rel err {err:.3e}"
+
+
+@pytest.mark.parametrize("shape,dh,rank,rank_v,L,append", [
+    ("llama8b_32k", 128, 128, 192, 4000, False),
+    ("llama8b_32k", 128, 128, 192, 3001, True),
+    ("llama8b_32k", 128, 96, 224, 2500, True),
+    ("llama8b_32k", 64, 96, 160, 1800, False),
+    ("qwen3_4b_120k", 128, 160, 224, 3000, True),
+    ("qwen3_4b_120k", 128, 128, 256, 2000, False),
+])
+def test_asymmetric_ranks(shape, dh, rank, rank_v, L, append):
+    """Key rank r^K below the value rank r^V (Appendix D.2): the fused step
+    (appended rows included) and full reconstruction against the oracle, rows
+    past L poisoned with NaN."""
+    base = W.CONFIGS[shape]
+    wl = base.scaled(N=L + base.n_sink, batch=2, head_dim=dh, rank=rank, rank_v=rank_v, topk=200, n_needles=3)
+    cap = ((L + 15) // 16) * 16 + 16
+    st = W.latent_state(wl, seed=rank_v + L, capacity=cap, L=L)
+    c = cfg_from_workload(wl, capacity=cap)
+    st_gpu = dict(st)
+    for key in ("coef_k", "coef_v"):
+        x = st[key].copy()
+        x[:, L - (1 if append else 0):] = np.nan
+        st_gpu[key] = x
+    g = to_gpu_state(c, st_gpu)
+    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    kw = {}
+    if append:
+        rng = np.random.default_rng(L)
+        kn = W.round_storage(rng.standard_normal((2, wl.Dp)), "bf16")
+        vn = W.round_storage(rng.standard_normal((2, wl.Dp)), "bf16")
+        kw = dict(k_new=dev(kn, torch.bfloat16), v_new=dev(vn, torch.bfloat16))
+    ws = s4r.alloc_workspace(c)
+    m = s4r.num_selected(c, L)
+    idx = torch.empty((2, m), dtype=torch.int32, device="cuda")
+    scores = torch.empty((2, L), dtype=torch.float32, device="cuda")
+    out = s4r.decode_step(c, L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
+                          g["coef_v"], ws, qwin_prev=qwin, idx_out=idx, scores_out=scores, **kw)
+    torch.cuda.synchronize()
+    rows_k = s4r.unpack_coef(c, L, g["coef_k"]).float().cpu().numpy().astype(np.float64)
+    rows_v = s4r.unpack_coef(s4r.value_config(c), L, g["coef_v"]).float().cpu().numpy().astype(np.float64)
+    assert rows_k.shape[-1] == wl.R and rows_v.shape[-1] == wl.R_v
+    oc = oracle_cfg(c, wl.pool_mode, wl.group_agg)
+    if append:
+        ck, cv = decode.project_append(kn, vn, st["bases_k"], st["bases_v"], oc["dtype"])
+        assert np.abs(rows_k[:, L - 1] - ck).max() <= 2 ** -7 * np.abs(ck).max()
+        assert np.abs(rows_v[:, L - 1] - cv).max() <= 2 ** -7 * np.abs(cv).max()
+        assert (rows_v[:, L - 1] == cv).mean() > 0.99
+    ref = decode.decode_step(oc, L, st["q"], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"], rows_k,
+                             rows_v, qwin_prev=st["qwin_prev"])
+    a = ref["a_tilde"]
+    err = np.abs(scores.cpu().numpy() - a) / np.maximum(np.abs(a), 1e-30)
+    assert err.max() <= SCORE_TOL, f"score rel err {err.max():.3e}"
+    idx_np = idx.cpu().numpy().astype(np.int64)
+    check_selection(idx_np, ref["idx"], a, L, wl.window, wl.topk)
+    theta = oc["rope_theta"]
+    o_ref, _, _ = decode.sparse_attention(st["q"], idx_np, st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                                          rows_k, rows_v, L, wl.n_kv_heads, theta)
+    err = rel_err_rows(out.cpu().numpy(), o_ref)
+    assert err <= OUT_TOL["bf16"], f"output rel err {err:.3e}"
+    # full reconstruction over the same caches
+    outf = s4r.full_recon_decode(c, L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
+                                 g["coef_v"], ws)
+    torch.cuda.synchronize()
+    f_ref = decode.full_reconstruction_decode(st["q"], st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                                              rows_k, rows_v, L, wl.n_kv_heads, theta)
+    err = rel_err_rows(outf.cpu().numpy(), f_ref)
+    assert err <= OUT_TOL["bf16"], f"full reconstruction rel err {err:.3e}"

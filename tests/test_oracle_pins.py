@@ -312,19 +312,20 @@ def check_dense_comparator(seed=11):
     return np.allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
-def check_full_reconstruction(seed=12, nb=1):
+def check_full_reconstruction(seed=12, nb=1, rank_v=5):
     """Full-reconstruction decoding (Appendix B.1) equals torch SDPA over the
     cache rebuilt with torch matrix products, C B^T per basis group, sinks
-    first, complex-form RoPE at positions 0..s+L-1."""
+    first, complex-form RoPE at positions 0..s+L-1 (also with a value rank
+    other than the key rank, Appendix D.2)."""
     rng = np.random.default_rng(seed)
     B, hq, hkv, dh, L, s, rank = 2, 8, 2, 16, 23, 3, 5
     Dp = hkv * dh
     Dg = Dp // nb
     q = rng.standard_normal((B, hq, dh))
     bases_k = rng.standard_normal((B, nb, Dg, rank))
-    bases_v = rng.standard_normal((B, nb, Dg, rank))
+    bases_v = rng.standard_normal((B, nb, Dg, rank_v))
     ck = rng.standard_normal((B, L + 4, nb * rank))           # rows past L are never used
-    cv = rng.standard_normal((B, L + 4, nb * rank))
+    cv = rng.standard_normal((B, L + 4, nb * rank_v))
     sk = rng.standard_normal((B, s, Dp))
     sv = rng.standard_normal((B, s, Dp))
     theta = 10000.0
@@ -332,7 +333,8 @@ def check_full_reconstruction(seed=12, nb=1):
     def rebuild(c, bases):
         tc = torch.from_numpy(c[:, :L])
         tb = torch.from_numpy(bases)
-        parts = [tc[:, :, g * rank:(g + 1) * rank] @ tb[:, g].transpose(1, 2) for g in range(nb)]
+        r = bases.shape[-1]
+        parts = [tc[:, :, g * r:(g + 1) * r] @ tb[:, g].transpose(1, 2) for g in range(nb)]
         return torch.cat(parts, dim=2).numpy()
     K = np.concatenate([sk, rebuild(ck, bases_k)], axis=1)
     V = np.concatenate([sv, rebuild(cv, bases_v)], axis=1)
@@ -386,9 +388,9 @@ def test_dense_comparator_matches_torch_sdpa():
     assert check_dense_comparator()
 
 
-@pytest.mark.parametrize("nb", [1, 2])
-def test_full_reconstruction_matches_torch_sdpa(nb):
-    assert check_full_reconstruction(nb=nb)
+@pytest.mark.parametrize("nb,rank_v", [(1, 5), (2, 5), (1, 9), (2, 7)])
+def test_full_reconstruction_matches_torch_sdpa(nb, rank_v):
+    assert check_full_reconstruction(nb=nb, rank_v=rank_v)
 
 
 def test_full_reconstruction_over_every_index_is_sparse_attention():

@@ -61,6 +61,7 @@ class Workload:
     group_agg: str = "mean"
     layers: int = 1
     steps: int = 1
+    rank_v: int = 0          # value rank per basis group (Appendix D.2); 0 = rank
 
     @property
     def G(self):
@@ -73,6 +74,14 @@ class Workload:
     @property
     def R(self):
         return self.rank * self.basis_groups
+
+    @property
+    def rank_value(self):
+        return self.rank_v or self.rank
+
+    @property
+    def R_v(self):
+        return self.rank_value * self.basis_groups
 
     @property
     def L(self):
@@ -234,27 +243,31 @@ def latent_state(wl, seed=0, layer=0, capacity=None, L=None):
     cap = L if capacity is None else capacity
     out = {k: None for k in ("bases_k", "bases_v", "coef_k", "coef_v", "sink_k", "sink_v", "q", "qwin_prev")}
     bk = np.empty((B, nb, dg, wl.rank))
-    bv = np.empty((B, nb, dg, wl.rank))
+    bv = np.empty((B, nb, dg, wl.rank_value))
+    Rv = wl.R_v
     ck = np.zeros((B, cap, R))
-    cv = np.zeros((B, cap, R))
+    cv = np.zeros((B, cap, Rv))
     sk = np.empty((B, wl.n_sink, Dp))
     sv = np.empty((B, wl.n_sink, Dp))
     qg = np.empty((B, wl.G, Dp))
     qwin = np.empty((B, wl.G, wl.q_window - 1, R))
     needles = []
     spectrum = 1.0 / (1.0 + np.arange(R) / 16.0)
+    spectrum_v = 1.0 / (1.0 + np.arange(Rv) / 16.0)
     for b in range(B):
         rbk = _rng(wl, seed, layer, b, _T_BASIS_K)
         rbv = _rng(wl, seed, layer, b, _T_BASIS_V)
         for g in range(nb):
             bk[b, g] = _orthonormal(rbk, dg, wl.rank)
-            bv[b, g] = _orthonormal(rbv, dg, wl.rank)
+            bv[b, g] = _orthonormal(rbv, dg, wl.rank_value)
         rk, rv, rq, rs = (_rng(wl, seed, layer, b, t) for t in (_T_KEY, _T_VAL, _T_QRY, _T_SINK))
         scale = np.sqrt(Dp) / np.sqrt((spectrum ** 2).sum())
+        scale_v = np.sqrt(Dp) / np.sqrt((spectrum_v ** 2).sum())
         Mk = rk.standard_normal((wl.r_true, R)) * spectrum / np.sqrt(wl.r_true) * scale
-        Mv = rv.standard_normal((wl.r_true, R)) * spectrum / np.sqrt(wl.r_true) * scale
+        Mv = rv.standard_normal((wl.r_true, Rv)) * spectrum_v / np.sqrt(wl.r_true) * scale_v
         ck[b, :L] = _signal(rk, L, wl.r_true, wl.heavy_tail) @ Mk + wl.noise * scale * rk.standard_normal((L, R)) * spectrum
-        cv[b, :L] = _signal(rv, L, wl.r_true, wl.heavy_tail) @ Mv + wl.noise * scale * rv.standard_normal((L, R)) * spectrum
+        cv[b, :L] = (_signal(rv, L, wl.r_true, wl.heavy_tail) @ Mv
+                     + wl.noise * scale_v * rv.standard_normal((L, Rv)) * spectrum_v)
         sk[b] = 10.0 * rs.standard_normal((wl.n_sink, Dp))
         sv[b] = 10.0 * rs.standard_normal((wl.n_sink, Dp))
         # query: latent direction u_g in the span of Mk's rows, mapped through B^K
