@@ -355,6 +355,28 @@ def main():
             "frac_of_hbm_peak": round(pf_bytes / (pf_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         }
         log(f"[bench] prefill bulk projection: {pf_us:.1f} us ({comparator['prefill_projection']['achieved_GBps']:.0f} GB/s)")
+        # the prefill's basis construction for the same prompt (sample, normalise,
+        # Gram in fp64, eigenvectors), 20% of the rows sampled
+        wsb = torch.empty(s4r.api.prefill_bases_workspace_size(cpf, n_pf, 0.2), dtype=torch.uint8, device="cuda")
+        bkp, bvp = s4r.prefill_bases(cpf, n_pf, dk, dv, eta=0.2, center=True, ws=wsb)
+        torch.cuda.synchronize()
+        q0 = torch.cuda.Event(enable_timing=True)
+        q1 = torch.cuda.Event(enable_timing=True)
+        nq = 3
+        q0.record(stream)
+        for _ in range(nq):
+            s4r.prefill_bases(cpf, n_pf, dk, dv, eta=0.2, center=True, bases_k=bkp, bases_v=bvp, ws=wsb)
+        q1.record(stream)
+        torch.cuda.synchronize()
+        pb_ms = q0.elapsed_time(q1) / nq
+        comparator["prefill_bases"] = {
+            "what": f"s4r_prefill_bases: hybrid sample of {s4r.num_samples(n_pf, 0.2)} of {n_pf} rows, token-wise "
+                    f"normalisation, centring, fp64 Gram and top-{wl.rank} eigenvectors for K and V of "
+                    f"{wl.batch} sequences (Section 3.1.2)",
+            "ms": round(pb_ms, 2),
+        }
+        log(f"[bench] prefill basis construction: {pb_ms:.2f} ms")
+        del wsb, bkp, bvp
         del dk, dv, wsd, pk, pv, wspf
         torch.cuda.synchronize()
         # full-reconstruction low-rank decoding (Appendix B.1) over the same

@@ -226,6 +226,34 @@ s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q
                                  size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Basis construction of the prefill stage (Section 3.1.2, Eq. svd), per
+ * sequence, key/value and basis group: the hybrid sample of the n_rows
+ * non-sink rows (T' = max(1, floor(eta * n_rows)) rows: the most recent
+ * round(0.7 T') as a contiguous block, the rest spaced uniformly over the
+ * earlier positions, numpy's linspace then round-half-even), each sampled
+ * row's group slice L2-normalised, optionally mean-centred (center = 1),
+ * and the right singular vectors of the `rank` largest singular values
+ * (rank_v for the values), largest first, written as bases_k / bases_v
+ * [B, basis_groups, Dp / basis_groups, rank] in the storage dtype.  Signs of
+ * the singular vectors are arbitrary (the decode step depends on B B^T only).
+ * s_k / s_v: [B, n_rows, Dp] raw pre-RoPE rows, bf16.  sample_idx_out
+ * (optional, device, s4r_prefill_num_samples entries) receives the sample.
+ * The Gram matrices are formed in fp64 by this library's kernels; their
+ * symmetric eigenproblems run in rocSOLVER (fp64, divide and conquer) within
+ * the caller's workspace of s4r_prefill_bases_workspace_size bytes; the first
+ * call on a device creates one rocBLAS handle, kept until the process ends.
+ * bf16 storage, bases_shared = 0, (Dp / basis_groups) % 256 == 0 and at least
+ * max(rank, rank_v) sampled rows (otherwise S4R_ERR_UNSUPPORTED /
+ * S4R_ERR_BAD_SHAPE).
+ */
+int64_t s4r_prefill_num_samples(int64_t n_rows, double eta);
+s4r_status s4r_prefill_bases_workspace_size(const s4r_config* cfg, int64_t n_rows, double eta,
+                                            size_t* bytes);
+s4r_status s4r_prefill_bases(const s4r_config* cfg, int64_t n_rows, const void* s_k, const void* s_v,
+                             double eta, int32_t center, void* bases_k, void* bases_v,
+                             int32_t* sample_idx_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Bulk projection of the prefill stage (Section 3.1, the coefficient
  * equation): C^K = S^K B^K and C^V = S^V B^V per basis group for the prompt's
  * non-sink rows, written into rows [0, n_rows) of the tiled coefficient caches

@@ -20,6 +20,8 @@ from .api import (  # noqa: E402,F401
     make_config,
     num_selected,
     pack_coef,
+    num_samples,
+    prefill_bases,
     prefill_project,
     project_append,
     read_bandwidth,

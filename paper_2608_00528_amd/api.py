@@ -191,6 +191,39 @@ def decode_step_ragged(cfg, lengths, q, sink_k, sink_v, bases_k, bases_v, coef_k
     return out
 
 
+def prefill_bases(cfg, n_rows, s_k, s_v, eta=0.2, center=False, bases_k=None, bases_v=None, sample_idx=None,
+                  ws=None):
+    """Bases of a prompt's non-sink raw K/V rows [B, n_rows, Dp] (hybrid
+    sample, token-wise normalisation, truncated SVD; Section 3.1.2).  Returns
+    (bases_k, bases_v); sample_idx (int32, num_samples entries) receives the
+    sampled positions when given."""
+    dt = storage_dtype(cfg)
+    lib = L.load()
+    dg = cfg.n_kv_heads * cfg.head_dim // cfg.basis_groups
+    shape = lambda r: (cfg.batch, cfg.basis_groups, dg, r)  # noqa: E731
+    if bases_k is None:
+        bases_k = torch.empty(shape(cfg.rank), dtype=dt, device=s_k.device)
+    if bases_v is None:
+        bases_v = torch.empty(shape(cfg.rank_v or cfg.rank), dtype=dt, device=s_k.device)
+    if ws is None:
+        ws = torch.empty(prefill_bases_workspace_size(cfg, n_rows, eta), dtype=torch.uint8, device=s_k.device)
+    L.check(lib.s4r_prefill_bases(_cfgp(cfg), n_rows, _ptr(s_k, "s_k", dt), _ptr(s_v, "s_v", dt), float(eta),
+                                  int(bool(center)), _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt),
+                                  _ptr(sample_idx, "sample_idx", torch.int32, False), _ptr(ws, "ws", torch.uint8),
+                                  ws.numel(), _stream()))
+    return bases_k, bases_v
+
+
+def prefill_bases_workspace_size(cfg, n_rows, eta=0.2):
+    sz = ctypes.c_size_t()
+    L.check(L.load().s4r_prefill_bases_workspace_size(_cfgp(cfg), n_rows, float(eta), ctypes.byref(sz)))
+    return sz.value
+
+
+def num_samples(n_rows, eta=0.2):
+    return L.load().s4r_prefill_num_samples(n_rows, float(eta))
+
+
 def prefill_project(cfg, n_rows, s_k, s_v, bases_k, bases_v, coef_k, coef_v, ws):
     """Bulk projection of a prompt's non-sink raw K/V rows [B, n_rows, Dp]
     into rows [0, n_rows) of the tiled coefficient caches (ws: the decode

@@ -62,7 +62,10 @@ def build(verbose=True, jobs=None):
     tmp = LIB + ".tmp"
     # no undefined symbols: a kernel whose host-side launch stub was not
     # emitted fails here instead of at load time
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", "-o", tmp, *objs]
+    # rocSOLVER (with rocBLAS) solves the prefill's symmetric eigenproblems
+    rocm_lib = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "lib")
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", "-o", tmp, *objs,
+           f"-L{rocm_lib}", "-lrocsolver", "-lrocblas"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")

@@ -2,6 +2,7 @@
 // launch sequence of each entry point.  All validation happens on the host
 // before anything is launched; see include/s4r.h for the contract.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstddef>
@@ -416,6 +417,60 @@ s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q
   Workspace w = carve_workspace(P, ws);
   return hip_status(launch_full_recon(P, w, L, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, out, stream),
                     "s4r_full_recon_decode launch");
+}
+
+// ---- basis construction of the prefill ------------------------------------------------
+static s4r_status check_bases_args(const s4r_config* cfg, int64_t n_rows, double eta, Problem& P, int* nu, int* nr) {
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (P.dtype != S4R_BF16) return fail(S4R_ERR_UNSUPPORTED, "basis construction is built for bf16 storage only");
+  if (P.bases_shared) return fail(S4R_ERR_BAD_SHAPE, "basis construction writes per-sequence bases (bases_shared = 0)");
+  if (P.Dg % 256) return fail(S4R_ERR_UNSUPPORTED, "basis construction needs Dp / basis_groups %% 256 == 0");
+  if (n_rows < 1 || n_rows > INT32_MAX) return fail(S4R_ERR_BAD_SHAPE, "n_rows = %lld outside [1, 2^31)", (long long)n_rows);
+  if (!(eta > 0.0 && eta <= 1.0)) return fail(S4R_ERR_BAD_SHAPE, "eta must lie in (0, 1]");
+  bases_sample_counts(n_rows, eta, nu, nr);
+  if (*nu + *nr < std::max(P.rank, P.rank_v))
+    return fail(S4R_ERR_BAD_SHAPE, "%d sampled rows cannot give %d singular vectors", *nu + *nr,
+                std::max(P.rank, P.rank_v));
+  return S4R_OK;
+}
+
+int64_t s4r_prefill_num_samples(int64_t n_rows, double eta) {
+  if (n_rows < 1 || !(eta > 0.0 && eta <= 1.0)) return -1;
+  int nu = 0, nr = 0;
+  bases_sample_counts(n_rows, eta, &nu, &nr);
+  return nu + nr;
+}
+
+s4r_status s4r_prefill_bases_workspace_size(const s4r_config* cfg, int64_t n_rows, double eta, size_t* bytes) {
+  Problem P;
+  int nu = 0, nr = 0;
+  s4r_status st = check_bases_args(cfg, n_rows, eta, P, &nu, &nr);
+  if (st) return st;
+  if (!bytes) return fail(S4R_ERR_NULL_ARG, "bytes is NULL");
+  return hip_status(prefill_bases_ws_bytes(P, nu + nr, bytes), "s4r_prefill_bases_workspace_size");
+}
+
+s4r_status s4r_prefill_bases(const s4r_config* cfg, int64_t n_rows, const void* s_k, const void* s_v, double eta,
+                             int32_t center, void* bases_k, void* bases_v, int32_t* sample_idx_out, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  int nu = 0, nr = 0;
+  s4r_status st = check_bases_args(cfg, n_rows, eta, P, &nu, &nr);
+  if (st) return st;
+  S4R_REQ(s_k);
+  S4R_REQ(s_v);
+  S4R_REQ(bases_k);
+  S4R_REQ(bases_v);
+  S4R_REQ(ws);
+  if (center != 0 && center != 1) return fail(S4R_ERR_BAD_SHAPE, "center must be 0 or 1");
+  size_t need = 0;
+  if ((st = hip_status(prefill_bases_ws_bytes(P, nu + nr, &need), "s4r_prefill_bases workspace query"))) return st;
+  if (ws_bytes < need)
+    return fail(S4R_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes, need);
+  return hip_status(launch_prefill_bases(P, n_rows, s_k, s_v, nu, nr, center, sample_idx_out, bases_k, bases_v, ws,
+                                         ws_bytes, stream),
+                    "s4r_prefill_bases launch");
 }
 
 // the fused step for a uniform (P.lens.n == 0) or ragged batch; L is the

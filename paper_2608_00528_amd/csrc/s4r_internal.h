@@ -111,6 +111,12 @@ hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const
 hipError_t launch_full_recon(const Problem& P, const Workspace& ws, int64_t L, const void* q, const void* sink_k,
                              const void* sink_v, const void* bases_k, const void* bases_v, const void* coef_k,
                              const void* coef_v, float* out, hipStream_t st);
+// basis construction of the prefill (bases.hip)
+void bases_sample_counts(int64_t T, double eta, int* n_uniform, int* n_recent);
+hipError_t prefill_bases_ws_bytes(const Problem& P, int n_s, size_t* bytes);
+hipError_t launch_prefill_bases(const Problem& P, int64_t n_rows, const void* s_k, const void* s_v, int n_uniform,
+                                int n_recent, int center, int32_t* idx_out, void* bases_k, void* bases_v, void* ws,
+                                size_t ws_bytes, hipStream_t st);
 hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
                                const void* v_cache, float* out, hipStream_t st);
 hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,

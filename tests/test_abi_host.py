@@ -238,6 +238,35 @@ def test_full_recon_argument_errors():
     assert call(cfg(head_dim=32)) == L.S4R_ERR_UNSUPPORTED
 
 
+def test_prefill_sample_counts_match_oracle():
+    """The library's sample count is the length of the oracle's hybrid sample
+    (Section 3.1.2) for lengths and ratios around every rounding case."""
+    from oracle import prefill
+    lib = L.load()
+    for T in (1, 2, 3, 7, 10, 15, 16, 100, 101, 999, 3000, 4096, 120000):
+        for eta in (0.01, 0.05, 0.1, 0.2, 0.25, 0.5, 0.75, 1.0):
+            assert lib.s4r_prefill_num_samples(T, eta) == len(prefill.sample_hybrid(T, eta)), (T, eta)
+    assert lib.s4r_prefill_num_samples(0, 0.2) == -1
+    assert lib.s4r_prefill_num_samples(100, 0.0) == -1
+
+
+def test_prefill_bases_argument_errors():
+    lib = L.load()
+
+    def call(c, n=1000, eta=0.2, s=FAKE, center=0):
+        return lib.s4r_prefill_bases(ctypes.byref(c), n, s, FAKE, eta, center, FAKE, FAKE, None, FAKE, 1 << 40, None)
+    c = cfg(head_dim=128)                                                  # Dg = 256
+    assert call(cfg(head_dim=128, dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
+    assert call(cfg(head_dim=128, bases_shared=True)) == L.S4R_ERR_BAD_SHAPE
+    assert call(cfg(head_dim=64)) == L.S4R_ERR_UNSUPPORTED                 # Dg = 128
+    assert call(c, n=0) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, eta=0.0) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, eta=1.5) == L.S4R_ERR_BAD_SHAPE
+    assert call(c, n=100) == L.S4R_ERR_BAD_SHAPE                           # 20 samples < rank 32
+    sz = ctypes.c_size_t()
+    assert lib.s4r_prefill_bases_workspace_size(ctypes.byref(c), 100, 0.2, ctypes.byref(sz)) == L.S4R_ERR_BAD_SHAPE
+
+
 def test_prefill_projection_argument_errors():
     lib = L.load()
 

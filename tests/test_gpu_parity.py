@@ -624,3 +624,46 @@ def test_asymmetric_ranks(shape, dh, rank, rank_v, L, append):
                                               rows_k, rows_v, L, wl.n_kv_heads, theta)
     err = rel_err_rows(outf.cpu().numpy(), f_ref)
     assert err <= OUT_TOL["bf16"], f"full reconstruction rel err {err:.3e}"
+
+
+@pytest.mark.parametrize("shape,n_rows,eta,center,rank,rank_v", [
+    ("llama8b_32k", 3000, 0.2, True, 128, 0),
+    ("llama8b_32k", 2000, 0.5, False, 160, 0),
+    ("qwen3_4b_120k", 4000, 0.2, True, 160, 224),
+])
+def test_prefill_bases(shape, n_rows, eta, center, rank, rank_v):
+    """Basis construction (Section 3.1.2) against the oracle's prefill: the
+    sample bit-exact; the stored bases span, after the bf16 rounding of their
+    entries, a subspace that captures the optimal energy sum_{i<r} s_i^2 of
+    the normalised (centred) sample to 1e-4, and lie within bf16 rounding of
+    orthonormal."""
+    from oracle import prefill
+    base = W.CONFIGS[shape]
+    wl = base.scaled(N=n_rows + base.n_sink, batch=2, rank=rank, rank_v=rank_v, n_needles=2)
+    raw = W.raw_kv(wl, seed=n_rows)
+    c = cfg_from_workload(wl, capacity=((n_rows + 15) // 16) * 16)
+    sk = dev(raw["S_k"][:, wl.n_sink:], torch.bfloat16)
+    sv = dev(raw["S_v"][:, wl.n_sink:], torch.bfloat16)
+    n_s = s4r.num_samples(n_rows, eta)
+    idx = torch.empty(n_s, dtype=torch.int32, device="cuda")
+    bk, bv = s4r.prefill_bases(c, n_rows, sk, sv, eta=eta, center=center, sample_idx=idx)
+    torch.cuda.synchronize()
+    ref_idx = prefill.sample_hybrid(n_rows, eta)
+    assert np.array_equal(idx.cpu().numpy().astype(np.int64), ref_idx)
+    for side, (x, got, r) in enumerate(((sk, bk, rank), (sv, bv, rank_v or rank))):
+        X = x.float().cpu().numpy().astype(np.float64)
+        B_gpu = got.float().cpu().numpy().astype(np.float64)
+        assert B_gpu.shape == (2, 1, wl.Dp, r)
+        for b in range(2):
+            Xs = prefill.normalize_rows(X[b, ref_idx])
+            if center:
+                Xs = Xs - Xs.mean(axis=0, keepdims=True)
+            sv_ = np.linalg.svd(Xs, compute_uv=False)
+            e_opt = (sv_[:r] ** 2).sum()
+            Bb = B_gpu[b, 0]
+            assert np.abs(Bb.T @ Bb - np.eye(r)).max() <= 2e-2
+            Q, _ = np.linalg.qr(Bb)
+            e_gpu = (np.linalg.norm(Xs @ Q) ** 2)
+            rel = (e_opt - e_gpu) / e_opt
+            print(f"[bases] side {side} seq {b}: energy shortfall {rel:.2e}", flush=True)
+            assert -1e-9 <= rel <= 1e-4
