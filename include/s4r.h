@@ -226,6 +226,20 @@ s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q
                                  size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Query coefficients of several queries (Section 3.2.1, c^Q = s^Q B^K per
+ * query group; Section 3.1 builds the initial query window C^Q this way from
+ * the prompt's last queries): q_rows [B, n_rows, h_q, d_h] pre-RoPE queries in
+ * the storage dtype, row i of every sequence projected like the query of a
+ * decode step; qcoef_out [B, G, n_rows, R] fp32, the layout of qwin_prev when
+ * n_rows = W_q - 1 (oldest first).  fp64 sums in the order the scoring kernel
+ * uses, rounded once to fp32.  ws / ws_bytes: the decode workspace.
+ * 1 <= n_rows <= 4096.
+ */
+s4r_status s4r_project_queries(const s4r_config* cfg, int64_t n_rows, const void* q_rows,
+                               const void* bases_k, float* qcoef_out, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
  * Basis construction of the prefill stage (Section 3.1.2, Eq. svd), per
  * sequence, key/value and basis group: the hybrid sample of the n_rows
  * non-sink rows (T' = max(1, floor(eta * n_rows)) rows: the most recent

@@ -24,6 +24,7 @@ from .api import (  # noqa: E402,F401
     prefill_bases,
     prefill_project,
     project_append,
+    project_queries,
     read_bandwidth,
     reconstruct,
     score_latent,

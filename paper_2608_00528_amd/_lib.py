@@ -21,6 +21,7 @@ EXPORTS = (
     "s4r_timing_enable", "s4r_timing_read", "s4r_read_bandwidth_sink_len", "s4r_read_bandwidth",
     "s4r_dense_decode", "s4r_prefill_project", "s4r_decode_step_ragged",
     "s4r_full_recon_decode", "s4r_prefill_num_samples", "s4r_prefill_bases_workspace_size", "s4r_prefill_bases",
+    "s4r_project_queries",
 )
 
 
@@ -73,6 +74,7 @@ _SIGS = {
     "s4r_read_bandwidth": (_I32, [_P, _I64, _P, _P]),
     "s4r_dense_decode": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "s4r_prefill_project": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "s4r_project_queries": (_I32, [_CFG, _I64, _P, _P, _P, _P, _SZ, _P]),
     "s4r_prefill_num_samples": (_I64, [_I64, ctypes.c_double]),
     "s4r_prefill_bases_workspace_size": (_I32, [_CFG, _I64, ctypes.c_double, ctypes.POINTER(_SZ)]),
     "s4r_prefill_bases": (_I32, [_CFG, _I64, _P, _P, ctypes.c_double, _I32, _P, _P, _P, _P, _SZ, _P]),

@@ -191,6 +191,20 @@ def decode_step_ragged(cfg, lengths, q, sink_k, sink_v, bases_k, bases_v, coef_k
     return out
 
 
+def project_queries(cfg, q_rows, bases_k, ws, out=None):
+    """C^Q rows [B, G, n, R] fp32 of the queries q_rows [B, n, h_q, d_h] (the
+    initial query window of the prefill: qwin_prev for n = W_q - 1)."""
+    dt = storage_dtype(cfg)
+    n = q_rows.shape[1]
+    G = cfg.n_q_heads // cfg.n_kv_heads
+    if out is None:
+        out = torch.empty((cfg.batch, G, n, _R(cfg)), dtype=torch.float32, device=q_rows.device)
+    L.check(L.load().s4r_project_queries(_cfgp(cfg), n, _ptr(q_rows, "q_rows", dt), _ptr(bases_k, "bases_k", dt),
+                                         _ptr(out, "out", torch.float32), _ptr(ws, "ws", torch.uint8), ws.numel(),
+                                         _stream()))
+    return out
+
+
 def prefill_bases(cfg, n_rows, s_k, s_v, eta=0.2, center=False, bases_k=None, bases_v=None, sample_idx=None,
                   ws=None):
     """Bases of a prompt's non-sink raw K/V rows [B, n_rows, Dp] (hybrid

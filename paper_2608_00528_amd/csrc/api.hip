@@ -419,6 +419,21 @@ s4r_status s4r_full_recon_decode(const s4r_config* cfg, int64_t L, const void* q
                     "s4r_full_recon_decode launch");
 }
 
+s4r_status s4r_project_queries(const s4r_config* cfg, int64_t n_rows, const void* q_rows, const void* bases_k,
+                               float* qcoef_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (n_rows < 1 || n_rows > 4096) return fail(S4R_ERR_BAD_SHAPE, "n_rows = %lld outside [1, 4096]", (long long)n_rows);
+  S4R_REQ(q_rows);
+  S4R_REQ(bases_k);
+  S4R_REQ(qcoef_out);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  return hip_status(launch_project_queries(P, w, n_rows, q_rows, bases_k, qcoef_out, stream),
+                    "s4r_project_queries launch");
+}
+
 // ---- basis construction of the prefill ------------------------------------------------
 static s4r_status check_bases_args(const s4r_config* cfg, int64_t n_rows, double eta, Problem& P, int* nu, int* nr) {
   s4r_status st = make_problem(cfg, P);

@@ -285,6 +285,38 @@ hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist,
   return hipGetLastError();
 }
 
+// rows of C^Q from the query-projection partials: out[b][g][row][r] = the fp32
+// rounding of the chunk partials summed in chunk order (the order the scoring
+// kernel sums them in)
+__global__ __launch_bounds__(256) void k_qcoef_row(const double* __restrict__ qpart, float* __restrict__ out, int B,
+                                                   int G, int R, int nch, int64_t n_rows, int64_t row) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * G * R) return;
+  const int b = i / (G * R), g = (i / R) % G, r = i % R;
+  double x = qpart[(((int64_t)b * nch) * G + g) * R + r];
+  for (int c = 1; c < nch; ++c) x += qpart[(((int64_t)b * nch + c) * G + g) * R + r];
+  out[(((int64_t)b * G + g) * n_rows + row) * R + r] = (float)x;
+}
+
+// C^Q rows of n_rows queries [B, n_rows, h_q, d_h]: each row staged as
+// [B, h_q, d_h] in the workspace, projected, and its partials summed
+hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t n_rows, const void* q_rows,
+                                  const void* bases_k, float* out, hipStream_t st) {
+  const size_t es = P.dtype == S4R_BF16 ? 2 : 4;
+  const size_t row_bytes = (size_t)P.hq * P.dh * es;
+  void* staged = ws.part_o;                       // >= B * h_q * d_h * 4 bytes
+  const int n = P.B * P.G * P.R;
+  for (int64_t row = 0; row < n_rows; ++row) {
+    hipError_t e = hipMemcpy2DAsync(staged, row_bytes, static_cast<const char*>(q_rows) + row * row_bytes,
+                                    (size_t)n_rows * row_bytes, row_bytes, P.B, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess) e = launch_project_query(P, ws.qpart, ws.hist, staged, bases_k, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_qcoef_row, dim3((n + 255) / 256), dim3(256), 0, st, ws.qpart, out, P.B, P.G, P.R,
+                       project_chunks(P), n_rows, row);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
   dim3 grid(std::max(P.R, P.Rv) / 32, P.B, 2);

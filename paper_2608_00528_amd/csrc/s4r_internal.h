@@ -117,6 +117,8 @@ hipError_t prefill_bases_ws_bytes(const Problem& P, int n_s, size_t* bytes);
 hipError_t launch_prefill_bases(const Problem& P, int64_t n_rows, const void* s_k, const void* s_v, int n_uniform,
                                 int n_recent, int center, int32_t* idx_out, void* bases_k, void* bases_v, void* ws,
                                 size_t ws_bytes, hipStream_t st);
+hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t n_rows, const void* q_rows,
+                                  const void* bases_k, float* out, hipStream_t st);
 hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
                                const void* v_cache, float* out, hipStream_t st);
 hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,

@@ -238,6 +238,18 @@ def test_full_recon_argument_errors():
     assert call(cfg(head_dim=32)) == L.S4R_ERR_UNSUPPORTED
 
 
+def test_project_queries_argument_errors():
+    lib = L.load()
+
+    def call(n=3, q=FAKE, out=FAKE, wsb=1 << 40):
+        return lib.s4r_project_queries(ctypes.byref(cfg()), n, q, FAKE, out, FAKE, wsb, None)
+    assert call(n=0) == L.S4R_ERR_BAD_SHAPE
+    assert call(n=5000) == L.S4R_ERR_BAD_SHAPE
+    assert call(q=None) == L.S4R_ERR_NULL_ARG
+    assert call(out=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert call(wsb=16) == L.S4R_ERR_WORKSPACE
+
+
 def test_prefill_sample_counts_match_oracle():
     """The library's sample count is the length of the oracle's hybrid sample
     (Section 3.1.2) for lengths and ratios around every rounding case."""

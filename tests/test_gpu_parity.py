@@ -667,3 +667,32 @@ def test_prefill_bases(shape, n_rows, eta, center, rank, rank_v):
             rel = (e_opt - e_gpu) / e_opt
             print(f"[bases] side {side} seq {b}: energy shortfall {rel:.2e}", flush=True)
             assert -1e-9 <= rel <= 1e-4
+
+
+@pytest.mark.parametrize("shape,n", [("qwen3_4b_120k", 3), ("llama8b_32k", 5), ("qwen7b_128k", 1)])
+def test_project_queries(shape, n):
+    """Query coefficients of n queries (the prefill's initial query window)
+    against the oracle's projection (fp64, rounded once to fp32: at most an
+    ulp apart); the row of the step's own query is bit-identical to the
+    c_t^Q the scoring entry point reports."""
+    wl = W.CONFIGS[shape].scaled(N=2048 + 4, batch=2, topk=64)
+    st = W.latent_state(wl, seed=n)
+    c = cfg_from_workload(wl)
+    g = to_gpu_state(c, st)
+    ws = s4r.alloc_workspace(c)
+    rng = np.random.default_rng(n)
+    qrows = W.round_storage(rng.standard_normal((2, n, wl.n_q_heads, wl.head_dim)), "bf16")
+    qrows[:, -1] = st["q"]
+    got = s4r.project_queries(c, dev(qrows, torch.bfloat16), g["bases_k"], ws)
+    qco = torch.empty((2, wl.G, wl.R), dtype=torch.float32, device="cuda")
+    s4r.score_latent(c, wl.L, g["q"], g["bases_k"], g["coef_k"], ws, qcoef=qco,
+                     qwin_prev=None if wl.q_window == 1 else torch.zeros((2, wl.G, wl.q_window - 1, wl.R),
+                                                                         dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    assert got.shape == (2, wl.G, n, wl.R)
+    for i in range(n):
+        ref = decode.project(decode.group_queries(qrows[:, i], wl.n_kv_heads), st["bases_k"])    # [B, G, R]
+        err = np.abs(got[:, :, i] - ref).max() / np.abs(ref).max()
+        assert err <= 2e-7, f"row {i}: rel err {err:.2e}"
+    assert np.array_equal(got[:, :, -1], qco.cpu().numpy().astype(np.float64))
