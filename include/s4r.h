@@ -137,7 +137,8 @@ s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q,
  * Index selection (Section 3.2.3): I_local = [max(L - W, 0), L),
  * I_global = the k_eff largest scores[b, 0 : L - W] (equal scores go to the
  * lower position), idx[b] = sorted(I_global) followed by I_local.  Bit-exact
- * and deterministic for a given scores array.
+ * and deterministic for a given scores array.  Scores must be non-negative
+ * and finite (as the relevance A~ is); their order is taken from their bits.
  */
 s4r_status s4r_select_topk(const s4r_config* cfg, int64_t L, const float* scores,
                            int32_t* idx, void* ws, size_t ws_bytes, hipStream_t stream);

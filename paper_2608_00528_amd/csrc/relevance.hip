@@ -4,6 +4,7 @@
 // histogram; k_hist_scores builds it for caller-given scores.
 #include "s4r_device.h"
 #include "s4r_internal.h"
+#include "select_key.h"
 
 namespace s4r {
 
@@ -272,7 +273,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
       atilde[(int64_t)b * cap + x] = af[j];
       if (scores_out) scores_out[(int64_t)b * score_stride + x] = af[j];
     }
-    if (x < n_hist) atomicAdd(&hl[score_key(af[j]) >> kHistShift], 1u);
+    if (x < n_hist) atomicAdd(&hl[selection_key(af[j]) >> kHistShift], 1u);
   }
   __syncthreads();
   // this workgroup's histogram into the sequence's (zeroed by the query
@@ -300,7 +301,7 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
   const int t0 = blockIdx.x * kHistChunk;
   for (int i = threadIdx.x; i < kHistChunk; i += blockDim.x) {
     const int x = t0 + i;
-    if (x < n_hist) atomicAdd(&hl[score_key(scores[(int64_t)b * L + x]) >> kHistShift], 1u);
+    if (x < n_hist) atomicAdd(&hl[selection_key(scores[(int64_t)b * L + x]) >> kHistShift], 1u);
   }
   __syncthreads();
   uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;

@@ -215,7 +215,4 @@ __device__ __forceinline__ float exp_neg_accurate(double x) {
   return ldexpf(__builtin_amdgcn_exp2f(f), (int)fmax(n, -300.0));
 }
 
-// order-preserving key of a non-negative fp32 score (sign bit is clear)
-__device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s); }
-
 }  // namespace s4r

@@ -4,7 +4,8 @@
 //              [0, L - W), equal scores going to the lower position
 //   idx      = sorted(I_global) ++ I_local
 //
-// Scores are non-negative fp32, so their bit patterns order like the values;
+// Scores are non-negative fp32, so their bit patterns (sign bit shifted out)
+// order like the values;
 // a candidate is the composite (key << 32) | ~position, unique, and larger
 // exactly when it goes first (higher score, then lower position).
 //
@@ -26,6 +27,7 @@
 // Integer work on the given scores: bit-exact and deterministic.
 #include "s4r_device.h"
 #include "s4r_internal.h"
+#include "select_key.h"
 
 namespace s4r {
 
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
 #pragma unroll
   for (int i = 0; i < kSelPer; ++i) {
     const int x = c0 + t * kSelPer + i;
-    const uint32_t key = score_key(v[i]);
+    const uint32_t key = selection_key(v[i]);
     const int bin = (int)(key >> kHistShift);
     const bool valid = x < n_hist;
     if (valid && bin > b1) mask8 |= 1u << i;
