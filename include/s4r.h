@@ -256,7 +256,10 @@ s4r_status s4r_project_queries(const s4r_config* cfg, int64_t n_rows, const void
  * The Gram matrices are formed in fp64 by this library's kernels; their
  * symmetric eigenproblems run in rocSOLVER (fp64, divide and conquer) within
  * the caller's workspace of s4r_prefill_bases_workspace_size bytes; the first
- * call on a device creates one rocBLAS handle, kept until the process ends.
+ * call on a device creates one rocBLAS handle, kept until the process ends
+ * (host threads calling on one device are serialised around it).  The
+ * solver's per-matrix convergence flag is not read back (the call stays
+ * asynchronous); the Gram matrices are symmetric positive semi-definite.
  * bf16 storage, bases_shared = 0, (Dp / basis_groups) % 256 == 0 and at least
  * max(rank, rank_v) sampled rows (otherwise S4R_ERR_UNSUPPORTED /
  * S4R_ERR_BAD_SHAPE).

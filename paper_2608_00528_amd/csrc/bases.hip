@@ -199,7 +199,9 @@ __global__ __launch_bounds__(256) void k_write_bases(const double* __restrict__ 
 // ---- host side -----------------------------------------------------------------------------
 
 // one rocBLAS handle per device, created on first use and kept until the
-// process ends (its workspace is always the caller's)
+// process ends (its workspace is always the caller's); handle_mutex(dev)
+// serialises the set-stream / set-workspace / solve sequence of host threads
+static std::mutex g_handle_mu[64];
 static rocblas_handle device_handle(hipError_t& err) {
   static std::mutex mu;
   static rocblas_handle handles[64] = {};
@@ -259,6 +261,9 @@ hipError_t solver_bytes(const Problem& P, size_t* bytes) {
   if (!h) return err == hipSuccess ? hipErrorUnknown : err;
   const int nmat = P.B * 2 * P.nb, Dg = P.Dg;
   double* dummy = reinterpret_cast<double*>(256);   // never dereferenced in a size query
+  int dev = 0;
+  if ((err = hipGetDevice(&dev)) != hipSuccess) return err;
+  std::lock_guard<std::mutex> lk(g_handle_mu[dev]);
   if (rocblas_start_device_memory_size_query(h) != rocblas_status_success) return hipErrorUnknown;
   rocsolver_dsyevd_strided_batched(h, rocblas_evect_original, rocblas_fill_upper, Dg, dummy, Dg,
                                    (rocblas_stride)Dg * Dg, dummy, Dg, dummy, Dg,
@@ -311,6 +316,9 @@ hipError_t launch_prefill_bases(const Problem& P, int64_t n_rows, const void* s_
   if ((e = hipGetLastError()) != hipSuccess) return e;
   rocblas_handle h = device_handle(e);
   if (!h) return e == hipSuccess ? hipErrorUnknown : e;
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_handle_mu[dev]);
   if (rocblas_set_stream(h, st) != rocblas_status_success) return hipErrorUnknown;
   if (rocblas_set_workspace(h, w + l.solver, sb) != rocblas_status_success) return hipErrorUnknown;
   const rocblas_status rs = rocsolver_dsyevd_strided_batched(
