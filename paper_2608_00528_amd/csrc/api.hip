@@ -13,6 +13,7 @@
 
 #include "s4r_device.h"
 #include "s4r_internal.h"
+#include "select_key.h"
 
 static_assert(sizeof(s4r_config) == 80 && offsetof(s4r_config, capacity) == 56 &&
                   offsetof(s4r_config, rank_v) == 72,
@@ -552,7 +553,9 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);
   e = mark(e, 2, false);
   e = mark(e, 3, true);
-  if (e == hipSuccess) e = launch_select(P, w, L, w.atilde, P.cap, w.idx, idx_out, stream);
+  // the key the relevance kernel built the histogram with
+  if (e == hipSuccess)
+    e = launch_select_keyed(P, w, L, w.atilde, P.cap, w.idx, idx_out, fused_key_shift(P, L), stream);
   e = mark(e, 3, false);
   if (e == hipSuccess)
     e = launch_attention(P, w, L, m, k_eff, q, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, out,

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
     int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
-    Lens lens) {
+    Lens lens, int key_shift) {
   constexpr int GWP = 4 * NQ;
   constexpr int CHUNK = kRelThreads * TPT;
   constexpr int SPAN_MAX = CHUNK + 64;
@@ -273,7 +273,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
       atilde[(int64_t)b * cap + x] = af[j];
       if (scores_out) scores_out[(int64_t)b * score_stride + x] = af[j];
     }
-    if (x < n_hist) atomicAdd(&hl[selection_key(af[j]) >> kHistShift], 1u);
+    if (x < n_hist) atomicAdd(&hl[selection_key_shift(af[j], key_shift) >> kHistShift], 1u);
   }
   __syncthreads();
   // this workgroup's histogram into the sequence's (zeroed by the query
@@ -363,7 +363,7 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), nwg, P.lens);
+                     (int)(P.cap / kTileTok), nwg, P.lens, fused_key_shift(P, L));
 }
 
 template <int NQ>

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
     const float* __restrict__ scores, int64_t score_stride, uint32_t* __restrict__ hist_all,
     uint64_t* __restrict__ cand_all, uint32_t* __restrict__ bitmap_all, uint32_t* __restrict__ cand_count,
     uint32_t* __restrict__ above_count, uint32_t* __restrict__ sel_info, int64_t cand_stride, int64_t cnt_stride,
-    int64_t cap, int L, int W, int k, Lens lens) {
+    int64_t cap, int L, int W, int k, Lens lens, int key_shift) {
   const int b = blockIdx.y, c = blockIdx.x;
   L = (int)len_of(lens, b, L);
   const int t = threadIdx.x, lane = t & 63;
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
 #pragma unroll
   for (int i = 0; i < kSelPer; ++i) {
     const int x = c0 + t * kSelPer + i;
-    const uint32_t key = selection_key(v[i]);
+    const uint32_t key = selection_key_shift(v[i], key_shift);
     const int bin = (int)(key >> kHistShift);
     const bool valid = x < n_hist;
     if (valid && bin > b1) mask8 |= 1u << i;
@@ -397,13 +397,18 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
 
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st) {
+  return launch_select_keyed(P, ws, L, scores, score_stride, idx, idx_copy, 1, st);
+}
+
+hipError_t launch_select_keyed(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
+                               int64_t score_stride, int32_t* idx, int32_t* idx_copy, int key_shift, hipStream_t st) {
   const int64_t n_hist = std::max<int64_t>(L - P.W, 0);
   const int m = (int)(std::min<int64_t>(P.k, n_hist) + std::min<int64_t>(P.W, L));
   const int nch = (int)((n_hist + kSelChunk - 1) / kSelChunk);
   if (std::min<int64_t>(P.k, n_hist) > 0) {
     hipLaunchKernelGGL(k_select_classify, dim3(nch, P.B), dim3(kSelThreads), 0, st, scores, score_stride, ws.hist,
                        ws.cand, ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P),
-                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens);
+                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens, key_shift);
   }
   hipLaunchKernelGGL(k_select_finish, dim3(std::max(nch, 1), P.B), dim3(kSelThreads), 0, st, ws.hist, ws.cand,
                      ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, idx, idx_copy, (int64_t)m,
