@@ -596,3 +596,22 @@ def test_hybrid_sampler_split():
 def test_oracle_package_exports():
     for name in ("decode_step", "select", "pool", "rope", "attend", "reconstruct"):
         assert hasattr(oracle, name)
+
+
+@pytest.mark.parametrize("pool_mode,agg,wq", [("max", "mean", 1), ("avg", "max", 4), ("max", "max", 2),
+                                              ("avg", "mean", 4)])
+def test_relevance_lies_in_unit_interval(pool_mode, agg, wq):
+    """A~ is a mean or maximum over groups of pooled window means of softmax
+    probabilities (Section 3.2.2-3.2.3), so it lies in [0, 1] whatever the
+    logits; the selection's finer key for the fused step relies on it."""
+    rng = np.random.default_rng(21 + wq)
+    B, hq, hkv, dh, L, r = 2, 8, 2, 16, 300, 8
+    Dp = hkv * dh
+    bases = np.linalg.qr(rng.standard_normal((Dp, r)))[0][None, None]
+    for scale in (0.1, 10.0, 1e4):                        # flat to one-hot softmaxes
+        q = scale * rng.standard_normal((B, hq, dh))
+        coef = rng.standard_normal((B, L, r))
+        qwin = scale * rng.standard_normal((B, hq // hkv, wq - 1, r)) if wq > 1 else None
+        a = decode.relevance(q, qwin, bases, coef, L, hkv, 7, pool_mode, agg)["a_tilde"]
+        assert np.all(a >= 0.0) and np.all(a <= 1.0 + 1e-12), (scale, a.min(), a.max())
+        assert a.max() > 0.0
