@@ -21,8 +21,14 @@ storage  Rounding of float64 values to the storage formats (bf16, fp32).
 
 Readings of points the paper leaves open are listed in the module docstrings
 where they are applied.  Every function here is pinned by a CPU test against
-something other than itself (identities, library routines, brute force, the
-worked example of Appendix B.4); none is marked "parity unpinned".
+something other than itself: identities, library routines, brute force, loop
+forms written from the equations (group aggregation, the query FIFO and its
+causal limits), hand-computed sample positions of the hybrid sampler, and the
+worked example of Appendix B.4.  Mutation tests plant plausible mistakes
+(a dropped scale, wrong query grouping, pooling off by one, ties to the higher
+index, a RoPE sign, a transposed basis, a dropped window row, mean and max
+aggregation exchanged, a newest-first query FIFO, a sampler that takes the
+first early positions) and check that a pin fails for each.
 """
 
 from . import cost, decode, prefill, storage  # noqa: F401

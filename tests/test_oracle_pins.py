@@ -344,10 +344,114 @@ def check_full_reconstruction(seed=12, nb=1, rank_v=5):
     return np.allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
+def ref_relevance_loop(q_rows, pos_rows, bases_k, coef_k, L, hkv, kappa, pool_mode, agg):
+    """A~ written out in loops from the equations of Sections 3.2.1-3.2.3.
+
+    q_rows: W_q raw query arrays [B, h_q, d_h], oldest first, the query of row
+    i sitting at non-sink position pos_rows[i].  Per group g: the latent query
+    of every row (s^Q B^K, group g's heads concatenated over the KV heads), its
+    logits against every key l <= its position divided by sqrt(R), a softmax
+    over those keys, the mean over the rows, pooling over [l - h, l + h]
+    clipped to the sequence (max of the in-range values, or their sum / kappa),
+    and the group aggregation: sum over g / G (mean) or the largest (max)."""
+    B = coef_k.shape[0]
+    G = q_rows[0].shape[1] // hkv
+    nb, dg, rank = bases_k.shape[1:]
+    R = nb * rank
+    h = kappa // 2
+    out = np.zeros((B, L))
+    for b in range(B):
+        bk = bases_k[b if bases_k.shape[0] > 1 else 0]
+        pooled = np.zeros((G, L))
+        for g in range(G):
+            aq = np.zeros(L)
+            for qr, pos in zip(q_rows, pos_rows):
+                qg = ref_group_query(qr, hkv, g)[b]                  # [Dp]
+                cq = np.zeros(R)
+                for k in range(nb):
+                    for rr in range(rank):
+                        cq[k * rank + rr] = sum(qg[k * dg + d] * bk[k, d, rr] for d in range(dg))
+                z = [sum(cq[c] * coef_k[b, l, c] for c in range(R)) / np.sqrt(R) for l in range(pos + 1)]
+                zmax = max(z)
+                e = [np.exp(v - zmax) for v in z]
+                tot = sum(e)
+                for l in range(pos + 1):
+                    aq[l] += e[l] / tot / len(q_rows)
+            for l in range(L):
+                nbrs = [aq[x] for x in range(l - h, l + h + 1) if 0 <= x < L]
+                pooled[g, l] = max(nbrs) if pool_mode == "max" else sum(nbrs) / kappa
+        for l in range(L):
+            if agg == "mean":
+                out[b, l] = sum(pooled[g, l] for g in range(G)) / G
+            else:
+                best = pooled[0, l]
+                for g in range(1, G):
+                    if pooled[g, l] > best:
+                        best = pooled[g, l]
+                out[b, l] = best
+    return out
+
+
+def _agg_problem(seed):
+    """G = 3 groups whose softmaxes peak at different positions, so the mean and
+    the maximum over the groups rank the tokens differently."""
+    p = small_problem(seed, B=2, hkv=2, G=3, dh=4, rank=5, L=18)
+    p["q"] = p["q"] * 3.0
+    return p
+
+
+def check_group_aggregation_mean(seed=13):
+    """F_G = mean over the G groups (Section 3.2.3) against the loop form."""
+    p = _agg_problem(seed)
+    got = decode.relevance(p["q"], None, p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "max", "mean")["a_tilde"]
+    want = ref_relevance_loop([p["q"]], [p["L"] - 1], p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "max", "mean")
+    return np.allclose(got, want, rtol=1e-12, atol=1e-15)
+
+
+def check_group_aggregation_max(seed=14):
+    """F_G = max over the G groups (the max variant) against the loop form,
+    with average pooling."""
+    p = _agg_problem(seed)
+    got = decode.relevance(p["q"], None, p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "avg", "max")["a_tilde"]
+    want = ref_relevance_loop([p["q"]], [p["L"] - 1], p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "avg", "max")
+    return np.allclose(got, want, rtol=1e-12, atol=1e-15)
+
+
+def check_query_fifo_order(seed=15):
+    """The FIFO of Section 3.2.1: W_q raw queries, oldest first, the current one
+    last.  The earlier rows are projected here in loop form and handed over as
+    qwin_prev; the current query goes in as q.  Row i is the query at position
+    L - W_q + i and sees keys up to that position only (Section 3.2.2), so a
+    FIFO that put the current query first would mask it at L - W_q and change
+    A~.  Also checks that the oracle's C^Q rows are those projections, in order."""
+    p = small_problem(seed, B=2, hkv=2, G=2, dh=4, rank=5, L=16)
+    rng = np.random.default_rng(seed + 100)
+    Wq = 4
+    B, hq, dh = p["q"].shape
+    rows = [2.0 * rng.standard_normal((B, hq, dh)) for _ in range(Wq - 1)] + [2.0 * p["q"]]
+    bk = p["bases_k"]
+    rank = bk.shape[-1]
+    G = p["G"]
+    cq_rows = np.zeros((B, G, Wq, rank))
+    for i, qr in enumerate(rows):
+        for b in range(B):
+            for g in range(G):
+                qg = ref_group_query(qr, p["hkv"], g)[b]
+                for rr in range(rank):
+                    cq_rows[b, g, i, rr] = sum(qg[d] * bk[b, 0, d, rr] for d in range(qg.size))
+    rel = decode.relevance(rows[-1], cq_rows[:, :, :Wq - 1], bk, p["coef_k"], p["L"], p["hkv"], 3, "max", "mean")
+    if not np.allclose(rel["cQ"], cq_rows, rtol=1e-12, atol=1e-13):
+        return False
+    pos = [p["L"] - Wq + i for i in range(Wq)]
+    want = ref_relevance_loop(rows, pos, bk, p["coef_k"], p["L"], p["hkv"], 3, "max", "mean")
+    return np.allclose(rel["a_tilde"], want, rtol=1e-12, atol=1e-15)
+
+
 ALL_CHECKS = [check_latent_identity, check_rotation_invariance, check_pool_vs_torch,
               check_topk_special_case, check_select_bruteforce, check_full_rank_exact,
               check_full_budget_dense, check_rope_complex, check_rope_shift_invariance,
-              check_plain_gqa, check_causal_window, check_dense_comparator, check_full_reconstruction]
+              check_plain_gqa, check_causal_window, check_dense_comparator, check_full_reconstruction,
+              check_group_aggregation_mean, check_group_aggregation_max, check_query_fifo_order]
 
 
 # ----------------------------------------------------------------------------
@@ -423,6 +527,26 @@ def test_plain_gqa_decode_special_case():
 
 def test_causal_query_window():
     assert check_causal_window()
+
+
+@pytest.mark.parametrize("check", [check_group_aggregation_mean, check_group_aggregation_max])
+def test_group_aggregation_matches_loop_form(check):
+    assert check()
+
+
+def test_group_aggregation_modes_differ_on_the_pin_inputs():
+    """The aggregation pins use inputs on which mean and max give different
+    rankings, so exchanging the two modes cannot pass them."""
+    p = _agg_problem(13)
+    a_mean = decode.relevance(p["q"], None, p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "max", "mean")["a_tilde"]
+    a_max = decode.relevance(p["q"], None, p["bases_k"], p["coef_k"], p["L"], p["hkv"], 3, "max", "max")["a_tilde"]
+    assert not np.allclose(a_mean, a_max)
+    assert any(not np.array_equal(np.argsort(-a_mean[b], kind="stable")[:5], np.argsort(-a_max[b], kind="stable")[:5])
+               for b in range(a_mean.shape[0]))
+
+
+def test_query_fifo_oldest_first():
+    assert check_query_fifo_order()
 
 
 def test_exact_window_kv_replaces_reconstruction():
@@ -550,6 +674,25 @@ def test_mutation_window_mean_drops_row(monkeypatch):
     assert "check_causal_window" in _fails(monkeypatch, decode, "window_mean", bad)
 
 
+def test_mutation_group_aggregation_swapped(monkeypatch):
+    def bad(P, mode="mean"):
+        P = np.asarray(P, dtype=np.float64)
+        return np.max(P, axis=1) if mode == "mean" else np.mean(P, axis=1)
+    failed = _fails(monkeypatch, decode, "aggregate", bad)
+    assert "check_group_aggregation_mean" in failed and "check_group_aggregation_max" in failed
+
+
+def test_mutation_fifo_newest_first(monkeypatch):
+    orig = decode.query_window
+
+    def bad(q, qwin_prev, bases_k, n_kv_heads):
+        cq = orig(q, None, bases_k, n_kv_heads)
+        if qwin_prev is None or np.asarray(qwin_prev).shape[2] == 0:
+            return cq
+        return np.concatenate([cq, np.asarray(qwin_prev, dtype=np.float64)], axis=2)
+    assert "check_query_fifo_order" in _fails(monkeypatch, decode, "query_window", bad)
+
+
 # ----------------------------------------------------------------------------
 # prefill (Section 3.1)
 # ----------------------------------------------------------------------------
@@ -591,6 +734,64 @@ def test_hybrid_sampler_split():
     recent = idx[idx >= 1000 - 140]
     assert recent.size == 140 and recent.max() == 999
     assert np.all(np.diff(idx) > 0)
+
+
+# Hybrid sampling of Section 3.1.2 with the 7:3 recent-to-uniform split of
+# Section 4: T' = floor(eta * T) rows, round(0.7 T') of them the contiguous
+# block of the latest positions, the rest spread evenly over the earlier
+# positions from the first to the last one before the block (reading: evenly
+# spaced real positions, rounded to the nearest integer, halves to even).
+# Worked by hand:
+#   T = 100, eta = 0.2:  T' = 20, 14 recent = 86..99, 6 uniform over [0, 85]
+#                        step 85/5 = 17 -> 0 17 34 51 68 85
+#   T = 25, eta = 0.4:   T' = 10, 7 recent = 18..24, 3 uniform over [0, 17]
+#                        step 8.5 -> 0, 8.5 -> 8 (half to even), 17
+#   T = 61, eta = 0.25:  T' = 15, round(10.5) = 10 recent (half to even) =
+#                        51..60, 5 uniform over [0, 50] step 12.5 -> 0, 12.5 -> 12,
+#                        25, 37.5 -> 38, 50
+#   T = 9, eta = 0.3:    T' = 2, round(1.4) = 1 recent = 8, 1 uniform = 0
+HYBRID_CASES = [
+    (100, 0.2, [0, 17, 34, 51, 68, 85] + list(range(86, 100))),
+    (25, 0.4, [0, 8, 17] + list(range(18, 25))),
+    (61, 0.25, [0, 12, 25, 38, 50] + list(range(51, 61))),
+    (9, 0.3, [0, 8]),
+]
+
+
+@pytest.mark.parametrize("T,eta,want", HYBRID_CASES)
+def test_hybrid_sampler_positions_by_hand(T, eta, want):
+    assert prefill.sample_hybrid(T, eta).tolist() == want
+
+
+def test_mutation_sampler_first_positions(monkeypatch):
+    """Taking the first n_uniform early positions instead of spreading them
+    over the early part is caught by the hand-computed lists."""
+    def bad(T, eta, recent_share=0.7):
+        n = max(1, int(np.floor(eta * T)))
+        n_recent = min(T, int(round(recent_share * n)))
+        return np.concatenate([np.arange(n - n_recent), np.arange(T - n_recent, T)]).astype(np.int64)
+    with monkeypatch.context() as m:
+        m.setattr(prefill, "sample_hybrid", bad)
+        assert any(prefill.sample_hybrid(T, eta).tolist() != want for T, eta, want in HYBRID_CASES)
+
+
+def test_prefill_initial_query_window_loop_form():
+    """The prefill's initial C^Q (Section 3.1, the most recent W queries
+    projected on the key basis) row by row against the loop-form grouping and
+    an explicit sum over the basis rows."""
+    rng = np.random.default_rng(16)
+    B, hkv, G, dh, W, N, s, rank = 2, 2, 3, 4, 3, 40, 2, 5
+    Dp = hkv * dh
+    S = rng.standard_normal((B, N, Dp))
+    qr = rng.standard_normal((B, hkv * G, W, dh))
+    st = prefill.prefill(S, S, s, rank=rank, dtype="fp32", q_recent=qr, n_kv_heads=hkv)
+    bk = st["bases_k"]
+    for b in range(B):
+        for g in range(G):
+            for w in range(W):
+                qg = ref_group_query(qr[:, :, w, :], hkv, g)[b]
+                want = [sum(qg[d] * bk[b, 0, d, r] for d in range(Dp)) for r in range(rank)]
+                assert np.allclose(st["qwin"][b, g, w], want, rtol=1e-6, atol=1e-6)
 
 
 def test_oracle_package_exports():
