@@ -470,7 +470,7 @@ def main():
             "avg_launch_us": round(stream_us, 3),
         },
         "reconstruction_mfma": {
-            "kernel": "k_attn_split (reconstruction + attention)",
+            "kernel": "k_attn_tiles (reconstruction + attention on bf16 MFMA)",
             "achieved_TFLOPs": round(rec_tflops, 2),
             "peak_TFLOPs": BF16_PEAK_TFLOPS,
             "frac": round(rec_tflops / BF16_PEAK_TFLOPS, 5),

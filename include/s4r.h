@@ -345,8 +345,10 @@ s4r_status s4r_timing_read(double* total_ms, int64_t* steps);
 
 /*
  * Read-bandwidth reference for roofline calibration (not part of the method):
- * reads `bytes` (a positive multiple of 16) from the device buffer `buf` once,
- * 16-byte loads, grid-stride over the whole GPU.  `sink` (device, uint32,
+ * reads `bytes` (a positive multiple of 16) from the device buffer `buf` once
+ * with non-temporal 16-byte loads, each workgroup reading one contiguous range
+ * of the buffer (the fastest read pattern measured on this GPU; grid-stride
+ * patterns were slower).  `sink` (device, uint32,
  * s4r_read_bandwidth_sink_len() entries) receives one XOR of the words each
  * thread read; the XOR of all entries is the XOR of every 32-bit word of
  * the buffer.  buf must be 16-byte aligned.

@@ -2,6 +2,7 @@
 // launch sequence of each entry point.  All validation happens on the host
 // before anything is launched; see include/s4r.h for the contract.
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -200,7 +201,7 @@ s4r_status hip_status(hipError_t e, const char* what) {
 // ---- kernel timing ------------------------------------------------------------------
 struct Timing {
   std::mutex mu;
-  bool enabled = false;
+  std::atomic<bool> enabled{false};   // read without the lock on every step call
   std::vector<hipEvent_t> start, stop;   // [steps][S4R_TIMED_KERNELS]
   int steps = 0;
   int used = 0;
@@ -533,8 +534,11 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
 
-  std::lock_guard<std::mutex> lk(g_timing.mu);
-  const bool timed = g_timing.enabled && g_timing.used < g_timing.steps;
+  // the timing state is locked only while timing is enabled: untimed steps
+  // from several host threads do not serialise on it
+  std::unique_lock<std::mutex> lk;
+  if (g_timing.enabled.load(std::memory_order_acquire)) lk = std::unique_lock<std::mutex>(g_timing.mu);
+  const bool timed = lk.owns_lock() && g_timing.enabled && g_timing.used < g_timing.steps;
   const int slot = timed ? g_timing.used * S4R_TIMED_KERNELS : 0;
   auto mark = [&](hipError_t e, int kernel, bool start) -> hipError_t {
     if (e != hipSuccess || !timed) return e;
