@@ -188,6 +188,27 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q,
                            hipStream_t stream);
 
 /*
+ * s4r_decode_step without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Arguments, outputs and errors are those
+ * of s4r_decode_step without ws / ws_bytes.  The workspace is a 64 MiB array
+ * the library holds on each device that runs this call (from its first call
+ * on the device until the process ends); the call itself allocates nothing.
+ * A configuration whose s4r_workspace_size exceeds 64 MiB returns
+ * S4R_ERR_WORKSPACE before anything is launched.  The stream must belong to
+ * the current device.  Every call on a device shares that device's array and
+ * leaves its contents behind (the step clears what it needs cleared itself):
+ * calls that overlap on one device, from several streams or host threads,
+ * race on it and must be serialised by the caller.
+ */
+s4r_status s4r_decode_step_noalloc(const s4r_config* cfg, int64_t L, const void* q,
+                                   const float* qwin_prev, const void* sink_k, const void* sink_v,
+                                   const void* win_k, const void* win_v, const void* bases_k,
+                                   const void* bases_v, void* coef_k, void* coef_v,
+                                   const void* k_new, const void* v_new, float* out,
+                                   int32_t* idx_out, float* scores_out, hipStream_t stream);
+
+/*
  * The fused decode step over a ragged batch (Section 3.2, each sequence at
  * its own length): lengths[b] (host memory, B entries, read before the call
  * returns) is sequence b's L, counted with the appended token when k_new /

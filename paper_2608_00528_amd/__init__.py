@@ -14,6 +14,7 @@ _lib.load()
 from .api import (  # noqa: E402,F401
     alloc_workspace,
     decode_step,
+    decode_step_noalloc,
     decode_step_ragged,
     dense_decode,
     full_recon_decode,

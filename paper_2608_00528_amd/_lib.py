@@ -21,7 +21,7 @@ EXPORTS = (
     "s4r_timing_enable", "s4r_timing_read", "s4r_read_bandwidth_sink_len", "s4r_read_bandwidth",
     "s4r_dense_decode", "s4r_prefill_project", "s4r_decode_step_ragged",
     "s4r_full_recon_decode", "s4r_prefill_num_samples", "s4r_prefill_bases_workspace_size", "s4r_prefill_bases",
-    "s4r_project_queries",
+    "s4r_project_queries", "s4r_decode_step_noalloc",
 )
 
 
@@ -79,6 +79,8 @@ _SIGS = {
     "s4r_prefill_bases_workspace_size": (_I32, [_CFG, _I64, ctypes.c_double, ctypes.POINTER(_SZ)]),
     "s4r_prefill_bases": (_I32, [_CFG, _I64, _P, _P, ctypes.c_double, _I32, _P, _P, _P, _P, _SZ, _P]),
     "s4r_full_recon_decode": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "s4r_decode_step_noalloc": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                       _P, _P]),
     "s4r_decode_step_ragged": (_I32, [_CFG, ctypes.POINTER(_I64), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       _P, _P, _P, _P, _P, _SZ, _P]),
 }

@@ -168,6 +168,25 @@ def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v
     return out
 
 
+def decode_step_noalloc(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, qwin_prev=None,
+                        win_k=None, win_v=None, k_new=None, v_new=None, out=None, idx_out=None, scores_out=None):
+    """The fused step on the library's own per-device scratch (no workspace
+    argument); configurations needing more than 64 MiB of it are refused."""
+    dt = storage_dtype(cfg)
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    need_sink = cfg.n_sink > 0
+    L.check(L.load().s4r_decode_step_noalloc(
+        _cfgp(cfg), length, _ptr(q, "q", dt), _ptr(qwin_prev, "qwin_prev", torch.float32, False),
+        _ptr(sink_k, "sink_k", dt, need_sink), _ptr(sink_v, "sink_v", dt, need_sink),
+        _ptr(win_k, "win_k", dt, False), _ptr(win_v, "win_v", dt, False),
+        _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt), _ptr(coef_k, "coef_k", dt),
+        _ptr(coef_v, "coef_v", dt), _ptr(k_new, "k_new", dt, False), _ptr(v_new, "v_new", dt, False),
+        _ptr(out, "out", torch.float32), _ptr(idx_out, "idx_out", torch.int32, False),
+        _ptr(scores_out, "scores_out", torch.float32, False), _stream()))
+    return out
+
+
 def decode_step_ragged(cfg, lengths, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, ws, qwin_prev=None,
                        win_k=None, win_v=None, k_new=None, v_new=None, out=None, idx_out=None, scores_out=None):
     """The fused step over a ragged batch: lengths is a sequence of B ints

@@ -207,6 +207,48 @@ struct Timing {
   int used = 0;
 } g_timing;
 
+// ---- scratch for the step without a caller workspace -------------------------------
+// A file-scope device array that s4r_decode_step_noalloc uses as its
+// workspace.  In host code `scratch` names a host-side stand-in, not device
+// memory: its device address is taken once per device with
+// hipGetSymbolAddress (with that device current) and only that address is
+// handed to kernels.  Each device that runs the entry point keeps its copy
+// until the process ends.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;                                   // first lookup per device only
+std::atomic<void*> g_scratch_addr[kMaxScratchDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// the device address of this device's `scratch` (looked up on the first call
+// on the device; later calls read the cached address without locking)
+s4r_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(S4R_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(S4R_ERR_UNSUPPORTED, "device %d outside the %d devices the scratch table holds", dev,
+                kMaxScratchDevices);
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(S4R_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return S4R_OK;
+}
+
 }  // namespace
 
 Workspace carve_workspace(const Problem& P, void* base) {
@@ -608,6 +650,25 @@ s4r_status s4r_decode_step_ragged(const s4r_config* cfg, const int64_t* lengths,
   }
   return decode_step_impl(P, L, q, qwin_prev, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
                           v_new, out, idx_out, scores_out, ws, ws_bytes, stream);
+}
+
+s4r_status s4r_decode_step_noalloc(const s4r_config* cfg, int64_t L, const void* q, const float* qwin_prev,
+                                   const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
+                                   const void* bases_k, const void* bases_v, void* coef_k, void* coef_v,
+                                   const void* k_new, const void* v_new, float* out, int32_t* idx_out,
+                                   float* scores_out, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  const size_t need = layout(P).total;
+  if (need > kScratchBytes)
+    return fail(S4R_ERR_WORKSPACE, "this configuration needs %zu bytes of scratch, more than the %zu the library "
+                "holds per device; use s4r_decode_step with a workspace", need, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws))) return st;
+  return decode_step_impl(P, L, q, qwin_prev, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
+                          v_new, out, idx_out, scores_out, ws, kScratchBytes, stream);
 }
 
 s4r_status s4r_project_append(const s4r_config* cfg, int64_t row, const void* k_new, const void* v_new,

@@ -292,3 +292,18 @@ def test_prefill_projection_argument_errors():
     assert call(c, wsb=16) == L.S4R_ERR_WORKSPACE
     assert call(cfg(dtype="fp32")) == L.S4R_ERR_UNSUPPORTED
     assert call(cfg(head_dim=128, rank=256)) == L.S4R_ERR_UNSUPPORTED      # rank > 192
+
+
+def test_noalloc_step_refuses_beyond_its_scratch():
+    """The step on the library's own scratch refuses a configuration whose
+    workspace exceeds the 64 MiB the library holds, before any HIP call."""
+    lib = L.load()
+    big = cfg(batch=32, n_q_heads=32, n_kv_heads=8, head_dim=128, rank=160, capacity=40960, window=64, topk=1024)
+    assert s4r.workspace_size(big) > 64 << 20
+    args = [FAKE] * 15
+    st = lib.s4r_decode_step_noalloc(ctypes.byref(big), 40000, *args, None)
+    assert st == L.S4R_ERR_WORKSPACE
+    assert b"64" in lib.s4r_last_error() or b"67108864" in lib.s4r_last_error()
+    # argument errors come first, as for the workspace step
+    assert lib.s4r_decode_step_noalloc(None, 10, *args, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_decode_step_noalloc(ctypes.byref(cfg()), 0, *args, None) == L.S4R_ERR_BAD_SHAPE
