@@ -1,22 +1,29 @@
 """Benchmark of the fused S^4R decode step on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload llama8b_128k] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--workload llama8b_128k] [--gpus 1] [--no-extra]
 
 A step is one call of s4r_decode_step: one layer, all heads, the whole batch
 (latent scoring of every cached token, top-k selection, sparse
-reconstruction with RoPE, attention).  The default workload is the
-Llama-3.1-8B-shaped layer at 128k context (B=4, 32/8 heads, d_h=128, rank 160,
-4 sinks, window 128, top-k 2048, bf16 storage), seeded synthetic data drawn in
-latent coordinates (workloads.latent_state), inputs resident in HBM.
+reconstruction with RoPE, attention).  The main line is the Llama-3.1-8B-shaped
+layer at 128k context (B=4, 32/8 heads, d_h=128, rank 160, 4 sinks, window
+128, top-k 2048, bf16 storage), seeded synthetic data drawn in latent
+coordinates (workloads.latent_state), inputs resident in HBM.  The same run
+then measures every other workload and reports each under "configs": the tiny
+fp32 layer, the Llama 32k layer at batch 1, the Qwen2.5-7B-shaped 128k layer
+at batch 8, the paper's efficiency setting (Qwen3-4B shape at 120k, W = W_q =
+4, k = 0.2 L - W, with its dense and full-reconstruction comparators) and the
+32-layer sustained run (16 warm-up + 256 timed steps, the new token appended
+in every layer).
 
 Timing: W untimed steps, then K timed steps between two device
 synchronisations, measured with HIP events on the launch stream.  Steps
-rotate over 4 independent copies of the coefficient caches so that no step
-finds its 168 MB key cache in the 256 MB Infinity Cache.  A second pass with
-the library's per-kernel event hook gives the average duration of the
-dominant kernel (the latent-score stream over C^K) for the roofline entry.
-The CPU oracle is timed on a bounded sample (one sequence of the same
-workload, repeated for ~10 s, one thread) for the cpu_baseline entry.
+rotate over independent copies of the coefficient caches (at least 4, and at
+least three times the 256 MB Infinity Cache in total) so that no step finds
+its coefficients in that cache.  A second pass with the library's per-kernel
+event hook gives the average duration of each kernel; the latent-score stream
+over C^K is the roofline entry.  The CPU oracle is timed on a bounded sample
+(one sequence of the same workload, repeated for ~10 s; ~5 s for the other
+workloads) for the cpu_baseline entries.
 
 Prints ONE JSON line on stdout.
 """
@@ -90,9 +97,10 @@ def traffic_from_profile(workload):
         return None
 
 
-def cpu_baseline(wl, st, budget_s=10.0):
+def cpu_baseline(wl, st, budget_s=10.0, one_thread=True):
     """The oracle as it stands (numpy with its default BLAS threads) on one
-    sequence of the workload, repeated for about budget_s seconds."""
+    sequence of the workload, repeated for about budget_s seconds (and, with
+    one_thread, again with one BLAS thread for half as long)."""
     from threadpoolctl import threadpool_info
 
     from oracle import decode
@@ -111,6 +119,13 @@ def cpu_baseline(wl, st, budget_s=10.0):
         if time.perf_counter() > t_end:
             break
     per_seq = float(np.median(times))
+    sample = (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
+              f"{len(times)} runs in {sum(times):.1f} s, median per sequence x {wl.batch} sequences; "
+              f"BLAS threads {threads}")
+    res = {"value": round(per_seq * wl.batch * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+           "host_cpus": os.cpu_count(), "sample": sample}
+    if not one_thread:
+        return res
     # the same sample with one BLAS thread, for about half the budget
     from threadpoolctl import threadpool_limits
     times1 = []
@@ -124,12 +139,10 @@ def cpu_baseline(wl, st, budget_s=10.0):
             if time.perf_counter() > t_end:
                 break
     per_seq1 = float(np.median(times1))
-    return {"value": round(per_seq * wl.batch * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
-            "host_cpus": os.cpu_count(), "value_1_thread": round(per_seq1 * wl.batch * 1e6, 1),
-            "sample": (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
-                       f"{len(times)} runs in {sum(times):.1f} s, median per sequence x {wl.batch} sequences; "
-                       f"BLAS threads {threads}; value_1_thread: the same with one BLAS thread, "
-                       f"{len(times1)} runs in {sum(times1):.1f} s")}
+    res["value_1_thread"] = round(per_seq1 * wl.batch * 1e6, 1)
+    res["sample"] += (f"; value_1_thread: the same with one BLAS thread, {len(times1)} runs in "
+                      f"{sum(times1):.1f} s")
+    return res
 
 
 def copy_calibration(nbytes, reps):
@@ -144,6 +157,11 @@ def copy_calibration(nbytes, reps):
                       "reps": reps, "kernel": "torch.neg (elementwise, float32)"}), flush=True)
 
 
+EXTRA_SINGLE = ("tiny_fp32", "llama8b_32k", "qwen7b_128k", "qwen3_4b_120k")
+EXTRA_STEPS, EXTRA_WARMUP = 100, 10
+MALL_BYTES = 256 << 20          # MI355X Infinity Cache
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +171,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true",
                     help="skip the dense Full-KV comparator (uncompressed bf16 KV of the same shape)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="measure the named workload only (by default the headline run also measures every "
+                         "other workload and reports it under 'configs')")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES bytes (counter calibration) and exit")
@@ -168,13 +189,53 @@ def main():
         copy_calibration(args.copy_calibration, 5)
         return
 
-    import paper_2608_00528_amd as s4r
     import workloads as W
 
     wl = W.CONFIGS[args.workload]
     if wl.layers != 1:
-        bench_sustained(args, wl)
+        print(json.dumps(bench_sustained(args, wl, args.steps, args.warmup)), flush=True)
         return
+    result = measure_single(args, wl, args.steps, args.warmup, full=True,
+                            comparators=not args.no_comparator)
+    if not args.no_extra and wl.name == W.HEADLINE:
+        # every other workload, each with its own step counts, roofline entry and
+        # CPU-oracle baseline (a shorter sample than the headline's)
+        result["configs"] = {}
+        for name in EXTRA_SINGLE:
+            r = measure_single(args, W.CONFIGS[name], EXTRA_STEPS, EXTRA_WARMUP, full=False,
+                               comparators=(name == "qwen3_4b_120k" and not args.no_comparator), cpu_budget=5.0)
+            result["configs"][name] = summary_entry(r)
+        torch.cuda.empty_cache()
+        sw = W.CONFIGS["llama8b_32L_sustained"]
+        r = bench_sustained(args, sw, sw.steps, 16, cpu_budget=5.0)
+        result["configs"][sw.name] = summary_entry(r)
+    print(json.dumps(result), flush=True)
+
+
+def summary_entry(r):
+    """The per-workload entry of the headline line's 'configs' object."""
+    keep = ("metric", "value", "unit", "steps", "warmup", "higher_is_better", "dtype", "config",
+            "achieved_step_GBps", "step_frac_of_hbm_peak", "algorithmic_bytes_per_step", "read_ceiling_GBps",
+            "kernels_us", "kernels_us_per_layer", "roofline", "reconstruction_mfma", "comparator_full_kv",
+            "cpu_baseline")
+    return {k: r[k] for k in keep if k in r}
+
+
+def replicas_for(bytes_per_replica):
+    """Cache replicas to rotate over so that consecutive steps never find their
+    coefficients in the Infinity Cache: at least 4 and at least 3x its size."""
+    return int(max(N_REPLICAS, -(-3 * MALL_BYTES // max(1, bytes_per_replica))))
+
+
+def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
+    """One single-layer workload: the fused step timed over `steps` steps
+    after `warmup`, the per-kernel pass, the roofline entry of the latent-score
+    stream and the CPU-oracle baseline; with `full`, also the per-step
+    distribution, the graph replay and the read ceiling; with `comparators`,
+    the dense Full-KV and full-reconstruction decodes of the same shape."""
+    import paper_2608_00528_amd as s4r
+    import workloads as W
+
     log(f"[bench] generating {wl.describe()}")
     t0 = time.perf_counter()
     st = W.latent_state(wl, seed=args.seed)
@@ -197,20 +258,21 @@ def main():
         rm = np.zeros((wl.batch, cap, wl.R))
         rm[:, :wl.L] = st[key]
         reps.append(s4r.pack_coef(c, cap, up(rm)))
-    replicas = [(reps[0], reps[1])] + [(reps[0].clone(), reps[1].clone()) for _ in range(N_REPLICAS - 1)]
+    n_rep = replicas_for(sum(t.numel() * t.element_size() for t in reps))
+    replicas = [(reps[0], reps[1])] + [(reps[0].clone(), reps[1].clone()) for _ in range(n_rep - 1)]
     ws = s4r.alloc_workspace(c)
     out = torch.empty((wl.batch, wl.n_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
     m = s4r.num_selected(c, wl.L)
     torch.cuda.synchronize()
 
     def step(i):
-        ck, cv = replicas[i % N_REPLICAS]
+        ck, cv = replicas[i % n_rep]
         s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, ck, cv, ws, qwin_prev=qwin, out=out)
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    log(f"[bench] warmup done ({args.warmup} steps)")
+    log(f"[bench] warmup done ({warmup} steps)")
 
     stream = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -218,24 +280,114 @@ def main():
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     e0.record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
         step(i)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_total = e0.elapsed_time(e1)
-    ms_step = ms_total / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step * 1e3:.2f} us/step (events), wall {wall / args.steps * 1e6:.2f} us/step")
+    ms_step = ms_total / steps
+    log(f"[bench] {wl.name}: {steps} steps: {ms_step * 1e3:.2f} us/step (events), "
+        f"wall {wall / steps * 1e6:.2f} us/step")
 
-    # per-step distribution (an event between consecutive steps)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    result_extra = {}
+    if full:
+        result_extra = step_distribution_graph_ceiling(s4r, step, out, replicas, n_rep, steps)
+    comparator = None
+    if comparators and wl.dtype == "bf16" and wl.head_dim == 128:
+        comparator = run_comparators(s4r, W, args, wl, c, q, sk, sv, bk, bv, replicas[0], ws, out, ms_step,
+                                     prefill=full)
+
+    # per-kernel pass (events between kernels), same steps again
+    nk = min(steps, 200)
+    s4r.timing_enable(nk)
+    for i in range(nk):
+        step(i)
+    torch.cuda.synchronize()
+    kms, nsteps = s4r.timing_read()
+    kus = {k: v / nsteps * 1e3 for k, v in kms.items()}
+    log(f"[bench] {wl.name} per-kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in kus.items()))
+
+    alg = algorithmic(wl, m)
+    stream_us = kus["score_stream"]
+    achieved = alg["stream_bytes"] / (stream_us * 1e-6) / 1e9
+    traffic = traffic_from_profile(wl.name)
+    step_gbps = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
+    rec_tflops = alg["rec_flops"] / (kus["attn_split"] * 1e-6) / 1e12
+
+    metric = "us per decode step (all heads, 1 layer) at 128k ctx; achieved HBM GB/s vs peak"
+    if wl.name != W.HEADLINE:
+        metric = f"us per decode step (all heads, 1 layer) at N={wl.N}; achieved HBM GB/s vs peak"
+    result = {
+        "metric": metric,
+        "value": round(ms_step * 1e3, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: {SHAPES.get(wl.name, 'single')} layer, B={wl.batch}, N={wl.N} "
+                         f"(L={wl.L} non-sink), h_q/h_kv={wl.n_q_heads}/{wl.n_kv_heads}, d_h={wl.head_dim}, "
+                         f"rank {wl.R}, s={wl.n_sink}, W={wl.window}, W_q={wl.q_window}, k={wl.topk}, m={m}, "
+                         f"{wl.dtype} storage"),
+            "batch": wl.batch, "context": wl.N, "rank": wl.R, "window": wl.window, "topk": wl.topk,
+            "selected": m, "replicas": n_rep,
+        },
+        **result_extra,
+        "achieved_step_GBps": round(step_gbps, 1),
+        "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "algorithmic_bytes_per_step": alg["step_bytes"],
+        "kernels_us": {k: round(v, 3) for k, v in kus.items()},
+        "roofline": {
+            "kernel": "k_score_stream (latent scoring over C^K)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg["stream_bytes"],
+            "avg_launch_us": round(stream_us, 3),
+        },
+        "reconstruction_mfma": {
+            "kernel": "k_attn_tiles (reconstruction + attention on bf16 MFMA)" if wl.dtype == "bf16"
+                      else "k_attn_split (reconstruction + attention, fp32 storage)",
+            "flops": alg["rec_flops"],
+            "avg_launch_us": round(kus["attn_split"], 3),
+            "achieved_TFLOPs": round(rec_tflops, 2),
+            "peak_TFLOPs": BF16_PEAK_TFLOPS,
+            "frac": round(rec_tflops / BF16_PEAK_TFLOPS, 5),
+        },
+    }
+    if comparator is not None:
+        result["comparator_full_kv"] = comparator
+    del replicas, ws
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the CPU oracle on a bounded sample of {wl.name}")
+        result["cpu_baseline"] = cpu_baseline(wl, st, budget_s=cpu_budget, one_thread=full)
+    del st
+    torch.cuda.empty_cache()
+    return result
+
+
+def step_distribution_graph_ceiling(s4r, step, out, replicas, n_rep, steps):
+    """Headline extras: per-step distribution, HIP-graph replay and the read
+    ceiling over the same coefficient bytes."""
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     ev[0].record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
         step(i)
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    per = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(args.steps)])
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(steps)])
     p10, p50, p90 = (float(np.percentile(per, x)) for x in (10, 50, 90))
     log(f"[bench] per-step us: p10 {p10:.2f}  median {p50:.2f}  p90 {p90:.2f}")
 
@@ -244,18 +396,18 @@ def main():
     graph_us = None
     try:
         ref_out = []
-        for r in range(N_REPLICAS):
+        for r in range(n_rep):
             step(r)
             ref_out.append(out.clone())
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            for r in range(N_REPLICAS):
+            for r in range(n_rep):
                 step(r)
         g.replay()
         torch.cuda.synchronize()
-        if torch.equal(out, ref_out[N_REPLICAS - 1]):
-            reps_g = max(1, args.steps // N_REPLICAS)
+        if torch.equal(out, ref_out[n_rep - 1]):
+            reps_g = max(1, steps // n_rep)
             g0 = torch.cuda.Event(enable_timing=True)
             g1 = torch.cuda.Event(enable_timing=True)
             g0.record(stream)
@@ -263,7 +415,7 @@ def main():
                 g.replay()
             g1.record(stream)
             torch.cuda.synchronize()
-            graph_us = g0.elapsed_time(g1) * 1e3 / (reps_g * N_REPLICAS)
+            graph_us = g0.elapsed_time(g1) * 1e3 / (reps_g * n_rep)
             log(f"[bench] graph replay: {graph_us:.2f} us/step")
         else:
             log("[bench] graph replay output differs from the eager step; graph timing not reported")
@@ -276,58 +428,65 @@ def main():
     # loads) over one C^K replica per launch, rotating replicas
     cks = [r[0] for r in replicas]
     sink = None
-    for r in range(N_REPLICAS):
+    for r in range(n_rep):
         sink = s4r.read_bandwidth(cks[r], sink)
     torch.cuda.synchronize()
     r0 = torch.cuda.Event(enable_timing=True)
     r1 = torch.cuda.Event(enable_timing=True)
-    nrd = 4 * N_REPLICAS
+    nrd = 4 * n_rep
     r0.record(stream)
     for i in range(nrd):
-        s4r.read_bandwidth(cks[i % N_REPLICAS], sink)
+        s4r.read_bandwidth(cks[i % n_rep], sink)
     r1.record(stream)
     torch.cuda.synchronize()
     read_gbps = cks[0].numel() * cks[0].element_size() * nrd / (r0.elapsed_time(r1) * 1e-3) / 1e9
     log(f"[bench] read ceiling (contiguous non-temporal 16-byte stream over C^K): {read_gbps:.0f} GB/s")
+    return {"step_us_p10_median_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
+            "graph_replay_us_per_step": None if graph_us is None else round(graph_us, 3),
+            "read_ceiling_GBps": round(read_gbps, 1)}
 
-    # comparator: dense GQA decode over the uncompressed bf16 KV cache of the
-    # same shape (the paper's "Full KV" baseline), on the same GPU
-    comparator = None
-    if not args.no_comparator and wl.dtype == "bf16" and wl.head_dim == 128:
-        dc = W.dense_cache(wl, seed=args.seed)
-        cd = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads,
-                             head_dim=wl.head_dim, rank=wl.rank, n_sink=wl.n_sink, window=wl.window, topk=wl.topk,
-                             rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=((wl.N + 15) // 16) * 16)
-        dk = torch.zeros((wl.batch, cd.capacity, wl.Dp), dtype=torch.bfloat16, device="cuda")
-        dv = torch.zeros_like(dk)
-        dk[:, :wl.N], dv[:, :wl.N] = dc["k"], dc["v"]
-        del dc["k"], dc["v"]
-        wsd = s4r.alloc_workspace(cd)
-        outd = torch.empty_like(out)
-        for _ in range(3):
-            s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
-        torch.cuda.synchronize()
-        nd = 20
-        d0 = torch.cuda.Event(enable_timing=True)
-        d1 = torch.cuda.Event(enable_timing=True)
-        d0.record(stream)
-        for _ in range(nd):
-            s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
-        d1.record(stream)
-        torch.cuda.synchronize()
-        dense_us = d0.elapsed_time(d1) * 1e3 / nd
-        dense_bytes = 2 * wl.batch * wl.N * wl.Dp * 2
-        comparator = {
-            "what": "dense GQA decode over the uncompressed bf16 KV cache of the same shape (Full KV), "
-                    "s4r_dense_decode: k_dense_decode + k_attn_combine",
-            "us_per_step": round(dense_us, 2),
-            "kv_bytes_per_step": dense_bytes,
-            "achieved_GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
-            "frac_of_hbm_peak": round(dense_bytes / (dense_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-            "s4r_step_speedup": round(dense_us / (ms_step * 1e3), 2),
-        }
-        log(f"[bench] dense Full-KV comparator: {dense_us:.1f} us/step "
-            f"({comparator['achieved_GBps']:.0f} GB/s), S4R step {comparator['s4r_step_speedup']:.2f}x faster")
+
+def run_comparators(s4r, W, args, wl, c, q, sk, sv, bk, bv, coef0, ws, out, ms_step, prefill):
+    """The comparators on the same GPU: dense GQA decode over the uncompressed
+    bf16 KV cache of the same shape (the paper's Full KV), full-reconstruction
+    low-rank decoding over the same coefficient caches (Appendix B.1), and with
+    `prefill` the prefill's bulk projection and basis construction."""
+    stream = torch.cuda.current_stream()
+    dc = W.dense_cache(wl, seed=args.seed)
+    cd = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads,
+                         head_dim=wl.head_dim, rank=wl.rank, n_sink=wl.n_sink, window=wl.window, topk=wl.topk,
+                         rope_theta=wl.rope_theta, dtype=wl.dtype, capacity=((wl.N + 15) // 16) * 16)
+    dk = torch.zeros((wl.batch, cd.capacity, wl.Dp), dtype=torch.bfloat16, device="cuda")
+    dv = torch.zeros_like(dk)
+    dk[:, :wl.N], dv[:, :wl.N] = dc["k"], dc["v"]
+    del dc["k"], dc["v"]
+    wsd = s4r.alloc_workspace(cd)
+    outd = torch.empty_like(out)
+    for _ in range(3):
+        s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
+    torch.cuda.synchronize()
+    nd = 20
+    d0 = torch.cuda.Event(enable_timing=True)
+    d1 = torch.cuda.Event(enable_timing=True)
+    d0.record(stream)
+    for _ in range(nd):
+        s4r.dense_decode(cd, wl.N, dc["q"], dk, dv, wsd, out=outd)
+    d1.record(stream)
+    torch.cuda.synchronize()
+    dense_us = d0.elapsed_time(d1) * 1e3 / nd
+    dense_bytes = 2 * wl.batch * wl.N * wl.Dp * 2
+    comparator = {
+        "what": "dense GQA decode over the uncompressed bf16 KV cache of the same shape (Full KV), "
+                "s4r_dense_decode: k_dense_decode + k_attn_combine",
+        "us_per_step": round(dense_us, 2),
+        "kv_bytes_per_step": dense_bytes,
+        "achieved_GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
+        "frac_of_hbm_peak": round(dense_bytes / (dense_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        "s4r_step_speedup": round(dense_us / (ms_step * 1e3), 2),
+    }
+    log(f"[bench] {wl.name} dense Full-KV comparator: {dense_us:.1f} us/step "
+        f"({comparator['achieved_GBps']:.0f} GB/s), S4R step {comparator['s4r_step_speedup']:.2f}x faster")
+    if prefill:
         # the prefill's bulk projection C = S B of the same prompt (those rows as S)
         n_pf = cd.capacity
         cpf = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads,
@@ -354,7 +513,8 @@ def main():
             "achieved_GBps": round(pf_bytes / (pf_us * 1e-6) / 1e9, 1),
             "frac_of_hbm_peak": round(pf_bytes / (pf_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         }
-        log(f"[bench] prefill bulk projection: {pf_us:.1f} us ({comparator['prefill_projection']['achieved_GBps']:.0f} GB/s)")
+        log(f"[bench] prefill bulk projection: {pf_us:.1f} us "
+            f"({comparator['prefill_projection']['achieved_GBps']:.0f} GB/s)")
         # the prefill's basis construction for the same prompt (sample, normalise,
         # Gram in fp64, eigenvectors), 20% of the rows sampled
         wsb = torch.empty(s4r.api.prefill_bases_workspace_size(cpf, n_pf, 0.2), dtype=torch.uint8, device="cuda")
@@ -376,115 +536,42 @@ def main():
             "ms": round(pb_ms, 2),
         }
         log(f"[bench] prefill basis construction: {pb_ms:.2f} ms")
-        del wsb, bkp, bvp
-        del dk, dv, wsd, pk, pv, wspf
-        torch.cuda.synchronize()
-        # full-reconstruction low-rank decoding (Appendix B.1) over the same
-        # coefficient caches: every one of the L tokens reconstructed
-        ck0, cv0 = replicas[0]
-        outf = torch.empty_like(out)
-        for _ in range(2):
-            s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
-        torch.cuda.synchronize()
-        f0 = torch.cuda.Event(enable_timing=True)
-        f1 = torch.cuda.Event(enable_timing=True)
-        nfr = 10
-        f0.record(stream)
-        for _ in range(nfr):
-            s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
-        f1.record(stream)
-        torch.cuda.synchronize()
-        fr_us = f0.elapsed_time(f1) * 1e3 / nfr
-        fr_flops = 2 * 2 * wl.batch * wl.L * wl.R * wl.Dp
-        comparator["full_reconstruction"] = {
-            "what": "full-reconstruction low-rank decoding (Appendix B.1): s4r_full_recon_decode, every non-sink "
-                    "token reconstructed on the matrix cores (k_attn_tiles over all tokens + k_attn_combine)",
-            "us_per_step": round(fr_us, 2),
-            "reconstruction_flops": fr_flops,
-            "achieved_TFLOPs": round(fr_flops / (fr_us * 1e-6) / 1e12, 1),
-            "frac_of_bf16_peak": round(fr_flops / (fr_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
-            "s4r_step_speedup": round(fr_us / (ms_step * 1e3), 2),
-        }
-        log(f"[bench] full-reconstruction comparator: {fr_us:.1f} us/step "
-            f"({comparator['full_reconstruction']['achieved_TFLOPs']:.0f} TFLOP/s), "
-            f"S4R step {comparator['full_reconstruction']['s4r_step_speedup']:.2f}x faster")
-        del outf
-
-    # per-kernel pass (events between kernels), same steps again
-    nk = min(args.steps, 200)
-    s4r.timing_enable(nk)
-    for i in range(nk):
-        step(i)
+        del wsb, bkp, bvp, pk, pv, wspf
+    del dk, dv, wsd
     torch.cuda.synchronize()
-    kms, nsteps = s4r.timing_read()
-    kus = {k: v / nsteps * 1e3 for k, v in kms.items()}
-    log("[bench] per-kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in kus.items()))
-
-    alg = algorithmic(wl, m)
-    stream_us = kus["score_stream"]
-    achieved = alg["stream_bytes"] / (stream_us * 1e-6) / 1e9
-    traffic = traffic_from_profile(wl.name)
-    step_gbps = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
-    rec_tflops = alg["rec_flops"] / (kus["attn_split"] * 1e-6) / 1e12
-
-    metric = "us per decode step (all heads, 1 layer) at 128k ctx; achieved HBM GB/s vs peak"
-    if wl.name != W.HEADLINE:
-        metric = f"us per decode step (all heads, 1 layer) at N={wl.N}; achieved HBM GB/s vs peak"
-    result = {
-        "metric": metric,
-        "value": round(ms_step * 1e3, 3),
-        "unit": "us/step",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
-        "data": "synthetic",
-        "config": {
-            "workload": (f"{wl.name}: {SHAPES.get(wl.name, 'single')} layer, B={wl.batch}, N={wl.N} "
-                         f"(L={wl.L} non-sink), h_q/h_kv={wl.n_q_heads}/{wl.n_kv_heads}, d_h={wl.head_dim}, "
-                         f"rank {wl.R}, s={wl.n_sink}, W={wl.window}, W_q={wl.q_window}, k={wl.topk}, m={m}, "
-                         f"{wl.dtype} storage"),
-            "batch": wl.batch, "context": wl.N, "rank": wl.R, "window": wl.window, "topk": wl.topk,
-            "selected": m, "replicas": N_REPLICAS,
-        },
-        "step_us_p10_median_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
-        "graph_replay_us_per_step": None if graph_us is None else round(graph_us, 3),
-        "achieved_step_GBps": round(step_gbps, 1),
-        "read_ceiling_GBps": round(read_gbps, 1),
-        "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
-        "algorithmic_bytes_per_step": alg["step_bytes"],
-        "kernels_us": {k: round(v, 3) for k, v in kus.items()},
-        "roofline": {
-            "kernel": "k_score_stream (latent scoring over C^K)",
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": alg["stream_bytes"],
-            "avg_launch_us": round(stream_us, 3),
-        },
-        "reconstruction_mfma": {
-            "kernel": "k_attn_tiles (reconstruction + attention on bf16 MFMA)",
-            "achieved_TFLOPs": round(rec_tflops, 2),
-            "peak_TFLOPs": BF16_PEAK_TFLOPS,
-            "frac": round(rec_tflops / BF16_PEAK_TFLOPS, 5),
-        },
+    # full-reconstruction low-rank decoding (Appendix B.1) over the same
+    # coefficient caches: every one of the L tokens reconstructed
+    ck0, cv0 = coef0
+    outf = torch.empty_like(out)
+    for _ in range(2):
+        s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
+    torch.cuda.synchronize()
+    f0 = torch.cuda.Event(enable_timing=True)
+    f1 = torch.cuda.Event(enable_timing=True)
+    nfr = 10
+    f0.record(stream)
+    for _ in range(nfr):
+        s4r.full_recon_decode(c, wl.L, q, sk, sv, bk, bv, ck0, cv0, ws, out=outf)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fr_us = f0.elapsed_time(f1) * 1e3 / nfr
+    fr_flops = 2 * 2 * wl.batch * wl.L * wl.R * wl.Dp
+    comparator["full_reconstruction"] = {
+        "what": "full-reconstruction low-rank decoding (Appendix B.1): s4r_full_recon_decode, every non-sink "
+                "token reconstructed on the matrix cores (k_attn_tiles over all tokens + k_attn_combine)",
+        "us_per_step": round(fr_us, 2),
+        "reconstruction_flops": fr_flops,
+        "achieved_TFLOPs": round(fr_flops / (fr_us * 1e-6) / 1e12, 1),
+        "frac_of_bf16_peak": round(fr_flops / (fr_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "s4r_step_speedup": round(fr_us / (ms_step * 1e3), 2),
     }
-    if comparator is not None:
-        result["comparator_full_kv"] = comparator
-    if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(wl, st)
-    print(json.dumps(result), flush=True)
+    log(f"[bench] {wl.name} full-reconstruction comparator: {fr_us:.1f} us/step "
+        f"({comparator['full_reconstruction']['achieved_TFLOPs']:.0f} TFLOP/s), "
+        f"S4R step {comparator['full_reconstruction']['s4r_step_speedup']:.2f}x faster")
+    return comparator
 
 
-def bench_sustained(args, wl, kernel_steps=8):
+def bench_sustained(args, wl, steps, warmup, kernel_steps=8, cpu_budget=10.0):
     """Sustained multi-layer decode: every step runs all layers one after the
     other, each layer appending the new token's key/value coefficients (row
     L - 1) before scoring, so the context grows by one token per step.  Steps
@@ -493,7 +580,6 @@ def bench_sustained(args, wl, kernel_steps=8):
     import paper_2608_00528_amd as s4r
     import workloads as W
 
-    warmup, steps = args.warmup, args.steps
     total = warmup + steps + kernel_steps
     L0 = wl.L - 1                       # the first step appends row L0 and runs at L = wl.L
     cap = ((L0 + total + 15) // 16) * 16
@@ -600,10 +686,12 @@ def bench_sustained(args, wl, kernel_steps=8):
             "avg_launch_us": round(kus["score_stream"], 3),
         },
     }
+    del layers, ws
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline_sustained(wl, host0, L0 + 1)
-    print(json.dumps(result), flush=True)
+        result["cpu_baseline"] = cpu_baseline_sustained(wl, host0, L0 + 1, budget_s=cpu_budget)
+    return result
 
 
 def cpu_baseline_sustained(wl, one, L, budget_s=10.0):
