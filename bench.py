@@ -46,6 +46,7 @@ BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 N_REPLICAS = 4
 SHAPES = {"llama8b_32k": "Llama-3.1-8B-shaped", "llama8b_128k": "Llama-3.1-8B-shaped",
           "qwen7b_128k": "Qwen2.5-7B-shaped", "qwen3_4b_120k": "Qwen3-4B-shaped (the paper's efficiency setting)",
+          "qwen3_4b_120k_w32": "Qwen3-4B-shaped (the paper's default W = W_q = 32)",
           "tiny_fp32": "tiny"}
 
 
@@ -157,7 +158,7 @@ def copy_calibration(nbytes, reps):
                       "reps": reps, "kernel": "torch.neg (elementwise, float32)"}), flush=True)
 
 
-EXTRA_SINGLE = ("tiny_fp32", "llama8b_32k", "qwen7b_128k", "qwen3_4b_120k")
+EXTRA_SINGLE = ("tiny_fp32", "llama8b_32k", "qwen7b_128k", "qwen3_4b_120k", "qwen3_4b_120k_w32")
 EXTRA_STEPS, EXTRA_WARMUP = 100, 10
 MALL_BYTES = 256 << 20          # MI355X Infinity Cache
 
@@ -251,12 +252,15 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     def up(x):
         return torch.from_numpy(np.ascontiguousarray(x)).to(device="cuda", dtype=dt)
 
-    q, sk, sv, bk, bv = (up(st[k]) for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v"))
-    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    # latent axes in the library's storage width (ranks rounded up to 32, zero columns)
+    q, sk, sv = (up(st[k]) for k in ("q", "sink_k", "sink_v"))
+    bk, bv = (up(s4r.pad_latent(st[k], wl.rank)) for k in ("bases_k", "bases_v"))
+    qwin = None if st["qwin_prev"] is None else torch.from_numpy(
+        s4r.pad_latent(st["qwin_prev"], wl.rank, wl.basis_groups)).to("cuda", torch.float32)
     reps = []
     for key in ("coef_k", "coef_v"):
-        rm = np.zeros((wl.batch, cap, wl.R))
-        rm[:, :wl.L] = st[key]
+        rm = np.zeros((wl.batch, cap, s4r.rank_stride(wl.rank) * wl.basis_groups))
+        rm[:, :wl.L] = s4r.pad_latent(st[key], wl.rank, wl.basis_groups)
         reps.append(s4r.pack_coef(c, cap, up(rm)))
     n_rep = replicas_for(sum(t.numel() * t.element_size() for t in reps))
     replicas = [(reps[0], reps[1])] + [(reps[0].clone(), reps[1].clone()) for _ in range(n_rep - 1)]

@@ -12,8 +12,11 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Array pointers are DEVICE pointers, 16-byte aligned, densely packed in
- *    the layouts stated below.  The caller owns all memory; the library never
- *    allocates device memory.  Scratch lives in the caller's workspace, whose
+ *    the layouts stated below.  The caller owns all memory; the library does
+ *    not allocate device memory on any compute call (the exceptions are named
+ *    where they apply: the rocBLAS handle of the basis construction and the
+ *    fixed scratch array of s4r_decode_step_noalloc).  Scratch lives in the
+ *    caller's workspace, whose
  *    size s4r_workspace_size() returns; its initial contents do not matter.
  *  - Every call is asynchronous on the caller's hipStream_t and performs no
  *    host synchronisation.  Calls that share a workspace must not overlap.
@@ -30,6 +33,17 @@
  * the paper), s sinks, W local window, W_q query-coefficient rows, k global
  * budget, L the current non-sink length (the token appended this step
  * included), m = min(k, max(L - W, 0)) + min(W, L) selected tokens.
+ *
+ * Rank stride: every latent axis is stored rank_s = 32 * ceil(rank / 32)
+ * columns wide per basis group (the coefficient layout works in 32-column
+ * blocks).  When rank is not a multiple of 32 (the paper's r = 204 of
+ * Appendix B.4 is stored in 224 columns), group beta's columns are
+ * beta * rank_s .. beta * rank_s + rank - 1 and the rest of its rank_s
+ * columns must hold zeros in the bases (the library's own basis construction
+ * writes them; projections from zero-padded bases write zero coefficients).
+ * Below, R stands for basis_groups * rank_s in every layout; the 1 / sqrt(R)
+ * scale of the latent logits (Section 3.2.2) takes the configured
+ * basis_groups * rank.
  *
  * Layouts
  * -------
@@ -87,11 +101,13 @@ typedef struct {
   int32_t n_kv_heads;    /* h_kv                                                   */
   int32_t head_dim;      /* d_h: 64 or 128                                         */
   int32_t basis_groups;  /* 1 = one basis over Dp (paper); must divide n_kv_heads  */
-  int32_t rank;          /* rank per basis group, multiple of 32, <= Dp/basis_groups;
+  int32_t rank;          /* rank per basis group, <= Dp/basis_groups, stored in
+                            32 * ceil(rank / 32) columns (the rank stride above);
                             the key rank r^K when rank_v is set                    */
   int32_t n_sink;        /* s, sink tokens kept at full precision (Section 3.1.1)  */
   int32_t window;        /* W, local window always kept (Section 3.2.3)            */
-  int32_t q_window;      /* W_q >= 1 query-coefficient rows used for scoring (3.2.2) */
+  int32_t q_window;      /* W_q >= 1 query-coefficient rows used for scoring (3.2.2);
+                            G * W_q <= 128 (the paper's W_q = 32 at G = 4), G <= 16 */
   int32_t topk;          /* k, global budget; clamped to max(L - W, 0)             */
   int32_t pool_kernel;   /* kappa, odd, 1 = no pooling                             */
   int32_t pool_mode;     /* S4R_POOL_MAX | S4R_POOL_AVG                            */
@@ -101,8 +117,8 @@ typedef struct {
   float rope_theta;      /* RoPE base; 0 disables RoPE                             */
   int32_t dtype;         /* S4R_FP32 | S4R_BF16                                    */
   int32_t rank_v;        /* 0: values share `rank`; else the value rank r^V per basis
-                            group (Appendix D.2: r^K <= r^V), a multiple of 32 <=
-                            Dp/basis_groups.  The value cache and basis are then
+                            group (Appendix D.2: r^K <= r^V), <= Dp/basis_groups,
+                            stored with its own rank stride.  The value cache and basis are then
                             [.., R_V = basis_groups * rank_v] wide; asymmetric
                             ranks run on the bf16 matrix-core path for the rank
                             pairs s4r_decode_step lists                            */
@@ -270,17 +286,23 @@ s4r_status s4r_project_queries(const s4r_config* cfg, int64_t n_rows, const void
  * row's group slice L2-normalised, optionally mean-centred (center = 1),
  * and the right singular vectors of the `rank` largest singular values
  * (rank_v for the values), largest first, written as bases_k / bases_v
- * [B, basis_groups, Dp / basis_groups, rank] in the storage dtype.  Signs of
+ * [B, basis_groups, Dp / basis_groups, rank_s] in the storage dtype (columns
+ * from rank to the rank stride rank_s are written as zeros).  Signs of
  * the singular vectors are arbitrary (the decode step depends on B B^T only).
  * s_k / s_v: [B, n_rows, Dp] raw pre-RoPE rows, bf16.  sample_idx_out
  * (optional, device, s4r_prefill_num_samples entries) receives the sample.
  * The Gram matrices are formed in fp64 by this library's kernels; their
  * symmetric eigenproblems run in rocSOLVER (fp64, divide and conquer) within
  * the caller's workspace of s4r_prefill_bases_workspace_size bytes; the first
- * call on a device creates one rocBLAS handle, kept until the process ends
- * (host threads calling on one device are serialised around it).  The
- * solver's per-matrix convergence flag is not read back (the call stays
- * asynchronous); the Gram matrices are symmetric positive semi-definite.
+ * call on a device (this one, or s4r_prefill_bases_workspace_size) creates
+ * one rocBLAS handle, kept until the process ends (host threads calling on
+ * one device are serialised around it).  Creating the handle is the one
+ * place where the library may allocate device memory itself (rocBLAS's own
+ * handle state; the solver's workspace is always the caller's).  The call
+ * stays asynchronous: the solver's per-matrix convergence flag is consumed
+ * on the device, where a matrix that did not converge writes quiet-NaN bases
+ * for its (sequence, side, basis group), so the failure reaches the caller
+ * through the output instead of passing silently.
  * bf16 storage, bases_shared = 0, (Dp / basis_groups) % 256 == 0 and at least
  * max(rank, rank_v) sampled rows (otherwise S4R_ERR_UNSUPPORTED /
  * S4R_ERR_BAD_SHAPE).
@@ -303,10 +325,10 @@ s4r_status s4r_prefill_bases(const s4r_config* cfg, int64_t n_rows, const void* 
  * bf16 ulp from the fp64-rounded value where the fp32 sum lies next to a
  * rounding boundary).  bf16 storage, rank 32..192 and equal key and value
  * ranks only (otherwise S4R_ERR_UNSUPPORTED).  ws / ws_bytes: the workspace
- * of s4r_decode_step (s4r_workspace_size); its first B * 2 * Dp * rank * 2 bytes hold the bases
- * transposed while the call runs.  The bases themselves come from a truncated
- * SVD of sampled, normalised rows (Section 3.1), which this library does not
- * compute.
+ * of s4r_decode_step (s4r_workspace_size); its first B * 2 * Dp * rank * 2
+ * bytes hold the bases transposed while the call runs.  The bases themselves
+ * come from a truncated SVD of sampled, normalised rows (Section 3.1), which
+ * s4r_prefill_bases computes.
  */
 s4r_status s4r_prefill_project(const s4r_config* cfg, int64_t n_rows, const void* s_k,
                                const void* s_v, const void* bases_k, const void* bases_v,

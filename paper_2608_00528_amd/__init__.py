@@ -21,11 +21,13 @@ from .api import (  # noqa: E402,F401
     make_config,
     num_selected,
     pack_coef,
+    pad_latent,
     num_samples,
     prefill_bases,
     prefill_project,
     project_append,
     project_queries,
+    rank_stride,
     read_bandwidth,
     reconstruct,
     score_latent,

@@ -95,8 +95,36 @@ def _G(cfg):
     return cfg.n_q_heads // cfg.n_kv_heads
 
 
+def rank_stride(rank):
+    """Storage width of a rank: the rank rounded up to a multiple of 32 (the
+    coefficient layout works in 32-column blocks; the extra columns hold zeros)."""
+    return (rank + 31) // 32 * 32
+
+
 def _R(cfg):
-    return cfg.rank * cfg.basis_groups
+    return rank_stride(cfg.rank) * cfg.basis_groups
+
+
+def pad_latent(x, rank, basis_groups=1):
+    """Lay latent data out in the library's storage width: the last axis of
+    `x` holds basis_groups blocks of `rank` columns (bases: one block); each
+    block moves to its own rank_stride(rank) columns, the padding columns zero.
+    Works on torch tensors and numpy arrays; returns `x` itself when the rank
+    is already a multiple of 32."""
+    rs = rank_stride(rank)
+    if rs == rank:
+        return x
+    if x.shape[-1] != rank * basis_groups:
+        raise ValueError(f"last axis {x.shape[-1]} is not {basis_groups} x rank {rank}")
+    shape = tuple(x.shape[:-1]) + (basis_groups * rs,)
+    if isinstance(x, torch.Tensor):
+        out = torch.zeros(shape, dtype=x.dtype, device=x.device)
+    else:
+        import numpy as np
+        out = np.zeros(shape, dtype=x.dtype)
+    for g in range(basis_groups):
+        out[..., g * rs:g * rs + rank] = x[..., g * rank:(g + 1) * rank]
+    return out
 
 
 def score_latent(cfg, length, q, bases_k, coef_k, ws, qwin_prev=None, scores=None, qcoef=None):
@@ -233,7 +261,7 @@ def prefill_bases(cfg, n_rows, s_k, s_v, eta=0.2, center=False, bases_k=None, ba
     dt = storage_dtype(cfg)
     lib = L.load()
     dg = cfg.n_kv_heads * cfg.head_dim // cfg.basis_groups
-    shape = lambda r: (cfg.batch, cfg.basis_groups, dg, r)  # noqa: E731
+    shape = lambda r: (cfg.batch, cfg.basis_groups, dg, rank_stride(r))  # noqa: E731
     if bases_k is None:
         bases_k = torch.empty(shape(cfg.rank), dtype=dt, device=s_k.device)
     if bases_v is None:

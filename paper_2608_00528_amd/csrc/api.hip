@@ -57,15 +57,17 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   const int Dg = Dp / c->basis_groups;
   if (c->rank < 1 || c->rank > Dg)
     return fail(S4R_ERR_BAD_SHAPE, "rank %d must be in [1, Dp/basis_groups = %d]", c->rank, Dg);
-  if (c->rank % 32) return fail(S4R_ERR_UNSUPPORTED, "rank %d must be a multiple of 32", c->rank);
   if (Dg > kQMaxChunks * kPChunk)
     return fail(S4R_ERR_UNSUPPORTED, "Dp / basis_groups = %d > %d not supported", Dg, kQMaxChunks * kPChunk);
-  const int R = c->rank * c->basis_groups;
-  if (R > 256) return fail(S4R_ERR_UNSUPPORTED, "latent width %d > 256 not supported", R);
-  const int rank_v = c->rank_v ? c->rank_v : c->rank;
-  if (rank_v < 1 || rank_v > Dg)
+  // storage widths: the configured ranks rounded up to 32 columns (Dg is a
+  // multiple of 64, so the rounded rank still fits the basis group)
+  const int rank_s = (c->rank + 31) / 32 * 32;
+  const int R = rank_s * c->basis_groups;
+  if (R > 256) return fail(S4R_ERR_UNSUPPORTED, "latent width %d (rank stride %d) > 256 not supported", R, rank_s);
+  const int rank_v_cfg = c->rank_v ? c->rank_v : c->rank;
+  if (rank_v_cfg < 1 || rank_v_cfg > Dg)
     return fail(S4R_ERR_BAD_SHAPE, "rank_v %d must be 0 or in [1, Dp/basis_groups = %d]", c->rank_v, Dg);
-  if (rank_v % 32) return fail(S4R_ERR_UNSUPPORTED, "rank_v %d must be a multiple of 32", rank_v);
+  const int rank_v = (rank_v_cfg + 31) / 32 * 32;
   if (rank_v * c->basis_groups > 256)
     return fail(S4R_ERR_UNSUPPORTED, "value latent width %d > 256 not supported", rank_v * c->basis_groups);
   if (c->n_sink < 0 || c->n_sink > 1024) return fail(S4R_ERR_BAD_SHAPE, "n_sink %d outside [0, 1024]", c->n_sink);
@@ -80,8 +82,9 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   if (c->group_agg != S4R_AGG_MEAN && c->group_agg != S4R_AGG_MAX)
     return fail(S4R_ERR_BAD_SHAPE, "group_agg %d invalid", c->group_agg);
   const int G = c->n_q_heads / c->n_kv_heads;
+  if (G > kMaxG) return fail(S4R_ERR_UNSUPPORTED, "G = n_q_heads / n_kv_heads = %d > %d not supported", G, kMaxG);
   if ((int64_t)G * c->q_window > kMaxGW)
-    return fail(S4R_ERR_UNSUPPORTED, "G * q_window = %d > %d not supported", G * c->q_window, kMaxGW);
+    return fail(S4R_ERR_UNSUPPORTED, "G * q_window = %lld > %d not supported", (long long)G * c->q_window, kMaxGW);
   if (c->capacity < 16 || c->capacity % 16)
     return fail(S4R_ERR_BAD_SHAPE, "capacity %lld must be a positive multiple of 16", (long long)c->capacity);
   if (c->capacity > (int64_t)kMaxSelGroups * kSelChunk)
@@ -99,10 +102,13 @@ s4r_status make_problem(const s4r_config* c, Problem& P) {
   P.G = G;
   P.Dp = Dp;
   P.nb = c->basis_groups;
-  P.rank = c->rank;
+  P.rank = rank_s;
   P.R = R;
   P.rank_v = rank_v;
   P.Rv = rank_v * c->basis_groups;
+  P.rank_cfg = c->rank;
+  P.rank_v_cfg = rank_v_cfg;
+  P.R_cfg = c->rank * c->basis_groups;
   P.Dg = Dg;
   P.s = c->n_sink;
   P.W = c->window;

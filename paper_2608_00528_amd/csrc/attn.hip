@@ -363,7 +363,8 @@ bool attention_supported(const Problem& P) {
            tiles_rank_pair(P.rank / 32, P.rank_v / 32);
   const int rb = P.rank / 32;
   const bool g_ok = P.G == 1 || P.G == 2 || P.G == 4 || P.G == 7 || P.G == 8;
-  const bool rb_ok = (rb >= 1 && rb <= 6) || rb == 8;
+  // seven blocks (rank 224, the padded r = 204) only on the bf16 MFMA kernel
+  const bool rb_ok = (rb >= 1 && rb <= 6) || rb == 8 || (rb == 7 && P.dtype == S4R_BF16);
   return g_ok && rb_ok && (P.dh == 64 || P.dh == 128);
 }
 

@@ -367,6 +367,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
+// 8 fp32 values -> one bf16 operand (round to nearest even)
+__device__ __forceinline__ void round_f32x8(const float* x, Op8& o) {
+  o.u = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                   pack_bf16x2(x[6], x[7]));
+}
+
 // 8 fp32 values -> bf16 hi and lo parts (x ~= hi + lo to about 2^-17)
 __device__ __forceinline__ void split2_f32x8(const float* x, Op8& hi, Op8& lo) {
   uint32_t ph[4], pl[4];

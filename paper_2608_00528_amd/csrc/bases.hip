@@ -178,21 +178,25 @@ __global__ __launch_bounds__(256) void k_gram(const uint16_t* __restrict__ s_k, 
 
 // ---- bases ----------------------------------------------------------------------------------
 // bases[b][g][d][c] = eigenvector (Dg - 1 - c) of M[(b * 2 + side) * nb + g],
-// component d (eigenvalues ascending), in the storage format
+// component d (eigenvalues ascending), in the storage format, for the
+// configured rank's columns c < rank_*; the padding columns up to the storage
+// width (stride_*) are zero.  A matrix whose eigensolve did not converge
+// (info != 0) gets quiet-NaN bases, so the failure reaches the caller.
 template <typename T>
-__global__ __launch_bounds__(256) void k_write_bases(const double* __restrict__ V, T* __restrict__ bases_k,
-                                                     T* __restrict__ bases_v, int B, int nb, int Dg, int rank_k,
-                                                     int rank_v) {
+__global__ __launch_bounds__(256) void k_write_bases(const double* __restrict__ V, const rocblas_int* __restrict__ info,
+                                                     T* __restrict__ bases_k, T* __restrict__ bases_v, int B, int nb,
+                                                     int Dg, int stride_k, int stride_v, int rank_k, int rank_v) {
   const int side = blockIdx.y;
-  const int rank = side ? rank_v : rank_k;
-  const int64_t n = (int64_t)B * nb * Dg * rank;
+  const int stride = side ? stride_v : stride_k, rank = side ? rank_v : rank_k;
+  const int64_t n = (int64_t)B * nb * Dg * stride;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(e % rank);
-    const int d = (int)((e / rank) % Dg);
-    const int g = (int)((e / ((int64_t)rank * Dg)) % nb);
-    const int b = (int)(e / ((int64_t)rank * Dg * nb));
+    const int c = (int)(e % stride);
+    const int d = (int)((e / stride) % Dg);
+    const int g = (int)((e / ((int64_t)stride * Dg)) % nb);
+    const int b = (int)(e / ((int64_t)stride * Dg * nb));
     const int mat = (b * 2 + side) * nb + g;
-    store_elem(side ? bases_v : bases_k, e, V[(int64_t)mat * Dg * Dg + d + (int64_t)(Dg - 1 - c) * Dg]);
+    const double v = c < rank ? V[(int64_t)mat * Dg * Dg + d + (int64_t)(Dg - 1 - c) * Dg] : 0.0;
+    store_elem(side ? bases_v : bases_k, e, info[mat] == 0 ? v : __builtin_nan(""));
   }
 }
 
@@ -241,7 +245,7 @@ BasesLayout bases_layout(const Problem& P, int n_s, size_t solver_bytes) {
   l.e = o;
   o = al(o + nmat * Dg * 8);
   l.info = o;
-  o = al(o + nmat * 4);
+  o = al(o + nmat * sizeof(rocblas_int));
   l.inv = o;
   o = al(o + nmat * (size_t)n_s * 8);
   l.part = o;
@@ -330,11 +334,11 @@ hipError_t launch_prefill_bases(const Problem& P, int64_t n_rows, const void* s_
   const int64_t nel = (int64_t)P.B * nb * Dg * std::max(P.rank, P.rank_v);
   const dim3 grid((unsigned)std::min<int64_t>((nel + 255) / 256, 4096), 2);
   if (P.dtype == S4R_BF16)
-    hipLaunchKernelGGL(k_write_bases<uint16_t>, grid, dim3(256), 0, st, M, (uint16_t*)bases_k, (uint16_t*)bases_v,
-                       P.B, nb, Dg, P.rank, P.rank_v);
+    hipLaunchKernelGGL(k_write_bases<uint16_t>, grid, dim3(256), 0, st, M, info, (uint16_t*)bases_k,
+                       (uint16_t*)bases_v, P.B, nb, Dg, P.rank, P.rank_v, P.rank_cfg, P.rank_v_cfg);
   else
-    hipLaunchKernelGGL(k_write_bases<float>, grid, dim3(256), 0, st, M, (float*)bases_k, (float*)bases_v, P.B, nb,
-                       Dg, P.rank, P.rank_v);
+    hipLaunchKernelGGL(k_write_bases<float>, grid, dim3(256), 0, st, M, info, (float*)bases_k, (float*)bases_v, P.B,
+                       nb, Dg, P.rank, P.rank_v, P.rank_cfg, P.rank_v_cfg);
   if (idx_out) e = hipMemcpyAsync(idx_out, idx, (size_t)n_s * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess) e = hipGetLastError();
   return e;

@@ -125,7 +125,7 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   if (cblk == 0 && ch == 0)
     for (int i = t; i < 2 * kHistBins; i += blockDim.x) hist[(int64_t)b * 2 * kHistBins + i] = 0u;
 
-  __shared__ float xs[kMaxGW][kPChunk];
+  __shared__ float xs[kMaxG][kPChunk];
   __shared__ double red[4][kPVec][32];
   const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + ((int64_t)grp * Dg + r0) * rank +
                    (c0 - grp * rank) + cg * 8;
@@ -134,7 +134,7 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   typename Raw8<T>::type bw[kPRows];
 #pragma unroll
   for (int i = 0; i < kPRows; ++i) bw[i].load(bases + (int64_t)min(rg + 64 * i, nrow - 1) * rank);
-  batched_copy4<kMaxGW * kPChunk / 256>(
+  batched_copy4<kMaxG * kPChunk / 256>(
       G * kPChunk,
       [&](int i) -> float {
         const int v = i >> 8, d = grp * Dg + r0 + min(i & (kPChunk - 1), nrow - 1);   // feature index in Dp

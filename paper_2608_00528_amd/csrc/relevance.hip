@@ -285,6 +285,91 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   }
 }
 
+// K2 for more than 16 query columns (G * W_q up to 128, the paper's tied
+// W_q = W = 32): grid (ceil(L / 256), B), 256 threads, 256 tokens per
+// workgroup.  The global (M, 1 / S) of every column comes from k_fold_stats;
+// the per-tile factors exp(ref - M) / S of the chunk's tiles (and halo) go to
+// LDS; thread (position, group) forms the window mean of its group's W_q
+// columns from the exp values (contiguous per position) with an fp64 sum of
+// the fp32 products, then pooling and group aggregation run as in k_relevance.
+constexpr int kWideChunk = kRelThreads;
+constexpr int kWideMaxTiles = (kWideChunk + 64) / kTileTok + 2;
+
+template <int GMAX>
+__global__ __launch_bounds__(kRelThreads) void k_relevance_wide(
+    const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ col_stats,
+    float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out, int64_t cap, int L,
+    int n_hist, int G, int Wq, int gwp, int kappa, int pool_mode, int agg, int ntiles_cap, Lens lens, int key_shift) {
+  const int b = blockIdx.y;
+  const int score_stride = L;
+  {
+    const int Lb = (int)len_of(lens, b, L);
+    n_hist += Lb - L;
+    L = Lb;
+  }
+  if ((int)blockIdx.x * kWideChunk >= L) return;
+  const int t = threadIdx.x;
+  const int GW = G * Wq;
+  const int h = kappa / 2;
+  const int t0 = blockIdx.x * kWideChunk;
+  const int x0 = t0 - h;
+  const int span = kWideChunk + 2 * h;
+  const int tile_lo = max(x0, 0) / kTileTok;
+  const int tile_hi = (min(t0 + kWideChunk + h, L) - 1) / kTileTok;
+  const int ntl = tile_hi - tile_lo + 1;                   // <= kWideMaxTiles
+
+  __shared__ uint32_t hl[kHistBins];
+  __shared__ float fac[kWideMaxTiles * kMaxGW];            // [tile][column]
+  extern __shared__ float vs[];                            // [G][span]
+  for (int i = t; i < kHistBins; i += kRelThreads) hl[i] = 0;
+  const double2* cs = reinterpret_cast<const double2*>(col_stats) + (int64_t)b * GW;
+  for (int i = t; i < ntl * GW; i += kRelThreads) {
+    const int tl = i / GW, c = i % GW;
+    const float r = tref[((int64_t)b * ntiles_cap + tile_lo + tl) * gwp + c];
+    const double2 st = cs[c];
+    fac[tl * GW + c] = (r != -INFINITY) ? (float)((double)exp_neg_accurate((double)r - st.x) * st.y) : 0.f;
+  }
+  __syncthreads();
+  // window mean over the W_q rows of group g at every staged position
+  const float pad = (pool_mode == S4R_POOL_MAX) ? -INFINITY : 0.f;
+  const double inv_wq = 1.0 / (double)Wq;
+  for (int i = t; i < span * G; i += kRelThreads) {
+    const int xi = i / G, g = i % G;
+    const int x = x0 + xi;
+    float v = pad;
+    if (x >= 0 && x < L) {
+      const float* ep = e + ((int64_t)b * cap + x) * gwp + g * Wq;
+      const float* fr = fac + (x / kTileTok - tile_lo) * GW + g * Wq;
+      double sum = 0.0;                            // W_q products summed in fp64
+      for (int c = 0; c < Wq; ++c) sum += (double)ep[c] * (double)fr[c];
+      v = (float)(sum * inv_wq);
+    }
+    vs[g * span + xi] = v;
+  }
+  __syncthreads();
+  float af[1];
+  switch (h) {
+    case 0: pool_aggregate<0, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 1: pool_aggregate<1, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 2: pool_aggregate<2, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 3: pool_aggregate<3, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    case 4: pool_aggregate<4, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+    default: pool_aggregate<-1, 1, GMAX>(vs, span, t, G, kappa, pool_mode, agg, af); break;
+  }
+  const int x = t0 + t;
+  if (x < L) {
+    atilde[(int64_t)b * cap + x] = af[0];
+    if (scores_out) scores_out[(int64_t)b * score_stride + x] = af[0];
+  }
+  if (x < n_hist) atomicAdd(&hl[selection_key_shift(af[0], key_shift) >> kHistShift], 1u);
+  __syncthreads();
+  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
+  for (int i = t; i < kHistBins; i += kRelThreads) {
+    const uint32_t c = hl[i];
+    if (c) atomicAdd(&hs[i], c);
+  }
+}
+
 // histogram of caller-provided scores (standalone selection), into a
 // histogram zeroed by k_zero_hist
 __global__ __launch_bounds__(256) void k_zero_hist(uint32_t* __restrict__ hist, int n) {
@@ -375,7 +460,24 @@ static void launch_rel_nq(const Problem& P, const Workspace& ws, int64_t L, floa
   }
 }
 
+// more than 16 query columns: the statistics are always folded first
+static void launch_rel_wide(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
+  const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
+  const int nwg = score_workgroups(P, L);
+  hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
+  const size_t lds = (size_t)P.G * (kWideChunk + 2 * (P.kappa / 2)) * sizeof(float);
+  dim3 grid((unsigned)((L + kWideChunk - 1) / kWideChunk), P.B);
+  auto kern = P.G <= 4 ? k_relevance_wide<4> : (P.G <= 8 ? k_relevance_wide<8> : k_relevance_wide<16>);
+  hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.col_stats, ws.atilde, ws.hist,
+                     scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, gw_padded(P), P.kappa, P.pool_mode, P.agg,
+                     (int)(P.cap / kTileTok), P.lens, fused_key_shift(P, L));
+}
+
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
+  if (P.GW > kColBlk) {
+    launch_rel_wide(P, ws, L, scores_out, st);
+    return hipGetLastError();
+  }
   switch (gw_padded(P) / 4) {
     case 1: launch_rel_nq<1>(P, ws, L, scores_out, st); break;
     case 2: launch_rel_nq<2>(P, ws, L, scores_out, st); break;

@@ -20,7 +20,9 @@ constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capac
 constexpr int kMaxSplit = 64;         // attention splits per (sequence, kv head)
 constexpr int kMaxTilesPerSplit = 512; // 16-token tiles per split (index list staged in LDS)
 constexpr int kTileMax = 32;          // tiles per workgroup of the MFMA attention kernel (index list in LDS)
-constexpr int kMaxGW = 16;            // G * W_q columns handled by one MFMA block
+constexpr int kMaxG = 16;             // query groups G = h_q / h_kv
+constexpr int kColBlk = 16;           // query columns (G * W_q) per scoring workgroup
+constexpr int kMaxGW = 128;           // G * W_q: up to 8 column blocks
 constexpr int kPChunk = 256;          // basis rows per query-projection workgroup
 constexpr int kQMaxChunks = 8;        // row chunks per basis group (Dp / basis_groups <= 2048)
 
@@ -34,18 +36,22 @@ struct Lens {
 __host__ __device__ inline int64_t len_of(const Lens& l, int b, int64_t L) { return l.n ? (int64_t)l.v[b] : L; }
 
 // the (key, value) rank pairs the kernel is built for, in 32-column blocks:
-// equal ranks 32 .. 192 and 256, and the value-heavy pairs near 1:1.5 and
-// 1:2 of Appendix D.2 for the totals 2 r = 256, 320 and 384
+// equal ranks 32 .. 256 (224 holds the paper's r = 204 of Appendix B.4), and
+// the value-heavy pairs near 1:1.5 and 1:2 of Appendix D.2 for the totals
+// 2 r = 256, 320 and 384
 constexpr bool tiles_rank_pair(int rbk, int rbv) {
-  return (rbk == rbv && ((rbk >= 1 && rbk <= 6) || rbk == 8)) || (rbk == 3 && rbv == 5) ||
+  return (rbk == rbv && rbk >= 1 && rbk <= 8) || (rbk == 3 && rbv == 5) ||
          (rbk == 2 && rbv == 6) || (rbk == 4 && rbv == 6) || (rbk == 3 && rbv == 7) || (rbk == 5 && rbv == 7) ||
          (rbk == 4 && rbv == 8);
 }
 
 struct Problem {
   int B, hq, hkv, dh, G, Dp;
-  int nb, rank, R, Dg;                // basis groups, rank per group, R = nb*rank, Dg = Dp/nb
+  int nb, rank, R, Dg;                // basis groups, rank per group, R = nb*rank, Dg = Dp/nb; rank is
+                                      // the storage width (the configured rank rounded up to 32)
   int rank_v, Rv;                     // the value side's (= rank, R unless asymmetric)
+  int rank_cfg, rank_v_cfg;           // the configured ranks (columns past them are zero padding)
+  int R_cfg;                          // nb * rank_cfg: the latent width of the 1 / sqrt(R) scale
   int s, W, Wq, k, kappa, pool_mode, agg;
   int bases_shared, dtype;
   int64_t cap;
@@ -86,7 +92,9 @@ inline int64_t sel_groups_max(const Problem& P) { return (P.cap + kSelChunk - 1)
 inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelChunk; }
 // query columns G * W_q rounded up to a multiple of 4 (one 16-byte group per
 // MFMA of the scoring kernel): the column stride of the exp values
-inline int gw_padded(const Problem& P) { return (P.GW + 3) / 4 * 4; }
+inline int gw_padded(const Problem& P) { return P.GW <= kColBlk ? (P.GW + 3) / 4 * 4 : (P.GW + kColBlk - 1) / kColBlk * kColBlk; }
+// column blocks of the scoring pass (one per kColBlk query columns)
+inline int col_blocks(const Problem& P) { return (P.GW + kColBlk - 1) / kColBlk; }
 // RoPE: ratio of consecutive frequencies theta^(-2 / d_h) (0 when RoPE is off)
 inline double rope_ratio(const Problem& P) { return P.theta == 0.f ? 0.0 : pow((double)P.theta, -2.0 / P.dh); }
 

@@ -11,11 +11,13 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 // K1: the coefficient stream
 // ---------------------------------------------------------------------------
-// grid (workgroups per sequence, B), 256 threads = 4 waves.  A wave owns a
-// contiguous range of 16-token tiles.  Each 16x32 block of C^K is one
-// coalesced 1 KiB wave load that is used directly as the B operand of a
-// 16x16x32 bf16 MFMA (lane l: token l%16, latent columns 8*(l/16)..+7).  The A
-// operand holds the query-coefficient columns, four per MFMA, each as its
+// grid (workgroups per sequence, B, column blocks), 256 threads = 4 waves.  A
+// wave owns a contiguous range of 16-token tiles; a workgroup scores them
+// against one block of up to 16 query columns (blockIdx.z; more than one block
+// only when G * W_q > 16, the blocks re-reading the tiles from L2 / MALL).
+// Each 16x32 block of C^K is one coalesced 1 KiB wave load that is used
+// directly as the B operand of a 16x16x32 bf16 MFMA (lane l: token l%16,
+// latent columns 8*(l/16)..+7).  The A operand holds the query-coefficient columns, four per MFMA, each as its
 // hi / mid / lo bf16 parts in rows 4*c + part (row 4*c + 3 is zero), so lane
 // (token t, k-group c) receives the three partial products of query column c
 // against token t.  The MFMA rounds once per instruction, like an fp32 sum
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     const T* __restrict__ coef_k, const double* __restrict__ qpart, const float* __restrict__ qwin_prev,
     float* __restrict__ qcoef_out, float* __restrict__ e_out, float* __restrict__ tref,
     double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int nch, int ntiles_cap, int tiles_per_wave,
-    int nwg, double scale, Lens lens) {
+    int nwg, int gwp, double scale, Lens lens) {
   constexpr int R = RB * kBlkCol;
   constexpr int NP = BLoad<T>::kParts;
   const int b = blockIdx.y;
@@ -75,6 +77,8 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int slot = lane & 15, kg = lane >> 4;      // token slot / k-group (= query column within an MFMA)
   const int GW = G * Wq;
+  const int c0 = blockIdx.z * kColBlk;             // first query column of this workgroup's block
+  const int GWl = min(GW - c0, 4 * NM);            // its columns
   const T* cb = coef_k + (int64_t)b * cap * R;
   const int ntiles = (L + 15) / 16;
 
@@ -101,8 +105,8 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
   double part[kQPre][kQMaxChunks];
   float old[kQPre];
   auto load_q = [&](int i0, int u) {
-    const int i = min(i0 + u * (int)blockDim.x + t, GW * R - 1);
-    const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
+    const int i = min(i0 + u * (int)blockDim.x + t, GWl * R - 1);
+    const int gi = c0 + i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
 #pragma unroll
     for (int c = 0; c < kQMaxChunks; ++c) part[u][c] = qp[((int64_t)min(c, nch - 1) * G + g) * R + r];
     old[u] = qw[(Wq > 1) ? ((int64_t)g * (Wq - 1) + min(wi, Wq - 2)) * R + r : 0];
@@ -125,7 +129,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
       *reinterpret_cast<uint4*>(&qsh[m][r][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
     }
     lds_barrier();
-    for (int i0 = 0; i0 < GW * R; i0 += kQPre * (int)blockDim.x) {
+    for (int i0 = 0; i0 < GWl * R; i0 += kQPre * (int)blockDim.x) {
       if (i0 > 0) {                                // more than kQPre * 256 elements
 #pragma unroll
         for (int u = 0; u < kQPre; ++u) load_q(i0, u);
@@ -133,15 +137,15 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
 #pragma unroll
       for (int u = 0; u < kQPre; ++u) {
         const int i = i0 + u * (int)blockDim.x + t;
-        if (i >= GW * R) break;
-        const int gi = i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
+        if (i >= GWl * R) break;
+        const int gl = i / R, gi = c0 + gl, r = i % R, g = gi / Wq, wi = gi % Wq;
         double x = part[u][0];
 #pragma unroll
         for (int c = 1; c < kQMaxChunks; ++c)
           if (c < nch) x += part[u][c];
         if (wi < Wq - 1) x = (double)old[u];
         const Split3 sp = split3(x);
-        const int m = gi >> 2, row = 4 * (gi & 3);
+        const int m = gl >> 2, row = 4 * (gl & 3);
         qsh[m][row + 0][r] = sp.hi;
         qsh[m][row + 1][r] = sp.mid;
         qsh[m][row + 2][r] = sp.lo;
@@ -177,7 +181,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
   double Srun[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
-    const int gi = 4 * m + kg;
+    const int gi = c0 + 4 * m + kg;
     lim[m] = (gi < GW) ? (L - Wq + gi % Wq) : -1;
     Mrun[m] = -INFINITY;
     Srun[m] = 0.0;
@@ -211,11 +215,11 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
         const float ref = fmaxf(slot_max16((float)z), Mrun[m]);
         const float ev = (z == -INFINITY) ? 0.f : exp_neg_accurate(z - (double)ref);
         const float ts = slot_sum16(ev);
-        // token-major stores: the wave's tile is one contiguous run of 16 * 4 * NM
-        // values (padding columns hold exp(-inf) = 0)
+        // token-major stores: with one column block the wave's tile is one
+        // contiguous run of 16 * 4 * NM values (padding columns hold exp(-inf) = 0)
         if (tile < tile1) {
-          e_out[((int64_t)b * cap + tok) * (4 * NM) + 4 * m + kg] = ev;
-          if (slot == 0) tref[((int64_t)b * ntiles_cap + tile) * (4 * NM) + 4 * m + kg] = ref;
+          e_out[((int64_t)b * cap + tok) * gwp + c0 + 4 * m + kg] = ev;
+          if (slot == 0) tref[((int64_t)b * ntiles_cap + tile) * gwp + c0 + 4 * m + kg] = ref;
         }
         if (ref > Mrun[m]) {                       // the running maximum grew
           if (Mrun[m] != -INFINITY) Srun[m] *= (double)exp_neg_accurate((double)Mrun[m] - (double)ref);
@@ -226,7 +230,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     }
   }
   // workgroup statistics: the four waves' (max, sum) folded in a fixed order
-  __shared__ double wm[kScoreWaves][kMaxGW], wsum[kScoreWaves][kMaxGW];
+  __shared__ double wm[kScoreWaves][kColBlk], wsum[kScoreWaves][kColBlk];
   if (slot == 0) {
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
@@ -235,14 +239,14 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     }
   }
   __syncthreads();
-  if (t < GW) {
-    const int col = t;
+  if (t < GWl) {
+    const int col = c0 + t;
     double M = -INFINITY, S = 0.0;
     for (int w = 0; w < kScoreWaves; ++w) {
-      const double mw = wm[w][col];
+      const double mw = wm[w][t];
       if (mw == -INFINITY) continue;
       const double mn = fmax(M, mw);
-      S = (M == -INFINITY ? 0.0 : S * exp(M - mn)) + wsum[w][col] * exp(mw - mn);
+      S = (M == -INFINITY ? 0.0 : S * exp(M - mn)) + wsum[w][t] * exp(mw - mn);
       M = mn;
     }
     double* ws2 = wg_stats + (((int64_t)b * GW + col) * nwg + blockIdx.x) * 2;
@@ -273,15 +277,17 @@ static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, c
                              const float* qwin_prev, float* qcoef_out, hipStream_t st) {
   const int tpw = tiles_per_wave(P, L);
   const int nwg = score_workgroups(P, L);
-  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), dim3(nwg, P.B), dim3(256), 0, st, (const T*)coef_k, ws.qpart,
-                     qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
-                     (int)(P.cap / kTileTok), tpw, nwg, 1.0 / sqrt((double)P.R), P.lens);
+  // the scale takes the configured latent width (storage columns past it are zero)
+  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), dim3(nwg, P.B, col_blocks(P)), dim3(256), 0, st, (const T*)coef_k,
+                     ws.qpart, qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq,
+                     project_chunks(P), (int)(P.cap / kTileTok), tpw, nwg, gw_padded(P), 1.0 / sqrt((double)P.R_cfg),
+                     P.lens);
 }
 
 template <typename T, int RB>
 static void launch_stream_t(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
                             const float* qwin_prev, float* qcoef_out, hipStream_t st) {
-  switch ((P.GW + 3) / 4) {
+  switch (std::min((P.GW + 3) / 4, kColBlk / 4)) {
     case 1: launch_stream_nm<T, RB, 1>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
     case 2: launch_stream_nm<T, RB, 2>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
     case 3: launch_stream_nm<T, RB, 3>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;

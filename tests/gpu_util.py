@@ -34,20 +34,45 @@ def dev(x, dtype, device="cuda"):
 
 def to_gpu_state(c, st, device="cuda"):
     """Stored state (float64 numpy, rounded) -> GPU tensors; coefficient caches
-    are uploaded row-major and packed into the tiled layout by the library."""
+    are uploaded row-major and packed into the tiled layout by the library.
+    Latent axes are laid out in the library's storage width (a rank that is
+    not a multiple of 32 gets zero columns up to the next multiple)."""
     dt = s4r.storage_dtype(c)
+    rank_v = c.rank_v or c.rank
     g = {}
-    for k in ("q", "sink_k", "sink_v", "bases_k", "bases_v"):
+    for k in ("q", "sink_k", "sink_v"):
         if k in st and st[k] is not None:
             g[k] = dev(st[k], dt, device)
-    for k in ("coef_k", "coef_v"):
-        rm = st[k]
+    for k, r in (("bases_k", c.rank), ("bases_v", rank_v)):
+        if k in st and st[k] is not None:
+            g[k] = dev(s4r.pad_latent(st[k], r), dt, device)
+    for k, r in (("coef_k", c.rank), ("coef_v", rank_v)):
+        rm = s4r.pad_latent(st[k], r, c.basis_groups)
         n = rm.shape[1]
         full = np.zeros((rm.shape[0], c.capacity, rm.shape[2]))
         full[:, :n] = rm
         ck = c if k == "coef_k" else s4r.value_config(c)       # the value cache has its own width
         g[k] = s4r.pack_coef(ck, c.capacity, dev(full, dt, device))
+    if st.get("qwin_prev") is not None:
+        g["qwin_prev"] = dev(s4r.pad_latent(st["qwin_prev"], c.rank, c.basis_groups), torch.float32, device)
     return g
+
+
+def unpad_latent(x, rank, basis_groups=1):
+    """The configured columns of latent data read back in the library's storage
+    width (inverse of pad_latent); asserts the padding columns hold zeros
+    (NaN rows, which the tests plant past a sequence's end, are left alone)."""
+    x = np.asarray(x)
+    rs = s4r.rank_stride(rank)
+    if rs == rank:
+        return x
+    assert x.shape[-1] == rs * basis_groups
+    parts = []
+    for g in range(basis_groups):
+        pad = x[..., g * rs + rank:(g + 1) * rs]
+        assert np.all((pad == 0) | np.isnan(pad)), "padding columns are not zero"
+        parts.append(x[..., g * rs:g * rs + rank])
+    return np.concatenate(parts, axis=-1)
 
 
 def rel_err_rows(gpu, ref):

@@ -68,12 +68,13 @@ def test_version_and_sizes():
     ("n_q_heads", 7, L.S4R_ERR_BAD_SHAPE),
     ("head_dim", 96, L.S4R_ERR_UNSUPPORTED),
     ("basis_groups", 3, L.S4R_ERR_BAD_SHAPE),
-    ("rank", 48, L.S4R_ERR_UNSUPPORTED),
+    ("rank", 0, L.S4R_ERR_BAD_SHAPE),
     ("rank", 4096, L.S4R_ERR_BAD_SHAPE),
     ("pool_kernel", 4, L.S4R_ERR_BAD_SHAPE),
     ("pool_kernel", 0, L.S4R_ERR_BAD_SHAPE),
     ("q_window", 0, L.S4R_ERR_BAD_SHAPE),
-    ("q_window", 5, L.S4R_ERR_UNSUPPORTED),      # G * W_q = 20 > 16
+    ("q_window", 33, L.S4R_ERR_UNSUPPORTED),     # G * W_q = 132 > 128
+    ("n_q_heads", 34, L.S4R_ERR_UNSUPPORTED),    # G = 17 > 16
     ("capacity", 1000, L.S4R_ERR_BAD_SHAPE),
     ("dtype", 7, L.S4R_ERR_BAD_SHAPE),
     ("topk", -1, L.S4R_ERR_BAD_SHAPE),
@@ -90,10 +91,11 @@ def test_config_validation(field, value, status):
     assert L.load().s4r_last_error().decode()
 
 
-@pytest.mark.parametrize("rank_v,status", [(16, L.S4R_ERR_UNSUPPORTED), (-32, L.S4R_ERR_BAD_SHAPE),
+@pytest.mark.parametrize("rank_v,status", [(16, L.S4R_OK), (-32, L.S4R_ERR_BAD_SHAPE),
                                            (160, L.S4R_ERR_BAD_SHAPE)])
 def test_value_rank_validation(rank_v, status):
-    """rank_v: 0 (= rank) or a multiple of 32 within Dp / basis_groups = 128."""
+    """rank_v: 0 (= rank) or a rank within Dp / basis_groups = 128 (stored
+    with its own stride of 32 * ceil(rank_v / 32) columns)."""
     lib = L.load()
     sz = ctypes.c_size_t()
     assert lib.s4r_workspace_size(ctypes.byref(cfg(rank_v=rank_v)), ctypes.byref(sz)) == status
@@ -307,3 +309,37 @@ def test_noalloc_step_refuses_beyond_its_scratch():
     # argument errors come first, as for the workspace step
     assert lib.s4r_decode_step_noalloc(None, 10, *args, None) == L.S4R_ERR_NULL_ARG
     assert lib.s4r_decode_step_noalloc(ctypes.byref(cfg()), 0, *args, None) == L.S4R_ERR_BAD_SHAPE
+
+
+def test_rank_stride_and_query_window_limits():
+    """A rank that is not a multiple of 32 is stored at the next multiple (the
+    paper's r = 204 in 224 columns): the workspace is that of the stored width;
+    a stored width beyond 256 is refused; G * W_q runs up to 128 (the paper's
+    W_q = 32 at G = 4)."""
+    lib = L.load()
+    n48, n64, n = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=48)), ctypes.byref(n48)) == L.S4R_OK
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=64)), ctypes.byref(n64)) == L.S4R_OK
+    assert n48.value == n64.value
+    paper = dict(n_q_heads=32, n_kv_heads=8, head_dim=128, capacity=120_000, window=32, topk=23_968)
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=204, q_window=32, **paper)), ctypes.byref(n)) == L.S4R_OK
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=232, **paper)), ctypes.byref(n)) == L.S4R_OK
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=260, **paper)), ctypes.byref(n)) == L.S4R_ERR_UNSUPPORTED
+    assert lib.s4r_workspace_size(ctypes.byref(cfg(rank=204, q_window=33, **paper)),
+                                  ctypes.byref(n)) == L.S4R_ERR_UNSUPPORTED
+    assert s4r.rank_stride(204) == 224 and s4r.rank_stride(224) == 224 and s4r.rank_stride(1) == 32
+
+
+def test_pad_latent_layout():
+    """pad_latent moves each basis group's rank columns to its own 32-aligned
+    block, zeros elsewhere; multiples of 32 pass through unchanged."""
+    import numpy as np
+    x = np.arange(2 * 3 * 2 * 40, dtype=np.float64).reshape(2, 3, 80) + 1.0
+    y = s4r.pad_latent(x, 40, basis_groups=2)
+    assert y.shape == (2, 3, 128)
+    assert np.array_equal(y[..., 0:40], x[..., 0:40]) and np.array_equal(y[..., 64:104], x[..., 40:80])
+    assert not y[..., 40:64].any() and not y[..., 104:128].any()
+    t = torch.from_numpy(x)
+    assert torch.equal(s4r.pad_latent(t, 40, 2), torch.from_numpy(y))
+    z = np.ones((2, 64))
+    assert s4r.pad_latent(z, 32, 2) is z

@@ -22,7 +22,8 @@ pytestmark = pytest.mark.gpu
 OUT_TOL = {"bf16": 2e-2, "fp32": 1e-4}
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k", "qwen7b_128k", "qwen3_4b_120k"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k", "qwen7b_128k", "qwen3_4b_120k",
+                                  "qwen3_4b_120k_w32"])
 def test_full_size_decode_step(name):
     wl = W.CONFIGS[name]
     print(f"[full-size] {wl.describe()}", flush=True)
@@ -33,7 +34,7 @@ def test_full_size_decode_step(name):
     m = s4r.num_selected(c, wl.L)
     idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
     scores = torch.empty((wl.batch, wl.L), dtype=torch.float32, device="cuda")
-    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    qwin = g.get("qwin_prev")
     out = s4r.decode_step(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
                           g["coef_v"], ws, qwin_prev=qwin, idx_out=idx, scores_out=scores)
     out_bench = s4r.decode_step(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"],

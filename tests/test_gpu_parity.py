@@ -20,7 +20,8 @@ import torch
 import paper_2608_00528_amd as s4r
 import workloads as W
 from oracle import decode, prefill
-from gpu_util import (cfg_from_workload, check_selection, dev, oracle_cfg, rel_err_rows, to_gpu_state)
+from gpu_util import (cfg_from_workload, check_selection, dev, oracle_cfg, rel_err_rows, to_gpu_state,
+                      unpad_latent)
 
 pytestmark = pytest.mark.gpu
 
@@ -51,6 +52,11 @@ CASES = {
                              _raw_state(W.CONFIGS["llama8b_32k"].scaled(N=8192, batch=2, topk=256))),
     "qwen_8k_latent": lambda: (W.CONFIGS["qwen7b_128k"].scaled(N=8192 + 4, batch=3, topk=300),
                                W.latent_state(W.CONFIGS["qwen7b_128k"].scaled(N=8192 + 4, batch=3, topk=300), seed=2)),
+    # the paper's default operating point at a short context: W = W_q = 32
+    # (G * W_q = 128 query columns in 8 scoring blocks), rank 204 stored in 224
+    "qwen3_w32_5k": lambda: (W.CONFIGS["qwen3_4b_120k_w32"].scaled(N=5000 + 4, batch=2, topk=968),
+                             W.latent_state(W.CONFIGS["qwen3_4b_120k_w32"].scaled(N=5000 + 4, batch=2, topk=968),
+                                            seed=4)),
 }
 
 
@@ -85,21 +91,24 @@ def test_score_latent(case):
     c = cfg_from_workload(wl)
     g = to_gpu_state(c, st)
     ws = s4r.alloc_workspace(c)
-    qco = torch.empty((wl.batch, wl.G, wl.R), dtype=torch.float32, device="cuda")
-    sc = s4r.score_latent(c, wl.L, g["q"], g["bases_k"], g["coef_k"], ws, qcoef=qco)
+    qco = torch.empty((wl.batch, wl.G, s4r.rank_stride(c.rank) * c.basis_groups), dtype=torch.float32,
+                      device="cuda")
+    sc = s4r.score_latent(c, wl.L, g["q"], g["bases_k"], g["coef_k"], ws, qcoef=qco, qwin_prev=g.get("qwin_prev"))
     torch.cuda.synchronize()
-    ref = _oracle(c, wl, st)
+    ref = _oracle(c, wl, st, qwin_prev=st.get("qwin_prev"))
     a = ref["a_tilde"]
     got = sc.cpu().numpy().astype(np.float64)
     err = np.abs(got - a) / np.maximum(np.abs(a), 1e-30)
+    print(f"[score_latent] {case}: score err {err.max():.2e}", flush=True)
     assert err.max() <= SCORE_TOL, f"score rel err {err.max():.3e}"
     cq = ref["cQ"][:, :, -1, :]
-    assert rel_err_rows(qco.cpu().numpy(), cq) < 1e-6
+    assert rel_err_rows(unpad_latent(qco.cpu().numpy(), c.rank, c.basis_groups), cq) < 1e-6
 
 
 @pytest.mark.parametrize("wq,kappa,pool_mode,agg", [(2, 7, "max", "mean"), (4, 5, "avg", "max"),
                                                     (1, 1, "max", "mean"), (1, 9, "avg", "mean"),
-                                                    (3, 3, "max", "max")])
+                                                    (3, 3, "max", "max"), (5, 7, "max", "mean"),
+                                                    (32, 7, "max", "mean"), (17, 9, "avg", "max")])
 def test_score_latent_variants(wq, kappa, pool_mode, agg):
     wl = W.CONFIGS["llama8b_32k"].scaled(N=3000 + 4, batch=2, topk=100, q_window=wq, pool_kernel=kappa,
                                          pool_mode=pool_mode, group_agg=agg)
@@ -184,15 +193,16 @@ def test_decode_step(case):
     idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
     scores = torch.empty((wl.batch, wl.L), dtype=torch.float32, device="cuda")
     out = s4r.decode_step(c, wl.L, g["q"], g["sink_k"], g["sink_v"], g["bases_k"], g["bases_v"], g["coef_k"],
-                          g["coef_v"], ws, idx_out=idx, scores_out=scores)
+                          g["coef_v"], ws, qwin_prev=g.get("qwin_prev"), idx_out=idx, scores_out=scores)
     torch.cuda.synchronize()
-    ref = _oracle(c, wl, st)
+    ref = _oracle(c, wl, st, qwin_prev=st.get("qwin_prev"))
     idx_np = idx.cpu().numpy().astype(np.int64)
     flips = check_selection(idx_np, ref["idx"], ref["a_tilde"], wl.L, wl.window, wl.topk)
     o_ref, _, _ = decode.sparse_attention(st["q"], idx_np, st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
                                           st["coef_k"], st["coef_v"], wl.L, wl.n_kv_heads,
                                           oracle_cfg(c)["rope_theta"])
     err = rel_err_rows(out.cpu().numpy(), o_ref)
+    print(f"[decode_step] {case}: out err {err:.2e}, tie flips {flips}", flush=True)
     assert err <= OUT_TOL[wl.dtype], f"output rel err {err:.3e} (tie flips {flips})"
     # the step's own selection is the exact top-k of its own scores
     assert np.array_equal(idx_np, decode.select(scores.cpu().numpy().astype(np.float64), wl.L, wl.window, wl.topk))
@@ -214,7 +224,12 @@ def test_fused_equals_composition(case):
     out_c = s4r.sparse_attn(c, wl.L, g["q"], g["sink_k"], g["sink_v"], idx_c, kh, vh, ws)
     torch.cuda.synchronize()
     assert torch.equal(idx_f, idx_c)
-    assert rel_err_rows(out_f.cpu().numpy(), out_c.cpu().numpy()) < 1e-4
+    # the composition reconstructs K^ / V^ in fp32; the fused bf16 kernel
+    # rounds K~ and V^ once to bf16 (the output bound for bf16 storage), the
+    # fp32 path runs the same arithmetic as the composition
+    err = rel_err_rows(out_f.cpu().numpy(), out_c.cpu().numpy())
+    print(f"[fused vs composition] {case}: {err:.2e}", flush=True)
+    assert err < (OUT_TOL["bf16"] if wl.dtype == "bf16" else 1e-4)
 
 
 def test_decode_step_deterministic():
@@ -277,7 +292,7 @@ def test_decode_step_capacity_odd_multiple_of_16():
     c = cfg_from_workload(wl)
     assert c.capacity == L and c.window == 4
     g = to_gpu_state(c, st)
-    qwin = torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    qwin = g["qwin_prev"]
     ws = s4r.alloc_workspace(c)
     m = s4r.num_selected(c, L)
     idx = torch.empty((wl.batch, m), dtype=torch.int32, device="cuda")
@@ -451,7 +466,7 @@ def test_ragged_decode_step(shape, lengths, append):
             x[b, L_b - (1 if append else 0):] = np.nan
         st_gpu[key] = x
     g = to_gpu_state(c, st_gpu)
-    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    qwin = g.get("qwin_prev")
     kw = {}
     if append:
         rng = np.random.default_rng(12)
@@ -471,8 +486,10 @@ def test_ragged_decode_step(shape, lengths, append):
     assert np.isfinite(o).all()
     idx_np = idx.cpu().numpy().astype(np.int64)
     sc = scores.cpu().numpy()
-    rows_k = s4r.unpack_coef(c, Lmax, g["coef_k"]).float().cpu().numpy().astype(np.float64)
-    rows_v = s4r.unpack_coef(c, Lmax, g["coef_v"]).float().cpu().numpy().astype(np.float64)
+    rows_k = unpad_latent(s4r.unpack_coef(c, Lmax, g["coef_k"]).float().cpu().numpy().astype(np.float64),
+                          c.rank, c.basis_groups)
+    rows_v = unpad_latent(s4r.unpack_coef(c, Lmax, g["coef_v"]).float().cpu().numpy().astype(np.float64),
+                          c.rank, c.basis_groups)
     theta = oracle_cfg(c)["rope_theta"]
     for b, L_b in enumerate(lengths):
         one = _slice_state(st, b, L_b)
@@ -581,7 +598,7 @@ def test_asymmetric_ranks(shape, dh, rank, rank_v, L, append):
         x[:, L - (1 if append else 0):] = np.nan
         st_gpu[key] = x
     g = to_gpu_state(c, st_gpu)
-    qwin = None if st["qwin_prev"] is None else torch.from_numpy(st["qwin_prev"]).to("cuda", torch.float32)
+    qwin = g.get("qwin_prev")
     kw = {}
     if append:
         rng = np.random.default_rng(L)
@@ -684,12 +701,14 @@ def test_project_queries(shape, n):
     qrows = W.round_storage(rng.standard_normal((2, n, wl.n_q_heads, wl.head_dim)), "bf16")
     qrows[:, -1] = st["q"]
     got = s4r.project_queries(c, dev(qrows, torch.bfloat16), g["bases_k"], ws)
-    qco = torch.empty((2, wl.G, wl.R), dtype=torch.float32, device="cuda")
+    Rs = s4r.rank_stride(c.rank) * c.basis_groups
+    qco = torch.empty((2, wl.G, Rs), dtype=torch.float32, device="cuda")
     s4r.score_latent(c, wl.L, g["q"], g["bases_k"], g["coef_k"], ws, qcoef=qco,
-                     qwin_prev=None if wl.q_window == 1 else torch.zeros((2, wl.G, wl.q_window - 1, wl.R),
+                     qwin_prev=None if wl.q_window == 1 else torch.zeros((2, wl.G, wl.q_window - 1, Rs),
                                                                          dtype=torch.float32, device="cuda"))
     torch.cuda.synchronize()
-    got = got.cpu().numpy().astype(np.float64)
+    got = unpad_latent(got.cpu().numpy().astype(np.float64), c.rank, c.basis_groups)
+    qco = torch.from_numpy(unpad_latent(qco.cpu().numpy(), c.rank, c.basis_groups))
     assert got.shape == (2, wl.G, n, wl.R)
     for i in range(n):
         ref = decode.project(decode.group_queries(qrows[:, i], wl.n_kv_heads), st["bases_k"])    # [B, G, R]

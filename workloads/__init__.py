@@ -98,11 +98,12 @@ class Workload:
 
 # The workloads: one tiny fp32 layer, Llama-3.1-8B-shaped layers at 32k and
 # 128k, a Qwen2.5-7B-shaped layer at 128k, the 32-layer sustained run, and
-# the paper's own efficiency setting (Section 4.2 / Appendix B.4): a
-# Qwen3-4B-shaped layer (32/8 heads, d_h = 128, D' = 1024) at a 120k context,
-# query window tied to the local window W = 4, reconstruction ratio 0.2 so
-# k = floor(0.2 L) - W, rank 192 (the paper's 204 rounded down to the
-# coefficient layout's 32-column blocks).
+# the paper's own operating points on a Qwen3-4B-shaped layer (32/8 heads,
+# d_h = 128, D' = 1024) at a 120k context with reconstruction ratio 0.2, so
+# k = floor(0.2 L) - W (Section 3.2.3), and rank 204 (Appendix B.4, the rank
+# that the memory-ratio equation gives for eta = 0.2 at D' = 1024): the
+# efficiency setting of Section 4.2 with the query window tied to the local
+# window W = W_q = 4, and the default setting of Section 4 with W = W_q = 32.
 CONFIGS = {
     "tiny_fp32": Workload("tiny_fp32", 1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64,
                           N=4096, n_sink=4, rank=32, basis_groups=2, window=64, topk=128,
@@ -125,9 +126,13 @@ CONFIGS = {
                                       r_true=128, noise=0.05, n_needles=32, outlier_channels=4,
                                       outlier_scale=8.0, layers=32, steps=256),
     "qwen3_4b_120k": Workload("qwen3_4b_120k", 6, batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
-                              N=120_004, n_sink=4, rank=192, basis_groups=1, window=4,
+                              N=120_004, n_sink=4, rank=204, basis_groups=1, window=4,
                               topk=int(0.2 * 120_000) - 4, dtype="bf16", rope_theta=1000000.0, r_true=160,
                               noise=0.05, n_needles=32, q_window=4),
+    "qwen3_4b_120k_w32": Workload("qwen3_4b_120k_w32", 7, batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                                  N=120_004, n_sink=4, rank=204, basis_groups=1, window=32,
+                                  topk=int(0.2 * 120_000) - 32, dtype="bf16", rope_theta=1000000.0, r_true=160,
+                                  noise=0.05, n_needles=32, q_window=32),
 }
 
 HEADLINE = "llama8b_128k"
