@@ -120,9 +120,11 @@ def cpu_baseline(wl, st, budget_s=10.0, one_thread=True):
         if time.perf_counter() > t_end:
             break
     per_seq = float(np.median(times))
-    sample = (f"float64 numpy oracle, sequence 0 of the {wl.name} workload (1 of {wl.batch}), "
-              f"{len(times)} runs in {sum(times):.1f} s, median per sequence x {wl.batch} sequences; "
-              f"BLAS threads {threads}")
+    src = ("one sequence of the same shape drawn on the host in latent coordinates (the oracle never reads a "
+           "GPU-built state; its time does not depend on the values)" if wl.recipe == "raw"
+           else f"sequence 0 of the {wl.name} workload (1 of {wl.batch})")
+    sample = (f"float64 numpy oracle, {src}, {len(times)} runs in {sum(times):.1f} s, median per sequence x "
+              f"{wl.batch} sequences; BLAS threads {threads}")
     res = {"value": round(per_seq * wl.batch * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
            "host_cpus": os.cpu_count(), "sample": sample}
     if not one_thread:
@@ -160,6 +162,7 @@ def copy_calibration(nbytes, reps):
 
 EXTRA_SINGLE = ("tiny_fp32", "llama8b_32k", "qwen7b_128k", "qwen3_4b_120k", "qwen3_4b_120k_w32")
 EXTRA_STEPS, EXTRA_WARMUP = 100, 10
+PREFILL_ETA = 0.2                # the paper's sampling ratio (Section 4 implementation settings)
 MALL_BYTES = 256 << 20          # MI355X Infinity Cache
 
 
@@ -213,9 +216,22 @@ def main():
     print(json.dumps(result), flush=True)
 
 
+def data_recipe(wl):
+    """How the measured inputs were drawn (seeded, synthetic)."""
+    if wl.recipe == "raw":
+        extra = (f", {wl.outlier_channels} outlier key channels x{wl.outlier_scale:g}" if wl.outlier_channels else "")
+        tail = ", Student-t (nu=3) coefficients" if wl.heavy_tail else ""
+        return (f"raw pre-RoPE K/V drawn on the GPU: low rank (true rank {wl.r_true}) + {wl.noise:g} noise{tail}"
+                f"{extra}, sinks x10, {wl.n_needles} needles at per-sequence positions; bases and coefficient caches "
+                f"by the library's GPU prefill (hybrid sample eta={PREFILL_ETA}, token-wise normalisation, "
+                f"truncated SVD, bulk projection)")
+    return ("stored state drawn in latent coordinates: per-sequence orthonormal bases (QR of a Gaussian), "
+            f"low-rank coefficient rows (true rank {wl.r_true}) + noise, sinks x10, {wl.n_needles} needles")
+
+
 def summary_entry(r):
     """The per-workload entry of the headline line's 'configs' object."""
-    keep = ("metric", "value", "unit", "steps", "warmup", "higher_is_better", "dtype", "config",
+    keep = ("metric", "value", "unit", "steps", "warmup", "higher_is_better", "dtype", "data_recipe", "config",
             "achieved_step_GBps", "step_frac_of_hbm_peak", "algorithmic_bytes_per_step", "read_ceiling_GBps",
             "kernels_us", "kernels_us_per_layer", "roofline", "reconstruction_mfma", "comparator_full_kv",
             "cpu_baseline")
@@ -237,11 +253,8 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     import paper_2608_00528_amd as s4r
     import workloads as W
 
-    log(f"[bench] generating {wl.describe()}")
+    log(f"[bench] generating {wl.describe()} ({wl.recipe} recipe)")
     t0 = time.perf_counter()
-    st = W.latent_state(wl, seed=args.seed)
-    log(f"[bench] generated in {time.perf_counter() - t0:.1f} s")
-
     cap = ((wl.L + 15) // 16) * 16
     c = s4r.make_config(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                         rank=wl.rank, basis_groups=wl.basis_groups, n_sink=wl.n_sink, window=wl.window,
@@ -252,16 +265,34 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     def up(x):
         return torch.from_numpy(np.ascontiguousarray(x)).to(device="cuda", dtype=dt)
 
-    # latent axes in the library's storage width (ranks rounded up to 32, zero columns)
-    q, sk, sv = (up(st[k]) for k in ("q", "sink_k", "sink_v"))
-    bk, bv = (up(s4r.pad_latent(st[k], wl.rank)) for k in ("bases_k", "bases_v"))
-    qwin = None if st["qwin_prev"] is None else torch.from_numpy(
-        s4r.pad_latent(st["qwin_prev"], wl.rank, wl.basis_groups)).to("cuda", torch.float32)
-    reps = []
-    for key in ("coef_k", "coef_v"):
-        rm = np.zeros((wl.batch, cap, s4r.rank_stride(wl.rank) * wl.basis_groups))
-        rm[:, :wl.L] = s4r.pad_latent(st[key], wl.rank, wl.basis_groups)
-        reps.append(s4r.pack_coef(c, cap, up(rm)))
+    if wl.recipe == "raw":
+        # raw prompt K/V of the workload's recipe (low rank, outlier key
+        # channels, sinks x10, needles) drawn on the GPU, then the prefill of
+        # Section 3.1 on the GPU: hybrid sample (eta = 0.2), token-wise
+        # normalisation, truncated SVD, bulk projection into the tiled caches
+        raw = W.raw_kv_device(wl, seed=args.seed)
+        pf = s4r.prefill(c, raw["S_k"], raw["S_v"], eta=PREFILL_ETA)
+        q, sk, sv, bk, bv = raw["q"], pf["sink_k"], pf["sink_v"], pf["bases_k"], pf["bases_v"]
+        qwin = None
+        reps = [pf["coef_k"], pf["coef_v"]]
+        del raw, pf
+        # the CPU oracle's timing sample: one sequence of the same shape drawn
+        # on the host (the oracle never reads a state built by the GPU)
+        st = W.latent_state(wl.scaled(batch=1), seed=args.seed)
+    else:
+        st = W.latent_state(wl, seed=args.seed)
+        # latent axes in the library's storage width (ranks rounded up to 32, zero columns)
+        q, sk, sv = (up(st[k]) for k in ("q", "sink_k", "sink_v"))
+        bk, bv = (up(s4r.pad_latent(st[k], wl.rank)) for k in ("bases_k", "bases_v"))
+        qwin = None if st["qwin_prev"] is None else torch.from_numpy(
+            s4r.pad_latent(st["qwin_prev"], wl.rank, wl.basis_groups)).to("cuda", torch.float32)
+        reps = []
+        for key in ("coef_k", "coef_v"):
+            rm = np.zeros((wl.batch, cap, s4r.rank_stride(wl.rank) * wl.basis_groups))
+            rm[:, :wl.L] = s4r.pad_latent(st[key], wl.rank, wl.basis_groups)
+            reps.append(s4r.pack_coef(c, cap, up(rm)))
+    torch.cuda.synchronize()
+    log(f"[bench] generated in {time.perf_counter() - t0:.1f} s")
     n_rep = replicas_for(sum(t.numel() * t.element_size() for t in reps))
     replicas = [(reps[0], reps[1])] + [(reps[0].clone(), reps[1].clone()) for _ in range(n_rep - 1)]
     ws = s4r.alloc_workspace(c)
@@ -335,6 +366,7 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "fp32",
         "data": "synthetic",
+        "data_recipe": data_recipe(wl),
         "config": {
             "workload": (f"{wl.name}: {SHAPES.get(wl.name, 'single')} layer, B={wl.batch}, N={wl.N} "
                          f"(L={wl.L} non-sink), h_q/h_kv={wl.n_q_heads}/{wl.n_kv_heads}, d_h={wl.head_dim}, "

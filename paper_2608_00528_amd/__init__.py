@@ -22,6 +22,7 @@ from .api import (  # noqa: E402,F401
     num_selected,
     pack_coef,
     pad_latent,
+    prefill,
     num_samples,
     prefill_bases,
     prefill_project,

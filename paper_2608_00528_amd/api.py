@@ -296,6 +296,29 @@ def prefill_project(cfg, n_rows, s_k, s_v, bases_k, bases_v, coef_k, coef_v, ws)
                                          _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
 
 
+def prefill(cfg, S_k, S_v, eta=0.2, center=False, ws=None):
+    """The prefill stage of Section 3.1 on the GPU for a prompt's raw pre-RoPE
+    keys / values S_k, S_v [B, N, Dp] (sinks first): the first n_sink rows
+    kept as the sinks, the bases of the non-sink rows (s4r_prefill_bases:
+    hybrid sample with ratio eta, token-wise normalisation, optional
+    centring, truncated SVD) and their bulk projection into tiled coefficient
+    caches of cfg.capacity rows (s4r_prefill_project).  Returns a dict of
+    device tensors sink_k, sink_v, bases_k, bases_v, coef_k, coef_v."""
+    s = cfg.n_sink
+    n = S_k.shape[1] - s
+    sink_k, sink_v = S_k[:, :s].contiguous(), S_v[:, :s].contiguous()
+    X_k, X_v = S_k[:, s:].contiguous(), S_v[:, s:].contiguous()
+    bases_k, bases_v = prefill_bases(cfg, n, X_k, X_v, eta=eta, center=center)
+    dt = storage_dtype(cfg)
+    coef_k = torch.zeros((cfg.batch, cfg.capacity, _R(cfg)), dtype=dt, device=S_k.device)
+    coef_v = torch.zeros((cfg.batch, cfg.capacity, _R(value_config(cfg))), dtype=dt, device=S_k.device)
+    if ws is None:
+        ws = alloc_workspace(cfg, S_k.device)
+    prefill_project(cfg, n, X_k, X_v, bases_k, bases_v, coef_k, coef_v, ws)
+    return {"sink_k": sink_k, "sink_v": sink_v, "bases_k": bases_k, "bases_v": bases_v, "coef_k": coef_k,
+            "coef_v": coef_v}
+
+
 def full_recon_decode(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, ws, out=None):
     """Comparator (Appendix B.1): attention over the sinks and every one of
     the `length` tokens reconstructed from the coefficient caches."""

@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance_wide(
   const int ntl = tile_hi - tile_lo + 1;                   // <= kWideMaxTiles
 
   __shared__ uint32_t hl[kHistBins];
-  __shared__ float fac[kWideMaxTiles * kMaxGW];            // [tile][column]
+  __shared__ __align__(16) float fac[kWideMaxTiles * kMaxGW];   // [tile][column]
   extern __shared__ float vs[];                            // [G][span]
   for (int i = t; i < kHistBins; i += kRelThreads) hl[i] = 0;
   const double2* cs = reinterpret_cast<const double2*>(col_stats) + (int64_t)b * GW;
@@ -341,7 +341,17 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance_wide(
       const float* ep = e + ((int64_t)b * cap + x) * gwp + g * Wq;
       const float* fr = fac + (x / kTileTok - tile_lo) * GW + g * Wq;
       double sum = 0.0;                            // W_q products summed in fp64
-      for (int c = 0; c < Wq; ++c) sum += (double)ep[c] * (double)fr[c];
+      if ((Wq & 3) == 0) {                         // 16-byte loads (rows of gwp, a multiple of 16, floats)
+        const float4* e4 = reinterpret_cast<const float4*>(ep);
+        const float4* f4 = reinterpret_cast<const float4*>(fr);
+        for (int c = 0; c < Wq / 4; ++c) {
+          const float4 a = e4[c], f = f4[c];
+          sum += (double)a.x * (double)f.x + (double)a.y * (double)f.y + (double)a.z * (double)f.z +
+                 (double)a.w * (double)f.w;
+        }
+      } else {
+        for (int c = 0; c < Wq; ++c) sum += (double)ep[c] * (double)fr[c];
+      }
       v = (float)(sum * inv_wq);
     }
     vs[g * span + xi] = v;

@@ -69,15 +69,31 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
     const T* __restrict__ coef_k, const double* __restrict__ qpart, const float* __restrict__ qwin_prev,
     float* __restrict__ qcoef_out, float* __restrict__ e_out, float* __restrict__ tref,
     double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int nch, int ntiles_cap, int tiles_per_wave,
-    int nwg, int gwp, double scale, Lens lens) {
+    int nwg, int gwp, int ncb, int B, double scale, Lens lens) {
   constexpr int R = RB * kBlkCol;
   constexpr int NP = BLoad<T>::kParts;
-  const int b = blockIdx.y;
+  // work item (token workgroup x of sequence b, column block cb).  One column
+  // block: grid (nwg, B).  Several: a 1-D grid in which the column blocks of
+  // one token range are 8 ids apart, so they run on one XCD (workgroup id i
+  // goes to XCD i % 8) at about the same time and share its L2 copy of the tiles
+  int xw, b, cbk;
+  if (ncb == 1) {
+    xw = blockIdx.x;
+    b = blockIdx.y;
+    cbk = 0;
+  } else {
+    const int id = blockIdx.x, rest = id >> 3;
+    const int tw = (rest / ncb) * 8 + (id & 7);
+    if (tw >= nwg * B) return;                     // padding of the last group of 8
+    cbk = rest % ncb;
+    b = tw / nwg;
+    xw = tw % nwg;
+  }
   L = (int)len_of(lens, b, L);                     // this sequence's length (ragged batch)
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int slot = lane & 15, kg = lane >> 4;      // token slot / k-group (= query column within an MFMA)
   const int GW = G * Wq;
-  const int c0 = blockIdx.z * kColBlk;             // first query column of this workgroup's block
+  const int c0 = cbk * kColBlk;                    // first query column of this workgroup's block
   const int GWl = min(GW - c0, 4 * NM);            // its columns
   const T* cb = coef_k + (int64_t)b * cap * R;
   const int ntiles = (L + 15) / 16;
@@ -85,9 +101,10 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
   // tiles in flight per wave and whether the A operands stay in registers:
   // as much as fits in 256 registers without spilling
   constexpr bool A_REG = NM * RB * NP <= 10;
-  constexpr int PF = (NP == 1) ? ((NM <= 2 && RB * (A_REG ? 1 + NM / 2 : 1) <= 6) ? 4 : (NM * RB <= 16 ? 2 : 1))
+  constexpr int PF = (NP == 1) ? ((NM <= 2 && RB * (A_REG ? 1 + NM / 2 : 1) <= 6) ? 4
+                                  : (!A_REG ? (RB <= 5 ? 4 : 2) : (NM * RB <= 16 ? 2 : 1)))
                                 : ((NM <= 2 && RB <= 3) ? 2 : 1);
-  const int tile0 = (blockIdx.x * kScoreWaves + wave) * tiles_per_wave;
+  const int tile0 = (xw * kScoreWaves + wave) * tiles_per_wave;
   const int tile1 = min(tile0 + tiles_per_wave, ntiles);
 
   // A operands: query column gi = g * Wq + i (row i of group g's window, oldest
@@ -149,7 +166,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
         qsh[m][row + 0][r] = sp.hi;
         qsh[m][row + 1][r] = sp.mid;
         qsh[m][row + 2][r] = sp.lo;
-        if (qcoef_out && blockIdx.x == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
+        if (qcoef_out && xw == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
       }
     }
     lds_barrier();                                 // the tile requested above stays in flight
@@ -164,12 +181,16 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
 #pragma unroll
       for (int kb = 0; kb < RB; ++kb) areg[m][kb].u = *reinterpret_cast<const uint4*>(&qsh[m][slot][kb * 32 + kg * 8]);
   }
+  // (re-read per tile: `aoff` is redefined by an empty asm statement in every
+  // tile iteration, so the reads are not hoisted out of the loop into
+  // NM * RB * 4 live registers)
+  int aoff = kg * 8;
   auto aop = [&](int m, int kb) -> Op8 {
     if constexpr (A_REG) {
       return areg[m][kb];
     } else {
       Op8 o;
-      o.u = *reinterpret_cast<const uint4*>(&qsh[m][slot][kb * 32 + kg * 8]);
+      o.u = *reinterpret_cast<const uint4*>(&qsh[m][slot][kb * 32 + aoff]);
       return o;
     }
   };
@@ -191,6 +212,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
       const int tile = tb + p;
+      if constexpr (!A_REG) asm volatile("" : "+v"(aoff));
       double acc[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) acc[m] = 0.0;
@@ -249,7 +271,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
       S = (M == -INFINITY ? 0.0 : S * exp(M - mn)) + wsum[w][t] * exp(mw - mn);
       M = mn;
     }
-    double* ws2 = wg_stats + (((int64_t)b * GW + col) * nwg + blockIdx.x) * 2;
+    double* ws2 = wg_stats + (((int64_t)b * GW + col) * nwg + xw) * 2;
     ws2[0] = M;
     ws2[1] = S;
   }
@@ -262,7 +284,7 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
 static int tiles_per_wave(const Problem& P, int64_t L) {
   const int64_t ntiles = (L + kTileTok - 1) / kTileTok;
   const int64_t waves = 256 * 2 * kScoreWaves;
-  const int64_t t = std::max<int64_t>(1, (P.B * ntiles + waves - 1) / waves);
+  const int64_t t = std::max<int64_t>(1, (P.B * ntiles * col_blocks(P) + waves - 1) / waves);
   return (int)((t + 3) / 4 * 4);
 }
 
@@ -277,11 +299,12 @@ static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, c
                              const float* qwin_prev, float* qcoef_out, hipStream_t st) {
   const int tpw = tiles_per_wave(P, L);
   const int nwg = score_workgroups(P, L);
+  const int ncb = col_blocks(P);
+  const dim3 grid = ncb == 1 ? dim3(nwg, P.B) : dim3(8 * ncb * ((nwg * P.B + 7) / 8));
   // the scale takes the configured latent width (storage columns past it are zero)
-  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), dim3(nwg, P.B, col_blocks(P)), dim3(256), 0, st, (const T*)coef_k,
-                     ws.qpart, qwin_prev, qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq,
-                     project_chunks(P), (int)(P.cap / kTileTok), tpw, nwg, gw_padded(P), 1.0 / sqrt((double)P.R_cfg),
-                     P.lens);
+  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), grid, dim3(256), 0, st, (const T*)coef_k, ws.qpart, qwin_prev,
+                     qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
+                     (int)(P.cap / kTileTok), tpw, nwg, gw_padded(P), ncb, P.B, 1.0 / sqrt((double)P.R_cfg), P.lens);
 }
 
 template <typename T, int RB>

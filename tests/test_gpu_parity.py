@@ -46,12 +46,43 @@ def _raw_state(wl, seed=0):
     return st
 
 
+_STATE_CACHE = {}
+
+
+def _cached(key, make):
+    """States the oracle's prefill builds (seconds each), drawn once per run
+    and shared read-only by the tests of a case."""
+    if key not in _STATE_CACHE:
+        _STATE_CACHE[key] = make()
+    return _STATE_CACHE[key]
+
+
+def _raw_hybrid_state(wl, seed=0, eta=0.2):
+    """The benchmark's recipe for its raw workloads at a size the oracle's
+    prefill handles in seconds: raw K/V (outlier key channels, heavy tails),
+    the paper's hybrid sample (eta = 0.2), no centring."""
+    raw = W.raw_kv(wl, seed=seed)
+    idx = prefill.sample_hybrid(wl.L, eta)
+    st = prefill.prefill(raw["S_k"], raw["S_v"], wl.n_sink, wl.rank, wl.basis_groups, sample_idx=idx,
+                         center=False, dtype=wl.dtype)
+    st["q"] = raw["q"]
+    return st
+
+
 CASES = {
     "tiny_fp32": lambda: _tiny_state(),
     "llama_8k_raw": lambda: (W.CONFIGS["llama8b_32k"].scaled(N=8192, batch=2, topk=256),
                              _raw_state(W.CONFIGS["llama8b_32k"].scaled(N=8192, batch=2, topk=256))),
     "qwen_8k_latent": lambda: (W.CONFIGS["qwen7b_128k"].scaled(N=8192 + 4, batch=3, topk=300),
                                W.latent_state(W.CONFIGS["qwen7b_128k"].scaled(N=8192 + 4, batch=3, topk=300), seed=2)),
+    # the benchmark's raw recipe (hybrid-sampled bases of raw K/V with outlier
+    # key channels / Student-t coefficients) at 16k context
+    "llama_8k_raw_hybrid": lambda: _cached("llama_8k_raw_hybrid", lambda: (
+        W.CONFIGS["llama8b_128k"].scaled(N=8192, batch=2, topk=384),
+        _raw_hybrid_state(W.CONFIGS["llama8b_128k"].scaled(N=8192, batch=2, topk=384)))),
+    "qwen_8k_raw_hybrid": lambda: _cached("qwen_8k_raw_hybrid", lambda: (
+        W.CONFIGS["qwen7b_128k"].scaled(N=8192, batch=2, topk=256),
+        _raw_hybrid_state(W.CONFIGS["qwen7b_128k"].scaled(N=8192, batch=2, topk=256), seed=1))),
     # the paper's default operating point at a short context: W = W_q = 32
     # (G * W_q = 128 query columns in 8 scoring blocks), rank 204 stored in 224
     "qwen3_w32_5k": lambda: (W.CONFIGS["qwen3_4b_120k_w32"].scaled(N=5000 + 4, batch=2, topk=968),
@@ -715,3 +746,59 @@ def test_project_queries(shape, n):
         err = np.abs(got[:, :, i] - ref).max() / np.abs(ref).max()
         assert err <= 2e-7, f"row {i}: rel err {err:.2e}"
     assert np.array_equal(got[:, :, -1], qco.cpu().numpy().astype(np.float64))
+
+
+def _rounding_ties_only(got, ref_rounded, ref_exact, dtype):
+    """Elements where the GPU's stored value differs from the oracle's rounded
+    one must be ones whose exact (float64) value lies within float64 noise of
+    a rounding midpoint of the storage format (the two sides sum in different
+    orders); returns the number of such elements."""
+    diff = got != ref_rounded
+    if not diff.any():
+        return 0
+    ulp_bits = 7 if dtype == "bf16" else 23
+    x = ref_exact[diff]
+    e = np.floor(np.log2(np.maximum(np.abs(x), 1e-300)))
+    half = 2.0 ** (e - ulp_bits - 1)
+    r = np.abs(x) / half
+    gap = np.abs(r - np.round(r)) * half                     # distance to the nearest half-ulp grid point
+    assert np.all(gap <= 1e-12 * np.abs(x)), f"append differs beyond rounding ties: {gap.max():.3e}"
+    return int(diff.sum())
+
+
+@pytest.mark.parametrize("dtype,rank,rank_v,row", [("bf16", 160, 0, 37), ("fp32", 64, 0, 1000),
+                                                   ("bf16", 128, 192, 511), ("bf16", 204, 0, 0)])
+def test_project_append_standalone(dtype, rank, rank_v, row):
+    """s4r_project_append (Section 3.2.1's cache update) on its own: the new
+    token's key / value coefficient rows land in row `row` of the tiled caches,
+    equal to the oracle's projection rounded once to the storage format (up to
+    a rounding tie of the different summation order); every other row keeps
+    its bits; padding columns of a rank that is not a multiple of 32 are zero."""
+    B, cap = 3, 1024
+    wl = W.CONFIGS["llama8b_32k"].scaled(N=cap + 4, batch=B, rank=rank, rank_v=rank_v, dtype=dtype, topk=64)
+    st = W.latent_state(wl, seed=21, capacity=cap, L=cap)
+    c = cfg_from_workload(wl, capacity=cap)
+    g = to_gpu_state(c, st)
+    rng = np.random.default_rng(22)
+    kn = W.round_storage(rng.standard_normal((B, wl.Dp)), dtype)
+    vn = W.round_storage(rng.standard_normal((B, wl.Dp)), dtype)
+    dt = s4r.storage_dtype(c)
+    cvc = s4r.value_config(c)
+    before_k = s4r.unpack_coef(c, cap, g["coef_k"]).cpu()
+    before_v = s4r.unpack_coef(cvc, cap, g["coef_v"]).cpu()
+    s4r.project_append(c, row, dev(kn, dt), dev(vn, dt), g["bases_k"], g["bases_v"], g["coef_k"], g["coef_v"])
+    after_k = s4r.unpack_coef(c, cap, g["coef_k"]).cpu()
+    after_v = s4r.unpack_coef(cvc, cap, g["coef_v"]).cpu()
+    torch.cuda.synchronize()
+    others = torch.ones(cap, dtype=torch.bool)
+    others[row] = False
+    assert torch.equal(after_k[:, others], before_k[:, others])
+    assert torch.equal(after_v[:, others], before_v[:, others])
+    ck, cv = decode.project_append(kn, vn, st["bases_k"], st["bases_v"], dtype)
+    ck_x = decode.project(kn[:, None, :], st["bases_k"])[:, 0]
+    cv_x = decode.project(vn[:, None, :], st["bases_v"])[:, 0]
+    got_k = unpad_latent(after_k[:, row].double().numpy(), rank, c.basis_groups)
+    got_v = unpad_latent(after_v[:, row].double().numpy(), rank_v or rank, c.basis_groups)
+    nk = _rounding_ties_only(got_k, ck, ck_x, dtype)
+    nv = _rounding_ties_only(got_v, cv, cv_x, dtype)
+    print(f"[project_append] {dtype} rank {rank}/{rank_v or rank} row {row}: rounding ties {nk}, {nv}", flush=True)

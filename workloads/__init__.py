@@ -62,6 +62,8 @@ class Workload:
     layers: int = 1
     steps: int = 1
     rank_v: int = 0          # value rank per basis group (Appendix D.2); 0 = rank
+    recipe: str = "latent"   # how the benchmark draws the stored state: "latent" (latent_state) or
+                             # "raw" (raw_kv_device, then the GPU prefill turns it into bases and caches)
 
     @property
     def G(self):
@@ -111,15 +113,15 @@ CONFIGS = {
     "llama8b_32k": Workload("llama8b_32k", 2, batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
                             N=32768, n_sink=4, rank=160, basis_groups=1, window=64, topk=1024,
                             dtype="bf16", rope_theta=500000.0, r_true=128, noise=0.05,
-                            n_needles=32, outlier_channels=4, outlier_scale=8.0),
+                            n_needles=32, outlier_channels=4, outlier_scale=8.0, recipe="raw"),
     "llama8b_128k": Workload("llama8b_128k", 3, batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
                              N=131072, n_sink=4, rank=160, basis_groups=1, window=128, topk=2048,
                              dtype="bf16", rope_theta=500000.0, r_true=128, noise=0.05,
-                             n_needles=32, outlier_channels=4, outlier_scale=8.0),
+                             n_needles=32, outlier_channels=4, outlier_scale=8.0, recipe="raw"),
     "qwen7b_128k": Workload("qwen7b_128k", 4, batch=8, n_q_heads=28, n_kv_heads=4, head_dim=128,
                             N=131072, n_sink=4, rank=96, basis_groups=1, window=64, topk=1024,
                             dtype="bf16", rope_theta=1000000.0, r_true=80, noise=0.1,
-                            n_needles=32, heavy_tail=True),
+                            n_needles=32, heavy_tail=True, recipe="raw"),
     "llama8b_32L_sustained": Workload("llama8b_32L_sustained", 5, batch=32, n_q_heads=32, n_kv_heads=8,
                                       head_dim=128, N=32768, n_sink=4, rank=160, basis_groups=1,
                                       window=64, topk=1024, dtype="bf16", rope_theta=500000.0,
@@ -383,6 +385,69 @@ def sustained_layer(wl, seed, layer, L0, capacity, steps, device="cuda"):
     out["k_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
     out["v_new"] = torch.randn((steps, B, Dp), generator=gd, device=device).to(dt)
     return out
+
+
+def _student_t3(shape, gen, device):
+    """Student-t samples with 3 degrees of freedom, scaled to unit variance:
+    a Gaussian over the root of a chi-square(3) / 3 (three squared Gaussians)."""
+    z = torch.randn(shape, generator=gen, device=device)
+    chi = torch.randn((3,) + tuple(shape), generator=gen, device=device).pow(2).sum(0)
+    return z / torch.sqrt(chi / 3.0) / np.sqrt(3.0)
+
+
+def raw_kv_device(wl, seed=0, layer=0, device="cuda"):
+    """The raw_kv recipe drawn on `device` with torch's generator (for the
+    full-size workloads, whose float64 host copies would take gigabytes):
+    raw pre-RoPE keys / values [B, N, Dp] = F P / sqrt(r_true) + noise * E
+    with F Gaussian (Student-t nu = 3 when heavy_tail), `outlier_channels` key
+    channels scaled by `outlier_scale`, sinks x10, and the group queries 0.9 of
+    a direction in P's row space plus 0.1 noise, scaled for latent logits of
+    standard deviation about 1.5; needle keys at seeded positions in
+    [0, L - W) get the kv-head slices of the mean group-query direction added.
+    Everything is rounded once to the storage dtype.  Returns a dict of device
+    tensors S_k, S_v [B, N, Dp], q [B, h_q, d_h] and needles (host arrays)."""
+    B, N, Dp = wl.batch, wl.N, wl.Dp
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    S_k = torch.empty((B, N, Dp), dtype=dt, device=device)
+    S_v = torch.empty((B, N, Dp), dtype=dt, device=device)
+    qg = torch.empty((B, wl.G, Dp), dtype=torch.float32, device=device)
+    needles = []
+    g = torch.Generator(device=device)
+    for b in range(B):
+        g.manual_seed(_torch_seed(wl, seed, layer, 1000 * b + _T_KEY))
+        Pk = torch.randn((wl.r_true, Dp), generator=g, device=device) / np.sqrt(wl.r_true)
+        Pv = torch.randn((wl.r_true, Dp), generator=g, device=device) / np.sqrt(wl.r_true)
+        sig = (lambda n: _student_t3((n, wl.r_true), g, device)) if wl.heavy_tail else \
+            (lambda n: torch.randn((n, wl.r_true), generator=g, device=device))
+        sk = torch.mm(sig(N), Pk) + wl.noise * torch.randn((N, Dp), generator=g, device=device)
+        sv = torch.mm(sig(N), Pv) + wl.noise * torch.randn((N, Dp), generator=g, device=device)
+        if wl.outlier_channels:
+            ch = torch.randperm(Dp, generator=g, device=device)[:wl.outlier_channels]
+            sk[:, ch] *= wl.outlier_scale
+        sk[:wl.n_sink] *= 10.0
+        sv[:wl.n_sink] *= 10.0
+        sq = torch.mm(torch.randn((wl.G, wl.r_true), generator=g, device=device), Pk)
+        sq /= sq.norm(dim=-1, keepdim=True)
+        nq = torch.randn((wl.G, Dp), generator=g, device=device)
+        nq /= nq.norm(dim=-1, keepdim=True)
+        qdir = 0.9 * sq + 0.1 * nq
+        qdir /= qdir.norm(dim=-1, keepdim=True)
+        qnorm = 1.5 * np.sqrt(wl.R) / (float(sk[wl.n_sink:].norm(dim=-1).mean()) / np.sqrt(wl.r_true))
+        qg[b] = qdir * qnorm
+        hi = max(wl.L - wl.window, 1)
+        count = min(wl.n_needles, hi)
+        pos = torch.sort(torch.randperm(hi, generator=g, device=device)[:count]).values
+        lift = (10.0 + 4.0 * torch.rand((count,), generator=g, device=device)) * (np.sqrt(wl.R) / qnorm)
+        mean_dir = qdir.mean(dim=0)
+        md = mean_dir / torch.clamp(mean_dir.norm(), min=1e-12)
+        sk[wl.n_sink + pos] += lift[:, None] * md[None, :]
+        needles.append(pos.cpu().numpy())
+        S_k[b] = sk.to(dt)
+        S_v[b] = sv.to(dt)
+        del sk, sv
+    q = (qg.reshape(B, wl.G, wl.n_kv_heads, wl.head_dim).transpose(1, 2)
+         .reshape(B, wl.n_q_heads, wl.head_dim).to(dt).contiguous())
+    return {"S_k": S_k, "S_v": S_v, "q": q, "needles": needles}
 
 
 def dense_cache(wl, seed=0, device="cuda", n_tokens=None):
