@@ -330,8 +330,9 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
         result_extra = step_distribution_graph_ceiling(s4r, step, out, replicas, n_rep, steps)
     comparator = None
     if comparators and wl.dtype == "bf16" and wl.head_dim == 128:
+        # the prefill's bulk projection is built for ranks up to 192
         comparator = run_comparators(s4r, W, args, wl, c, q, sk, sv, bk, bv, replicas[0], ws, out, ms_step,
-                                     prefill=full)
+                                     prefill=full and s4r.rank_stride(wl.rank) <= 192)
 
     # per-kernel pass (events between kernels), same steps again
     nk = min(steps, 200)

@@ -11,8 +11,8 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 // K2: relevance A~ and its radix histogram
 // ---------------------------------------------------------------------------
-// grid (ceil(L / chunk), B), 256 threads; chunk = 1024 / 512 / 256 tokens for
-// G <= 4 / 8 / 16.  The stream's exp values are stored token-major,
+// grid (ceil(L / chunk), B), 256 threads; chunk = 1024 / 512 tokens for
+// G <= 8 / 16.  The stream's exp values are stored token-major,
 // e[b][x][c] for query column c = g * W_q + i (GWP = G * W_q rounded up to a
 // multiple of 4, padding columns zero), with one reference per 16-token tile,
 // tref[b][tile][c].  One memory latency: the scoring workgroups' statistics,
@@ -32,10 +32,13 @@ constexpr int kRelThreads = 256;
 constexpr int kRelStatPer = 2;   // scoring-workgroup statistics per lane folded inside the relevance kernel
 constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk and its halo (h <= 32)
 
-// tokens per workgroup: 1024 (G <= 4), 512 (G <= 8) or 256, halved while the
-// grid would give fewer than two workgroups per CU (small batches)
+// tokens per workgroup: 1024 (G <= 8) or 512, halved while the grid would give
+// fewer than two workgroups per CU (small batches).  Every workgroup flushes
+// its histogram with one global atomic per non-empty bin, so fewer, larger
+// chunks cost fewer atomics (Qwen2.5 shape, B = 8 at 128k: 2048 -> 1024
+// workgroups)
 int relevance_chunk(const Problem& P, int64_t L) {
-  int c = P.G <= 4 ? 1024 : (P.G <= 8 ? 512 : 256);
+  int c = P.G <= 8 ? 1024 : 512;
   while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < 512) c >>= 1;
   return c;
 }
