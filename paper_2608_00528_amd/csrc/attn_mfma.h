@@ -129,7 +129,6 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) v
   __shared__ __align__(16) uint16_t gkB[2][RBH][512], gvB[2][RBV][512];
   __shared__ int32_t sidx[kTileMax * 16];
   __shared__ float xl[2][NW][NMH][4][16];                // partial logits [tile of pair][wave][mh][head][slot]
-  __shared__ __align__(16) uint16_t ps[2][NMH][4][2][16]; // P parts [tile of pair][mh][head][hi|lo][slot]
 
   // ---- 1. index list, bases and query requested; then the first two pairs' gathers ---------
   int32_t xi[kTileMax * 16 / (NW * 64)];
@@ -318,6 +317,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) v
         sl[u][mh] = valid ? s * inv_sqrt_d : -INFINITY;
       }
     // online softmax of (token slot, head 4 mh + kg); the 16 slots share the maximum
+    uint32_t phi[NMH], plo[NMH];
 #pragma unroll
     for (int mh = 0; mh < NMH; ++mh) {
       const float pmax = slot_max16(fmaxf(sl[0][mh], sl[1][mh]));
@@ -328,20 +328,22 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) v
         oacc[mh][1] *= alpha;
         Mrun[mh] = pmax;
       }
+      float pr[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const float pr = (sl[u][mh] == -INFINITY) ? 0.f : __expf(sl[u][mh] - Mrun[mh]);
-        lrun[mh] += pr;
-        if (w == 0) {                              // one wave stages P for all
-          const uint32_t ph = pack_bf16x2(pr, 0.f);
-          ps[u][mh][kg][0][slot] = (uint16_t)ph;
-          ps[u][mh][kg][1][slot] = (uint16_t)pack_bf16x2(pr - __uint_as_float(ph << 16), 0.f);
-        }
+        pr[u] = (sl[u][mh] == -INFINITY) ? 0.f : __expf(sl[u][mh] - Mrun[mh]);
+        lrun[mh] += pr[u];
       }
+      // P's hi / lo bf16 parts of both tiles, packed (tile 0 low half, tile 1 high half)
+      const uint32_t h01 = pack_bf16x2(pr[0], pr[1]);
+      phi[mh] = h01;
+      plo[mh] = pack_bf16x2(pr[0] - __uint_as_float(h01 << 16), pr[1] - __uint_as_float(h01 & 0xFFFF0000u));
     }
-    lds_barrier();                                 // P staged
     // P V^: A = P parts (row 4 h + part, k = tokens 4 kg + v of both tiles), B = V^
-    // rounded to bf16
+    // rounded to bf16.  Every wave builds its own A operand from the softmax
+    // lanes with lane permutes (lane (row 4 h + part, k-group c) takes the part
+    // of token 4 c + v, head h from lane (4 c + v) + 16 h), so P never goes
+    // through LDS and needs no barrier
     Op8 vb16[2];
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
@@ -349,17 +351,20 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) v
                           dv[1][m][0], dv[1][m][1], dv[1][m][2], dv[1][m][3]};
       round_f32x8(x, vb16[m]);
     }
+    const int hh = slot >> 2, part = slot & 3;
 #pragma unroll
     for (int mh = 0; mh < NMH; ++mh) {
-      const int hh = slot >> 2, part = slot & 3;
-      Op8 ap;
-      if (part < 2) {
-        const uint2 a0 = *reinterpret_cast<const uint2*>(&ps[0][mh][hh][part][4 * kg]);
-        const uint2 a1 = *reinterpret_cast<const uint2*>(&ps[1][mh][hh][part][4 * kg]);
-        ap.u = make_uint4(a0.x, a0.y, a1.x, a1.y);
-      } else {
-        ap.u = make_uint4(0, 0, 0, 0);
+      uint32_t r[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int src = ((4 * kg + v) + 16 * hh) << 2;
+        const uint32_t rh = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)phi[mh]);
+        const uint32_t rl = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)plo[mh]);
+        r[v] = part == 0 ? rh : (part == 1 ? rl : 0u);
       }
+      Op8 ap;
+      ap.u = make_uint4((r[0] & 0xFFFFu) | (r[1] << 16), (r[2] & 0xFFFFu) | (r[3] << 16),
+                        (r[0] >> 16) | (r[1] & 0xFFFF0000u), (r[2] >> 16) | (r[3] & 0xFFFF0000u));
 #pragma unroll
       for (int m = 0; m < 2; ++m) oacc[mh][m] = mfma16x16x32(ap, vb16[m], oacc[mh][m]);
     }

@@ -17,6 +17,7 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 constexpr int kPRows = 4;                     // basis rows per thread
 constexpr int kPVec = 4;                      // vectors accumulated per pass
+constexpr int kRowPre = 4;                    // 256-row chunks of a new row's projection loaded together
 
 // 8 consecutive basis elements, kept in their storage format until used
 struct Raw8bf16 {
@@ -198,7 +199,7 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
   const T* x_new = which == 0 ? k_new : v_new;
   T* coef = which == 0 ? coef_k : coef_v;
 
-  __shared__ float xs[1][kPChunk];
+  __shared__ float xs[kRowPre][kPChunk];
   __shared__ double red[4][kPVec][32];
   const T* bases = (which == 0 ? bases_k : bases_v) + (bases_shared ? 0 : (int64_t)b * Dp * rank) +
                    (int64_t)grp * Dg * rank + (c0 - grp * rank) + cg * 8;
@@ -207,16 +208,30 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
   for (int v = 0; v < kPVec; ++v)
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[v][c] = 0.0;
-  for (int r0 = 0; r0 < Dg; r0 += kPChunk) {
-    const int nrow = min(kPChunk, Dg - r0);
-    typename Raw8<T>::type bw[kPRows];
+  // kRowPre chunks of 256 rows at a time: every basis row and vector element
+  // of the group is requested before any is used (one memory latency for a
+  // basis group of up to 1024 rows), then the chunks are summed in order
+  for (int r00 = 0; r00 < Dg; r00 += kRowPre * kPChunk) {
+    typename Raw8<T>::type bw[kRowPre][kPRows];
+    float x[kRowPre];
 #pragma unroll
-    for (int i = 0; i < kPRows; ++i) bw[i].load(bases + (int64_t)(r0 + min(rg + 64 * i, nrow - 1)) * rank);
-    const float x = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r0 + min(t, nrow - 1));
-    if (r0 > 0) __syncthreads();                  // previous chunk's xs reads are done
-    xs[0][t] = (t < nrow) ? x : 0.f;
+    for (int ci = 0; ci < kRowPre; ++ci) {
+      const int r0 = min(r00 + ci * kPChunk, Dg - 1);   // past the group's end: a re-read, never summed
+      const int nrow = min(kPChunk, Dg - r0);
+#pragma unroll
+      for (int i = 0; i < kPRows; ++i) bw[ci][i].load(bases + (int64_t)(r0 + min(rg + 64 * i, nrow - 1)) * rank);
+      x[ci] = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r0 + min(t, nrow - 1));
+    }
+    if (r00 > 0) __syncthreads();                 // previous group's xs reads are done
+#pragma unroll
+    for (int ci = 0; ci < kRowPre; ++ci) {
+      const int r0 = r00 + ci * kPChunk;
+      xs[ci][t] = (r0 + t < Dg) ? x[ci] : 0.f;
+    }
     __syncthreads();
-    accumulate_rows<1>(bw, xs, rg, acc);
+#pragma unroll
+    for (int ci = 0; ci < kRowPre; ++ci)
+      if (r00 + ci * kPChunk < Dg) accumulate_rows<1>(bw[ci], &xs[ci], rg, acc);
   }
   reduce_rows<1>(acc, red, wave, lane, cg);
   __syncthreads();

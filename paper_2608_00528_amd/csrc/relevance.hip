@@ -37,9 +37,12 @@ constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk 
 // its histogram with one global atomic per non-empty bin, so fewer, larger
 // chunks cost fewer atomics (Qwen2.5 shape, B = 8 at 128k: 2048 -> 1024
 // workgroups)
+#ifndef S4R_REL_MIN_WG
+#define S4R_REL_MIN_WG 512
+#endif
 int relevance_chunk(const Problem& P, int64_t L) {
   int c = P.G <= 8 ? 1024 : 512;
-  while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < 512) c >>= 1;
+  while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < S4R_REL_MIN_WG) c >>= 1;
   return c;
 }
 
