@@ -135,7 +135,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t elem_size(const Problem& P) { return P.dtype == S4R_BF16 ? 2 : 4; }
 
 enum Region {
-  kQpart, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits,
+  kQimg, kQcoef, kE, kRunM, kWgStats, kAtilde, kHist, kCand, kBitmap, kIdx, kPartMl, kPartO, kAttnLogits,
   kCandCount, kAboveCount, kSelInfo, kColStats, kRegions
 };
 struct Layout {
@@ -146,7 +146,8 @@ struct Layout {
 Layout layout(const Problem& P) {
   const size_t B = P.B, GW = P.GW, cap = P.cap;
   size_t sizes[kRegions];
-  sizes[kQpart] = B * project_chunks(P) * P.G * P.R * 8;
+  sizes[kQimg] = B * col_blocks(P) * qimg_mfmas(P) * 16 * (size_t)P.R * 2;
+  sizes[kQcoef] = B * P.G * (size_t)P.R * 4;
   sizes[kE] = B * (size_t)gw_padded(P) * cap * 4;
   sizes[kRunM] = B * (size_t)gw_padded(P) * P.nruns_max * 4;
   sizes[kWgStats] = B * GW * P.nwg_max * 2 * 8;
@@ -261,7 +262,8 @@ Workspace carve_workspace(const Problem& P, void* base) {
   const Layout l = layout(P);
   char* b = (char*)base;
   Workspace w;
-  w.qpart = (double*)(b + l.off[kQpart]);
+  w.qimg = (uint16_t*)(b + l.off[kQimg]);
+  w.qcoef = (float*)(b + l.off[kQcoef]);
   w.e = (float*)(b + l.off[kE]);
   w.run_m = (float*)(b + l.off[kRunM]);
   w.wg_stats = (double*)(b + l.off[kWgStats]);
@@ -327,8 +329,8 @@ s4r_status s4r_score_latent(const s4r_config* cfg, int64_t L, const void* q, con
   else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
   if ((st = check_ws(P, ws, ws_bytes))) return st;
   Workspace w = carve_workspace(P, ws);
-  hipError_t e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
-  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, qcoef_out, stream);
+  hipError_t e = launch_project_query(P, w, q, bases_k, qwin_prev, qcoef_out, true, stream);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores, stream);
   return hip_status(e, "s4r_score_latent launch");
 }
@@ -594,12 +596,12 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
   };
   hipError_t e = mark(hipSuccess, 0, true);
   if (e == hipSuccess && k_new)   // the new token's rows with the query coefficients: the scoring pass reads row L - 1
-    e = launch_project_step(P, w.qpart, w.hist, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, L - 1, stream);
+    e = launch_project_step(P, w, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, L - 1, stream);
   else if (e == hipSuccess)
-    e = launch_project_query(P, w.qpart, w.hist, q, bases_k, stream);
+    e = launch_project_query(P, w, q, bases_k, qwin_prev, nullptr, true, stream);
   e = mark(e, 0, false);
   e = mark(e, 1, true);
-  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, qwin_prev, nullptr, stream);
+  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
   e = mark(e, 1, false);
   e = mark(e, 2, true);
   if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);

@@ -7,17 +7,21 @@
 namespace s4r {
 
 // ---------------------------------------------------------------------------
-// Both kernels: 256 threads = 4 column groups of 8 latent columns x 64 row
-// groups; a workgroup owns 32 latent columns of one basis group.  A thread
-// holds 4 basis rows (rg + 64 i) of its 8 columns in registers, in storage
-// format; the projected vectors are staged in LDS as fp32 (their exact
-// values).  Products are accumulated in fp64 and reduced over the 64 row
-// groups (DPP within 16-lane rows, shuffles across rows, then the 4 waves
-// through LDS) in a fixed order, so results are deterministic.
+// Both projections are short dot products (a basis group of up to 2048 rows)
+// for few vectors, so they are latency-bound: the work is spread over many
+// small workgroups, each thread's operands are requested together, and the
+// reduction is short.  A workgroup owns 8 latent columns of one basis group;
+// thread t holds basis rows t + 256 i (i < NCH, the group's 256-row chunks
+// rounded up to a power of two) of its 8 columns in registers, in storage
+// format, and the projected vectors' elements of the same rows, read straight
+// from memory (no staging).  Products are accumulated in fp64 (exact: a
+// bf16 or fp32 basis element times an fp32 vector element) per thread in row
+// order, then summed over the wave's 64 lanes (two gfx950 lane swaps that
+// halve the values per lane, then DPP within 16-lane rows) and over the 4
+// waves through LDS, in a fixed order, so the results are deterministic.
 // ---------------------------------------------------------------------------
-constexpr int kPRows = 4;                     // basis rows per thread
-constexpr int kPVec = 4;                      // vectors accumulated per pass
-constexpr int kRowPre = 4;                    // 256-row chunks of a new row's projection loaded together
+constexpr int kPCols = 8;                     // latent columns per workgroup
+constexpr int kQVec = 4;                      // query vectors per pass
 
 // 8 consecutive basis elements, kept in their storage format until used
 struct Raw8bf16 {
@@ -51,197 +55,231 @@ struct Raw8<float> {
   using type = Raw8f32;
 };
 
-// fp64 move within 16-lane rows (row_ror)
+// fp64 move within 16-lane rows (DPP)
 template <int CTRL>
 __device__ __forceinline__ double dpp_move_d(double x) {
   const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xF, 0xF, false);
   const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xF, 0xF, false);
   return __hiloint2double(hi, lo);
 }
-// sum over the 16 lanes of a wave that share (lane & 3)
-__device__ __forceinline__ double wave_sum16(double a) {
-  a += dpp_move_d<0x124>(a);   // row_ror:4
-  a += dpp_move_d<0x128>(a);   // row_ror:8
-  a += shfl_xor_d(a, 16);
-  a += shfl_xor_d(a, 32);
-  return a;
+
+// x + y after the gfx950 lane swaps: permlane32_swap exchanges lanes 32..63 of
+// its first operand with lanes 0..31 of its second, permlane16_swap the odd
+// 16-lane rows of the first with the even rows of the second (each dword of
+// the fp64 values the same way).  Afterwards the lower half (even rows) holds
+// the first operand summed over the lane pair, the upper half (odd rows) the
+// second.
+__device__ __forceinline__ double swap32_add(double x, double y) {
+  const auto lo = __builtin_amdgcn_permlane32_swap((unsigned)__double2loint(x), (unsigned)__double2loint(y), false,
+                                                   false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)__double2hiint(x), (unsigned)__double2hiint(y), false,
+                                                   false);
+  return __hiloint2double((int)hi[0], (int)lo[0]) + __hiloint2double((int)hi[1], (int)lo[1]);
+}
+__device__ __forceinline__ double swap16_add(double x, double y) {
+  const auto lo = __builtin_amdgcn_permlane16_swap((unsigned)__double2loint(x), (unsigned)__double2loint(y), false,
+                                                   false);
+  const auto hi = __builtin_amdgcn_permlane16_swap((unsigned)__double2hiint(x), (unsigned)__double2hiint(y), false,
+                                                   false);
+  return __hiloint2double((int)hi[0], (int)lo[0]) + __hiloint2double((int)hi[1], (int)lo[1]);
 }
 
-template <int NV, typename RawT>
-__device__ __forceinline__ void accumulate_rows(const RawT (&bw)[kPRows], const float (*xs)[kPChunk], int rg,
-                                                double (&acc)[kPVec][8]) {
+// sums of a[0..N) over the 64 lanes of a wave, written to red[wave][0..N):
+// the lane swaps leave row r (lanes 16 r .. 16 r + 15) with values
+// r N / 4 .. + N / 4 - 1 summed over the four rows, DPP sums them within the
+// row (row_ror 8 and 4, then the quad swaps), and lane 16 r writes them
+template <int N>
+__device__ __forceinline__ void reduce_wave(double (&a)[N], double (*red)[32], int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < kPRows; ++i) {
-    const int r = rg + 64 * i;
-    double xv[NV];
+  for (int j = 0; j < N / 2; ++j) a[j] = swap32_add(a[j], a[j + N / 2]);
 #pragma unroll
-    for (int v = 0; v < NV; ++v) xv[v] = (double)xs[v][r];
+  for (int j = 0; j < N / 4; ++j) a[j] = swap16_add(a[j], a[j + N / 4]);
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const double bc = (double)bw[i][c];
+  for (int j = 0; j < N / 4; ++j) {
+    a[j] += dpp_move_d<0x128>(a[j]);   // row_ror:8
+    a[j] += dpp_move_d<0x124>(a[j]);   // row_ror:4
+    a[j] += dpp_move_d<0x4E>(a[j]);    // quad_perm [2,3,0,1]
+    a[j] += dpp_move_d<0xB1>(a[j]);    // quad_perm [1,0,3,2]
+  }
+  if ((lane & 15) == 0) {
 #pragma unroll
-      for (int v = 0; v < NV; ++v) acc[v][c] = fma(xv[v], bc, acc[v][c]);
-    }
+    for (int j = 0; j < N / 4; ++j) red[wave][(lane >> 4) * (N / 4) + j] = a[j];
   }
 }
 
-// per-thread sums (NV vectors x 8 columns) -> per-wave sums in red[wave][v][32]
-template <int NV>
-__device__ __forceinline__ void reduce_rows(double (&acc)[kPVec][8], double (*red)[kPVec][32], int wave, int lane,
-                                            int cg) {
-#pragma unroll
-  for (int v = 0; v < NV; ++v)
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[v][c] = wave_sum16(acc[v][c]);
-  if (lane < 4) {
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-#pragma unroll
-      for (int c = 0; c < 8; ++c) red[wave][v][cg * 8 + c] = acc[v][c];
-  }
+// image address of query column gi, latent column col (part 0; part q is R further)
+__device__ __forceinline__ uint16_t* qimg_at(uint16_t* qimg, int b, int ncb, int nmb, int R, int gi, int col) {
+  const int cb = gi / kColBlk, gl = gi % kColBlk;
+  return qimg + ((((int64_t)b * ncb + cb) * nmb + (gl >> 2)) * 16 + 4 * (gl & 3)) * R + col;
+}
+
+// four consecutive latent columns' parts, packed per part (4 bf16 in 8 bytes)
+__device__ __forceinline__ void qimg_pack4(float4 x, uint2 (&pk)[3]) {
+  const Split3 s0 = split3((double)x.x), s1 = split3((double)x.y), s2 = split3((double)x.z),
+               s3 = split3((double)x.w);
+  pk[0] = make_uint2(s0.hi | ((uint32_t)s1.hi << 16), s2.hi | ((uint32_t)s3.hi << 16));
+  pk[1] = make_uint2(s0.mid | ((uint32_t)s1.mid << 16), s2.mid | ((uint32_t)s3.mid << 16));
+  pk[2] = make_uint2(s0.lo | ((uint32_t)s1.lo << 16), s2.lo | ((uint32_t)s3.lo << 16));
 }
 
 // ---------------------------------------------------------------------------
-// query coefficients: grid (R / 32, ceil(Dg / 256) row chunks, B).  Each
-// workgroup writes the partial sums of its 256-row chunk for all G query
-// groups to qpart [B][chunks][G][R] (fp64); the scoring kernel adds the
-// chunks in a fixed order.  Splitting the rows over workgroups keeps every
-// thread's work to one load round trip and a short fp64 dot product.
+// query coefficients: grid (R / 8, B).  A workgroup forms, for its 8 latent
+// columns and every query group g, c^Q[g] = q_g B^K over all rows of the
+// basis group (kQVec groups per pass), and writes it (1) rounded to fp32 into
+// qcoef [B][G][R] (and the caller's qcoef_out), (2) as the hi / mid / lo bf16
+// parts the scoring kernel's MFMA A operand holds, into the operand image
+// qimg [B][column blocks][NMB][16][R] (query column gi = g W_q + i in block
+// gi / 16, MFMA (gi % 16) / 4, rows 4 (gi % 4) + part), together with the
+// window's older rows from qwin_prev when given.  The image's other rows are
+// never read.
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, int NCH>
 __device__ __forceinline__ void project_query_body(const T* __restrict__ q, const T* __restrict__ bases_k,
-                                                   double* __restrict__ qpart, uint32_t* __restrict__ hist, int hq,
-                                                   int hkv, int dh, int G, int nb, int rank, int R, int bases_shared,
-                                                   int cblk, int ch, int b, int nch) {
+                                                   const float* __restrict__ qwin_prev, uint16_t* __restrict__ qimg,
+                                                   float* __restrict__ qcoef, float* __restrict__ qcoef_out,
+                                                   uint32_t* __restrict__ hist, int hq, int hkv, int dh, int G,
+                                                   int Wq, int nb, int rank, int R, int bases_shared, int ncb,
+                                                   int nmb, int cblk, int b) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int cg = t & 3, rg = t >> 2;
   const int Dp = hkv * dh, Dg = Dp / nb;
   const int ldh = __builtin_ctz(dh);              // head_dim is a power of two
-  const int c0 = cblk * 32;                       // first latent column of the block
+  const int c0 = cblk * kPCols;                   // first latent column of the block
   const int grp = c0 / rank;                      // its basis group
-  const int r0 = ch * kPChunk;                    // first row of the chunk in the group
-  const int nrow = min(kPChunk, Dg - r0);
+  // the window's older query rows (oldest first): unit t is latent columns
+  // c0 + 4 (t % 2) .. + 3 of older row j = t / 2, i.e. group j / (W_q - 1),
+  // window row j % (W_q - 1) (G (W_q - 1) <= 127 rows, so one unit per
+  // thread).  Requested first, written last.
+  const bool old_rows = qimg && qwin_prev && Wq > 1;
+  const int n_old = old_rows ? G * (Wq - 1) : 0;
+  const int jo = min(t >> 1, max(n_old - 1, 0));
+  const int go = n_old ? jo / (Wq - 1) : 0, wo = n_old ? jo - go * (Wq - 1) : 0;
+  const int oc = c0 + 4 * (t & 1);
+  float4 oldv = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (old_rows) oldv = *reinterpret_cast<const float4*>(qwin_prev + (((int64_t)b * G + go) * (Wq - 1) + wo) * R + oc);
+
+  // basis rows t + 256 i of the block's columns (rows past the group's end:
+  // a re-read of its last row, met by x = 0)
+  const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank + (c0 - grp * rank);
+  typename Raw8<T>::type bw[NCH];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) bw[i].load(bases + (int64_t)min(t + 256 * i, Dg - 1) * rank);
+  // the group's query elements of those rows, for vectors v0 .. v0 + 3 (the
+  // last vector repeated past G)
+  float x[kQVec][NCH];
+  auto load_x = [&](int v0) {
+#pragma unroll
+    for (int v = 0; v < kQVec; ++v)
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int d = grp * Dg + min(t + 256 * i, Dg - 1);   // feature index in Dp
+        x[v][i] = load_elem(q, ((int64_t)b * hq + (int64_t)(d >> ldh) * G + min(v0 + v, G - 1)) * dh + (d & (dh - 1)));
+      }
+  };
+  load_x(0);
   // the step's two selection histograms start from zero (the relevance and
   // classify kernels add to them later in the step)
-  if (cblk == 0 && ch == 0)
+  if (cblk == 0)
     for (int i = t; i < 2 * kHistBins; i += blockDim.x) hist[(int64_t)b * 2 * kHistBins + i] = 0u;
 
-  __shared__ float xs[kMaxG][kPChunk];
-  __shared__ double red[4][kPVec][32];
-  const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + ((int64_t)grp * Dg + r0) * rank +
-                   (c0 - grp * rank) + cg * 8;
-  // basis rows rg + 64 i (addresses clamped; rows past nrow meet x = 0) and
-  // the chunk of every group query, all requested before any is used
-  typename Raw8<T>::type bw[kPRows];
+  __shared__ double red[4][32];
+  for (int v0 = 0; v0 < G; v0 += kQVec) {
+    if (v0 > 0) load_x(v0);
+    double acc[kQVec * kPCols];                   // [vector][column]
 #pragma unroll
-  for (int i = 0; i < kPRows; ++i) bw[i].load(bases + (int64_t)min(rg + 64 * i, nrow - 1) * rank);
-  batched_copy4<kMaxG * kPChunk / 256>(
-      G * kPChunk,
-      [&](int i) -> float {
-        const int v = i >> 8, d = grp * Dg + r0 + min(i & (kPChunk - 1), nrow - 1);   // feature index in Dp
-        return load_elem(q, ((int64_t)b * hq + (int64_t)(d >> ldh) * G + v) * dh + (d & (dh - 1)));
-      },
-      [&](int i, float x) { xs[i >> 8][min(i & (kPChunk - 1), nrow - 1)] = x; });
-  if (nrow < kPChunk)
-    for (int i = t; i < G * kPChunk; i += blockDim.x)
-      if ((i & (kPChunk - 1)) >= nrow) xs[i >> 8][i & (kPChunk - 1)] = 0.f;
-  __syncthreads();
-
-  for (int v0 = 0; v0 < G; v0 += kPVec) {
-    const int nv = min(kPVec, G - v0);
-    double acc[kPVec][8];
+    for (int j = 0; j < kQVec * kPCols; ++j) acc[j] = 0.0;
 #pragma unroll
-    for (int v = 0; v < kPVec; ++v)
+    for (int i = 0; i < NCH; ++i) {
+      const bool in = t + 256 * i < Dg;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[v][c] = 0.0;
-    const float(*xv)[kPChunk] = xs + v0;
-    switch (nv) {
-      case 1: accumulate_rows<1>(bw, xv, rg, acc); reduce_rows<1>(acc, red, wave, lane, cg); break;
-      case 2: accumulate_rows<2>(bw, xv, rg, acc); reduce_rows<2>(acc, red, wave, lane, cg); break;
-      case 3: accumulate_rows<3>(bw, xv, rg, acc); reduce_rows<3>(acc, red, wave, lane, cg); break;
-      default: accumulate_rows<4>(bw, xv, rg, acc); reduce_rows<4>(acc, red, wave, lane, cg); break;
+      for (int c = 0; c < kPCols; ++c) {
+        const double bc = (double)bw[i][c];
+#pragma unroll
+        for (int v = 0; v < kQVec; ++v) acc[v * kPCols + c] = fma(in ? (double)x[v][i] : 0.0, bc, acc[v * kPCols + c]);
+      }
     }
+    reduce_wave<kQVec * kPCols>(acc, red, wave, lane);
     __syncthreads();
-    if (t < nv * 32) {
-      const int v = t >> 5, c = t & 31;
-      const double x = ((red[0][v][c] + red[1][v][c]) + red[2][v][c]) + red[3][v][c];
-      qpart[(((int64_t)b * nch + ch) * G + v0 + v) * R + c0 + c] = x;
+    if (t < kQVec * kPCols && v0 + (t >> 3) < G) {
+      const int g = v0 + (t >> 3), col = c0 + (t & 7);
+      const double xq = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
+      qcoef[((int64_t)b * G + g) * R + col] = (float)xq;
+      if (qcoef_out) qcoef_out[((int64_t)b * G + g) * R + col] = (float)xq;
+      if (qimg) {
+        const Split3 sp = split3(xq);
+        uint16_t* pi = qimg_at(qimg, b, ncb, nmb, R, g * Wq + Wq - 1, col);
+        pi[0] = sp.hi;
+        pi[R] = sp.mid;
+        pi[2 * R] = sp.lo;
+      }
     }
     __syncthreads();                              // red is reused by the next pass
   }
+  if (old_rows && (t >> 1) < n_old) {
+    uint2 pk[3];
+    qimg_pack4(oldv, pk);
+    uint16_t* p = qimg_at(qimg, b, ncb, nmb, R, go * Wq + wo, oc);
+#pragma unroll
+    for (int part = 0; part < 3; ++part) *reinterpret_cast<uint2*>(p + part * R) = pk[part];
+  }
 }
 
-template <typename T>
+template <typename T, int NCH>
 __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, const T* __restrict__ bases_k,
-                                                       double* __restrict__ qpart, uint32_t* __restrict__ hist,
-                                                       int hq, int hkv, int dh, int G, int nb, int rank, int R,
-                                                       int bases_shared) {
-  project_query_body<T>(q, bases_k, qpart, hist, hq, hkv, dh, G, nb, rank, R, bases_shared, blockIdx.x, blockIdx.y,
-                        blockIdx.z, gridDim.y);
+                                                       const float* __restrict__ qwin_prev, uint16_t* __restrict__ qimg,
+                                                       float* __restrict__ qcoef, float* __restrict__ qcoef_out,
+                                                       uint32_t* __restrict__ hist, int hq, int hkv, int dh, int G,
+                                                       int Wq, int nb, int rank, int R, int bases_shared, int ncb,
+                                                       int nmb) {
+  project_query_body<T, NCH>(q, bases_k, qwin_prev, qimg, qcoef, qcoef_out, hist, hq, hkv, dh, G, Wq, nb, rank, R,
+                             bases_shared, ncb, nmb, blockIdx.x, blockIdx.y);
 }
 
 // ---------------------------------------------------------------------------
-// new token's coefficient rows: grid (R / 32, B, 2 = {key, value}).  The
-// workgroup loops over 256-row chunks of its basis group and writes the full
-// sums into row append_row of the cache (rounded to the storage format).
+// new token's coefficient rows: grid (max(R, R_V) / 8, B, 2 = {key, value}).
+// A workgroup writes the full sums of its 8 columns into row append_row of
+// the cache (rounded to the storage format).
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, int NCH>
 __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
                                                   const T* __restrict__ k_new, const T* __restrict__ v_new,
                                                   T* __restrict__ coef_k, T* __restrict__ coef_v, int64_t append_row,
                                                   int hkv, int dh, int nb, int rank, int R, int bases_shared,
                                                   int64_t cap, int cblk, int b, int which) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int cg = t & 3, rg = t >> 2;
   const int Dp = hkv * dh, Dg = Dp / nb;
-  const int c0 = cblk * 32;
+  const int c0 = cblk * kPCols;
   const int grp = c0 / rank;
   const T* x_new = which == 0 ? k_new : v_new;
   T* coef = which == 0 ? coef_k : coef_v;
-
-  __shared__ float xs[kRowPre][kPChunk];
-  __shared__ double red[4][kPVec][32];
   const T* bases = (which == 0 ? bases_k : bases_v) + (bases_shared ? 0 : (int64_t)b * Dp * rank) +
-                   (int64_t)grp * Dg * rank + (c0 - grp * rank) + cg * 8;
-  double acc[kPVec][8];
+                   (int64_t)grp * Dg * rank + (c0 - grp * rank);
+  typename Raw8<T>::type bw[NCH];
+  float x[NCH];
 #pragma unroll
-  for (int v = 0; v < kPVec; ++v)
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[v][c] = 0.0;
-  // kRowPre chunks of 256 rows at a time: every basis row and vector element
-  // of the group is requested before any is used (one memory latency for a
-  // basis group of up to 1024 rows), then the chunks are summed in order
-  for (int r00 = 0; r00 < Dg; r00 += kRowPre * kPChunk) {
-    typename Raw8<T>::type bw[kRowPre][kPRows];
-    float x[kRowPre];
-#pragma unroll
-    for (int ci = 0; ci < kRowPre; ++ci) {
-      const int r0 = min(r00 + ci * kPChunk, Dg - 1);   // past the group's end: a re-read, never summed
-      const int nrow = min(kPChunk, Dg - r0);
-#pragma unroll
-      for (int i = 0; i < kPRows; ++i) bw[ci][i].load(bases + (int64_t)(r0 + min(rg + 64 * i, nrow - 1)) * rank);
-      x[ci] = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r0 + min(t, nrow - 1));
-    }
-    if (r00 > 0) __syncthreads();                 // previous group's xs reads are done
-#pragma unroll
-    for (int ci = 0; ci < kRowPre; ++ci) {
-      const int r0 = r00 + ci * kPChunk;
-      xs[ci][t] = (r0 + t < Dg) ? x[ci] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int ci = 0; ci < kRowPre; ++ci)
-      if (r00 + ci * kPChunk < Dg) accumulate_rows<1>(bw[ci], &xs[ci], rg, acc);
+  for (int i = 0; i < NCH; ++i) {
+    const int r = min(t + 256 * i, Dg - 1);
+    bw[i].load(bases + (int64_t)r * rank);
+    x[i] = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r);
   }
-  reduce_rows<1>(acc, red, wave, lane, cg);
+  __shared__ double red[4][32];
+  double acc[kPCols];
+#pragma unroll
+  for (int c = 0; c < kPCols; ++c) acc[c] = 0.0;
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const double xv = t + 256 * i < Dg ? (double)x[i] : 0.0;
+#pragma unroll
+    for (int c = 0; c < kPCols; ++c) acc[c] = fma(xv, (double)bw[i][c], acc[c]);
+  }
+  reduce_wave<kPCols>(acc, red, wave, lane);
   __syncthreads();
-  if (t < 32) {
-    const double v = ((red[0][0][t] + red[1][0][t]) + red[2][0][t]) + red[3][0][t];
+  if (t < kPCols) {
+    const double v = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
     store_elem(coef, (int64_t)b * cap * R + tiled_offset(append_row, c0 + t, R), v);
   }
 }
 
-template <typename T>
+template <typename T, int NCH>
 __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
                                                       const T* __restrict__ k_new, const T* __restrict__ v_new,
                                                       T* __restrict__ coef_k, T* __restrict__ coef_v,
@@ -249,72 +287,91 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
                                                       int rank_v, int Rv, int bases_shared, int64_t cap, Lens lens) {
   // the value side has its own width when the ranks are asymmetric
   const int which = blockIdx.z;
-  if ((int)blockIdx.x * 32 >= (which ? Rv : R)) return;
+  if ((int)blockIdx.x * kPCols >= (which ? Rv : R)) return;
   // a ragged batch appends at each sequence's own last row
   const int64_t row = lens.n ? (int64_t)lens.v[blockIdx.y] - 1 : append_row;
-  project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
-                       which ? Rv : R, bases_shared, cap, blockIdx.x, blockIdx.y, which);
+  project_rows_body<T, NCH>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
+                            which ? Rv : R, bases_shared, cap, blockIdx.x, blockIdx.y, which);
 }
 
 // both projections of a step that appends a token, in one launch: blocks
-// [0, nq) are the query-coefficient workgroups (R / 32 x chunks x B, in that
-// order), the rest the new rows' (max(R, R_V) / 32 x B x 2).  They touch disjoint
+// [0, nq) are the query-coefficient workgroups (R / 8 x B, in that order),
+// the rest the new rows' (max(R, R_V) / 8 x B x 2).  They touch disjoint
 // memory, and one launch saves a dispatch and a first-read latency.
-template <typename T>
+template <typename T, int NCH>
 __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, const T* __restrict__ bases_k,
                                                       const T* __restrict__ bases_v, const T* __restrict__ k_new,
                                                       const T* __restrict__ v_new, T* __restrict__ coef_k,
-                                                      T* __restrict__ coef_v, double* __restrict__ qpart,
+                                                      T* __restrict__ coef_v, const float* __restrict__ qwin_prev,
+                                                      uint16_t* __restrict__ qimg, float* __restrict__ qcoef,
                                                       uint32_t* __restrict__ hist, int64_t append_row, int hq,
-                                                      int hkv, int dh, int G, int nb, int rank, int R,
+                                                      int hkv, int dh, int G, int Wq, int nb, int rank, int R,
                                                       int rank_v, int Rv, int bases_shared, int64_t cap, int B,
-                                                      int nch, Lens lens) {
-  const int ncb = R / 32;
-  const int nq = ncb * nch * B;
+                                                      int ncb, int nmb, Lens lens) {
+  const int ncq = R / kPCols;
+  const int nq = ncq * B;
   int id = blockIdx.x;
   if (id < nq) {
-    const int cblk = id % ncb, ch = (id / ncb) % nch, b = id / (ncb * nch);
-    project_query_body<T>(q, bases_k, qpart, hist, hq, hkv, dh, G, nb, rank, R, bases_shared, cblk, ch, b, nch);
+    project_query_body<T, NCH>(q, bases_k, qwin_prev, qimg, qcoef, nullptr, hist, hq, hkv, dh, G, Wq, nb, rank, R,
+                               bases_shared, ncb, nmb, id % ncq, id / ncq);
   } else {
     id -= nq;
-    const int ncr = max(R, Rv) / 32;               // row blocks per (sequence, side)
+    const int ncr = max(R, Rv) / kPCols;           // row blocks per (sequence, side)
     const int cblk = id % ncr, b = (id / ncr) % B, which = id / (ncr * B);
-    if (cblk * 32 >= (which ? Rv : R)) return;
+    if (cblk * kPCols >= (which ? Rv : R)) return;
     const int64_t row = lens.n ? (int64_t)lens.v[b] - 1 : append_row;
-    project_rows_body<T>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
-                         which ? Rv : R,
-                         bases_shared, cap, cblk, b, which);
+    project_rows_body<T, NCH>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb,
+                              which ? rank_v : rank, which ? Rv : R, bases_shared, cap, cblk, b, which);
   }
 }
 
-hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
-                                hipStream_t st) {
-  dim3 grid(P.R / 32, project_chunks(P), P.B);
+// 256-row chunks of a basis group, rounded up to a power of two (<= 8)
+static int chunk_pow2(const Problem& P) {
+  const int nch = (P.Dg + kPChunk - 1) / kPChunk;
+  return nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8;
+}
+
+template <typename T, int NCH>
+static void launch_query_t(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                           const float* qwin_prev, float* qcoef_out, uint16_t* img, hipStream_t st) {
+  hipLaunchKernelGGL((k_project_query<T, NCH>), dim3(P.R / kPCols, P.B), dim3(256), 0, st, (const T*)q,
+                     (const T*)bases_k, qwin_prev, img, ws.qcoef, qcoef_out, ws.hist, P.hq, P.hkv, P.dh, P.G, P.Wq,
+                     P.nb, P.rank, P.R, P.bases_shared, col_blocks(P), qimg_mfmas(P));
+}
+
+template <typename T>
+static void launch_query_c(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                           const float* qwin_prev, float* qcoef_out, uint16_t* img, hipStream_t st) {
+  switch (chunk_pow2(P)) {
+    case 1: launch_query_t<T, 1>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st); break;
+    case 2: launch_query_t<T, 2>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st); break;
+    case 4: launch_query_t<T, 4>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st); break;
+    default: launch_query_t<T, 8>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st); break;
+  }
+}
+
+hipError_t launch_project_query(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                                const float* qwin_prev, float* qcoef_out, bool image, hipStream_t st) {
+  uint16_t* img = image ? ws.qimg : nullptr;
   if (P.dtype == S4R_BF16)
-    hipLaunchKernelGGL(k_project_query<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)bases_k, qpart, hist, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
-                       P.bases_shared);
+    launch_query_c<uint16_t>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st);
   else
-    hipLaunchKernelGGL(k_project_query<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k, qpart,
-                       hist, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.bases_shared);
+    launch_query_c<float>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st);
   return hipGetLastError();
 }
 
-// rows of C^Q from the query-projection partials: out[b][g][row][r] = the fp32
-// rounding of the chunk partials summed in chunk order (the order the scoring
-// kernel sums them in)
-__global__ __launch_bounds__(256) void k_qcoef_row(const double* __restrict__ qpart, float* __restrict__ out, int B,
-                                                   int G, int R, int nch, int64_t n_rows, int64_t row) {
+// row `row` of C^Q for n_rows queries: out[b][g][row][r] = qcoef[b][g][r]
+__global__ __launch_bounds__(256) void k_qcoef_row(const float* __restrict__ qcoef, float* __restrict__ out, int B,
+                                                   int G, int R, int64_t n_rows, int64_t row) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= B * G * R) return;
   const int b = i / (G * R), g = (i / R) % G, r = i % R;
-  double x = qpart[(((int64_t)b * nch) * G + g) * R + r];
-  for (int c = 1; c < nch; ++c) x += qpart[(((int64_t)b * nch + c) * G + g) * R + r];
-  out[(((int64_t)b * G + g) * n_rows + row) * R + r] = (float)x;
+  out[(((int64_t)b * G + g) * n_rows + row) * R + r] = qcoef[i];
 }
 
 // C^Q rows of n_rows queries [B, n_rows, h_q, d_h]: each row staged as
-// [B, h_q, d_h] in the workspace, projected, and its partials summed
+// [B, h_q, d_h] in the workspace, projected (the same fp64 sums as a decode
+// step's query, rounded once to fp32) and copied to its row
 hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t n_rows, const void* q_rows,
                                   const void* bases_k, float* out, hipStream_t st) {
   const size_t es = P.dtype == S4R_BF16 ? 2 : 4;
@@ -324,44 +381,72 @@ hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t
   for (int64_t row = 0; row < n_rows; ++row) {
     hipError_t e = hipMemcpy2DAsync(staged, row_bytes, static_cast<const char*>(q_rows) + row * row_bytes,
                                     (size_t)n_rows * row_bytes, row_bytes, P.B, hipMemcpyDeviceToDevice, st);
-    if (e == hipSuccess) e = launch_project_query(P, ws.qpart, ws.hist, staged, bases_k, st);
+    if (e == hipSuccess) e = launch_project_query(P, ws, staged, bases_k, nullptr, nullptr, false, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_qcoef_row, dim3((n + 255) / 256), dim3(256), 0, st, ws.qpart, out, P.B, P.G, P.R,
-                       project_chunks(P), n_rows, row);
+    hipLaunchKernelGGL(k_qcoef_row, dim3((n + 255) / 256), dim3(256), 0, st, ws.qcoef, out, P.B, P.G, P.R, n_rows,
+                       row);
   }
   return hipGetLastError();
 }
 
+template <typename T, int NCH>
+static void launch_rows_t(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
+                          const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
+  hipLaunchKernelGGL((k_project_rows<T, NCH>), dim3(std::max(P.R, P.Rv) / kPCols, P.B, 2), dim3(256), 0, st,
+                     (const T*)bases_k, (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v,
+                     row, P.hkv, P.dh, P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap, P.lens);
+}
+
+template <typename T>
+static void launch_rows_c(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
+                          const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
+  switch (chunk_pow2(P)) {
+    case 1: launch_rows_t<T, 1>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st); break;
+    case 2: launch_rows_t<T, 2>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st); break;
+    case 4: launch_rows_t<T, 4>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st); break;
+    default: launch_rows_t<T, 8>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st); break;
+  }
+}
+
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
-  dim3 grid(std::max(P.R, P.Rv) / 32, P.B, 2);
   if (P.dtype == S4R_BF16)
-    hipLaunchKernelGGL(k_project_rows<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)bases_k,
-                       (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
-                       (uint16_t*)coef_v, row, P.hkv, P.dh, P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap,
-                       P.lens);
+    launch_rows_c<uint16_t>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st);
   else
-    hipLaunchKernelGGL(k_project_rows<float>, grid, dim3(256), 0, st, (const float*)bases_k, (const float*)bases_v,
-                       (const float*)k_new, (const float*)v_new, (float*)coef_k, (float*)coef_v, row, P.hkv, P.dh,
-                       P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap, P.lens);
+    launch_rows_c<float>(P, bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, st);
   return hipGetLastError();
 }
 
-hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+template <typename T, int NCH>
+static void launch_step_t(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                          const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
+                          const float* qwin_prev, int64_t row, hipStream_t st) {
+  const dim3 grid((P.R / kPCols) * P.B + (std::max(P.R, P.Rv) / kPCols) * P.B * 2);
+  hipLaunchKernelGGL((k_project_step<T, NCH>), grid, dim3(256), 0, st, (const T*)q, (const T*)bases_k,
+                     (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v, qwin_prev, ws.qimg,
+                     ws.qcoef, ws.hist, row, P.hq, P.hkv, P.dh, P.G, P.Wq, P.nb, P.rank, P.R, P.rank_v, P.Rv,
+                     P.bases_shared, P.cap, P.B, col_blocks(P), qimg_mfmas(P), P.lens);
+}
+
+template <typename T>
+static void launch_step_c(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                          const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
+                          const float* qwin_prev, int64_t row, hipStream_t st) {
+  switch (chunk_pow2(P)) {
+    case 1: launch_step_t<T, 1>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st); break;
+    case 2: launch_step_t<T, 2>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st); break;
+    case 4: launch_step_t<T, 4>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st); break;
+    default: launch_step_t<T, 8>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st); break;
+  }
+}
+
+hipError_t launch_project_step(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
                                const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
-                               int64_t row, hipStream_t st) {
-  const int nch = project_chunks(P);
-  dim3 grid((P.R / 32) * nch * P.B + (std::max(P.R, P.Rv) / 32) * P.B * 2);
+                               const float* qwin_prev, int64_t row, hipStream_t st) {
   if (P.dtype == S4R_BF16)
-    hipLaunchKernelGGL(k_project_step<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)q, (const uint16_t*)bases_k,
-                       (const uint16_t*)bases_v, (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)coef_k,
-                       (uint16_t*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R,
-                       P.rank_v, P.Rv, P.bases_shared, P.cap, P.B, nch, P.lens);
+    launch_step_c<uint16_t>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st);
   else
-    hipLaunchKernelGGL(k_project_step<float>, grid, dim3(256), 0, st, (const float*)q, (const float*)bases_k,
-                       (const float*)bases_v, (const float*)k_new, (const float*)v_new, (float*)coef_k,
-                       (float*)coef_v, qpart, hist, row, P.hq, P.hkv, P.dh, P.G, P.nb, P.rank, P.R, P.rank_v, P.Rv,
-                       P.bases_shared, P.cap, P.B, nch, P.lens);
+    launch_step_c<float>(P, ws, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, row, st);
   return hipGetLastError();
 }
 

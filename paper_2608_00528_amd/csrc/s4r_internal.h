@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "s4r.h"
@@ -23,7 +24,7 @@ constexpr int kTileMax = 32;          // tiles per workgroup of the MFMA attenti
 constexpr int kMaxG = 16;             // query groups G = h_q / h_kv
 constexpr int kColBlk = 16;           // query columns (G * W_q) per scoring workgroup
 constexpr int kMaxGW = 128;           // G * W_q: up to 8 column blocks
-constexpr int kPChunk = 256;          // basis rows per query-projection workgroup
+constexpr int kPChunk = 256;          // basis rows per projection chunk (one per thread)
 constexpr int kQMaxChunks = 8;        // row chunks per basis group (Dp / basis_groups <= 2048)
 
 // per-sequence lengths of a ragged batch, passed to the kernels by value
@@ -64,7 +65,8 @@ struct Problem {
 };
 
 struct Workspace {
-  double* qpart;        // [B][row chunks][G][R] partial sums of the query coefficients
+  uint16_t* qimg;       // [B][column blocks][qimg_mfmas][16][R] the scoring kernel's A operands (bf16 parts)
+  float* qcoef;         // [B][G][R] the step's query coefficients c_t^Q (fp32)
   float* e;             // [B][cap][GWP]  exp(z - running max), fp32, token-major
   float* run_m;         // [B][cap / 16][GWP] per-tile softmax reference (running max of z)
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
@@ -95,21 +97,22 @@ inline int64_t cand_stride(const Problem& P) { return sel_groups_max(P) * kSelCh
 inline int gw_padded(const Problem& P) { return P.GW <= kColBlk ? (P.GW + 3) / 4 * 4 : (P.GW + kColBlk - 1) / kColBlk * kColBlk; }
 // column blocks of the scoring pass (one per kColBlk query columns)
 inline int col_blocks(const Problem& P) { return (P.GW + kColBlk - 1) / kColBlk; }
+// MFMAs (4 query columns each) per column block of the scoring pass
+inline int qimg_mfmas(const Problem& P) { return std::min((P.GW + 3) / 4, kColBlk / 4); }
 // RoPE: ratio of consecutive frequencies theta^(-2 / d_h) (0 when RoPE is off)
 inline double rope_ratio(const Problem& P) { return P.theta == 0.f ? 0.0 : pow((double)P.theta, -2.0 / P.dh); }
 
 // ---- launchers (each returns hipGetLastError() after its launches) --------
-inline int project_chunks(const Problem& P) { return (P.Dg + kPChunk - 1) / kPChunk; }
 
-// coefficient projections of Section 3.2.1: the query groups (row-chunk
-// partial sums into qpart) and a new token's key and value rows (into row
-// `row` of the caches)
-hipError_t launch_project_query(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
-                                hipStream_t st);
+// coefficient projections of Section 3.2.1: the query groups (fp32 c_t^Q
+// into ws.qcoef and qcoef_out when given; with `image`, the scoring kernel's
+// operand image ws.qimg, the window's older rows from qwin_prev) and a new
+// token's key and value rows (into row `row` of the caches)
+hipError_t launch_project_query(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
+                                const float* qwin_prev, float* qcoef_out, bool image, hipStream_t st);
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st);
-hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
-                               const float* qwin_prev, float* qcoef_out, hipStream_t st);
+hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st);
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out,
                             hipStream_t st);
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
@@ -129,9 +132,9 @@ hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t
                                   const void* bases_k, float* out, hipStream_t st);
 hipError_t launch_dense_decode(const Problem& P, const Workspace& ws, int64_t N, const void* q, const void* k_cache,
                                const void* v_cache, float* out, hipStream_t st);
-hipError_t launch_project_step(const Problem& P, double* qpart, uint32_t* hist, const void* q, const void* bases_k,
+hipError_t launch_project_step(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
                                const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
-                               int64_t row, hipStream_t st);
+                               const float* qwin_prev, int64_t row, hipStream_t st);
 size_t prefill_ws_bytes(const Problem& P);
 hipError_t launch_prefill_project(const Problem& P, int64_t n_rows, const void* s_k, const void* s_v,
                                   const void* bases_k, const void* bases_v, void* coef_k, void* coef_v, void* ws,

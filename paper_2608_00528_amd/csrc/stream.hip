@@ -11,14 +11,16 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 // K1: the coefficient stream
 // ---------------------------------------------------------------------------
-// grid (workgroups per sequence, B, column blocks), 256 threads = 4 waves.  A
-// wave owns a contiguous range of 16-token tiles; a workgroup scores them
-// against one block of up to 16 query columns (blockIdx.z; more than one block
-// only when G * W_q > 16, the blocks re-reading the tiles from L2 / MALL).
-// Each 16x32 block of C^K is one coalesced 1 KiB wave load that is used
-// directly as the B operand of a 16x16x32 bf16 MFMA (lane l: token l%16,
-// latent columns 8*(l/16)..+7).  The A operand holds the query-coefficient columns, four per MFMA, each as its
-// hi / mid / lo bf16 parts in rows 4*c + part (row 4*c + 3 is zero), so lane
+// grid (workgroups per sequence, B) with one block of query columns, else a
+// 1-D grid over (token range, column block); 256 threads = 4 waves.  A wave
+// owns a contiguous range of 16-token tiles; a workgroup scores them against
+// one block of up to 16 query columns (more than one block only when
+// G * W_q > 16, the blocks re-reading the tiles from L2 / MALL).  Each 16x32
+// block of C^K is one coalesced 1 KiB wave load that is used directly as the
+// B operand of a 16x16x32 bf16 MFMA (lane l: token l%16, latent columns
+// 8*(l/16)..+7).  The A operand holds the query-coefficient columns, four per
+// MFMA, each as its hi / mid / lo bf16 parts in rows 4*c + part (row 4*c + 3
+// is zero), as the projection kernel wrote them into the operand image, so lane
 // (token t, k-group c) receives the three partial products of query column c
 // against token t.  The MFMA rounds once per instruction, like an fp32 sum
 // aligned to its largest term; the parts of every 32-column block are folded
@@ -66,9 +68,9 @@ __device__ __forceinline__ void load_b_tile(const T* cb, int tile, int ntiles, i
 
 template <typename T, int RB, int NM>
 __global__ __launch_bounds__(256, 2) void k_score_stream(
-    const T* __restrict__ coef_k, const double* __restrict__ qpart, const float* __restrict__ qwin_prev,
-    float* __restrict__ qcoef_out, float* __restrict__ e_out, float* __restrict__ tref,
-    double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int nch, int ntiles_cap, int tiles_per_wave,
+    const T* __restrict__ coef_k, const uint16_t* __restrict__ qimg, float* __restrict__ e_out,
+    float* __restrict__ tref, double* __restrict__ wg_stats, int64_t cap, int L, int G, int Wq, int ntiles_cap,
+    int tiles_per_wave,
     int nwg, int gwp, int ncb, int B, double scale, Lens lens) {
   constexpr int R = RB * kBlkCol;
   constexpr int NP = BLoad<T>::kParts;
@@ -108,28 +110,22 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
   const int tile1 = min(tile0 + tiles_per_wave, ntiles);
 
   // A operands: query column gi = g * Wq + i (row i of group g's window, oldest
-  // first) sits in MFMA m = gi / 4, rows 4 * (gi % 4) + part.  The newest row
-  // is the sum of the projection's row-chunk partials (fixed order); older
-  // rows come from the caller.  Staged once per workgroup in LDS (rows padded
-  // by 16 bytes so the 16-byte operand reads of one MFMA hit distinct banks).
-  // The values of the first kQPre * 256 query elements are requested before
-  // the coefficient tiles, so they do not queue behind the streaming loads.
-  constexpr int kQPre = 4;
-  const double* qp = qpart + (int64_t)b * nch * G * R;
-  // older rows from the caller; with W_q = 1 there are none and the load
-  // below re-reads a partial sum (unused) so it needs no branch
-  const float* qw = (Wq > 1) ? qwin_prev + (int64_t)b * G * (Wq - 1) * R : reinterpret_cast<const float*>(qp);
-  double part[kQPre][kQMaxChunks];
-  float old[kQPre];
-  auto load_q = [&](int i0, int u) {
-    const int i = min(i0 + u * (int)blockDim.x + t, GWl * R - 1);
-    const int gi = c0 + i / R, r = i % R, g = gi / Wq, wi = gi % Wq;
+  // first) sits in MFMA m = gi / 4, rows 4 * (gi % 4) + part, as the bf16
+  // parts the projection kernel wrote into the operand image.  Staged once per
+  // workgroup in LDS (rows padded by 16 bytes so the 16-byte operand reads of
+  // one MFMA hit distinct banks); rows of no query column, and each column's
+  // fourth row, are zero.  The image is requested before the coefficient
+  // tiles, so it does not queue behind the streaming loads.
+  constexpr int K8 = R / 8;                        // 16-byte units per operand row
+  constexpr int kQU = (NM * 16 * K8 + 255) / 256;  // units per thread (<= 8)
+  const uint4* qi = reinterpret_cast<const uint4*>(qimg + ((int64_t)b * ncb + cbk) * (NM * 16) * R);
+  uint4 qv[kQU];
 #pragma unroll
-    for (int c = 0; c < kQMaxChunks; ++c) part[u][c] = qp[((int64_t)min(c, nch - 1) * G + g) * R + r];
-    old[u] = qw[(Wq > 1) ? ((int64_t)g * (Wq - 1) + min(wi, Wq - 2)) * R + r : 0];
-  };
-#pragma unroll
-  for (int u = 0; u < kQPre; ++u) load_q(0, u);
+  for (int u = 0; u < kQU; ++u) {
+    const int i = min(u * 256 + t, NM * 16 * K8 - 1), row = i / K8;   // row = 16 m + 4 c + part
+    const bool used = (row & 3) != 3 && (row >> 2) < GWl;
+    qv[u] = used ? qi[i] : make_uint4(0, 0, 0, 0);
+  }
 
   // the first tile now, the rest of the prefetch once the query is staged: the
   // two workgroups of a CU then start streaming together (a full prefetch here
@@ -139,38 +135,12 @@ __global__ __launch_bounds__(256, 2) void k_score_stream(
 
   constexpr int RS = R + 8;
   __shared__ __align__(16) uint16_t qsh[NM][16][RS];
-  {
-    constexpr int K8 = R / 8;
-    for (int i = t; i < NM * 16 * K8; i += blockDim.x) {   // zero every row first
-      const int m = i / (16 * K8), r = (i / K8) % 16;
-      *reinterpret_cast<uint4*>(&qsh[m][r][(i % K8) * 8]) = make_uint4(0, 0, 0, 0);
-    }
-    lds_barrier();
-    for (int i0 = 0; i0 < GWl * R; i0 += kQPre * (int)blockDim.x) {
-      if (i0 > 0) {                                // more than kQPre * 256 elements
 #pragma unroll
-        for (int u = 0; u < kQPre; ++u) load_q(i0, u);
-      }
-#pragma unroll
-      for (int u = 0; u < kQPre; ++u) {
-        const int i = i0 + u * (int)blockDim.x + t;
-        if (i >= GWl * R) break;
-        const int gl = i / R, gi = c0 + gl, r = i % R, g = gi / Wq, wi = gi % Wq;
-        double x = part[u][0];
-#pragma unroll
-        for (int c = 1; c < kQMaxChunks; ++c)
-          if (c < nch) x += part[u][c];
-        if (wi < Wq - 1) x = (double)old[u];
-        const Split3 sp = split3(x);
-        const int m = gl >> 2, row = 4 * (gl & 3);
-        qsh[m][row + 0][r] = sp.hi;
-        qsh[m][row + 1][r] = sp.mid;
-        qsh[m][row + 2][r] = sp.lo;
-        if (qcoef_out && xw == 0 && wi == Wq - 1) qcoef_out[((int64_t)b * G + g) * R + r] = (float)x;
-      }
-    }
-    lds_barrier();                                 // the tile requested above stays in flight
+  for (int u = 0; u < kQU; ++u) {
+    const int i = u * 256 + t;
+    if (i < NM * 16 * K8) *reinterpret_cast<uint4*>(&qsh[0][0][0] + (i / K8) * RS + (i % K8) * 8) = qv[u];
   }
+  lds_barrier();                                   // the tile requested above stays in flight
 #pragma unroll
   for (int p = 1; p < PF; ++p) load_b_tile<T, RB>(cb, min(tile0 + p, tile1 - 1), ntiles, slot, kg, bbuf[p]);
   // the A operands stay in registers when they fit, else they are re-read from LDS
@@ -295,49 +265,44 @@ int score_workgroups(const Problem& P, int64_t L) {
 }
 
 template <typename T, int RB, int NM>
-static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
-                             const float* qwin_prev, float* qcoef_out, hipStream_t st) {
+static void launch_stream_nm(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st) {
   const int tpw = tiles_per_wave(P, L);
   const int nwg = score_workgroups(P, L);
   const int ncb = col_blocks(P);
   const dim3 grid = ncb == 1 ? dim3(nwg, P.B) : dim3(8 * ncb * ((nwg * P.B + 7) / 8));
   // the scale takes the configured latent width (storage columns past it are zero)
-  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), grid, dim3(256), 0, st, (const T*)coef_k, ws.qpart, qwin_prev,
-                     qcoef_out, ws.e, ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, project_chunks(P),
-                     (int)(P.cap / kTileTok), tpw, nwg, gw_padded(P), ncb, P.B, 1.0 / sqrt((double)P.R_cfg), P.lens);
+  hipLaunchKernelGGL((k_score_stream<T, RB, NM>), grid, dim3(256), 0, st, (const T*)coef_k, ws.qimg, ws.e,
+                     ws.run_m, ws.wg_stats, P.cap, (int)L, P.G, P.Wq, (int)(P.cap / kTileTok), tpw, nwg, gw_padded(P), ncb, P.B, 1.0 / sqrt((double)P.R_cfg), P.lens);
 }
 
 template <typename T, int RB>
-static void launch_stream_t(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
-                            const float* qwin_prev, float* qcoef_out, hipStream_t st) {
-  switch (std::min((P.GW + 3) / 4, kColBlk / 4)) {
-    case 1: launch_stream_nm<T, RB, 1>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
-    case 2: launch_stream_nm<T, RB, 2>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
-    case 3: launch_stream_nm<T, RB, 3>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
-    default: launch_stream_nm<T, RB, 4>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); break;
+static void launch_stream_t(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st) {
+  switch (qimg_mfmas(P)) {                          // the operand image's MFMAs per column block
+    case 1: launch_stream_nm<T, RB, 1>(P, ws, L, coef_k, st); break;
+    case 2: launch_stream_nm<T, RB, 2>(P, ws, L, coef_k, st); break;
+    case 3: launch_stream_nm<T, RB, 3>(P, ws, L, coef_k, st); break;
+    default: launch_stream_nm<T, RB, 4>(P, ws, L, coef_k, st); break;
   }
 }
 
 template <typename T>
-static bool dispatch_rb(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, const float* qwin_prev,
-                        float* qcoef_out, hipStream_t st) {
+static bool dispatch_rb(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st) {
   switch (P.R / 32) {
-    case 1: launch_stream_t<T, 1>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 2: launch_stream_t<T, 2>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 3: launch_stream_t<T, 3>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 4: launch_stream_t<T, 4>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 5: launch_stream_t<T, 5>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 6: launch_stream_t<T, 6>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 7: launch_stream_t<T, 7>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
-    case 8: launch_stream_t<T, 8>(P, ws, L, coef_k, qwin_prev, qcoef_out, st); return true;
+    case 1: launch_stream_t<T, 1>(P, ws, L, coef_k, st); return true;
+    case 2: launch_stream_t<T, 2>(P, ws, L, coef_k, st); return true;
+    case 3: launch_stream_t<T, 3>(P, ws, L, coef_k, st); return true;
+    case 4: launch_stream_t<T, 4>(P, ws, L, coef_k, st); return true;
+    case 5: launch_stream_t<T, 5>(P, ws, L, coef_k, st); return true;
+    case 6: launch_stream_t<T, 6>(P, ws, L, coef_k, st); return true;
+    case 7: launch_stream_t<T, 7>(P, ws, L, coef_k, st); return true;
+    case 8: launch_stream_t<T, 8>(P, ws, L, coef_k, st); return true;
     default: return false;
   }
 }
 
-hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k,
-                               const float* qwin_prev, float* qcoef_out, hipStream_t st) {
-  bool ok = P.dtype == S4R_BF16 ? dispatch_rb<uint16_t>(P, ws, L, coef_k, qwin_prev, qcoef_out, st)
-                                : dispatch_rb<float>(P, ws, L, coef_k, qwin_prev, qcoef_out, st);
+hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st) {
+  bool ok = P.dtype == S4R_BF16 ? dispatch_rb<uint16_t>(P, ws, L, coef_k, st)
+                                : dispatch_rb<float>(P, ws, L, coef_k, st);
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();
 }
