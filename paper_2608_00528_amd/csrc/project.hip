@@ -235,10 +235,13 @@ __global__ __launch_bounds__(256) void k_project_query(const T* __restrict__ q, 
 }
 
 // ---------------------------------------------------------------------------
-// new token's coefficient rows: grid (max(R, R_V) / 8, B, 2 = {key, value}).
-// A workgroup writes the full sums of its 8 columns into row append_row of
-// the cache (rounded to the storage format).
+// new token's coefficient rows: grid (max(R, R_V) / 32, B, 2 = {key, value}).
+// One vector per side, so a workgroup takes 32 columns (4 groups of 8 per
+// thread, the same 32 sums per lane as a query pass) and writes their full
+// sums into row append_row of the cache (rounded to the storage format).
 // ---------------------------------------------------------------------------
+constexpr int kRCols = 32;                    // latent columns per new-row workgroup
+
 template <typename T, int NCH>
 __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k, const T* __restrict__ bases_v,
                                                   const T* __restrict__ k_new, const T* __restrict__ v_new,
@@ -247,33 +250,37 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
                                                   int64_t cap, int cblk, int b, int which) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int Dp = hkv * dh, Dg = Dp / nb;
-  const int c0 = cblk * kPCols;
+  const int c0 = cblk * kRCols;
   const int grp = c0 / rank;
   const T* x_new = which == 0 ? k_new : v_new;
   T* coef = which == 0 ? coef_k : coef_v;
   const T* bases = (which == 0 ? bases_k : bases_v) + (bases_shared ? 0 : (int64_t)b * Dp * rank) +
                    (int64_t)grp * Dg * rank + (c0 - grp * rank);
-  typename Raw8<T>::type bw[NCH];
+  constexpr int NG = kRCols / kPCols;             // column groups of 8
+  typename Raw8<T>::type bw[NCH][NG];
   float x[NCH];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) {
     const int r = min(t + 256 * i, Dg - 1);
-    bw[i].load(bases + (int64_t)r * rank);
+#pragma unroll
+    for (int k = 0; k < NG; ++k) bw[i][k].load(bases + (int64_t)r * rank + k * kPCols);
     x[i] = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r);
   }
   __shared__ double red[4][32];
-  double acc[kPCols];
+  double acc[kRCols];                             // [column group][column]
 #pragma unroll
-  for (int c = 0; c < kPCols; ++c) acc[c] = 0.0;
+  for (int j = 0; j < kRCols; ++j) acc[j] = 0.0;
 #pragma unroll
   for (int i = 0; i < NCH; ++i) {
     const double xv = t + 256 * i < Dg ? (double)x[i] : 0.0;
 #pragma unroll
-    for (int c = 0; c < kPCols; ++c) acc[c] = fma(xv, (double)bw[i][c], acc[c]);
+    for (int k = 0; k < NG; ++k)
+#pragma unroll
+      for (int c = 0; c < kPCols; ++c) acc[k * kPCols + c] = fma(xv, (double)bw[i][k][c], acc[k * kPCols + c]);
   }
-  reduce_wave<kPCols>(acc, red, wave, lane);
+  reduce_wave<kRCols>(acc, red, wave, lane);
   __syncthreads();
-  if (t < kPCols) {
+  if (t < kRCols) {
     const double v = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
     store_elem(coef, (int64_t)b * cap * R + tiled_offset(append_row, c0 + t, R), v);
   }
@@ -287,7 +294,7 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
                                                       int rank_v, int Rv, int bases_shared, int64_t cap, Lens lens) {
   // the value side has its own width when the ranks are asymmetric
   const int which = blockIdx.z;
-  if ((int)blockIdx.x * kPCols >= (which ? Rv : R)) return;
+  if ((int)blockIdx.x * kRCols >= (which ? Rv : R)) return;
   // a ragged batch appends at each sequence's own last row
   const int64_t row = lens.n ? (int64_t)lens.v[blockIdx.y] - 1 : append_row;
   project_rows_body<T, NCH>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb, which ? rank_v : rank,
@@ -296,7 +303,7 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
 
 // both projections of a step that appends a token, in one launch: blocks
 // [0, nq) are the query-coefficient workgroups (R / 8 x B, in that order),
-// the rest the new rows' (max(R, R_V) / 8 x B x 2).  They touch disjoint
+// the rest the new rows' (max(R, R_V) / 32 x B x 2).  They touch disjoint
 // memory, and one launch saves a dispatch and a first-read latency.
 template <typename T, int NCH>
 __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, const T* __restrict__ bases_k,
@@ -316,9 +323,9 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
                                bases_shared, ncb, nmb, id % ncq, id / ncq);
   } else {
     id -= nq;
-    const int ncr = max(R, Rv) / kPCols;           // row blocks per (sequence, side)
+    const int ncr = max(R, Rv) / kRCols;           // row blocks per (sequence, side)
     const int cblk = id % ncr, b = (id / ncr) % B, which = id / (ncr * B);
-    if (cblk * kPCols >= (which ? Rv : R)) return;
+    if (cblk * kRCols >= (which ? Rv : R)) return;
     const int64_t row = lens.n ? (int64_t)lens.v[b] - 1 : append_row;
     project_rows_body<T, NCH>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb,
                               which ? rank_v : rank, which ? Rv : R, bases_shared, cap, cblk, b, which);
@@ -392,7 +399,7 @@ hipError_t launch_project_queries(const Problem& P, const Workspace& ws, int64_t
 template <typename T, int NCH>
 static void launch_rows_t(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                           const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st) {
-  hipLaunchKernelGGL((k_project_rows<T, NCH>), dim3(std::max(P.R, P.Rv) / kPCols, P.B, 2), dim3(256), 0, st,
+  hipLaunchKernelGGL((k_project_rows<T, NCH>), dim3(std::max(P.R, P.Rv) / kRCols, P.B, 2), dim3(256), 0, st,
                      (const T*)bases_k, (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v,
                      row, P.hkv, P.dh, P.nb, P.rank, P.R, P.rank_v, P.Rv, P.bases_shared, P.cap, P.lens);
 }
@@ -421,7 +428,7 @@ template <typename T, int NCH>
 static void launch_step_t(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
                           const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                           const float* qwin_prev, int64_t row, hipStream_t st) {
-  const dim3 grid((P.R / kPCols) * P.B + (std::max(P.R, P.Rv) / kPCols) * P.B * 2);
+  const dim3 grid((P.R / kPCols) * P.B + (std::max(P.R, P.Rv) / kRCols) * P.B * 2);
   hipLaunchKernelGGL((k_project_step<T, NCH>), grid, dim3(256), 0, st, (const T*)q, (const T*)bases_k,
                      (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v, qwin_prev, ws.qimg,
                      ws.qcoef, ws.hist, row, P.hq, P.hkv, P.dh, P.G, P.Wq, P.nb, P.rank, P.R, P.rank_v, P.Rv,

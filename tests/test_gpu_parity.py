@@ -748,6 +748,51 @@ def test_project_queries(shape, n):
     assert np.array_equal(got[:, :, -1], qco.cpu().numpy().astype(np.float64))
 
 
+@pytest.mark.parametrize("hq,hkv,dh,nb,rank,dtype", [
+    (12, 6, 128, 1, 96, "bf16"),      # D'/s = 768: the last 256-row chunk of the four is masked
+    (16, 16, 128, 1, 64, "bf16"),     # G = 1, D'/s = 2048: eight chunks per basis group
+    (28, 4, 128, 2, 64, "fp32"),      # G = 7 (two passes of four groups), two basis groups
+    (4, 2, 64, 2, 32, "bf16"),        # one head per basis group (D'/s = 64)
+])
+def test_projection_shapes(hq, hkv, dh, nb, rank, dtype):
+    """Both projections of Section 3.2.1 at basis-group sizes and group counts
+    the workloads do not reach: the query coefficients of every group
+    (s4r_project_queries) at most an fp32 ulp from the oracle's fp64
+    projection, and the new token's key / value rows (s4r_project_append)
+    equal to the oracle's, rounded once to the storage format, up to
+    rounding ties."""
+    B, cap = 2, 64
+    wl = W.CONFIGS["llama8b_32k"].scaled(N=cap + 4, batch=B, n_q_heads=hq, n_kv_heads=hkv, head_dim=dh,
+                                         basis_groups=nb, rank=rank, dtype=dtype, topk=16, window=8)
+    st = W.latent_state(wl, seed=hq + nb, capacity=cap, L=cap)
+    c = cfg_from_workload(wl, capacity=cap)
+    g = to_gpu_state(c, st)
+    ws = s4r.alloc_workspace(c)
+    dt = s4r.storage_dtype(c)
+    rng = np.random.default_rng(hkv)
+    qrows = W.round_storage(rng.standard_normal((B, 2, hq, dh)), dtype)
+    got = s4r.project_queries(c, dev(qrows, dt), g["bases_k"], ws)
+    kn = W.round_storage(rng.standard_normal((B, wl.Dp)), dtype)
+    vn = W.round_storage(rng.standard_normal((B, wl.Dp)), dtype)
+    row = 5
+    s4r.project_append(c, row, dev(kn, dt), dev(vn, dt), g["bases_k"], g["bases_v"], g["coef_k"], g["coef_v"])
+    after_k = s4r.unpack_coef(c, cap, g["coef_k"]).cpu()
+    after_v = s4r.unpack_coef(s4r.value_config(c), cap, g["coef_v"]).cpu()
+    torch.cuda.synchronize()
+    got = unpad_latent(got.cpu().numpy().astype(np.float64), rank, nb)
+    for i in range(2):
+        ref = decode.project(decode.group_queries(qrows[:, i], hkv), st["bases_k"])    # [B, G, R]
+        err = np.abs(got[:, :, i] - ref).max() / np.abs(ref).max()
+        assert err <= 2e-7, f"query row {i}: rel err {err:.2e}"
+    ck, cv = decode.project_append(kn, vn, st["bases_k"], st["bases_v"], dtype)
+    ck_x = decode.project(kn[:, None, :], st["bases_k"])[:, 0]
+    cv_x = decode.project(vn[:, None, :], st["bases_v"])[:, 0]
+    nk = _rounding_ties_only(unpad_latent(after_k[:, row].double().numpy(), rank, nb), ck, ck_x, dtype)
+    nv = _rounding_ties_only(unpad_latent(after_v[:, row].double().numpy(), rank, nb), cv, cv_x, dtype)
+    print(f"[projection] h_q {hq} h_kv {hkv} d_h {dh} s {nb} rank {rank} {dtype}: rounding ties {nk}, {nv}",
+          flush=True)
+
+
 def _rounding_ties_only(got, ref_rounded, ref_exact, dtype):
     """Elements where the GPU's stored value differs from the oracle's rounded
     one must be ones whose exact (float64) value lies within float64 noise of
