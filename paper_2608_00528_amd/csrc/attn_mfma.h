@@ -49,11 +49,17 @@
 
 namespace s4r {
 
-// occupancy target: three workgroups per CU (at most 168 registers per lane;
-// the four tile slots of a workgroup take 4 * (RBH + RBV) KiB of LDS)
-template <int RBH, int RBV>
+// occupancy target (workgroups per CU = waves per SIMD): three (at most 168
+// registers per lane; the four tile slots of a workgroup take 4 * (RBH + RBV)
+// KiB of LDS) while the operands fit without spilling, else two (one for the
+// widest eight-head case)
+constexpr int attn_tiles_waves(int rbh, int rbv, int nmh) {
+  if (nmh == 1) return (rbh + rbv <= 10 && rbh <= 6 && rbv <= 6) ? 3 : 2;
+  return rbh + rbv <= 6 ? 3 : (rbh + rbv < 16 ? 2 : 1);
+}
+template <int RBH, int RBV, int NMH>
 constexpr int attn_tiles_waves_per_simd() {
-  return RBH + RBV <= 10 ? 3 : 2;
+  return attn_tiles_waves(RBH, RBV, NMH);
 }
 
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt not waited)
@@ -91,7 +97,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // RBH / RBV: 32-column blocks of one head's key / value basis group (they
 // differ when the ranks are asymmetric, Appendix D.2).
 template <int RBH, int RBV, int NW, int NMH, bool IDENT>
-__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) void k_attn_tiles(
+__global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>())) void k_attn_tiles(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ bases_k, const uint16_t* __restrict__ bases_v,
     const uint16_t* __restrict__ coef_k, const uint16_t* __restrict__ coef_v, const int32_t* __restrict__ idx_all,
     int64_t idx_stride, float* __restrict__ part_ml, float* __restrict__ part_o, int n_proc, int tpw, int nsplit,
@@ -399,11 +405,11 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV>())) v
 namespace s4r {
 
 // tiles per workgroup: the smallest even count whose workgroups fit in one
-// round of the chip (three per CU), at most kMaxSplit splits; with an index
-// list, 0 when the list needs more than kTileMax tiles per workgroup (the
-// general kernel then runs)
+// round of the chip (the kernel's workgroups per CU), at most kMaxSplit
+// splits; with an index list, 0 when the list needs more than kTileMax tiles
+// per workgroup (the general kernel then runs)
 inline int attn_tiles_per_wg(const Problem& P, int ntile, bool ident) {
-  const int slots = 256 * 3;
+  const int slots = 256 * attn_tiles_waves(P.rank / 32, P.rank_v / 32, P.G > 4 ? 2 : 1);
   const int ns_target = std::max(1, slots / std::max(1, P.B * P.hkv));
   int tpw = (ntile + ns_target - 1) / ns_target;
   tpw = std::max(2, (tpw + 1) / 2 * 2);
