@@ -54,8 +54,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic(wl, m):
-    """Bytes the method must move per step and MFMA flops of the reconstruction."""
+def algorithmic(wl, m, windowed=False):
+    """Bytes the method must move per step and MFMA flops of the reconstruction
+    (windowed: the older query rows' softmax read from the window state and
+    the newest row's written, instead of their coefficient rows)."""
     B, L, R, Dp, es = wl.batch, wl.L, wl.R, wl.Dp, (2 if wl.dtype == "bf16" else 4)
     ck = B * L * R * es                       # C^K streamed once (latent scoring)
     gather = 2 * B * m * R * es               # selected rows of C^K and C^V
@@ -64,6 +66,8 @@ def algorithmic(wl, m):
     q = B * wl.n_q_heads * wl.head_dim * es
     out = B * wl.n_q_heads * wl.head_dim * 4
     qwin = B * wl.G * (wl.q_window - 1) * R * 4  # the window's earlier query coefficients (fp32)
+    if windowed:
+        qwin = B * wl.G * wl.q_window * L * 4     # older rows' softmax read, the newest row's written
     rec_flops = 2 * 2 * B * m * R * Dp        # K^ and V^ of every selected token
     return {"step_bytes": ck + gather + bases + sinks + q + out + qwin, "stream_bytes": ck, "rec_flops": rec_flops}
 
@@ -300,9 +304,22 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     m = s4r.num_selected(c, wl.L)
     torch.cuda.synchronize()
 
+    # with a query window of several rows the step is the windowed one: the
+    # older rows' softmax stays resident in the window state (set up once from
+    # their coefficient rows; every replica holds the same cache), and only the
+    # newest row is scored
+    windowed = wl.q_window > 1
+    state = None
+    if windowed:
+        state = s4r.alloc_window_state(c)
+        s4r.window_state_init(c, wl.L, qwin, replicas[0][0], state, ws)
+
     def step(i):
         ck, cv = replicas[i % n_rep]
-        s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, ck, cv, ws, qwin_prev=qwin, out=out)
+        if windowed:
+            s4r.decode_step_windowed(c, wl.L, q, state, sk, sv, bk, bv, ck, cv, ws, out=out)
+        else:
+            s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, ck, cv, ws, qwin_prev=qwin, out=out)
 
     for i in range(warmup):
         step(i)
@@ -323,7 +340,20 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     ms_total = e0.elapsed_time(e1)
     ms_step = ms_total / steps
     log(f"[bench] {wl.name}: {steps} steps: {ms_step * 1e3:.2f} us/step (events), "
-        f"wall {wall / steps * 1e6:.2f} us/step")
+        f"wall {wall / steps * 1e6:.2f} us/step" + (" (windowed step)" if windowed else ""))
+    stateless_us = None
+    if windowed:
+        # the same step recomputing every window row from qwin_prev, for reference
+        ns = min(steps, 50)
+        for i in range(5):
+            s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, *replicas[i % n_rep], ws, qwin_prev=qwin, out=out)
+        e0.record(stream)
+        for i in range(ns):
+            s4r.decode_step(c, wl.L, q, sk, sv, bk, bv, *replicas[i % n_rep], ws, qwin_prev=qwin, out=out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        stateless_us = e0.elapsed_time(e1) / ns * 1e3
+        log(f"[bench] {wl.name}: stateless step (every window row scored): {stateless_us:.2f} us/step")
 
     result_extra = {}
     if full:
@@ -344,7 +374,7 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
     kus = {k: v / nsteps * 1e3 for k, v in kms.items()}
     log(f"[bench] {wl.name} per-kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in kus.items()))
 
-    alg = algorithmic(wl, m)
+    alg = algorithmic(wl, m, windowed)
     stream_us = kus["score_stream"]
     achieved = alg["stream_bytes"] / (stream_us * 1e-6) / 1e9
     traffic = traffic_from_profile(wl.name)
@@ -375,8 +405,11 @@ def measure_single(args, wl, steps, warmup, full, comparators, cpu_budget=10.0):
                          f"{wl.dtype} storage"),
             "batch": wl.batch, "context": wl.N, "rank": wl.R, "window": wl.window, "topk": wl.topk,
             "selected": m, "replicas": n_rep,
+            **({"step": "windowed (the older query rows' softmax resident in the window state; "
+                         "s4r_decode_step_windowed)"} if windowed else {}),
         },
         **result_extra,
+        **({"stateless_us_per_step": round(stateless_us, 3)} if windowed else {}),
         "achieved_step_GBps": round(step_gbps, 1),
         "step_frac_of_hbm_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": alg["step_bytes"],

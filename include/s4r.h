@@ -225,6 +225,44 @@ s4r_status s4r_decode_step_noalloc(const s4r_config* cfg, int64_t L, const void*
                                    int32_t* idx_out, float* scores_out, hipStream_t stream);
 
 /*
+ * Windowed decode (Section 3.2.2 with q_window >= 2): the latent scores of
+ * query row i of the window are the softmax over keys 0 .. L - W_q + i, and
+ * that key range and those keys' coefficients are the same at every later
+ * step the row stays in the window (the cache only grows by appended rows).
+ * The row's softmax over its keys therefore never changes once it has been
+ * computed, so a caller that keeps it on the device needs to score only the
+ * newest query row at each step.  The window state holds, per sequence, the
+ * softmax of the last W_q query rows over their keys:
+ *   state [B, q_window, G, capacity] fp32 (s4r_window_state_size bytes,
+ *   device, caller-owned, 16-byte aligned); the row that was the newest at
+ *   length L_r (it covers keys 0 .. L_r - 1) sits in slot L_r mod q_window.
+ *
+ * s4r_window_state_init fills the state for the q_window - 1 older rows of
+ * the window of a step at length L, from their coefficient rows qwin_prev
+ * [B, G, q_window - 1, R] fp32 (the qwin_prev of s4r_decode_step) and the
+ * coefficient cache (rows 0 .. L - 2 read).  s4r_decode_step_windowed then
+ * equals s4r_decode_step at length L with that qwin_prev (up to the rounding
+ * of the older rows' coefficients and of the summation order of the window
+ * mean), and stores the newest row's softmax in slot L mod q_window, so the
+ * next call, at length L + 1, finds the window of the step after: a sequence
+ * of windowed steps must run at consecutive lengths L, L + 1, ... (one
+ * appended token per step, as decoding does); the state is not valid for any
+ * other length.  Arguments and outputs of s4r_decode_step_windowed are those
+ * of s4r_decode_step with state in place of qwin_prev; q_window >= 2 and a
+ * uniform batch, else S4R_ERR_BAD_SHAPE / S4R_ERR_UNSUPPORTED.
+ */
+s4r_status s4r_window_state_size(const s4r_config* cfg, size_t* bytes);
+s4r_status s4r_window_state_init(const s4r_config* cfg, int64_t L, const float* qwin_prev,
+                                 const void* coef_k, float* state, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+s4r_status s4r_decode_step_windowed(const s4r_config* cfg, int64_t L, const void* q, float* state,
+                                    const void* sink_k, const void* sink_v, const void* win_k,
+                                    const void* win_v, const void* bases_k, const void* bases_v,
+                                    void* coef_k, void* coef_v, const void* k_new, const void* v_new,
+                                    float* out, int32_t* idx_out, float* scores_out, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/*
  * The fused decode step over a ragged batch (Section 3.2, each sequence at
  * its own length): lengths[b] (host memory, B entries, read before the call
  * returns) is sequence b's L, counted with the appended token when k_new /

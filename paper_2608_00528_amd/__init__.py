@@ -12,10 +12,12 @@ from ._lib import Config, S4RError  # noqa: F401
 _lib.load()
 
 from .api import (  # noqa: E402,F401
+    alloc_window_state,
     alloc_workspace,
     decode_step,
     decode_step_noalloc,
     decode_step_ragged,
+    decode_step_windowed,
     dense_decode,
     full_recon_decode,
     make_config,
@@ -38,6 +40,8 @@ from .api import (  # noqa: E402,F401
     timing_enable,
     timing_read,
     unpack_coef,
+    window_state_init,
+    window_state_size,
     value_config,
     version,
     workspace_size,

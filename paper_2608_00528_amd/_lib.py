@@ -22,6 +22,7 @@ EXPORTS = (
     "s4r_dense_decode", "s4r_prefill_project", "s4r_decode_step_ragged",
     "s4r_full_recon_decode", "s4r_prefill_num_samples", "s4r_prefill_bases_workspace_size", "s4r_prefill_bases",
     "s4r_project_queries", "s4r_decode_step_noalloc",
+    "s4r_window_state_size", "s4r_window_state_init", "s4r_decode_step_windowed",
 )
 
 
@@ -83,6 +84,10 @@ _SIGS = {
                                        _P, _P]),
     "s4r_decode_step_ragged": (_I32, [_CFG, ctypes.POINTER(_I64), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       _P, _P, _P, _P, _P, _SZ, _P]),
+    "s4r_window_state_size": (_I32, [_CFG, ctypes.POINTER(_SZ)]),
+    "s4r_window_state_init": (_I32, [_CFG, _I64, _P, _P, _P, _P, _SZ, _P]),
+    "s4r_decode_step_windowed": (_I32, [_CFG, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                        _P, _SZ, _P]),
 }
 
 _lib = None

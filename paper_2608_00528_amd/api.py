@@ -196,6 +196,49 @@ def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v
     return out
 
 
+def window_state_size(cfg):
+    """Bytes of the window state [B, q_window, G, capacity] fp32."""
+    n = ctypes.c_size_t()
+    L.check(L.load().s4r_window_state_size(_cfgp(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def alloc_window_state(cfg, device="cuda"):
+    G = cfg.n_q_heads // cfg.n_kv_heads
+    return torch.zeros((cfg.batch, cfg.q_window, G, cfg.capacity), dtype=torch.float32, device=device)
+
+
+def window_state_init(cfg, length, qwin_prev, coef_k, state, ws):
+    """Softmax rows of the window's q_window - 1 older queries (their
+    coefficient rows qwin_prev [B, G, q_window - 1, R]) for a windowed step at
+    `length`."""
+    dt = storage_dtype(cfg)
+    L.check(L.load().s4r_window_state_init(
+        _cfgp(cfg), length, _ptr(qwin_prev, "qwin_prev", torch.float32), _ptr(coef_k, "coef_k", dt),
+        _ptr(state, "state", torch.float32), _ptr(ws, "ws", torch.uint8), ws.numel(), _stream()))
+    return state
+
+
+def decode_step_windowed(cfg, length, q, state, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, ws,
+                         win_k=None, win_v=None, k_new=None, v_new=None, out=None, idx_out=None, scores_out=None):
+    """The fused step with the window state in place of qwin_prev (steps at
+    consecutive lengths); the newest query row's softmax is stored in it."""
+    dt = storage_dtype(cfg)
+    if out is None:
+        out = torch.empty((cfg.batch, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device=q.device)
+    need_sink = cfg.n_sink > 0
+    L.check(L.load().s4r_decode_step_windowed(
+        _cfgp(cfg), length, _ptr(q, "q", dt), _ptr(state, "state", torch.float32),
+        _ptr(sink_k, "sink_k", dt, need_sink), _ptr(sink_v, "sink_v", dt, need_sink),
+        _ptr(win_k, "win_k", dt, False), _ptr(win_v, "win_v", dt, False),
+        _ptr(bases_k, "bases_k", dt), _ptr(bases_v, "bases_v", dt), _ptr(coef_k, "coef_k", dt),
+        _ptr(coef_v, "coef_v", dt), _ptr(k_new, "k_new", dt, False), _ptr(v_new, "v_new", dt, False),
+        _ptr(out, "out", torch.float32), _ptr(idx_out, "idx_out", torch.int32, False),
+        _ptr(scores_out, "scores_out", torch.float32, False), _ptr(ws, "ws", torch.uint8), ws.numel(),
+        _stream()))
+    return out
+
+
 def decode_step_noalloc(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v, qwin_prev=None,
                         win_k=None, win_v=None, k_new=None, v_new=None, out=None, idx_out=None, scores_out=None):
     """The fused step on the library's own per-device scratch (no workspace

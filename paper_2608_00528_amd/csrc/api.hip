@@ -152,7 +152,7 @@ Layout layout(const Problem& P) {
   sizes[kRunM] = B * (size_t)gw_padded(P) * P.nruns_max * 4;
   sizes[kWgStats] = B * GW * P.nwg_max * 2 * 8;
   sizes[kAtilde] = B * cap * 4;
-  sizes[kHist] = B * 2 * kHistBins * 4;
+  sizes[kHist] = B * kHistStride * 4;
   sizes[kCand] = B * cand_stride(P) * 8;
   sizes[kBitmap] = B * bitmap_words(cap) * 4;
   sizes[kIdx] = B * P.m_max * 4;
@@ -542,11 +542,14 @@ s4r_status s4r_prefill_bases(const s4r_config* cfg, int64_t n_rows, const void* 
 
 // the fused step for a uniform (P.lens.n == 0) or ragged batch; L is the
 // largest length, already checked against the capacity
+// state (windowed step, q_window > 1): the window state replaces qwin_prev;
+// only the newest query row is projected and scored
 static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, const float* qwin_prev,
                                    const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
                                    const void* bases_k, const void* bases_v, void* coef_k, void* coef_v,
                                    const void* k_new, const void* v_new, float* out, int32_t* idx_out,
-                                   float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                                   float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream,
+                                   float* state = nullptr) {
   s4r_status st = S4R_OK;
   if (!attention_supported(P))
     return fail(S4R_ERR_UNSUPPORTED, "fused attention not built for G = %d, rank = %d", P.G, P.rank);
@@ -562,8 +565,15 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
     S4R_REQ(sink_k);
     S4R_REQ(sink_v);
   }
-  if (P.Wq > 1) S4R_REQ(qwin_prev);
-  else if (qwin_prev) return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
+  if (state) {
+    if (P.Wq < 2) return fail(S4R_ERR_BAD_SHAPE, "the windowed step needs q_window >= 2 (got %d)", P.Wq);
+    if (P.lens.n) return fail(S4R_ERR_UNSUPPORTED, "the windowed step takes a uniform batch");
+    S4R_REQ(state);
+  } else if (P.Wq > 1) {
+    S4R_REQ(qwin_prev);
+  } else if (qwin_prev) {
+    return fail(S4R_ERR_BAD_SHAPE, "qwin_prev must be NULL when q_window == 1");
+  }
   if ((win_k == nullptr) != (win_v == nullptr)) return fail(S4R_ERR_NULL_ARG, "win_k and win_v must both be given or both NULL");
   if ((k_new == nullptr) != (v_new == nullptr)) return fail(S4R_ERR_NULL_ARG, "k_new and v_new must both be given or both NULL");
   S4R_OPT(win_k);
@@ -594,22 +604,33 @@ static s4r_status decode_step_impl(const Problem& P, int64_t L, const void* q, c
     if (e != hipSuccess || !timed) return e;
     return hipEventRecord(start ? g_timing.start[slot + kernel] : g_timing.stop[slot + kernel], stream);
   };
+  // the projection and scoring problem: the whole window, or (windowed) the
+  // newest row alone, whose G columns see every key
+  Problem PS = P;
+  if (state) {
+    PS.Wq = 1;
+    PS.GW = P.G;
+  }
   hipError_t e = mark(hipSuccess, 0, true);
   if (e == hipSuccess && k_new)   // the new token's rows with the query coefficients: the scoring pass reads row L - 1
-    e = launch_project_step(P, w, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, qwin_prev, L - 1, stream);
+    e = launch_project_step(PS, w, q, bases_k, bases_v, k_new, v_new, coef_k, coef_v, state ? nullptr : qwin_prev,
+                            L - 1, stream);
   else if (e == hipSuccess)
-    e = launch_project_query(P, w, q, bases_k, qwin_prev, nullptr, true, stream);
+    e = launch_project_query(PS, w, q, bases_k, state ? nullptr : qwin_prev, nullptr, true, stream);
   e = mark(e, 0, false);
   e = mark(e, 1, true);
-  if (e == hipSuccess) e = launch_score_stream(P, w, L, coef_k, stream);
+  if (e == hipSuccess) e = launch_score_stream(PS, w, L, coef_k, stream);
   e = mark(e, 1, false);
   e = mark(e, 2, true);
-  if (e == hipSuccess) e = launch_relevance(P, w, L, scores_out, stream);
+  if (e == hipSuccess)
+    e = state ? launch_relevance_windowed(PS, w, L, scores_out, state, P.Wq, stream)
+              : launch_relevance(P, w, L, scores_out, stream);
   e = mark(e, 2, false);
   e = mark(e, 3, true);
   // the key the relevance kernel built the histogram with
   if (e == hipSuccess)
-    e = launch_select_keyed(P, w, L, w.atilde, P.cap, w.idx, idx_out, fused_key_shift(P, L), stream);
+    e = launch_select_keyed(P, w, L, w.atilde, P.cap, w.idx, idx_out, fused_key_shift(P, L),
+                            relevance_hist_copies(state ? PS : P, L, state ? P.Wq : 0), stream);
   e = mark(e, 3, false);
   if (e == hipSuccess)
     e = launch_attention(P, w, L, m, k_eff, q, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, out,
@@ -630,6 +651,53 @@ s4r_status s4r_decode_step(const s4r_config* cfg, int64_t L, const void* q, cons
   if ((st = check_L(P, L))) return st;
   return decode_step_impl(P, L, q, qwin_prev, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
                           v_new, out, idx_out, scores_out, ws, ws_bytes, stream);
+}
+
+s4r_status s4r_window_state_size(const s4r_config* cfg, size_t* bytes) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (!bytes) return fail(S4R_ERR_NULL_ARG, "bytes is NULL");
+  if (P.Wq < 2) return fail(S4R_ERR_BAD_SHAPE, "the window state needs q_window >= 2 (got %d)", P.Wq);
+  *bytes = (size_t)P.B * P.Wq * P.G * P.cap * sizeof(float);
+  return ok();
+}
+
+s4r_status s4r_window_state_init(const s4r_config* cfg, int64_t L, const float* qwin_prev, const void* coef_k,
+                                 float* state, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if (P.Wq < 2) return fail(S4R_ERR_BAD_SHAPE, "the window state needs q_window >= 2 (got %d)", P.Wq);
+  if ((st = check_L(P, L))) return st;
+  S4R_REQ(qwin_prev);
+  S4R_REQ(coef_k);
+  S4R_REQ(state);
+  if ((st = check_ws(P, ws, ws_bytes))) return st;
+  Workspace w = carve_workspace(P, ws);
+  // the window's W_q - 1 older rows as a query window of their own, scored
+  // to length L - 1: row r's causal limit is then key L - W_q + r, its own
+  Problem P0 = P;
+  P0.Wq = P.Wq - 1;
+  P0.GW = P.G * P0.Wq;
+  hipError_t e = launch_query_image_rows(P0, w, qwin_prev, stream);
+  if (e == hipSuccess) e = launch_score_stream(P0, w, L - 1, coef_k, stream);
+  if (e == hipSuccess) e = launch_window_store(P0, w, L, state, P.Wq, stream);
+  return hip_status(e, "s4r_window_state_init launch");
+}
+
+s4r_status s4r_decode_step_windowed(const s4r_config* cfg, int64_t L, const void* q, float* state,
+                                    const void* sink_k, const void* sink_v, const void* win_k, const void* win_v,
+                                    const void* bases_k, const void* bases_v, void* coef_k, void* coef_v,
+                                    const void* k_new, const void* v_new, float* out, int32_t* idx_out,
+                                    float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  s4r_status st = make_problem(cfg, P);
+  if (st) return st;
+  if ((st = check_L(P, L))) return st;
+  if (!state) return fail(S4R_ERR_NULL_ARG, "state is NULL");
+  return decode_step_impl(P, L, q, nullptr, sink_k, sink_v, win_k, win_v, bases_k, bases_v, coef_k, coef_v, k_new,
+                          v_new, out, idx_out, scores_out, ws, ws_bytes, stream, state);
 }
 
 s4r_status s4r_decode_step_ragged(const s4r_config* cfg, const int64_t* lengths, const void* q,

@@ -178,8 +178,10 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   load_x(0);
   // the step's two selection histograms start from zero (the relevance and
   // classify kernels add to them later in the step)
-  if (cblk == 0)
-    for (int i = t; i < 2 * kHistBins; i += blockDim.x) hist[(int64_t)b * 2 * kHistBins + i] = 0u;
+  if (cblk == 0) {
+    uint4* hz = reinterpret_cast<uint4*>(hist + (int64_t)b * kHistStride);
+    for (int i = t; i < kHistStride / 4; i += blockDim.x) hz[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
 
   __shared__ double red[4][32];
   for (int v0 = 0; v0 < G; v0 += kQVec) {
@@ -364,6 +366,31 @@ hipError_t launch_project_query(const Problem& P, const Workspace& ws, const voi
     launch_query_c<uint16_t>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st);
   else
     launch_query_c<float>(P, ws, q, bases_k, qwin_prev, qcoef_out, img, st);
+  return hipGetLastError();
+}
+
+// the scoring kernel's operand image of a query window given entirely as
+// coefficient rows (the window state's set-up): rows [B][G][n_rows][R] fp32,
+// one thread per four latent columns of a row
+__global__ __launch_bounds__(256) void k_query_image_rows(const float* __restrict__ rows, uint16_t* __restrict__ qimg,
+                                                          int B, int G, int n_rows, int R, int ncb, int nmb) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int nu = R / 4;
+  if (i >= (int64_t)B * G * n_rows * nu) return;
+  const int u = (int)(i % nu), j = (int)((i / nu) % n_rows), g = (int)((i / ((int64_t)nu * n_rows)) % G);
+  const int b = (int)(i / ((int64_t)nu * n_rows * G));
+  const float4 x = *reinterpret_cast<const float4*>(rows + (((int64_t)b * G + g) * n_rows + j) * R + 4 * u);
+  uint2 pk[3];
+  qimg_pack4(x, pk);
+  uint16_t* p = qimg_at(qimg, b, ncb, nmb, R, g * n_rows + j, 4 * u);
+#pragma unroll
+  for (int part = 0; part < 3; ++part) *reinterpret_cast<uint2*>(p + part * R) = pk[part];
+}
+
+hipError_t launch_query_image_rows(const Problem& P0, const Workspace& ws, const float* rows, hipStream_t st) {
+  const int64_t n = (int64_t)P0.B * P0.G * P0.Wq * (P0.R / 4);
+  hipLaunchKernelGGL(k_query_image_rows, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, rows, ws.qimg, P0.B,
+                     P0.G, P0.Wq, P0.R, col_blocks(P0), qimg_mfmas(P0));
   return hipGetLastError();
 }
 

@@ -98,12 +98,18 @@ __device__ __forceinline__ void pool_aggregate(const float* __restrict__ vs, int
   }
 }
 
-template <int NQ, int TPT, bool WQ1>
+// WIN (windowed step, query window of wrows rows): the stream scored only
+// the newest query row (its G columns, Wq = 1 here); the softmax of each
+// older row over its own keys comes from the window state
+// [B][wrows][G][cap], row slot L_r mod wrows for the row that was newest at
+// length L_r (it covers keys < L_r).  This kernel adds the newest row's
+// softmax to the older rows' for the window mean and stores it in its slot.
+template <int NQ, int TPT, bool WQ1, bool WIN>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
     int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
-    Lens lens, int key_shift) {
+    Lens lens, int key_shift, float* __restrict__ state, int wrows, int hist_nc) {
   constexpr int GWP = 4 * NQ;
   constexpr int CHUNK = kRelThreads * TPT;
   constexpr int SPAN_MAX = CHUNK + 64;
@@ -230,7 +236,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   __syncthreads();
   // ---- window mean over the W_q rows of every staged position -------------------------
   const float pad = (pool_mode == S4R_POOL_MAX) ? -INFINITY : 0.f;
-  const float inv_wq = 1.f / (float)Wq;
+  const float inv_wq = 1.f / (float)(WIN ? wrows : Wq);
 #pragma unroll
   for (int k = 0; k < PPT; ++k) {
     const int i = t + k * kRelThreads;
@@ -246,7 +252,20 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
         ex[4 * q + 2] = ev[k][q].z;
         ex[4 * q + 3] = ev[k][q].w;
       }
-      if constexpr (WQ1) {
+      if constexpr (WIN) {
+        // the newest row's softmax: into its slot (own chunk) and into LDS;
+        // the older rows are added below
+        float* sb = state + (int64_t)b * wrows * G * cap;
+        const int slot_new = L % wrows;
+#pragma unroll
+        for (int c = 0; c < GWP; ++c) {
+          if (c < G) {
+            const float pn = in ? ex[c] * fr[c] : 0.f;
+            if (in && x >= t0 && x < t0 + CHUNK) sb[((int64_t)slot_new * G + c) * cap + x] = pn;
+            vs[c * span + i] = pn;
+          }
+        }
+      } else if constexpr (WQ1) {
 #pragma unroll
         for (int c = 0; c < GWP; ++c)
           if (c < G) vs[c * span + i] = in ? ex[c] * fr[c] : pad;
@@ -262,6 +281,49 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     }
   }
   __syncthreads();
+  if constexpr (WIN) {
+    // ---- older rows of the window: row of age a = 1 .. wrows - 1 covers keys
+    // < L - a, in slot (L - a) mod wrows.  Unit u = four consecutive positions
+    // 4 (u0 + u) .. + 3 (16-byte loads, unconditional at clamped positions,
+    // masked after) of group g; eight rows in flight per batch
+    const float* sb = state + (int64_t)b * wrows * G * cap;
+    const int u0 = (x0 >= 0 ? x0 : x0 - 3) / 4;         // floor(x0 / 4)
+    const int nu = (x0 + span + 3) / 4 - u0;             // units covering the staged positions
+    for (int w = t; w < G * nu; w += kRelThreads) {
+      const int g = w / nu, xu = 4 * (u0 + w % nu);      // first position of the unit
+      const int xl = min(max(xu, 0), (int)(cap - 4));
+      float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int a0 = 1; a0 < wrows; a0 += 8) {
+        float4 o[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const int a = min(a0 + v, wrows - 1);
+          const int slot = ((L - a) % wrows + wrows) % wrows;   // L - a < 0 early on: masked below
+          o[v] = *reinterpret_cast<const float4*>(sb + ((int64_t)slot * G + g) * cap + xl);
+        }
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const int lim = L - (a0 + v);                  // keys of this row
+          if (a0 + v < wrows) {
+            if (xl + 0 < lim) sum.x += o[v].x;
+            if (xl + 1 < lim) sum.y += o[v].y;
+            if (xl + 2 < lim) sum.z += o[v].z;
+            if (xl + 3 < lim) sum.w += o[v].w;
+          }
+        }
+      }
+      const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int x = xu + j, i = x - x0;
+        if (i >= 0 && i < span) {
+          const bool in = x >= 0 && x < L && xl == xu;
+          vs[g * span + i] = in ? (vs[g * span + i] + sv[j]) * inv_wq : pad;
+        }
+      }
+    }
+    __syncthreads();
+  }
   // ---- pooling (kappa, stride 1, same length) and aggregation over G -------------------
   float af[TPT];
   switch (h) {
@@ -284,7 +346,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   __syncthreads();
   // this workgroup's histogram into the sequence's (zeroed by the query
   // projection earlier in the step): one global atomic per non-empty bin
-  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
+  uint32_t* hs = hist + (int64_t)b * kHistStride + (blockIdx.x & (hist_nc - 1)) * kHistBins;
   for (int i = t; i < kHistBins; i += kRelThreads) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
@@ -305,7 +367,8 @@ template <int GMAX>
 __global__ __launch_bounds__(kRelThreads) void k_relevance_wide(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ col_stats,
     float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out, int64_t cap, int L,
-    int n_hist, int G, int Wq, int gwp, int kappa, int pool_mode, int agg, int ntiles_cap, Lens lens, int key_shift) {
+    int n_hist, int G, int Wq, int gwp, int kappa, int pool_mode, int agg, int ntiles_cap, Lens lens, int key_shift,
+    int hist_nc) {
   const int b = blockIdx.y;
   const int score_stride = L;
   {
@@ -379,7 +442,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance_wide(
   }
   if (x < n_hist) atomicAdd(&hl[selection_key_shift(af[0], key_shift) >> kHistShift], 1u);
   __syncthreads();
-  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
+  uint32_t* hs = hist + (int64_t)b * kHistStride + (blockIdx.x & (hist_nc - 1)) * kHistBins;
   for (int i = t; i < kHistBins; i += kRelThreads) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
@@ -394,7 +457,7 @@ __global__ __launch_bounds__(256) void k_zero_hist(uint32_t* __restrict__ hist, 
 }
 
 __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ scores, uint32_t* __restrict__ hist,
-                                                     int L, int n_hist) {
+                                                     int L, int n_hist, int hist_nc) {
   const int b = blockIdx.y;
   __shared__ uint32_t hl[kHistBins];
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) hl[i] = 0;
@@ -405,7 +468,7 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
     if (x < n_hist) atomicAdd(&hl[selection_key(scores[(int64_t)b * L + x]) >> kHistShift], 1u);
   }
   __syncthreads();
-  uint32_t* hs = hist + (int64_t)b * 2 * kHistBins;
+  uint32_t* hs = hist + (int64_t)b * kHistStride + (blockIdx.x & (hist_nc - 1)) * kHistBins;
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
     const uint32_t c = hl[i];
     if (c) atomicAdd(&hs[i], c);
@@ -458,13 +521,14 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   constexpr int chunk = kRelThreads * TPT;
   const size_t lds = (size_t)P.G * (chunk + 2 * (P.kappa / 2)) * sizeof(float);
   dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
-  auto kern = P.Wq == 1 ? k_relevance<NQ, TPT, true> : k_relevance<NQ, TPT, false>;
+  auto kern = P.Wq == 1 ? k_relevance<NQ, TPT, true, false> : k_relevance<NQ, TPT, false, false>;
   const int nwg = score_workgroups(P, L);
   const bool fold = nwg > 64 * kRelStatPer;
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), nwg, P.lens, fused_key_shift(P, L));
+                     (int)(P.cap / kTileTok), nwg, P.lens, fused_key_shift(P, L), nullptr, 1,
+                     hist_copies(grid.x));
 }
 
 template <int NQ>
@@ -486,7 +550,7 @@ static void launch_rel_wide(const Problem& P, const Workspace& ws, int64_t L, fl
   auto kern = P.G <= 4 ? k_relevance_wide<4> : (P.G <= 8 ? k_relevance_wide<8> : k_relevance_wide<16>);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.col_stats, ws.atilde, ws.hist,
                      scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, gw_padded(P), P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), P.lens, fused_key_shift(P, L));
+                     (int)(P.cap / kTileTok), P.lens, fused_key_shift(P, L), hist_copies(grid.x));
 }
 
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out, hipStream_t st) {
@@ -503,12 +567,88 @@ hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, fl
   return hipGetLastError();
 }
 
+template <int NQ, int TPT>
+static void launch_rel_win_t(const Problem& P1, const Workspace& ws, int64_t L, float* scores_out, float* state,
+                             int wrows, hipStream_t st) {
+  const int n_hist = (int)std::max<int64_t>(L - P1.W, 0);
+  constexpr int chunk = kRelThreads * TPT;
+  const size_t lds = (size_t)P1.G * (chunk + 2 * (P1.kappa / 2)) * sizeof(float);
+  dim3 grid((unsigned)((L + chunk - 1) / chunk), P1.B);
+  const int nwg = score_workgroups(P1, L);
+  const bool fold = nwg > 64 * kRelStatPer;
+  if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P1.GW, P1.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P1.GW, nwg);
+  hipLaunchKernelGGL((k_relevance<NQ, TPT, true, true>), grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
+                     fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P1.cap, (int)L, n_hist, P1.G, 1,
+                     P1.kappa, P1.pool_mode, P1.agg, (int)(P1.cap / kTileTok), nwg, P1.lens, fused_key_shift(P1, L),
+                     state, wrows, hist_copies(grid.x));
+}
+
+int relevance_hist_copies(const Problem& P, int64_t L, int wrows) {
+  const int chunk = (wrows < 2 && P.GW > kColBlk) ? kWideChunk : relevance_chunk(P, L);
+  return hist_copies((L + chunk - 1) / chunk);
+}
+
+template <int NQ>
+static void launch_rel_win_nq(const Problem& P1, const Workspace& ws, int64_t L, float* scores_out, float* state,
+                              int wrows, hipStream_t st) {
+  switch (relevance_chunk(P1, L)) {
+    case 1024: launch_rel_win_t<NQ, 4>(P1, ws, L, scores_out, state, wrows, st); break;
+    case 512: launch_rel_win_t<NQ, 2>(P1, ws, L, scores_out, state, wrows, st); break;
+    default: launch_rel_win_t<NQ, 1>(P1, ws, L, scores_out, state, wrows, st); break;
+  }
+}
+
+hipError_t launch_relevance_windowed(const Problem& P1, const Workspace& ws, int64_t L, float* scores_out,
+                                     float* state, int wrows, hipStream_t st) {
+  switch (gw_padded(P1) / 4) {
+    case 1: launch_rel_win_nq<1>(P1, ws, L, scores_out, state, wrows, st); break;
+    case 2: launch_rel_win_nq<2>(P1, ws, L, scores_out, state, wrows, st); break;
+    case 3: launch_rel_win_nq<3>(P1, ws, L, scores_out, state, wrows, st); break;
+    default: launch_rel_win_nq<4>(P1, ws, L, scores_out, state, wrows, st); break;
+  }
+  return hipGetLastError();
+}
+
+// window state of the W_q - 1 older rows from a stream over them (P0: those
+// rows as the query window, scored to length L - 1): row r < wrows - 1 covers
+// keys < L_r = L - (wrows - 1 - r) and goes to slot L_r mod wrows.  grid
+// (ceil(L / 256), B); the softmax probability of (row, group, key) is its exp
+// value times exp(ref - M) / S of its tile and column (fp64 argument, as in
+// the relevance kernel).
+__global__ __launch_bounds__(256) void k_window_store(const float* __restrict__ e, const float* __restrict__ tref,
+                                                      const double* __restrict__ col_stats, float* __restrict__ state,
+                                                      int64_t cap, int L, int G, int wrows, int gwp, int ntiles_cap) {
+  const int b = blockIdx.y, x = blockIdx.x * 256 + threadIdx.x;
+  const int w0 = wrows - 1;                       // rows in the stream, column c = g * w0 + r
+  if (x >= L) return;
+  for (int g = 0; g < G; ++g)
+    for (int r = 0; r < w0; ++r) {
+      const int Lr = L - (w0 - r);
+      if (x >= Lr) continue;
+      const int c = g * w0 + r;
+      const double2 cs = reinterpret_cast<const double2*>(col_stats)[(int64_t)b * G * w0 + c];
+      const float ref = tref[((int64_t)b * ntiles_cap + x / kTileTok) * gwp + c];
+      const float fac = (ref != -INFINITY) ? (float)((double)exp_neg_accurate((double)ref - cs.x) * cs.y) : 0.f;
+      state[(((int64_t)b * wrows + Lr % wrows) * G + g) * cap + x] = e[((int64_t)b * cap + x) * gwp + c] * fac;
+    }
+}
+
+hipError_t launch_window_store(const Problem& P0, const Workspace& ws, int64_t L, float* state, int wrows,
+                               hipStream_t st) {
+  const int nwg = score_workgroups(P0, L - 1);
+  hipLaunchKernelGGL(k_fold_stats, dim3(P0.GW, P0.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P0.GW, nwg);
+  hipLaunchKernelGGL(k_window_store, dim3((unsigned)((L + 255) / 256), P0.B), dim3(256), 0, st, ws.e, ws.run_m,
+                     ws.col_stats, state, P0.cap, (int)L, P0.G, wrows, gw_padded(P0), (int)(P0.cap / kTileTok));
+  return hipGetLastError();
+}
+
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores, hipStream_t st) {
   const int n_hist = (int)std::max<int64_t>(L - P.W, 0);
   const int ng = std::max(1, (n_hist + kHistChunk - 1) / kHistChunk);
-  hipLaunchKernelGGL(k_zero_hist, dim3((P.B * 2 * kHistBins + 255) / 256), dim3(256), 0, st, ws.hist,
-                     P.B * 2 * kHistBins);
-  hipLaunchKernelGGL(k_hist_scores, dim3(ng, P.B), dim3(256), 0, st, scores, ws.hist, (int)L, n_hist);
+  hipLaunchKernelGGL(k_zero_hist, dim3((P.B * kHistStride + 255) / 256), dim3(256), 0, st, ws.hist,
+                     P.B * kHistStride);
+  hipLaunchKernelGGL(k_hist_scores, dim3(ng, P.B), dim3(256), 0, st, scores, ws.hist, (int)L, n_hist,
+                     hist_copies(ng));
   return hipGetLastError();
 }
 

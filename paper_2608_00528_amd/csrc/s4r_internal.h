@@ -15,6 +15,19 @@ namespace s4r {
 constexpr int kScoreWaves = 4;        // waves per scoring workgroup
 constexpr int kHistBins = 2048;       // top-11-bit radix histogram of the scores
 constexpr int kHistShift = 21;
+// copies of the top-level histogram: workgroup i of a sequence adds into copy
+// i mod nc and the selection sums the nc copies.  Global atomics on one address
+// from hundreds of workgroups serialise (about 4 us for 469 workgroups
+// flushing 32 bins into one copy on MI355X, none measurable with 8 copies).
+constexpr int kHistCopies = 8;
+constexpr int kHistStride = (kHistCopies + 1) * kHistBins;   // per sequence: the copies, then level 2
+// copies for a histogram that `wgs` workgroups per sequence flush: one per 64
+// workgroups, a power of two up to kHistCopies
+inline int hist_copies(int64_t wgs) {
+  int nc = 1;
+  while (nc < kHistCopies && wgs > 64 * nc) nc *= 2;
+  return nc;
+}
 constexpr int kHistChunk = 2048;      // tokens per histogram workgroup (standalone selection)
 constexpr int kSelChunk = 2048;       // tokens per selection workgroup (multiple of 32)
 constexpr int kMaxSelGroups = 4096;   // classify workgroups per sequence (capacity <= 4096 * kSelChunk)
@@ -72,7 +85,7 @@ struct Workspace {
   double* wg_stats;     // [B][GW][nwg_max][2] per scoring workgroup (max, sum)
   double* col_stats;    // [B][GW][2]     global (max, 1 / sum) per query column, when folded by k_fold_stats
   float* atilde;        // [B][cap]       relevance scores
-  uint32_t* hist;       // [B][2][kHistBins]  selection histograms: top 11 key bits, next 11 of the boundary bin
+  uint32_t* hist;       // [B][kHistCopies + 1][kHistBins]  selection histograms: copies of the top 11 key bits, next 11 of the boundary bin
   uint64_t* cand;       // [B][cand_stride]  per-classify-workgroup candidate regions (key << 32 | ~index)
   uint32_t* cand_count; // [B][sel_groups_max] candidates found by each classify workgroup
   uint32_t* above_count; // [B][sel_groups_max] positions above the boundary bin per classify workgroup
@@ -112,9 +125,21 @@ hipError_t launch_project_query(const Problem& P, const Workspace& ws, const voi
                                 const float* qwin_prev, float* qcoef_out, bool image, hipStream_t st);
 hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void* bases_v, const void* k_new,
                                const void* v_new, void* coef_k, void* coef_v, int64_t row, hipStream_t st);
+// the operand image of a window given as coefficient rows [B][G][Wq][R] (P0.Wq rows)
+hipError_t launch_query_image_rows(const Problem& P0, const Workspace& ws, const float* rows, hipStream_t st);
+// windowed relevance (P1: the newest row's G columns, Wq = 1): the older rows'
+// softmax from the window state [B][wrows][G][cap], the newest stored in its slot
+hipError_t launch_relevance_windowed(const Problem& P1, const Workspace& ws, int64_t L, float* scores_out,
+                                     float* state, int wrows, hipStream_t st);
+// window state of the older rows from a stream over them (P0: wrows - 1 rows, length L - 1)
+hipError_t launch_window_store(const Problem& P0, const Workspace& ws, int64_t L, float* state, int wrows,
+                               hipStream_t st);
 hipError_t launch_score_stream(const Problem& P, const Workspace& ws, int64_t L, const void* coef_k, hipStream_t st);
 hipError_t launch_relevance(const Problem& P, const Workspace& ws, int64_t L, float* scores_out,
                             hipStream_t st);
+// histogram copies the step's relevance kernel flushes into (wrows >= 2: the
+// windowed kernel over P with W_q = 1)
+int relevance_hist_copies(const Problem& P, int64_t L, int wrows);
 hipError_t launch_hist_only(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                             hipStream_t st);
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,

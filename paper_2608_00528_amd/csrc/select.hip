@@ -60,17 +60,37 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scratch /* >= 4 *
   return total;
 }
 
-// boundary bin of a 2048-bin histogram: the highest bin b with
-// count(bins >= b) >= kk; `above` = count(bins > b).  The bins are loaded
-// with unguarded, independent loads (8 per thread, thread 0 = top bins).
-__device__ void find_boundary(const uint32_t* __restrict__ hist, uint32_t kk, uint32_t* scratch, int& b1,
+// boundary bin of a 2048-bin histogram held as nc <= NC copies (summed here):
+// the highest bin b with count(bins >= b) >= kk; `above` = count(bins > b).
+// The bins are loaded with independent 16-byte loads (8 consecutive bins of
+// every copy per thread, thread 0 = top bins; copies past nc repeat the last
+// one's address, cache hits, and are not added).
+template <int NC>
+__device__ void find_boundary(const uint32_t* __restrict__ hist, int nc, uint32_t kk, uint32_t* scratch, int& b1,
                               uint32_t& above) {
   constexpr int per = kHistBins / kSelThreads;
+  static_assert(per == 8, "two 16-byte loads per copy");
   const int t = threadIdx.x;
-  uint32_t cnt[per];
-  uint32_t sum = 0;
+  const int lo = kHistBins - per * (t + 1);          // this thread's lowest bin
+  uint4 part[NC][2];
 #pragma unroll
-  for (int i = 0; i < per; ++i) cnt[i] = hist[kHistBins - 1 - (t * per + i)];
+  for (int c = 0; c < NC; ++c) {
+    const uint4* hp = reinterpret_cast<const uint4*>(hist + min(c, nc - 1) * kHistBins + lo);
+    part[c][0] = hp[0];
+    part[c][1] = hp[1];
+  }
+  uint32_t cnt[per];                                 // cnt[i]: bin kHistBins - 1 - (t * per + i)
+#pragma unroll
+  for (int i = 0; i < per; ++i) cnt[i] = 0u;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const uint32_t v[per] = {part[c][0].x, part[c][0].y, part[c][0].z, part[c][0].w,
+                             part[c][1].x, part[c][1].y, part[c][1].z, part[c][1].w};
+#pragma unroll
+    for (int i = 0; i < per; ++i)
+      if (c < nc) cnt[i] += v[per - 1 - i];
+  }
+  uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < per; ++i) sum += cnt[i];
   uint32_t excl;
@@ -101,15 +121,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
     const float* __restrict__ scores, int64_t score_stride, uint32_t* __restrict__ hist_all,
     uint64_t* __restrict__ cand_all, uint32_t* __restrict__ bitmap_all, uint32_t* __restrict__ cand_count,
     uint32_t* __restrict__ above_count, uint32_t* __restrict__ sel_info, int64_t cand_stride, int64_t cnt_stride,
-    int64_t cap, int L, int W, int k, Lens lens, int key_shift) {
+    int64_t cap, int L, int W, int k, Lens lens, int key_shift, int hist_nc) {
   const int b = blockIdx.y, c = blockIdx.x;
   L = (int)len_of(lens, b, L);
   const int t = threadIdx.x, lane = t & 63;
   const int n_hist = max(L - W, 0);
   const int k_eff = min(k, n_hist);
   if (k_eff == 0 || c * kSelChunk >= n_hist) return;   // (a shorter sequence of a ragged batch)
-  uint32_t* hist1 = hist_all + (int64_t)b * 2 * kHistBins;
-  uint32_t* hist2 = hist1 + kHistBins;
+  uint32_t* hist1 = hist_all + (int64_t)b * kHistStride;
+  uint32_t* hist2 = hist1 + kHistCopies * kHistBins;
   uint64_t* cand = cand_all + (int64_t)b * cand_stride + (int64_t)c * kSelChunk;
   const float* sc = scores + (int64_t)b * score_stride;
   const int c0 = c * kSelChunk;
@@ -125,7 +145,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
   if (t == 0) s_count = 0u;
   int b1;
   uint32_t above1;
-  find_boundary(hist1, (uint32_t)k_eff, scratch, b1, above1);
+  find_boundary<kHistCopies>(hist1, hist_nc, (uint32_t)k_eff, scratch, b1, above1);
   if (c == 0 && t == 0) {
     sel_info[b * 4 + 0] = (uint32_t)b1;
     sel_info[b * 4 + 1] = above1;
@@ -204,7 +224,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
     }
   }
   if (k_eff == 0 || c >= max(nch, 1)) return;          // (a shorter sequence of a ragged batch)
-  const uint32_t* hist2 = hist_all + (int64_t)b * 2 * kHistBins + kHistBins;
+  const uint32_t* hist2 = hist_all + (int64_t)b * kHistStride + kHistCopies * kHistBins;
   const uint64_t* cand_b = cand_all + (int64_t)b * cand_stride;
 
   __shared__ uint32_t scratch[kSelThreads / 64];
@@ -231,7 +251,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   const uint32_t need = (uint32_t)k_eff - above1;        // >= 1
   int b2;
   uint32_t above2;
-  find_boundary(hist2, need, scratch, b2, above2);
+  find_boundary<1>(hist2, 1, need, scratch, b2, above2);
   const uint32_t need3 = need - above2;                  // >= 1, taken from sub-bin b2
   // prefix of the candidate counts (chunk order), chosen counters cleared
   uint32_t csum = 0;
@@ -397,18 +417,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
 
 hipError_t launch_select(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
                          int64_t score_stride, int32_t* idx, int32_t* idx_copy, hipStream_t st) {
-  return launch_select_keyed(P, ws, L, scores, score_stride, idx, idx_copy, 1, st);
+  const int64_t n_hist = std::max<int64_t>(L - P.W, 0);
+  const int ng = (int)std::max<int64_t>(1, (n_hist + kHistChunk - 1) / kHistChunk);   // k_hist_scores' workgroups
+  return launch_select_keyed(P, ws, L, scores, score_stride, idx, idx_copy, 1, hist_copies(ng), st);
 }
 
 hipError_t launch_select_keyed(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
-                               int64_t score_stride, int32_t* idx, int32_t* idx_copy, int key_shift, hipStream_t st) {
+                               int64_t score_stride, int32_t* idx, int32_t* idx_copy, int key_shift, int hist_nc,
+                               hipStream_t st) {
   const int64_t n_hist = std::max<int64_t>(L - P.W, 0);
   const int m = (int)(std::min<int64_t>(P.k, n_hist) + std::min<int64_t>(P.W, L));
   const int nch = (int)((n_hist + kSelChunk - 1) / kSelChunk);
   if (std::min<int64_t>(P.k, n_hist) > 0) {
     hipLaunchKernelGGL(k_select_classify, dim3(nch, P.B), dim3(kSelThreads), 0, st, scores, score_stride, ws.hist,
                        ws.cand, ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P),
-                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens, key_shift);
+                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens, key_shift, hist_nc);
   }
   hipLaunchKernelGGL(k_select_finish, dim3(std::max(nch, 1), P.B), dim3(kSelThreads), 0, st, ws.hist, ws.cand,
                      ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, idx, idx_copy, (int64_t)m,

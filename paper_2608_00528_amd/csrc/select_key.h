@@ -38,7 +38,9 @@ inline int fused_key_shift(const Problem& P, int64_t L) {
 }
 
 // the selection kernels with the key the scores' range allows
+// (hist_nc: the copies of the top-level histogram that its producer flushed into)
 hipError_t launch_select_keyed(const Problem& P, const Workspace& ws, int64_t L, const float* scores,
-                               int64_t score_stride, int32_t* idx, int32_t* idx_copy, int key_shift, hipStream_t st);
+                               int64_t score_stride, int32_t* idx, int32_t* idx_copy, int key_shift, int hist_nc,
+                               hipStream_t st);
 
 }  // namespace s4r

@@ -162,6 +162,35 @@ def test_decode_step_argument_errors():
     assert call(c=c0, sink=None) == L.S4R_ERR_BAD_SHAPE
 
 
+def test_window_state_entry_points():
+    """Window state: its size is B * q_window * G * capacity floats; every
+    entry point refuses q_window = 1 and missing or misaligned buffers before
+    launching anything, and the windowed step never takes qwin_prev."""
+    lib = L.load()
+    c1 = cfg()
+    cw = cfg(q_window=4)
+    n = ctypes.c_size_t()
+    assert lib.s4r_window_state_size(ctypes.byref(c1), ctypes.byref(n)) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_window_state_size(ctypes.byref(cw), None) == L.S4R_ERR_NULL_ARG
+    assert s4r.window_state_size(cw) == 2 * 4 * 4 * 1024 * 4
+    assert lib.s4r_window_state_init(ctypes.byref(c1), 100, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_window_state_init(ctypes.byref(cw), 100, None, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_window_state_init(ctypes.byref(cw), 100, FAKE, FAKE, None, FAKE, 1 << 40, None) == L.S4R_ERR_NULL_ARG
+    assert lib.s4r_window_state_init(ctypes.byref(cw), 100, FAKE, FAKE, FAKE_MIS, FAKE, 1 << 40, None) == \
+        L.S4R_ERR_MISALIGNED
+    assert lib.s4r_window_state_init(ctypes.byref(cw), 3, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_BAD_SHAPE
+    assert lib.s4r_window_state_init(ctypes.byref(cw), 100, FAKE, FAKE, FAKE, FAKE, 0, None) == L.S4R_ERR_WORKSPACE
+
+    def step(c=cw, state=FAKE, Lval=100, wsb=1 << 40):
+        return lib.s4r_decode_step_windowed(ctypes.byref(c), Lval, FAKE, state, FAKE, FAKE, None, None, FAKE, FAKE,
+                                            FAKE, FAKE, None, None, FAKE, None, None, FAKE, wsb, None)
+    assert step(state=None) == L.S4R_ERR_NULL_ARG
+    assert step(state=FAKE_MIS) == L.S4R_ERR_MISALIGNED
+    assert step(c=c1) == L.S4R_ERR_BAD_SHAPE                    # q_window 1: nothing to keep
+    assert step(Lval=2) == L.S4R_ERR_BAD_SHAPE                  # fewer keys than window rows
+    assert step(wsb=0) == L.S4R_ERR_WORKSPACE
+
+
 def test_ragged_decode_step_argument_errors():
     lib = L.load()
 

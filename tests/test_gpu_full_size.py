@@ -64,6 +64,38 @@ def test_full_size_decode_step(name):
     for b in range(wl.batch):
         assert err_s[b].max() <= tol_s[b], f"sequence {b}: score rel err {err_s[b].max():.3e} > {tol_s[b]:.3e}"
 
+    if wl.q_window > 1:
+        # the windowed step bench.py times for a multi-row query window: the
+        # older rows' softmax set up in the window state, then the step, checked
+        # against the same oracle step with the same bars; the timed launch (no
+        # outputs) gives bit-identical outputs (re-storing the newest row is
+        # idempotent)
+        state = s4r.alloc_window_state(c)
+        s4r.window_state_init(c, wl.L, qwin, g["coef_k"], state, ws)
+        idx_w = torch.empty_like(idx)
+        scores_w = torch.empty_like(scores)
+        out_w = s4r.decode_step_windowed(c, wl.L, g["q"], state, g["sink_k"], g["sink_v"], g["bases_k"],
+                                         g["bases_v"], g["coef_k"], g["coef_v"], ws, idx_out=idx_w,
+                                         scores_out=scores_w)
+        out_wb = s4r.decode_step_windowed(c, wl.L, g["q"], state, g["sink_k"], g["sink_v"], g["bases_k"],
+                                          g["bases_v"], g["coef_k"], g["coef_v"], ws)
+        torch.cuda.synchronize()
+        assert torch.equal(out_w, out_wb), "the timed windowed launch differs from the checked one"
+        got_w = scores_w.cpu().numpy().astype(np.float64)
+        err_sw = np.abs(got_w - a) / np.maximum(np.abs(a), 1e-30)
+        idx_wn = idx_w.cpu().numpy().astype(np.int64)
+        flips_w = check_selection(idx_wn, ref["idx"], a, wl.L, wl.window, wl.topk)
+        assert np.array_equal(idx_wn, decode.select(got_w, wl.L, wl.window, wl.topk))
+        o_ref_w, _, _ = decode.sparse_attention(st["q"], idx_wn, st["sink_k"], st["sink_v"], st["bases_k"],
+                                                st["bases_v"], st["coef_k"], st["coef_v"], wl.L, wl.n_kv_heads,
+                                                oc["rope_theta"])
+        err_w = rel_err_rows(out_w.cpu().numpy(), o_ref_w)
+        print(f"[full-size] {name} windowed: score err {err_sw.max():.2e}, tie flips {flips_w}, out err {err_w:.2e}",
+              flush=True)
+        assert err_w <= OUT_TOL[wl.dtype]
+        for b in range(wl.batch):
+            assert err_sw[b].max() <= tol_s[b], f"windowed, sequence {b}: score rel err {err_sw[b].max():.3e}"
+
 
 def test_sustained_32_layers():
     """The 32-layer sustained run at full size, as bench.py runs it: every step

@@ -375,6 +375,61 @@ def test_append_then_step():
     assert rel_err_rows(out.cpu().numpy(), o_ref) <= 2e-2
 
 
+@pytest.mark.parametrize("wq,window,nsteps,append", [(4, 4, 9, True), (32, 32, 37, False), (5, 16, 12, True)])
+def test_windowed_steps(wq, window, nsteps, append):
+    """Windowed decode (Section 3.2.2's query window kept as its rows'
+    softmax): s4r_window_state_init at the first step's length, then
+    s4r_decode_step_windowed at consecutive lengths (appending the new token
+    when `append`), each step against the oracle's step with the window's
+    older query rows given explicitly as coefficient rows; more steps than
+    the window has rows, so the state's ring of slots wraps."""
+    B, L0 = 2, 2400
+    cap = ((L0 + nsteps + 15) // 16) * 16
+    wl = W.CONFIGS["qwen3_4b_120k"].scaled(N=L0 + 4, batch=B, window=window, q_window=wq, topk=200)
+    st = W.latent_state(wl, seed=wq + nsteps, capacity=cap, L=(L0 if append else cap))
+    c = cfg_from_workload(wl, capacity=cap)
+    g = to_gpu_state(c, st)
+    ws = s4r.alloc_workspace(c)
+    dt = s4r.storage_dtype(c)
+    oc = oracle_cfg(c)
+    rng = np.random.default_rng(wq)
+    # the window's query rows, oldest first: the initial older rows, then each step's c^Q
+    rows = [st["qwin_prev"][:, :, i] for i in range(wq - 1)]
+    coef_k, coef_v = st["coef_k"], st["coef_v"]
+    state = s4r.alloc_window_state(c)
+    s4r.window_state_init(c, L0 + 1, g["qwin_prev"], g["coef_k"], state, ws)
+    for t in range(nsteps):
+        L = L0 + 1 + t
+        # queries near the workload's (its logits have the recipe's spread), each step its own
+        q = W.round_storage(st["q"] + 0.3 * np.abs(st["q"]).mean() * rng.standard_normal(st["q"].shape), wl.dtype)
+        kn = W.round_storage(rng.standard_normal((B, wl.Dp)), wl.dtype) if append else None
+        vn = W.round_storage(rng.standard_normal((B, wl.Dp)), wl.dtype) if append else None
+        m = s4r.num_selected(c, L)
+        idx = torch.empty((B, m), dtype=torch.int32, device="cuda")
+        scores = torch.empty((B, L), dtype=torch.float32, device="cuda")
+        out = s4r.decode_step_windowed(c, L, dev(q, dt), state, g["sink_k"], g["sink_v"], g["bases_k"],
+                                       g["bases_v"], g["coef_k"], g["coef_v"], ws,
+                                       k_new=None if kn is None else dev(kn, dt),
+                                       v_new=None if vn is None else dev(vn, dt), idx_out=idx, scores_out=scores)
+        torch.cuda.synchronize()
+        qwin = np.stack([W.round_storage(r, "fp32") for r in rows[t:t + wq - 1]], axis=2)   # [B, G, wq - 1, R]
+        ref = decode.decode_step(oc, L, q, st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"], coef_k,
+                                 coef_v, qwin_prev=qwin, k_new=kn, v_new=vn)
+        coef_k, coef_v = ref["coef_k"], ref["coef_v"]
+        rows.append(decode.project(decode.group_queries(q, wl.n_kv_heads), st["bases_k"]))
+        idx_np = idx.cpu().numpy().astype(np.int64)
+        flips = check_selection(idx_np, ref["idx"], ref["a_tilde"], L, window, wl.topk)
+        sc = scores.cpu().numpy().astype(np.float64)
+        assert np.array_equal(idx_np, decode.select(sc, L, window, wl.topk))
+        serr = np.abs(sc - ref["a_tilde"][:, :L]).max() / np.abs(ref["a_tilde"][:, :L]).max()
+        o_ref, _, _ = decode.sparse_attention(q, idx_np, st["sink_k"], st["sink_v"], st["bases_k"], st["bases_v"],
+                                              coef_k, coef_v, L, wl.n_kv_heads, oc["rope_theta"])
+        err = rel_err_rows(out.cpu().numpy(), o_ref)
+        print(f"[windowed] W_q {wq} step {t} L {L}: scores {serr:.2e}, out {err:.2e}, tie flips {flips}", flush=True)
+        assert serr <= 1e-5
+        assert err <= OUT_TOL[wl.dtype]
+
+
 def test_exact_window_kv():
     wl = W.CONFIGS["llama8b_32k"].scaled(N=3000 + 4, batch=2, topk=100)
     L, Wn = wl.L, wl.window
