@@ -26,10 +26,15 @@
 //      online softmax of (token t, head h) with one running maximum per head
 //      shared by the 16 token slots;
 //   5. V^ = C^V B^V_j^T (D[token][dim]) of two tiles, rounded once to bf16,
-//      forms the B operand of P V^, with P's hi / lo bf16 parts (staged
-//      through LDS) as A rows 4 h + part; the output rows of head h land in
-//      the lanes that own head h's softmax state, which rescale them when
-//      its maximum grows.
+//      forms the B operand of P V^, with P's hi / lo bf16 parts (moved
+//      between lanes with permutes) as A rows 4 h + part; the output rows of
+//      head h land in the lanes that own head h's softmax state, which
+//      rescale them when its maximum grows.
+// Steps 3-5 are software-pipelined over the tile pairs: after one barrier
+// per pair, a wave runs the softmax and P V^ of pair p (from the partial
+// logits every wave wrote, double-buffered by pair parity) and then K^, RoPE,
+// the partial logits and V^ of pair p + 1, so the two chains' instructions
+// are independent within one basic block (the rescale is branch-free).
 //
 // Precision: the logits' operands carry about 16 significant bits each (the
 // rotated query and K~ as hi / lo parts), since a logit error enters the
@@ -134,7 +139,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
   __shared__ __align__(16) uint16_t gkA[2][RBH][512], gvA[2][RBV][512];
   __shared__ __align__(16) uint16_t gkB[2][RBH][512], gvB[2][RBV][512];
   __shared__ int32_t sidx[kTileMax * 16];
-  __shared__ float xl[2][NW][NMH][4][16];                // partial logits [tile of pair][wave][mh][head][slot]
+  __shared__ float xl[2][2][NW][NMH][4][16];             // partial logits [pair & 1][tile of pair][wave][mh][head][slot]
 
   // ---- 1. index list, bases and query requested; then the first two pairs' gathers ---------
   int32_t xi[kTileMax * 16 / (NW * 64)];
@@ -239,23 +244,15 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
   }
   const float inv_sqrt_d = 1.0f / sqrtf((float)DH);
 
-  // ---- 3-5. one tile pair from buffer (gk, gv) ---------------------------------------------
-  auto do_pair = [&](const int p, auto buf) __attribute__((always_inline)) {
+  // ---- 3-5. software-pipelined over tile pairs: the softmax and P V^ of pair p
+  // run beside the reconstruction of pair p + 1, with one barrier per pair ------------------
+  // stage: K^, RoPE and the wave's partial logits of pair q (buffer BUF) -> xl[q & 1]; V^ -> dv
+  auto stage_pair = [&](const int q, auto buf, floatx4 (&dv)[2][2], int32_t (&tokv)[2])
+                        __attribute__((always_inline)) {
     constexpr int BUF = decltype(buf)::value;
-    // this pair's rows have landed: each wave waits for its own loads (those
-    // of the next pair, issued later, may stay in flight), then for the others
-    const bool next_issued = (p == 0) || (p + 1 < npair);
-    if (next_issued && ((2 * p + 2) % NW == w || (2 * p + 3) % NW == w))
-      wait_vmcnt<RBH + RBV>();                   // one tile's gathers
-    else
-      wait_vmcnt<0>();
-    lds_barrier();
-    floatx4 dv[2][2];                              // V^ of the pair: [tile][dim block]
-    float sl[2][NMH];
-    int32_t tokv[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      tokv[u] = tok_at((2 * p + u) * 16 + slot);
+      tokv[u] = tok_at((2 * q + u) * 16 + slot);
       // K^ for the wave's two dimension blocks: lane (token slot, kg) gets dims 4 kg + v
       floatx4 dk[2];
 #pragma unroll
@@ -285,7 +282,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
       for (int mh = 0; mh < NMH; ++mh) {
         floatx4 dl = mfma16x16x32(aq[mh], khi, floatx4{0.f, 0.f, 0.f, 0.f});
         dl = mfma16x16x32(aq[mh], klo, dl);
-        xl[u][w][mh][kg][slot] = dl[0] + dl[1];
+        xl[q & 1][u][w][mh][kg][slot] = dl[0] + dl[1];
       }
       // V^ of this tile: lane (dim, kg) gets tokens 4 kg + v
 #pragma unroll
@@ -299,26 +296,18 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
         }
       }
     }
-    lds_barrier();                                 // partial logits of every wave; buffer read
-    if (p + 2 < npair) {                           // refill the buffer with pair p + 2
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int t = 2 * p + 4 + u;
-        if (t % NW == w) {
-          if constexpr (BUF == 0)
-            S4R_GATHER_TILE(gkA, gvA, u, t);
-          else
-            S4R_GATHER_TILE(gkB, gvB, u, t);
-        }
-      }
-    }
+  };
+  // finish: online softmax of pair q from every wave's partial logits, then P V^
+  auto finish_pair = [&](const int q, const floatx4 (&dv)[2][2], const int32_t (&tokv)[2])
+                         __attribute__((always_inline)) {
+    float sl[2][NMH];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int mh = 0; mh < NMH; ++mh) {
         float s = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) s += xl[u][ww][mh][kg][slot];
+        for (int ww = 0; ww < NW; ++ww) s += xl[q & 1][u][ww][mh][kg][slot];
         const bool valid = tokv[u] >= 0 && 4 * mh + kg < G;
         sl[u][mh] = valid ? s * inv_sqrt_d : -INFINITY;
       }
@@ -326,14 +315,14 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
     uint32_t phi[NMH], plo[NMH];
 #pragma unroll
     for (int mh = 0; mh < NMH; ++mh) {
-      const float pmax = slot_max16(fmaxf(sl[0][mh], sl[1][mh]));
-      if (pmax > Mrun[mh]) {                       // uniform within the row of head kg
-        const float alpha = __expf(Mrun[mh] - pmax);   // 0 when the maximum was -inf
-        lrun[mh] *= alpha;
-        oacc[mh][0] *= alpha;
-        oacc[mh][1] *= alpha;
-        Mrun[mh] = pmax;
-      }
+      // rescale without a branch (the pair's finish and the next pair's staging
+      // stay one basic block, so their instructions can interleave)
+      const float mnew = fmaxf(Mrun[mh], slot_max16(fmaxf(sl[0][mh], sl[1][mh])));
+      const float alpha = (mnew == -INFINITY) ? 1.f : __expf(Mrun[mh] - mnew);   // 0 when the maximum was -inf
+      lrun[mh] *= alpha;
+      oacc[mh][0] *= alpha;
+      oacc[mh][1] *= alpha;
+      Mrun[mh] = mnew;
       float pr[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -375,10 +364,61 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
       for (int m = 0; m < 2; ++m) oacc[mh][m] = mfma16x16x32(ap, vb16[m], oacc[mh][m]);
     }
   };
-  for (int p = 0; p < npair; p += 2) {
-    do_pair(p, std::integral_constant<int, 0>());
-    if (p + 1 < npair) do_pair(p + 1, std::integral_constant<int, 1>());
+  // refill the buffer of pair q - 2 (free once every wave staged it) with pair q
+  auto refill = [&](const int q, auto buf) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(buf)::value;
+    if (q < npair) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int t = 2 * q + u;
+        if (t % NW == w) {
+          if constexpr (BUF == 0)
+            S4R_GATHER_TILE(gkA, gvA, u, t);
+          else
+            S4R_GATHER_TILE(gkB, gvB, u, t);
+        }
+      }
+    }
+  };
+  // iteration p: pair p + 1's rows have landed (the only gathers in flight),
+  // every wave has staged pair p (xl[p & 1] complete, buffer of pair p free)
+  auto iterate = [&](const int p, auto buf, floatx4 (&dv)[2][2], int32_t (&tokv)[2])
+                     __attribute__((always_inline)) {
+    constexpr int BUF = decltype(buf)::value;    // buffer of pair p
+    wait_vmcnt<0>();
+    lds_barrier();
+    refill(p + 2, buf);
+    floatx4 dvn[2][2];
+    int32_t tokn[2];
+    finish_pair(p, dv, tokv);
+    stage_pair(p + 1, std::integral_constant<int, 1 - BUF>(), dvn, tokn);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      tokv[u] = tokn[u];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) dv[u][m] = dvn[u][m];
+    }
+  };
+  // pair 0's rows (pair 1's gathers may stay in flight), then stage it
+  if ((2 % NW) == w || (3 % NW) == w)
+    wait_vmcnt<RBH + RBV>();                       // one tile's gathers
+  else
+    wait_vmcnt<0>();
+  lds_barrier();
+  floatx4 dvc[2][2];
+  int32_t tokc[2];
+  stage_pair(0, std::integral_constant<int, 0>(), dvc, tokc);
+  int p = 0;
+  for (; p + 2 < npair; p += 2) {
+    iterate(p, std::integral_constant<int, 0>(), dvc, tokc);
+    iterate(p + 1, std::integral_constant<int, 1>(), dvc, tokc);
   }
+  if (p + 1 < npair) {
+    iterate(p, std::integral_constant<int, 0>(), dvc, tokc);
+    ++p;
+  }
+  lds_barrier();                                   // xl of the last pair complete
+  finish_pair(p, dvc, tokc);
   wait_vmcnt<0>();                                 // no gather left in flight (a second pair that
                                                    // was never used when there is one pair only)
 

@@ -20,7 +20,7 @@ namespace s4r {
 // halve the values per lane, then DPP within 16-lane rows) and over the 4
 // waves through LDS, in a fixed order, so the results are deterministic.
 // ---------------------------------------------------------------------------
-constexpr int kPCols = 8;                     // latent columns per workgroup
+constexpr int kPCols = 8;                     // latent columns per query workgroup (4 or 8)
 constexpr int kQVec = 4;                      // query vectors per pass
 
 // 8 consecutive basis elements, kept in their storage format until used
@@ -44,15 +44,39 @@ struct Raw8f32 {
     return k == 0 ? h.x : k == 1 ? h.y : k == 2 ? h.z : h.w;
   }
 };
-template <typename T>
-struct Raw8;
+// 4 consecutive basis elements
+struct Raw4bf16 {
+  uint2 u;
+  __device__ __forceinline__ void load(const uint16_t* p) { u = *reinterpret_cast<const uint2*>(p); }
+  __device__ __forceinline__ float operator[](int c) const {
+    const uint32_t w = (c >> 1) == 0 ? u.x : u.y;
+    return (c & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+  }
+};
+struct Raw4f32 {
+  float4 a;
+  __device__ __forceinline__ void load(const float* p) { a = *reinterpret_cast<const float4*>(p); }
+  __device__ __forceinline__ float operator[](int c) const {
+    return c == 0 ? a.x : c == 1 ? a.y : c == 2 ? a.z : a.w;
+  }
+};
+template <typename T, int N>
+struct RawN;
 template <>
-struct Raw8<uint16_t> {
+struct RawN<uint16_t, 8> {
   using type = Raw8bf16;
 };
 template <>
-struct Raw8<float> {
+struct RawN<float, 8> {
   using type = Raw8f32;
+};
+template <>
+struct RawN<uint16_t, 4> {
+  using type = Raw4bf16;
+};
+template <>
+struct RawN<float, 4> {
+  using type = Raw4f32;
 };
 
 // fp64 move within 16-lane rows (DPP)
@@ -146,21 +170,22 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   const int c0 = cblk * kPCols;                   // first latent column of the block
   const int grp = c0 / rank;                      // its basis group
   // the window's older query rows (oldest first): unit t is latent columns
-  // c0 + 4 (t % 2) .. + 3 of older row j = t / 2, i.e. group j / (W_q - 1),
-  // window row j % (W_q - 1) (G (W_q - 1) <= 127 rows, so one unit per
-  // thread).  Requested first, written last.
+  // c0 + 4 (t % U) .. + 3 of older row j = t / U (U = kPCols / 4 units per
+  // row), i.e. group j / (W_q - 1), window row j % (W_q - 1) (G (W_q - 1)
+  // <= 127 rows, so one unit per thread).  Requested first, written last.
+  constexpr int U = kPCols / 4;
   const bool old_rows = qimg && qwin_prev && Wq > 1;
   const int n_old = old_rows ? G * (Wq - 1) : 0;
-  const int jo = min(t >> 1, max(n_old - 1, 0));
+  const int jo = min(t / U, max(n_old - 1, 0));
   const int go = n_old ? jo / (Wq - 1) : 0, wo = n_old ? jo - go * (Wq - 1) : 0;
-  const int oc = c0 + 4 * (t & 1);
+  const int oc = c0 + 4 * (t % U);
   float4 oldv = make_float4(0.f, 0.f, 0.f, 0.f);
   if (old_rows) oldv = *reinterpret_cast<const float4*>(qwin_prev + (((int64_t)b * G + go) * (Wq - 1) + wo) * R + oc);
 
   // basis rows t + 256 i of the block's columns (rows past the group's end:
   // a re-read of its last row, met by x = 0)
   const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank + (c0 - grp * rank);
-  typename Raw8<T>::type bw[NCH];
+  typename RawN<T, kPCols>::type bw[NCH];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) bw[i].load(bases + (int64_t)min(t + 256 * i, Dg - 1) * rank);
   // the group's query elements of those rows, for vectors v0 .. v0 + 3 (the
@@ -176,11 +201,14 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
       }
   };
   load_x(0);
-  // the step's two selection histograms start from zero (the relevance and
-  // classify kernels add to them later in the step)
-  if (cblk == 0) {
+  // the step's selection histograms start from zero (the relevance and
+  // classify kernels add to them later in the step): the sequence's R / 8
+  // workgroups clear a slice each
+  {
+    const int nblk = R / kPCols, per = (kHistStride / 4 + nblk - 1) / nblk;
     uint4* hz = reinterpret_cast<uint4*>(hist + (int64_t)b * kHistStride);
-    for (int i = t; i < kHistStride / 4; i += blockDim.x) hz[i] = make_uint4(0u, 0u, 0u, 0u);
+    const int i1 = min((cblk + 1) * per, kHistStride / 4);
+    for (int i = cblk * per + t; i < i1; i += blockDim.x) hz[i] = make_uint4(0u, 0u, 0u, 0u);
   }
 
   __shared__ double red[4][32];
@@ -201,8 +229,8 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
     }
     reduce_wave<kQVec * kPCols>(acc, red, wave, lane);
     __syncthreads();
-    if (t < kQVec * kPCols && v0 + (t >> 3) < G) {
-      const int g = v0 + (t >> 3), col = c0 + (t & 7);
+    if (t < kQVec * kPCols && v0 + t / kPCols < G) {
+      const int g = v0 + t / kPCols, col = c0 + t % kPCols;
       const double xq = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
       qcoef[((int64_t)b * G + g) * R + col] = (float)xq;
       if (qcoef_out) qcoef_out[((int64_t)b * G + g) * R + col] = (float)xq;
@@ -216,7 +244,7 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
     }
     __syncthreads();                              // red is reused by the next pass
   }
-  if (old_rows && (t >> 1) < n_old) {
+  if (old_rows && t / U < n_old) {
     uint2 pk[3];
     qimg_pack4(oldv, pk);
     uint16_t* p = qimg_at(qimg, b, ncb, nmb, R, go * Wq + wo, oc);
@@ -258,14 +286,14 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
   T* coef = which == 0 ? coef_k : coef_v;
   const T* bases = (which == 0 ? bases_k : bases_v) + (bases_shared ? 0 : (int64_t)b * Dp * rank) +
                    (int64_t)grp * Dg * rank + (c0 - grp * rank);
-  constexpr int NG = kRCols / kPCols;             // column groups of 8
-  typename Raw8<T>::type bw[NCH][NG];
+  constexpr int NG = kRCols / 8;                  // column groups of 8
+  typename RawN<T, 8>::type bw[NCH][NG];
   float x[NCH];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) {
     const int r = min(t + 256 * i, Dg - 1);
 #pragma unroll
-    for (int k = 0; k < NG; ++k) bw[i][k].load(bases + (int64_t)r * rank + k * kPCols);
+    for (int k = 0; k < NG; ++k) bw[i][k].load(bases + (int64_t)r * rank + k * 8);
     x[i] = load_elem(x_new, (int64_t)b * Dp + grp * Dg + r);
   }
   __shared__ double red[4][32];
@@ -278,7 +306,7 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
 #pragma unroll
     for (int k = 0; k < NG; ++k)
 #pragma unroll
-      for (int c = 0; c < kPCols; ++c) acc[k * kPCols + c] = fma(xv, (double)bw[i][k][c], acc[k * kPCols + c]);
+      for (int c = 0; c < 8; ++c) acc[k * 8 + c] = fma(xv, (double)bw[i][k][c], acc[k * 8 + c]);
   }
   reduce_wave<kRCols>(acc, red, wave, lane);
   __syncthreads();
@@ -303,10 +331,14 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
                             which ? Rv : R, bases_shared, cap, blockIdx.x, blockIdx.y, which);
 }
 
-// both projections of a step that appends a token, in one launch: blocks
-// [0, nq) are the query-coefficient workgroups (R / 8 x B, in that order),
-// the rest the new rows' (max(R, R_V) / 32 x B x 2).  They touch disjoint
-// memory, and one launch saves a dispatch and a first-read latency.
+// both projections of a step that appends a token, in one launch: per
+// sequence R / 8 query-coefficient workgroups and max(R, R_V) / 32 new-row
+// workgroups per side.  They touch disjoint memory, and one launch saves a
+// dispatch and a first-read latency.  Every workgroup of sequence b runs on
+// XCD b mod 8 (workgroup i is dispatched to XCD i mod 8): the query and key
+// workgroups read different columns of the same basis rows (16 and 64 bytes
+// of each bf16 row), so a row's cache lines come from HBM once into that
+// XCD's L2 instead of once per XCD.
 template <typename T, int NCH>
 __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, const T* __restrict__ bases_k,
                                                       const T* __restrict__ bases_v, const T* __restrict__ k_new,
@@ -318,15 +350,16 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
                                                       int rank_v, int Rv, int bases_shared, int64_t cap, int B,
                                                       int ncb, int nmb, Lens lens) {
   const int ncq = R / kPCols;
-  const int nq = ncq * B;
-  int id = blockIdx.x;
-  if (id < nq) {
+  const int ncr = max(R, Rv) / kRCols;             // row blocks per (sequence, side)
+  const int per_seq = ncq + 2 * ncr;
+  const int xcd = blockIdx.x & 7, k = blockIdx.x >> 3;
+  const int b = xcd + 8 * (k / per_seq), id = k % per_seq;
+  if (b >= B) return;
+  if (id < ncq) {
     project_query_body<T, NCH>(q, bases_k, qwin_prev, qimg, qcoef, nullptr, hist, hq, hkv, dh, G, Wq, nb, rank, R,
-                               bases_shared, ncb, nmb, id % ncq, id / ncq);
+                               bases_shared, ncb, nmb, id, b);
   } else {
-    id -= nq;
-    const int ncr = max(R, Rv) / kRCols;           // row blocks per (sequence, side)
-    const int cblk = id % ncr, b = (id / ncr) % B, which = id / (ncr * B);
+    const int cblk = (id - ncq) % ncr, which = (id - ncq) / ncr;
     if (cblk * kRCols >= (which ? Rv : R)) return;
     const int64_t row = lens.n ? (int64_t)lens.v[b] - 1 : append_row;
     project_rows_body<T, NCH>(bases_k, bases_v, k_new, v_new, coef_k, coef_v, row, hkv, dh, nb,
@@ -455,7 +488,8 @@ template <typename T, int NCH>
 static void launch_step_t(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
                           const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                           const float* qwin_prev, int64_t row, hipStream_t st) {
-  const dim3 grid((P.R / kPCols) * P.B + (std::max(P.R, P.Rv) / kRCols) * P.B * 2);
+  const int per_seq = P.R / kPCols + 2 * (std::max(P.R, P.Rv) / kRCols);
+  const dim3 grid(8 * ((P.B + 7) / 8) * per_seq);  // sequence b on XCD b mod 8
   hipLaunchKernelGGL((k_project_step<T, NCH>), grid, dim3(256), 0, st, (const T*)q, (const T*)bases_k,
                      (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v, qwin_prev, ws.qimg,
                      ws.qcoef, ws.hist, row, P.hq, P.hkv, P.dh, P.G, P.Wq, P.nb, P.rank, P.R, P.rank_v, P.Rv,
