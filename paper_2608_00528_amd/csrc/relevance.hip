@@ -32,17 +32,16 @@ constexpr int kRelThreads = 256;
 constexpr int kRelStatPer = 2;   // scoring-workgroup statistics per lane folded inside the relevance kernel
 constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk and its halo (h <= 32)
 
-// tokens per workgroup: 1024 (G <= 8) or 512, halved while the grid would give
-// fewer than two workgroups per CU (small batches).  Every workgroup flushes
-// its histogram with one global atomic per non-empty bin, so fewer, larger
-// chunks cost fewer atomics (Qwen2.5 shape, B = 8 at 128k: 2048 -> 1024
-// workgroups)
-#ifndef S4R_REL_MIN_WG
-#define S4R_REL_MIN_WG 512
-#endif
+// tokens per workgroup: 1024 (G <= 8) or 512, halved (down to 256) while the
+// grid would give fewer than four workgroups per CU.  Measured at 1024, 512
+// and 256 tokens: about 1024 workgroups is best at batch 4 (512-token chunks,
+// relevance 11.9 -> 10.5 us at 128k), batch 8 and batch 32 (1024-token
+// chunks; 512 costs 2.7 and 1 us there).  The histogram copies keep the
+// flush atomics of more workgroups from serialising.
+constexpr int kRelMinWg = 1024;
 int relevance_chunk(const Problem& P, int64_t L) {
   int c = P.G <= 8 ? 1024 : 512;
-  while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < S4R_REL_MIN_WG) c >>= 1;
+  while (c > 256 && (int64_t)P.B * ((L + c - 1) / c) < kRelMinWg) c >>= 1;
   return c;
 }
 
