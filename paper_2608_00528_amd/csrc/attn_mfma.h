@@ -11,8 +11,10 @@
 //   1. the split's index list goes to LDS; the tiles are gathered in pairs
 //      into two LDS buffers (even pairs in one, odd pairs in the other) with
 //      16-byte global->LDS loads (lane l of a wave load lands at byte 16 l of
-//      the destination, so one wave load writes one 16-token x 32-column block
-//      in MFMA operand layout).  Pairs 0 and 1 are requested up front; pair
+//      the destination, so one wave load writes one 16-token x 32-column block;
+//      lane l fetches quarter (l % 4) ^ ((l / 8) % 4) of token l / 4's row, an
+//      XOR swizzle that keeps the operand reads free of bank conflicts).
+//      Pairs 0 and 1 are requested up front; pair
 //      p + 2 as soon as every wave has read pair p, so the gathers overlap
 //      the arithmetic of pair p + 1;
 //   2. wave w owns the dimension blocks {w, w + NW} (16 dims each), so each
@@ -76,14 +78,14 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // one wave's gather of one 16-token tile into slot u of a pair buffer: its RBH
 // 1 KiB blocks of C^K and RBV of C^V as 16-byte global->LDS loads (lane l: token
-// l / 4, quarter l % 4 of the 32 columns; a token past the list reads row 0,
-// never used).  T is the tile's number within the workgroup.  The LDS
+// l / 4, quarter (l % 4) ^ ((l / 8) % 4) of the 32 columns, stored at byte 16 l;
+// a token past the list reads row 0, never used).  T is the tile's number within the workgroup.  The LDS
 // destinations are named directly (plain LDS pointers for the builtin).
 #define S4R_GATHER_TILE(GK, GV, U, T)                                                       \
   do {                                                                                       \
     const int32_t x_ = tok_at((T) * 16 + (lane >> 2));                                       \
     const uint32_t tok_ = x_ < 0 ? 0u : (uint32_t)x_;                                        \
-    const int64_t in_ = (tok_ & 15) * 32 + (lane & 3) * 8;                                   \
+    const int64_t in_ = (tok_ & 15) * 32 + (((lane & 3) ^ ((lane >> 3) & 3)) * 8);          \
     const int64_t offk_ = (int64_t)(tok_ >> 4) * 16 * R + in_;                               \
     const int64_t offv_ = (int64_t)(tok_ >> 4) * 16 * Rv + in_;                              \
     _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb) {                                     \
@@ -123,6 +125,11 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = lane & 15, kg = lane >> 4;
+  // where token slot's k-group kg sits in a gathered block: quarter
+  // kg ^ ((slot >> 1) & 3) of its 64-byte row (the gathers store it there), so
+  // the eight lanes of one 128-byte LDS read cycle hit eight distinct bank
+  // groups instead of two
+  const int kq = slot * 32 + (kg ^ ((slot >> 1) & 3)) * 8;   // element offset in a block
   const int Dp = hkv * DH, Dg = Dp / nb;
   const int bgrp = j / (hkv / nb);                 // basis group of head j
   const int kb0 = bgrp * rank / 32;                // its first latent block (keys)
@@ -261,7 +268,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
 #pragma unroll
         for (int kb = 0; kb < RBH; ++kb) {
           Op8 c;
-          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gkA[u][kb][slot * 32 + kg * 8] : &gkB[u][kb][slot * 32 + kg * 8]);
+          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gkA[u][kb][kq] : &gkB[u][kb][kq]);
           dk[m] = mfma16x16x32(bk[m][kb], c, dk[m]);
         }
       }
@@ -291,7 +298,7 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
 #pragma unroll
         for (int kb = 0; kb < RBV; ++kb) {
           Op8 c;
-          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gvA[u][kb][slot * 32 + kg * 8] : &gvB[u][kb][slot * 32 + kg * 8]);
+          c.u = *reinterpret_cast<const uint4*>(BUF == 0 ? &gvA[u][kb][kq] : &gvB[u][kb][kq]);
           dv[u][m] = mfma16x16x32(c, bv[m][kb], dv[u][m]);
         }
       }
