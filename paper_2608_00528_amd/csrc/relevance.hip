@@ -29,7 +29,16 @@ namespace s4r {
 // pools outputs t, t + 256, ... (consecutive lanes read consecutive words: no
 // bank conflicts) and sums the groups in fp64.
 constexpr int kRelThreads = 256;
-constexpr int kRelStatPer = 2;   // scoring-workgroup statistics per lane folded inside the relevance kernel
+// scoring-workgroup statistics per lane that the relevance kernel folds itself
+// (KSP, all requested together): 2 (up to 128 scoring workgroups), or 8 (up to
+// 512) with one query column per wave: the paper's batch-1 setting at 120k
+// has 469, whose separate fold launch cost 4.6 us, while eight per lane cost
+// the 128-workgroup shapes 0.5 us.  Beyond that k_fold_stats folds them first.
+constexpr int kRelStatPer = 2, kRelStatWide = 8;
+template <int NQ>
+constexpr int rel_stat_max() {
+  return 64 * (NQ == 1 ? kRelStatWide : kRelStatPer);
+}
 constexpr int kRelMaxTiles = 1024 / kTileTok + 8;   // tiles touched by a chunk and its halo (h <= 32)
 
 // tokens per workgroup: 1024 (G <= 8) or 512, halved (down to 256) while the
@@ -103,7 +112,7 @@ __device__ __forceinline__ void pool_aggregate(const float* __restrict__ vs, int
 // [B][wrows][G][cap], row slot L_r mod wrows for the row that was newest at
 // length L_r (it covers keys < L_r).  This kernel adds the newest row's
 // softmax to the older rows' for the window mean and stores it in its slot.
-template <int NQ, int TPT, bool WQ1, bool WIN>
+template <int NQ, int TPT, bool WQ1, bool WIN, int KSP>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
@@ -139,7 +148,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
   // ---- all global reads of this workgroup, issued before any is used ----------
   // statistics: wave w folds columns w, w + 4, ...; two batches of 64 lanes in flight
   // (or, with many scoring workgroups, the global statistics k_fold_stats formed)
-  double2 st[NQ][kRelStatPer];
+  double2 st[NQ][KSP];
   const double2* stats = reinterpret_cast<const double2*>(wg_stats) + (int64_t)b * GW * nwg;
   double2 cs = make_double2(0.0, 0.0);
   if (col_stats) {
@@ -149,7 +158,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     for (int q = 0; q < NQ; ++q) {
       const int c = min(wave + 4 * q, GW - 1);
 #pragma unroll
-      for (int k = 0; k < kRelStatPer; ++k) st[q][k] = stats[(int64_t)c * nwg + min(lane + 64 * k, nwg - 1)];
+      for (int k = 0; k < KSP; ++k) st[q][k] = stats[(int64_t)c * nwg + min(lane + 64 * k, nwg - 1)];
     }
   }
   // tile references: thread t loads tile tile_lo + t (all columns)
@@ -183,10 +192,10 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     if (!col_stats && c < GW) {                            // wave-uniform
       const double* srow = wg_stats + ((int64_t)b * GW + c) * nwg * 2;
       double M = -INFINITY, S = 0.0;
-      for (int base = 0; base < nwg; base += 64 * kRelStatPer) {
-        double2 s2[kRelStatPer];
+      for (int base = 0; base < nwg; base += 64 * KSP) {
+        double2 s2[KSP];
 #pragma unroll
-        for (int k = 0; k < kRelStatPer; ++k) {
+        for (int k = 0; k < KSP; ++k) {
           if (base == 0) {
             s2[k] = st[q][k];
           } else {                                         // more than 128 scoring workgroups
@@ -196,13 +205,13 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
         }
         double m = -INFINITY;
 #pragma unroll
-        for (int k = 0; k < kRelStatPer; ++k)
+        for (int k = 0; k < KSP; ++k)
           if (base + lane + 64 * k < nwg) m = fmax(m, s2[k].x);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) m = fmax(m, shfl_xor_d(m, o));
         double s = 0.0;
 #pragma unroll
-        for (int k = 0; k < kRelStatPer; ++k)
+        for (int k = 0; k < KSP; ++k)
           if (base + lane + 64 * k < nwg && s2[k].x != -INFINITY) s += s2[k].y * (double)exp_neg_accurate(s2[k].x - m);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) s += shfl_xor_d(s, o);
@@ -476,7 +485,7 @@ __global__ __launch_bounds__(256) void k_hist_scores(const float* __restrict__ s
 
 // Global (max, 1 / sum) of every query column's softmax over the length,
 // folded once from the scoring workgroups' (max, sum) pairs when there are
-// more than the relevance kernel folds itself (64 * kRelStatPer): grid (GW,
+// more than the relevance kernel folds itself (rel_stat_max): grid (GW,
 // B), thread t folds pairs t, t + 256, ... in order, then a fixed-order tree
 // across the threads (deterministic).
 __global__ __launch_bounds__(256) void k_fold_stats(const double* __restrict__ wg_stats, double* __restrict__ col_stats,
@@ -520,9 +529,13 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   constexpr int chunk = kRelThreads * TPT;
   const size_t lds = (size_t)P.G * (chunk + 2 * (P.kappa / 2)) * sizeof(float);
   dim3 grid((unsigned)((L + chunk - 1) / chunk), P.B);
-  auto kern = P.Wq == 1 ? k_relevance<NQ, TPT, true, false> : k_relevance<NQ, TPT, false, false>;
   const int nwg = score_workgroups(P, L);
-  const bool fold = nwg > 64 * kRelStatPer;
+  const bool fold = nwg > rel_stat_max<NQ>();
+  constexpr int KW = NQ == 1 ? kRelStatWide : kRelStatPer;   // (only one column per wave folds 512)
+  auto kern = nwg > 64 * kRelStatPer && !fold
+                  ? (P.Wq == 1 ? k_relevance<NQ, TPT, true, false, KW> : k_relevance<NQ, TPT, false, false, KW>)
+                  : (P.Wq == 1 ? k_relevance<NQ, TPT, true, false, kRelStatPer>
+                               : k_relevance<NQ, TPT, false, false, kRelStatPer>);
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
@@ -574,9 +587,12 @@ static void launch_rel_win_t(const Problem& P1, const Workspace& ws, int64_t L, 
   const size_t lds = (size_t)P1.G * (chunk + 2 * (P1.kappa / 2)) * sizeof(float);
   dim3 grid((unsigned)((L + chunk - 1) / chunk), P1.B);
   const int nwg = score_workgroups(P1, L);
-  const bool fold = nwg > 64 * kRelStatPer;
+  const bool fold = nwg > rel_stat_max<NQ>();
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P1.GW, P1.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P1.GW, nwg);
-  hipLaunchKernelGGL((k_relevance<NQ, TPT, true, true>), grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
+  constexpr int KW = NQ == 1 ? kRelStatWide : kRelStatPer;
+  auto kern = nwg > 64 * kRelStatPer && !fold ? k_relevance<NQ, TPT, true, true, KW>
+                                              : k_relevance<NQ, TPT, true, true, kRelStatPer>;
+  hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P1.cap, (int)L, n_hist, P1.G, 1,
                      P1.kappa, P1.pool_mode, P1.agg, (int)(P1.cap / kTileTok), nwg, P1.lens, fused_key_shift(P1, L),
                      state, wrows, hist_copies(grid.x));
