@@ -57,7 +57,8 @@ def log(*a):
 def algorithmic(wl, m, windowed=False):
     """Bytes the method must move per step and MFMA flops of the reconstruction
     (windowed: the older query rows' softmax read from the window state and
-    the newest row's written, instead of their coefficient rows)."""
+    the newest row's written, instead of their coefficient rows; above five
+    rows their fp64 running sum read and written and the leaving row read)."""
     B, L, R, Dp, es = wl.batch, wl.L, wl.R, wl.Dp, (2 if wl.dtype == "bf16" else 4)
     ck = B * L * R * es                       # C^K streamed once (latent scoring)
     gather = 2 * B * m * R * es               # selected rows of C^K and C^V
@@ -66,7 +67,9 @@ def algorithmic(wl, m, windowed=False):
     q = B * wl.n_q_heads * wl.head_dim * es
     out = B * wl.n_q_heads * wl.head_dim * 4
     qwin = B * wl.G * (wl.q_window - 1) * R * 4  # the window's earlier query coefficients (fp32)
-    if windowed:
+    if windowed and wl.q_window > 5:
+        qwin = B * wl.G * L * 24                   # running sum read and written (fp64), leaving row read, newest written
+    elif windowed:
         qwin = B * wl.G * wl.q_window * L * 4     # older rows' softmax read, the newest row's written
     rec_flops = 2 * 2 * B * m * R * Dp        # K^ and V^ of every selected token
     return {"step_bytes": ck + gather + bases + sinks + q + out + qwin, "stream_bytes": ck, "rec_flops": rec_flops}

@@ -233,9 +233,14 @@ s4r_status s4r_decode_step_noalloc(const s4r_config* cfg, int64_t L, const void*
  * computed, so a caller that keeps it on the device needs to score only the
  * newest query row at each step.  The window state holds, per sequence, the
  * softmax of the last W_q query rows over their keys:
- *   state [B, q_window, G, capacity] fp32 (s4r_window_state_size bytes,
- *   device, caller-owned, 16-byte aligned); the row that was the newest at
- *   length L_r (it covers keys 0 .. L_r - 1) sits in slot L_r mod q_window.
+ *   state [B, q_window, G, capacity] fp32 (device, caller-owned, 16-byte
+ *   aligned, s4r_window_state_size bytes in all); the row that was the newest
+ *   at length L_r (it covers keys 0 .. L_r - 1) sits in slot L_r mod q_window.
+ *   With q_window > 5 the older rows' sum per key follows, as fp64
+ *   [2, B, G, capacity] (two buffers chosen by the parity of L): each step
+ *   reads one, writes the other with the newest row added and the row leaving
+ *   the window subtracted, so a step reads 20 bytes per key and group instead
+ *   of 4 per older row.  The state's contents are the library's.
  *
  * s4r_window_state_init fills the state for the q_window - 1 older rows of
  * the window of a step at length L, from their coefficient rows qwin_prev

@@ -197,15 +197,17 @@ def decode_step(cfg, length, q, sink_k, sink_v, bases_k, bases_v, coef_k, coef_v
 
 
 def window_state_size(cfg):
-    """Bytes of the window state [B, q_window, G, capacity] fp32."""
+    """Bytes of the window state: [B, q_window, G, capacity] fp32 softmax rows,
+    and for longer windows the older rows' running sum [2, B, G, capacity]
+    fp64 after them."""
     n = ctypes.c_size_t()
     L.check(L.load().s4r_window_state_size(_cfgp(cfg), ctypes.byref(n)))
     return n.value
 
 
 def alloc_window_state(cfg, device="cuda"):
-    G = cfg.n_q_heads // cfg.n_kv_heads
-    return torch.zeros((cfg.batch, cfg.q_window, G, cfg.capacity), dtype=torch.float32, device=device)
+    """A zeroed window state of window_state_size(cfg) bytes (fp32 elements)."""
+    return torch.zeros((window_state_size(cfg) // 4,), dtype=torch.float32, device=device)
 
 
 def window_state_init(cfg, length, qwin_prev, coef_k, state, ws):

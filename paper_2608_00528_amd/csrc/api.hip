@@ -659,7 +659,7 @@ s4r_status s4r_window_state_size(const s4r_config* cfg, size_t* bytes) {
   if (st) return st;
   if (!bytes) return fail(S4R_ERR_NULL_ARG, "bytes is NULL");
   if (P.Wq < 2) return fail(S4R_ERR_BAD_SHAPE, "the window state needs q_window >= 2 (got %d)", P.Wq);
-  *bytes = (size_t)P.B * P.Wq * P.G * P.cap * sizeof(float);
+  *bytes = window_state_bytes(P);
   return ok();
 }
 

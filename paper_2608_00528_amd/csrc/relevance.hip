@@ -112,12 +112,17 @@ __device__ __forceinline__ void pool_aggregate(const float* __restrict__ vs, int
 // [B][wrows][G][cap], row slot L_r mod wrows for the row that was newest at
 // length L_r (it covers keys < L_r).  This kernel adds the newest row's
 // softmax to the older rows' for the window mean and stores it in its slot.
+// With a running sum (rsum, longer windows) the older rows' sum per position
+// is kept in fp64 as well, in two buffers [2][B][G][cap] by the parity of L:
+// the step reads buffer L & 1 and writes buffer (L + 1) & 1 = that sum plus
+// the newest row minus the row leaving the window (the one newest at
+// L - wrows + 1, masked at its key limit), for the positions it owns.
 template <int NQ, int TPT, bool WQ1, bool WIN, int KSP>
 __global__ __launch_bounds__(kRelThreads) void k_relevance(
     const float* __restrict__ e, const float* __restrict__ tref, const double* __restrict__ wg_stats,
     const double* __restrict__ col_stats, float* __restrict__ atilde, uint32_t* __restrict__ hist, float* __restrict__ scores_out,
     int64_t cap, int L, int n_hist, int G, int Wq, int kappa, int pool_mode, int agg, int ntiles_cap, int nwg,
-    Lens lens, int key_shift, float* __restrict__ state, int wrows, int hist_nc) {
+    Lens lens, int key_shift, float* __restrict__ state, int wrows, double* __restrict__ rsum, int hist_nc) {
   constexpr int GWP = 4 * NQ;
   constexpr int CHUNK = kRelThreads * TPT;
   constexpr int SPAN_MAX = CHUNK + 64;
@@ -262,15 +267,37 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
       }
       if constexpr (WIN) {
         // the newest row's softmax: into its slot (own chunk) and into LDS;
-        // the older rows are added below
+        // the older rows are added from the running sum, else below
         float* sb = state + (int64_t)b * wrows * G * cap;
         const int slot_new = L % wrows;
+        const bool own = in && x >= t0 && x < t0 + CHUNK;
+        if (rsum) {
+          const double* scur = rsum + ((int64_t)(L & 1) * gridDim.y + b) * G * cap;
+          double* snext = rsum + ((int64_t)((L + 1) & 1) * gridDim.y + b) * G * cap;
+          const int Lo = L - wrows + 1;                        // the leaving row was newest at Lo
+          const float* sold = sb + (int64_t)((Lo % wrows + wrows) % wrows) * G * cap;
+          const int xc = min(max(x, 0), (int)cap - 1);
 #pragma unroll
-        for (int c = 0; c < GWP; ++c) {
-          if (c < G) {
-            const float pn = in ? ex[c] * fr[c] : 0.f;
-            if (in && x >= t0 && x < t0 + CHUNK) sb[((int64_t)slot_new * G + c) * cap + x] = pn;
-            vs[c * span + i] = pn;
+          for (int c = 0; c < GWP; ++c) {
+            if (c < G) {
+              const float pn = in ? ex[c] * fr[c] : 0.f;
+              const double so = scur[(int64_t)c * cap + xc];
+              const float po = sold[(int64_t)c * cap + xc];
+              if (own) {
+                sb[((int64_t)slot_new * G + c) * cap + x] = pn;
+                snext[(int64_t)c * cap + x] = (so + (double)pn) - (x < Lo ? (double)po : 0.0);
+              }
+              vs[c * span + i] = in ? (float)((so + (double)pn) * (double)inv_wq) : pad;
+            }
+          }
+        } else {
+#pragma unroll
+          for (int c = 0; c < GWP; ++c) {
+            if (c < G) {
+              const float pn = in ? ex[c] * fr[c] : 0.f;
+              if (own) sb[((int64_t)slot_new * G + c) * cap + x] = pn;
+              vs[c * span + i] = pn;
+            }
           }
         }
       } else if constexpr (WQ1) {
@@ -289,7 +316,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
     }
   }
   __syncthreads();
-  if constexpr (WIN) {
+  if (WIN && !rsum) {
     // ---- older rows of the window: row of age a = 1 .. wrows - 1 covers keys
     // < L - a, in slot (L - a) mod wrows.  Unit u = four consecutive positions
     // 4 (u0 + u) .. + 3 (16-byte loads, unconditional at clamped positions,
@@ -330,7 +357,7 @@ __global__ __launch_bounds__(kRelThreads) void k_relevance(
         }
       }
     }
-    __syncthreads();
+    __syncthreads();                                       // (wave-uniform: rsum is a kernel argument)
   }
   // ---- pooling (kappa, stride 1, same length) and aggregation over G -------------------
   float af[TPT];
@@ -539,7 +566,7 @@ static void launch_rel_t(const Problem& P, const Workspace& ws, int64_t L, float
   if (fold) hipLaunchKernelGGL(k_fold_stats, dim3(P.GW, P.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P.GW, nwg);
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P.cap, (int)L, n_hist, P.G, P.Wq, P.kappa, P.pool_mode, P.agg,
-                     (int)(P.cap / kTileTok), nwg, P.lens, fused_key_shift(P, L), nullptr, 1,
+                     (int)(P.cap / kTileTok), nwg, P.lens, fused_key_shift(P, L), nullptr, 1, nullptr,
                      hist_copies(grid.x));
 }
 
@@ -595,7 +622,7 @@ static void launch_rel_win_t(const Problem& P1, const Workspace& ws, int64_t L, 
   hipLaunchKernelGGL(kern, grid, dim3(kRelThreads), lds, st, ws.e, ws.run_m, ws.wg_stats,
                      fold ? ws.col_stats : nullptr, ws.atilde, ws.hist, scores_out, P1.cap, (int)L, n_hist, P1.G, 1,
                      P1.kappa, P1.pool_mode, P1.agg, (int)(P1.cap / kTileTok), nwg, P1.lens, fused_key_shift(P1, L),
-                     state, wrows, hist_copies(grid.x));
+                     state, wrows, window_rsum(P1, state, wrows), hist_copies(grid.x));
 }
 
 int relevance_hist_copies(const Problem& P, int64_t L, int wrows) {
@@ -627,16 +654,20 @@ hipError_t launch_relevance_windowed(const Problem& P1, const Workspace& ws, int
 // window state of the W_q - 1 older rows from a stream over them (P0: those
 // rows as the query window, scored to length L - 1): row r < wrows - 1 covers
 // keys < L_r = L - (wrows - 1 - r) and goes to slot L_r mod wrows.  grid
-// (ceil(L / 256), B); the softmax probability of (row, group, key) is its exp
-// value times exp(ref - M) / S of its tile and column (fp64 argument, as in
-// the relevance kernel).
+// (ceil(cap / 256), B); the softmax probability of (row, group, key) is its
+// exp value times exp(ref - M) / S of its tile and column (fp64 argument, as
+// in the relevance kernel).  With a running sum, buffer L & 1 gets the older
+// rows' fp64 sum (oldest row first; 0 where no row covers the key) and buffer
+// (L + 1) & 1 zeros, over the whole capacity.
 __global__ __launch_bounds__(256) void k_window_store(const float* __restrict__ e, const float* __restrict__ tref,
                                                       const double* __restrict__ col_stats, float* __restrict__ state,
-                                                      int64_t cap, int L, int G, int wrows, int gwp, int ntiles_cap) {
+                                                      double* __restrict__ rsum, int64_t cap, int L, int G, int wrows,
+                                                      int gwp, int ntiles_cap) {
   const int b = blockIdx.y, x = blockIdx.x * 256 + threadIdx.x;
   const int w0 = wrows - 1;                       // rows in the stream, column c = g * w0 + r
-  if (x >= L) return;
-  for (int g = 0; g < G; ++g)
+  if (x >= cap) return;
+  for (int g = 0; g < G; ++g) {
+    double sum = 0.0;
     for (int r = 0; r < w0; ++r) {
       const int Lr = L - (w0 - r);
       if (x >= Lr) continue;
@@ -644,16 +675,24 @@ __global__ __launch_bounds__(256) void k_window_store(const float* __restrict__ 
       const double2 cs = reinterpret_cast<const double2*>(col_stats)[(int64_t)b * G * w0 + c];
       const float ref = tref[((int64_t)b * ntiles_cap + x / kTileTok) * gwp + c];
       const float fac = (ref != -INFINITY) ? (float)((double)exp_neg_accurate((double)ref - cs.x) * cs.y) : 0.f;
-      state[(((int64_t)b * wrows + Lr % wrows) * G + g) * cap + x] = e[((int64_t)b * cap + x) * gwp + c] * fac;
+      const float p = e[((int64_t)b * cap + x) * gwp + c] * fac;
+      state[(((int64_t)b * wrows + Lr % wrows) * G + g) * cap + x] = p;
+      sum += (double)p;
     }
+    if (rsum) {
+      rsum[(((int64_t)(L & 1) * gridDim.y + b) * G + g) * cap + x] = sum;
+      rsum[(((int64_t)((L + 1) & 1) * gridDim.y + b) * G + g) * cap + x] = 0.0;
+    }
+  }
 }
 
 hipError_t launch_window_store(const Problem& P0, const Workspace& ws, int64_t L, float* state, int wrows,
                                hipStream_t st) {
   const int nwg = score_workgroups(P0, L - 1);
   hipLaunchKernelGGL(k_fold_stats, dim3(P0.GW, P0.B), dim3(256), 0, st, ws.wg_stats, ws.col_stats, P0.GW, nwg);
-  hipLaunchKernelGGL(k_window_store, dim3((unsigned)((L + 255) / 256), P0.B), dim3(256), 0, st, ws.e, ws.run_m,
-                     ws.col_stats, state, P0.cap, (int)L, P0.G, wrows, gw_padded(P0), (int)(P0.cap / kTileTok));
+  hipLaunchKernelGGL(k_window_store, dim3((unsigned)((P0.cap + 255) / 256), P0.B), dim3(256), 0, st, ws.e,
+                     ws.run_m, ws.col_stats, state, window_rsum(P0, state, wrows), P0.cap, (int)L, P0.G, wrows,
+                     gw_padded(P0), (int)(P0.cap / kTileTok));
   return hipGetLastError();
 }
 

@@ -129,6 +129,18 @@ hipError_t launch_project_rows(const Problem& P, const void* bases_k, const void
 hipError_t launch_query_image_rows(const Problem& P0, const Workspace& ws, const float* rows, hipStream_t st);
 // windowed relevance (P1: the newest row's G columns, Wq = 1): the older rows'
 // softmax from the window state [B][wrows][G][cap], the newest stored in its slot
+// window state: [B][W_q][G][cap] fp32 softmax rows; with more than
+// kWinDirectRows rows also the older rows' running sum [2][B][G][cap] fp64
+// (per step 20 bytes per position and group instead of 4 per older row)
+constexpr int kWinDirectRows = 5;
+inline size_t window_state_bytes(const Problem& P) {
+  size_t n = (size_t)P.B * P.Wq * P.G * P.cap * sizeof(float);
+  if (P.Wq > kWinDirectRows) n += (size_t)2 * P.B * P.G * P.cap * sizeof(double);
+  return n;
+}
+inline double* window_rsum(const Problem& P, float* state, int wrows) {
+  return wrows > kWinDirectRows ? reinterpret_cast<double*>(state + (size_t)P.B * wrows * P.G * P.cap) : nullptr;
+}
 hipError_t launch_relevance_windowed(const Problem& P1, const Workspace& ws, int64_t L, float* scores_out,
                                      float* state, int wrows, hipStream_t st);
 // window state of the older rows from a stream over them (P0: wrows - 1 rows, length L - 1)

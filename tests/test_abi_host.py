@@ -163,7 +163,8 @@ def test_decode_step_argument_errors():
 
 
 def test_window_state_entry_points():
-    """Window state: its size is B * q_window * G * capacity floats; every
+    """Window state: its size is B * q_window * G * capacity floats (plus the
+    running sum's 2 * B * G * capacity doubles above five rows); every
     entry point refuses q_window = 1 and missing or misaligned buffers before
     launching anything, and the windowed step never takes qwin_prev."""
     lib = L.load()
@@ -173,6 +174,9 @@ def test_window_state_entry_points():
     assert lib.s4r_window_state_size(ctypes.byref(c1), ctypes.byref(n)) == L.S4R_ERR_BAD_SHAPE
     assert lib.s4r_window_state_size(ctypes.byref(cw), None) == L.S4R_ERR_NULL_ARG
     assert s4r.window_state_size(cw) == 2 * 4 * 4 * 1024 * 4
+    # longer windows add the older rows' fp64 running sum in two buffers
+    assert s4r.window_state_size(cfg(q_window=5)) == 2 * 5 * 4 * 1024 * 4
+    assert s4r.window_state_size(cfg(q_window=6)) == 2 * 6 * 4 * 1024 * 4 + 2 * 2 * 4 * 1024 * 8
     assert lib.s4r_window_state_init(ctypes.byref(c1), 100, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_BAD_SHAPE
     assert lib.s4r_window_state_init(ctypes.byref(cw), 100, None, FAKE, FAKE, FAKE, 1 << 40, None) == L.S4R_ERR_NULL_ARG
     assert lib.s4r_window_state_init(ctypes.byref(cw), 100, FAKE, FAKE, None, FAKE, 1 << 40, None) == L.S4R_ERR_NULL_ARG

@@ -375,14 +375,16 @@ def test_append_then_step():
     assert rel_err_rows(out.cpu().numpy(), o_ref) <= 2e-2
 
 
-@pytest.mark.parametrize("wq,window,nsteps,append", [(4, 4, 9, True), (32, 32, 37, False), (5, 16, 12, True)])
+@pytest.mark.parametrize("wq,window,nsteps,append", [(4, 4, 9, True), (32, 32, 37, False), (5, 16, 12, True),
+                                                     (8, 8, 19, True)])
 def test_windowed_steps(wq, window, nsteps, append):
     """Windowed decode (Section 3.2.2's query window kept as its rows'
     softmax): s4r_window_state_init at the first step's length, then
     s4r_decode_step_windowed at consecutive lengths (appending the new token
     when `append`), each step against the oracle's step with the window's
     older query rows given explicitly as coefficient rows; more steps than
-    the window has rows, so the state's ring of slots wraps."""
+    the window has rows, so the state's ring of slots wraps (and, above five
+    rows, the older rows' running sum loses rows as they leave)."""
     B, L0 = 2, 2400
     cap = ((L0 + nsteps + 15) // 16) * 16
     wl = W.CONFIGS["qwen3_4b_120k"].scaled(N=L0 + 4, batch=B, window=window, q_window=wq, topk=200)
