@@ -93,8 +93,15 @@ __global__ __launch_bounds__(256) void k_col_partial(const uint16_t* __restrict_
 
 // ---- Gram matrix --------------------------------------------------------------------------
 // M[mat] (column-major Dg x Dg) = sum_s xh_s xh_s^T (- n_s mu mu^T when centred).
-// Grid (T (T + 1) / 2 upper tiles, 2 nb, B) with T = Dg / 64; 256 threads, a
-// thread owns a 4 x 4 block of the 64 x 64 tile.
+// Grid (T (T + 1) / 2 upper tiles, 2 nb, B) with T = Dg / 64; 256 threads.
+// The samples of a round (32 of them, both 64-column ranges, weighted by the
+// row norms' inverses) are staged in LDS as fp64, the next round's requested
+// while the current one is multiplied; wave w accumulates the
+// 32 x 32 quadrant (w / 2, w % 2) of the tile on the fp64 matrix cores
+// (16x16x4: lane l holds A[row l % 16][sample l / 16] and B[sample l / 16]
+// [column l % 16], and receives D rows l / 16 + 4 i of column l % 16, as
+// probed on gfx950), four 16 x 16 blocks per wave, four samples per step.
+typedef double double4_t __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(256) void k_gram(const uint16_t* __restrict__ s_k, const uint16_t* __restrict__ s_v,
                                               const int32_t* __restrict__ idx, const double* __restrict__ inv,
                                               const double* __restrict__ part, double* __restrict__ M,
@@ -110,69 +117,88 @@ __global__ __launch_bounds__(256) void k_gram(const uint16_t* __restrict__ s_k, 
   const int tj = ti + rem;
   const int side = blockIdx.y & 1, g = blockIdx.y >> 1, b = blockIdx.z;
   const int mat = (b * 2 + side) * nb + g;
-  const int t = threadIdx.x, ty = t >> 4, tx = t & 15;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int lr = lane & 15, lk = lane >> 4;       // MFMA operand row / column, sample within the step
+  const int qr = (wave >> 1) * 32, qc = (wave & 1) * 32;   // the wave's quadrant
   const uint16_t* base = (side ? s_v : s_k) + (int64_t)b * n_rows * Dp + (int64_t)g * Dg;
   const double* inv_m = inv + (int64_t)mat * n_s;
   __shared__ double xa[kGramChunk][kGramTile + 1], xb[kGramChunk][kGramTile + 1];
-  double acc[4][4];
+  double4_t acc[2][2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    for (int j = 0; j < 2; ++j) acc[i][j] = double4_t{0.0, 0.0, 0.0, 0.0};
   const int i0 = ti * kGramTile, j0 = tj * kGramTile;
+  // the next round's sample values are requested before this round's MFMAs
+  // run and written to LDS after them (8 per thread and column range)
+  constexpr int kPer = kGramChunk * kGramTile / 256;
+  uint16_t ra[kPer], rb[kPer];
+  double rw[kPer];
+  auto fetch = [&](int s0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = t + k * 256, r = e / kGramTile, col = e % kGramTile;
+      const int s = min(s0 + r, n_s - 1);
+      const uint16_t* row = base + (int64_t)idx[s] * Dp;
+      ra[k] = row[i0 + col];
+      rb[k] = row[j0 + col];
+      rw[k] = (s0 + r < n_s) ? inv_m[s] : 0.0;
+    }
+  };
+  auto stage = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = t + k * 256, r = e / kGramTile, col = e % kGramTile;
+      xa[r][col] = (double)bf16_bits_to_f32(ra[k]) * rw[k];
+      xb[r][col] = (double)bf16_bits_to_f32(rb[k]) * rw[k];
+    }
+  };
+  fetch(0);
+  stage();
+  __syncthreads();
   for (int s0 = 0; s0 < n_s; s0 += kGramChunk) {
-    // stage 32 samples x 64 columns of both column ranges (8 values per thread each)
+    if (s0 + kGramChunk < n_s) fetch(s0 + kGramChunk);
 #pragma unroll
-    for (int k = 0; k < kGramChunk * kGramTile / 256; ++k) {
-      const int e = t + k * 256;
-      const int r = e / kGramTile, col = e % kGramTile;
-      const int s = s0 + r;
-      double va = 0.0, vb = 0.0;
-      if (s < n_s) {
-        const uint16_t* row = base + (int64_t)idx[s] * Dp;
-        const double w = inv_m[s];
-        va = (double)bf16_bits_to_f32(row[i0 + col]) * w;
-        vb = (double)bf16_bits_to_f32(row[j0 + col]) * w;
-      }
-      xa[r][col] = va;
-      xb[r][col] = vb;
+    for (int k4 = 0; k4 < kGramChunk; k4 += 4) {
+      double a[2], bb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = xa[k4 + lk][qr + 16 * i + lr];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bb[j] = xb[k4 + lk][qc + 16 * j + lr];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], bb[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
-#pragma unroll 4
-    for (int r = 0; r < kGramChunk; ++r) {
-      double a[4], bb[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = xa[r][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bb[j] = xb[r][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], bb[j], acc[i][j]);
+    if (s0 + kGramChunk < n_s) {
+      stage();
+      __syncthreads();
     }
-    __syncthreads();
   }
   double* Mm = M + (int64_t)mat * Dg * Dg;
   const double* pm = part + (int64_t)mat * kMeanChunks * Dg;
   const double inv_n = 1.0 / (double)n_s;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int gi = i0 + ty * 4 + i;
-    double mi = 0.0;
+  for (int j = 0; j < 2; ++j) {
+    const int gj = j0 + qc + 16 * j + lr;
+    double mj = 0.0;
     if (center)
-      for (int c = 0; c < kMeanChunks; ++c) mi += pm[(int64_t)c * Dg + gi];
+      for (int c = 0; c < kMeanChunks; ++c) mj += pm[(int64_t)c * Dg + gj];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gj = j0 + tx * 4 + j;
-      double v = acc[i][j];
-      if (center) {
-        double mj = 0.0;
-        for (int c = 0; c < kMeanChunks; ++c) mj += pm[(int64_t)c * Dg + gj];
-        v -= (mi * inv_n) * (mj * inv_n) * (double)n_s;
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int gi = i0 + qr + 16 * i + lk + 4 * e;
+        double v = acc[i][j][e];
+        if (center) {
+          double mi = 0.0;
+          for (int c = 0; c < kMeanChunks; ++c) mi += pm[(int64_t)c * Dg + gi];
+          v -= (mi * inv_n) * (mj * inv_n) * (double)n_s;
+        }
+        Mm[gi + (int64_t)gj * Dg] = v;
+        Mm[gj + (int64_t)gi * Dg] = v;
       }
-      Mm[gi + (int64_t)gj * Dg] = v;
-      Mm[gj + (int64_t)gi * Dg] = v;
-    }
   }
 }
 
