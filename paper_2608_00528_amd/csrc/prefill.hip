@@ -3,8 +3,8 @@
 // into the tiled coefficient cache (bf16 storage).
 //
 // k_transpose_bases first writes every basis group transposed, [column][dim],
-// into the workspace.  k_prefill_project: grid (256-row blocks, basis group x
-// {key, value}, sequence), 4 waves; wave w owns 4 tiles of 16 rows.  The
+// into the workspace.  k_prefill_project: grid (128-row blocks, basis group x
+// {key, value}, sequence), 4 waves; wave w owns 2 tiles of 16 rows.  The
 // product runs on bf16 MFMA 16x16x32 with fp32 accumulation in the MFMA
 // accumulators: A = the prompt rows as loaded (lane: row l % 16, dims
 // 8 (l / 16) .. + 7 of a 32-dim block), B = the transposed basis slice of the
@@ -19,7 +19,9 @@
 namespace s4r {
 
 constexpr int kPfWaves = 4;
-constexpr int kPfTiles = 4;                       // 16-row tiles per wave
+constexpr int kPfTiles = 2;                       // 16-row tiles per wave (two waves per SIMD:
+                                                  // 737 us at the headline shape, 931 with four
+                                                  // tiles at one wave per SIMD, 864 with one tile)
 constexpr int kPfRows = kPfWaves * kPfTiles * 16;  // rows per workgroup
 
 // s_waitcnt vmcnt(N) alone (gfx9 encoding: expcnt and lgkmcnt not waited)
