@@ -187,7 +187,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
 // ---------------------------------------------------------------------------
 // finish: one workgroup per 2048 positions
 // ---------------------------------------------------------------------------
-constexpr int kFinCntPer = kMaxSelGroups / kSelThreads;   // per-chunk counters per thread (16)
+// per-chunk counters per thread: NCP (a template parameter, the smallest of
+// 1, 2, 4, 16 with 256 NCP >= the sequence's chunks), so a 128k sequence's 64
+// chunks cost one load per thread and counter instead of 16
+constexpr int kFinCntMax = kMaxSelGroups / kSelThreads;    // 16
 constexpr int kFinBatch = 8;                              // candidates per thread per batch
 
 // candidate i of the sequence, the chunks' lists concatenated in chunk order
@@ -201,6 +204,7 @@ __device__ __forceinline__ int cand_chunk_of(const uint32_t* cpre, int nch, int 
   return g;
 }
 
+template <int NCP>
 __global__ __launch_bounds__(kSelThreads) void k_select_finish(
     const uint32_t* __restrict__ hist_all, const uint64_t* __restrict__ cand_all,
     const uint32_t* __restrict__ bitmap_all, const uint32_t* __restrict__ cand_count,
@@ -237,10 +241,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
 
   // ---- every load the workgroup needs first, issued together ---------------------------
   const uint32_t b1 = sel_info[b * 4 + 0], above1 = sel_info[b * 4 + 1];
-  uint32_t cc[kFinCntPer], ac[kFinCntPer];
+  uint32_t cc[NCP], ac[NCP];
 #pragma unroll
-  for (int i = 0; i < kFinCntPer; ++i) {
-    const int g = min(t * kFinCntPer + i, nch - 1);
+  for (int i = 0; i < NCP; ++i) {
+    const int g = min(t * NCP + i, nch - 1);
     cc[i] = cand_count[(int64_t)b * cnt_stride + g];
     ac[i] = above_count[(int64_t)b * cnt_stride + g];
   }
@@ -256,14 +260,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   // prefix of the candidate counts (chunk order), chosen counters cleared
   uint32_t csum = 0;
 #pragma unroll
-  for (int i = 0; i < kFinCntPer; ++i) csum += (t * kFinCntPer + i < nch) ? cc[i] : 0u;
+  for (int i = 0; i < NCP; ++i) csum += (t * NCP + i < nch) ? cc[i] : 0u;
   uint32_t cex;
   const uint32_t n_cand = block_exclusive_scan(csum, scratch, cex);
   {
     uint32_t run = cex;
 #pragma unroll
-    for (int i = 0; i < kFinCntPer; ++i) {
-      const int g = t * kFinCntPer + i;
+    for (int i = 0; i < NCP; ++i) {
+      const int g = t * NCP + i;
       if (g < nch) cpre[g] = run;
       run += (g < nch) ? cc[i] : 0u;
       if (g < nch) chosen[g] = 0u;
@@ -386,8 +390,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_finish(
   // ---- output offset of this chunk: positions selected in earlier chunks ------------------
   uint32_t before = 0;
 #pragma unroll
-  for (int i = 0; i < kFinCntPer; ++i) {
-    const int g = t * kFinCntPer + i;
+  for (int i = 0; i < NCP; ++i) {
+    const int g = t * NCP + i;
     if (g < c) before += ac[i] + chosen[g];
   }
   uint32_t bex;
@@ -433,9 +437,12 @@ hipError_t launch_select_keyed(const Problem& P, const Workspace& ws, int64_t L,
                        ws.cand, ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P),
                        sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens, key_shift, hist_nc);
   }
-  hipLaunchKernelGGL(k_select_finish, dim3(std::max(nch, 1), P.B), dim3(kSelThreads), 0, st, ws.hist, ws.cand,
-                     ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, idx, idx_copy, (int64_t)m,
-                     cand_stride(P), sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens);
+  auto fin = nch <= kSelThreads ? k_select_finish<1>
+             : nch <= 2 * kSelThreads ? k_select_finish<2>
+             : nch <= 4 * kSelThreads ? k_select_finish<4> : k_select_finish<kFinCntMax>;
+  hipLaunchKernelGGL(fin, dim3(std::max(nch, 1), P.B), dim3(kSelThreads), 0, st, ws.hist, ws.cand, ws.bitmap,
+                     ws.cand_count, ws.above_count, ws.sel_info, idx, idx_copy, (int64_t)m, cand_stride(P),
+                     sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens);
   return hipGetLastError();
 }
 
