@@ -37,7 +37,9 @@ constexpr int kMaxExtra = 1024 + 64;   // sinks + exact window rows
 constexpr int kCombVec = kMaxSplit * 128 / (4 * 256);   // float4 of split outputs per thread
 constexpr int kPreTok = 4;             // extra tokens whose rows come with the first loads
 
-template <typename T>
+// CV: float4 of split outputs per thread, the smallest of 1, 2, 4, kCombVec
+// that covers nsplit * d_h / 4 (the launch picks it)
+template <typename T, int CV>
 __global__ __launch_bounds__(256) void k_attn_combine(
     const T* __restrict__ q, const T* __restrict__ sink_k, const T* __restrict__ sink_v,
     const T* __restrict__ win_k, const T* __restrict__ win_v, const float* __restrict__ part_ml,
@@ -64,10 +66,10 @@ __global__ __launch_bounds__(256) void k_attn_combine(
   // ---- every load of the split partials and the query, issued together -----------------
   const int ne4 = nsplit * dh / 4;                // float4 of split outputs (d_h is a multiple of 4)
   const int ldh = __builtin_ctz(dh);               // head_dim is a power of two
-  float4 po[kCombVec];
+  float4 po[CV];
   const float4* po4 = reinterpret_cast<const float4*>(part_o + pb * dh);
 #pragma unroll
-  for (int i = 0; i < kCombVec; ++i) po[i] = po4[max(min(t + 256 * i, ne4 - 1), 0)];   // masked below
+  for (int i = 0; i < CV; ++i) po[i] = po4[max(min(t + 256 * i, ne4 - 1), 0)];   // masked below
   float2 ml = make_float2(-INFINITY, 0.f);
   if (t < nsplit) ml = reinterpret_cast<const float2*>(part_ml)[pb + t];
   float xl = 0.f, xh = 0.f;
@@ -156,7 +158,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(
   // ---- weighted split outputs: thread t holds dims 4 t % dh .. + 3 -----------------------
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int i = 0; i < kCombVec; ++i) {
+  for (int i = 0; i < CV; ++i) {
     const int e4 = t + 256 * i;
     if (e4 < ne4) {
       const float a = s_as[(4 * e4) >> ldh];
@@ -183,6 +185,20 @@ __global__ __launch_bounds__(256) void k_attn_combine(
     }
     out[((int64_t)b * hq + h) * dh + t] = num / s_den;
   }
+}
+
+// the split merge of nsplit partials per (query head, sequence) with the extra
+// full-precision tokens (sinks, optional exact window) attended beside them
+template <typename T>
+static void launch_combine_t(const Problem& P, const Workspace& ws, int64_t L, int nsplit, const void* q,
+                             const void* sink_k, const void* sink_v, const void* win_k, const void* win_v, int s_sink,
+                             int W, float* out, hipStream_t st) {
+  const int need = (nsplit * P.dh + 1023) / 1024;
+  auto kern = need <= 1 ? k_attn_combine<T, 1>
+              : need <= 2 ? k_attn_combine<T, 2> : need <= 4 ? k_attn_combine<T, 4> : k_attn_combine<T, kCombVec>;
+  hipLaunchKernelGGL(kern, dim3(P.hq, P.B), dim3(256), 0, st, (const T*)q, (const T*)sink_k, (const T*)sink_v,
+                     (const T*)win_k, (const T*)win_v, ws.part_ml, ws.part_o, out, nsplit, P.hq, P.hkv, P.dh, s_sink,
+                     W, L, rope_ratio(P), P.lens);
 }
 
 // ---------------------------------------------------------------------------
@@ -398,15 +414,9 @@ hipError_t launch_attention(const Problem& P, const Workspace& ws, int64_t L, in
   if (t0 && hipEventRecord(t0[1], st) != hipSuccess) return hipErrorUnknown;
   const int ns_used = n_proc > 0 ? nsplit : 0;
   if (P.dtype == S4R_BF16)
-    hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)sink_k, (const uint16_t*)sink_v, (const uint16_t*)win_k,
-                       (const uint16_t*)win_v, ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L,
-                       rope_ratio(P), P.lens);
+    launch_combine_t<uint16_t>(P, ws, L, ns_used, q, sink_k, sink_v, win_k, win_v, P.s, P.W, out, st);
   else
-    hipLaunchKernelGGL(k_attn_combine<float>, dim3(P.hq, P.B), dim3(256), 0, st, (const float*)q,
-                       (const float*)sink_k, (const float*)sink_v, (const float*)win_k, (const float*)win_v,
-                       ws.part_ml, ws.part_o, out, ns_used, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P),
-                       P.lens);
+    launch_combine_t<float>(P, ws, L, ns_used, q, sink_k, sink_v, win_k, win_v, P.s, P.W, out, st);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && t1) e = hipEventRecord(t1[1], st);
   return e;
@@ -424,9 +434,7 @@ hipError_t launch_full_recon(const Problem& P, const Workspace& ws, int64_t L, c
           ? launch_tiles_bf16_128(P, ws, L, (int)L, (int)L, q, bases_k, bases_v, coef_k, coef_v, st, &ns, true)
           : launch_tiles_bf16_64(P, ws, L, (int)L, (int)L, q, bases_k, bases_v, coef_k, coef_v, st, &ns, true);
   if (!ok) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q,
-                     (const uint16_t*)sink_k, (const uint16_t*)sink_v, nullptr, nullptr, ws.part_ml, ws.part_o, out,
-                     ns, P.hq, P.hkv, P.dh, P.s, P.W, L, rope_ratio(P), P.lens);
+  launch_combine_t<uint16_t>(P, ws, L, ns, q, sink_k, sink_v, nullptr, nullptr, P.s, P.W, out, st);
   return hipGetLastError();
 }
 
@@ -434,9 +442,7 @@ hipError_t launch_full_recon(const Problem& P, const Workspace& ws, int64_t L, c
 // leave split partials in the workspace
 hipError_t launch_combine_only(const Problem& P, const Workspace& ws, int64_t L, int nsplit, const void* q, float* out,
                                hipStream_t st) {
-  hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(P.hq, P.B), dim3(256), 0, st, (const uint16_t*)q, nullptr,
-                     nullptr, nullptr, nullptr, ws.part_ml, ws.part_o, out, nsplit, P.hq, P.hkv, P.dh, 0, 0, L,
-                     rope_ratio(P), P.lens);
+  launch_combine_t<uint16_t>(P, ws, L, nsplit, q, nullptr, nullptr, nullptr, nullptr, 0, 0, out, st);
   return hipGetLastError();
 }
 

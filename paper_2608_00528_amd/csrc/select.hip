@@ -117,11 +117,12 @@ __device__ void find_boundary(const uint32_t* __restrict__ hist, int nc, uint32_
 // ---------------------------------------------------------------------------
 // classify: one workgroup per 2048 positions
 // ---------------------------------------------------------------------------
+template <int NC>   // copies of the top-level histogram (a power of two, at most kHistCopies)
 __global__ __launch_bounds__(kSelThreads) void k_select_classify(
     const float* __restrict__ scores, int64_t score_stride, uint32_t* __restrict__ hist_all,
     uint64_t* __restrict__ cand_all, uint32_t* __restrict__ bitmap_all, uint32_t* __restrict__ cand_count,
     uint32_t* __restrict__ above_count, uint32_t* __restrict__ sel_info, int64_t cand_stride, int64_t cnt_stride,
-    int64_t cap, int L, int W, int k, Lens lens, int key_shift, int hist_nc) {
+    int64_t cap, int L, int W, int k, Lens lens, int key_shift) {
   const int b = blockIdx.y, c = blockIdx.x;
   L = (int)len_of(lens, b, L);
   const int t = threadIdx.x, lane = t & 63;
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_classify(
   if (t == 0) s_count = 0u;
   int b1;
   uint32_t above1;
-  find_boundary<kHistCopies>(hist1, hist_nc, (uint32_t)k_eff, scratch, b1, above1);
+  find_boundary<NC>(hist1, NC, (uint32_t)k_eff, scratch, b1, above1);
   if (c == 0 && t == 0) {
     sel_info[b * 4 + 0] = (uint32_t)b1;
     sel_info[b * 4 + 1] = above1;
@@ -433,9 +434,12 @@ hipError_t launch_select_keyed(const Problem& P, const Workspace& ws, int64_t L,
   const int m = (int)(std::min<int64_t>(P.k, n_hist) + std::min<int64_t>(P.W, L));
   const int nch = (int)((n_hist + kSelChunk - 1) / kSelChunk);
   if (std::min<int64_t>(P.k, n_hist) > 0) {
-    hipLaunchKernelGGL(k_select_classify, dim3(nch, P.B), dim3(kSelThreads), 0, st, scores, score_stride, ws.hist,
-                       ws.cand, ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P),
-                       sel_groups_max(P), P.cap, (int)L, P.W, P.k, P.lens, key_shift, hist_nc);
+    static_assert(kHistCopies == 8, "classify instances for 1, 2, 4 and 8 copies");
+    auto cls = hist_nc == 1 ? k_select_classify<1>
+               : hist_nc == 2 ? k_select_classify<2> : hist_nc == 4 ? k_select_classify<4> : k_select_classify<8>;
+    hipLaunchKernelGGL(cls, dim3(nch, P.B), dim3(kSelThreads), 0, st, scores, score_stride, ws.hist, ws.cand,
+                       ws.bitmap, ws.cand_count, ws.above_count, ws.sel_info, cand_stride(P), sel_groups_max(P), P.cap,
+                       (int)L, P.W, P.k, P.lens, key_shift);
   }
   auto fin = nch <= kSelThreads ? k_select_finish<1>
              : nch <= 2 * kSelThreads ? k_select_finish<2>
