@@ -179,6 +179,8 @@ def _select_case(scores, L, W_, k, capacity=None):
     (20000, 16, 700, "equal"), (7001, 7, 6000, "equal"), (33000, 100, 2048, "tiny_range"),
     (263000, 900, 4000, "ints"),        # the most positions one selection workgroup takes
     (270000, 100, 3000, "pooled"),      # beyond it: the multi-workgroup selection
+    (600000, 64, 90000, "pooled"),      # 293 chunks: eight histogram copies, two chunk counters per thread
+    (1100000, 100, 20000, "ints"),      # 537 chunks: four chunk counters per thread
 ])
 def test_select_topk_bit_exact(L, W_, k, kind):
     rng = np.random.default_rng(L + k)
