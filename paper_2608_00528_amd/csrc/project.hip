@@ -27,6 +27,8 @@ constexpr int kQVec = 4;                      // query vectors per pass
 struct Raw8bf16 {
   uint4 u;
   __device__ __forceinline__ void load(const uint16_t* p) { u = *reinterpret_cast<const uint4*>(p); }
+  // an empty asm that "changes" the value: its conversions cannot be hoisted above this point
+  __device__ __forceinline__ void opaque() { asm volatile("" : "+v"(u.x), "+v"(u.y), "+v"(u.z), "+v"(u.w)); }
   __device__ __forceinline__ float operator[](int c) const {
     const uint32_t w = (c >> 1) == 0 ? u.x : (c >> 1) == 1 ? u.y : (c >> 1) == 2 ? u.z : u.w;
     return (c & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
@@ -37,6 +39,9 @@ struct Raw8f32 {
   __device__ __forceinline__ void load(const float* p) {
     a = *reinterpret_cast<const float4*>(p);
     b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void opaque() {
+    asm volatile("" : "+v"(a.x), "+v"(a.y), "+v"(a.z), "+v"(a.w), "+v"(b.x), "+v"(b.y), "+v"(b.z), "+v"(b.w));
   }
   __device__ __forceinline__ float operator[](int c) const {
     const float4& h = (c < 4) ? a : b;
@@ -220,9 +225,11 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const bool in = t + 256 * i < Dg;
+      typename RawN<T, kPCols>::type bi = bw[i];   // converted here, in every pass
+      bi.opaque();
 #pragma unroll
       for (int c = 0; c < kPCols; ++c) {
-        const double bc = (double)bw[i][c];
+        const double bc = (double)bi[c];
 #pragma unroll
         for (int v = 0; v < kQVec; ++v) acc[v * kPCols + c] = fma(in ? (double)x[v][i] : 0.0, bc, acc[v * kPCols + c]);
       }
@@ -304,9 +311,11 @@ __device__ __forceinline__ void project_rows_body(const T* __restrict__ bases_k,
   for (int i = 0; i < NCH; ++i) {
     const double xv = t + 256 * i < Dg ? (double)x[i] : 0.0;
 #pragma unroll
-    for (int k = 0; k < NG; ++k)
+    for (int k = 0; k < NG; ++k) {
+      bw[i][k].opaque();
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[k * 8 + c] = fma(xv, (double)bw[i][k][c], acc[k * 8 + c]);
+    }
   }
   reduce_wave<kRCols>(acc, red, wave, lane);
   __syncthreads();
