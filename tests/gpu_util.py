@@ -108,6 +108,18 @@ def check_selection(idx_gpu, idx_ref, a_ref, L, W, k, rel_tol=1e-6):
     return flips
 
 
+def slice_state(st, b, L_b):
+    """Sequence b of a batch state, coefficient rows cut at L_b."""
+    one = {}
+    for key, x in st.items():
+        if key == "needles" or x is None or not isinstance(x, np.ndarray):
+            one[key] = x
+            continue
+        one[key] = x[b:b + 1]
+    one["coef_k"], one["coef_v"] = st["coef_k"][b:b + 1, :L_b], st["coef_v"][b:b + 1, :L_b]
+    return one
+
+
 def latent_state_np(wl, seed=0, capacity=None, L=None):
     return W.latent_state(wl, seed=seed, capacity=capacity, L=L)
 
@@ -131,3 +143,37 @@ def score_tol(cq, coef_k, L, dtype):
         s_abs = np.abs(cq[b].reshape(-1, R)) @ np.abs(coef_k[b, :L]).T
         tol[b] = 2.0 * c * 2.0 ** -24 * s_abs.max() / np.sqrt(R) + 1e-6
     return tol
+
+
+def draw_random_workload(case, q_windows=(1, 1, 2, 3, 4), min_len=300, max_len=5000):
+    """A seeded random configuration within the fused attention kernel's
+    (G, rank) set (G in {1, 2, 4, 7, 8}, rank stride / 32 in 1..6 or 8, 7 for
+    bf16 only): returns (workload, capacity, whether the step appends)."""
+    rng = np.random.default_rng(1000 + case)
+    dtype = "fp32" if rng.random() < 0.25 else "bf16"
+    head_dim = 64 if rng.random() < 0.3 else 128
+    G = int(rng.choice([1, 2, 4, 7, 8]))
+    hkv = int(rng.choice([1, 2, 4, 8] if G <= 4 else [1, 2, 4]))
+    nb = 2 if (hkv >= 2 and rng.random() < 0.3) else 1
+    dg = hkv * head_dim // nb
+    blocks = [b for b in (1, 2, 3, 4, 5, 6, 7, 8) if (b != 7 or dtype == "bf16") and 32 * b * nb <= 256
+              and 32 * (b - 1) + 1 <= dg]
+    b = int(rng.choice(blocks))
+    rank = int(rng.integers(32 * (b - 1) + 1, min(32 * b, dg) + 1))
+    batch = int(rng.integers(1, 4))
+    L = int(rng.integers(min_len, max_len))
+    n_sink = int(rng.choice([0, 2, 4]))
+    window = int(rng.choice([0, 8, 32, 64]))
+    q_window = int(rng.choice(q_windows))
+    while G * q_window > 128:
+        q_window -= 1
+    topk = int(rng.integers(1, max(2, (L - window) // 3)))
+    wl = W.CONFIGS["llama8b_32k"].scaled(
+        name=f"random{case}", batch=batch, n_q_heads=G * hkv, n_kv_heads=hkv, head_dim=head_dim,
+        N=L + n_sink, n_sink=n_sink, rank=rank, basis_groups=nb, window=window, topk=topk, dtype=dtype,
+        r_true=max(4, (rank * nb * 3) // 4), q_window=q_window, pool_kernel=int(rng.choice([1, 3, 5, 7])),
+        pool_mode=str(rng.choice(["max", "avg"])), group_agg=str(rng.choice(["mean", "max"])), n_needles=4,
+        outlier_channels=0, recipe="latent")
+    cap = ((L + 15) // 16) * 16 + 16 * int(rng.integers(0, 3))
+    append = bool(rng.random() < 0.35)
+    return wl, cap, append

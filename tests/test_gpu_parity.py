@@ -20,7 +20,7 @@ import torch
 import paper_2608_00528_amd as s4r
 import workloads as W
 from oracle import decode, prefill
-from gpu_util import (cfg_from_workload, check_selection, dev, oracle_cfg, rel_err_rows, to_gpu_state,
+from gpu_util import (cfg_from_workload, check_selection, dev, oracle_cfg, rel_err_rows, slice_state, to_gpu_state,
                       unpad_latent)
 
 pytestmark = pytest.mark.gpu
@@ -523,18 +523,6 @@ def test_prefill_projection(n_rows, nb, rank):
         assert exact > 0.999, f"bit-equal fraction {exact:.5f}"
 
 
-def _slice_state(st, b, L_b):
-    """Sequence b of a batch state, coefficient rows cut at L_b."""
-    one = {}
-    for key, x in st.items():
-        if key == "needles" or x is None or not isinstance(x, np.ndarray):
-            one[key] = x
-            continue
-        one[key] = x[b:b + 1]
-    one["coef_k"], one["coef_v"] = st["coef_k"][b:b + 1, :L_b], st["coef_v"][b:b + 1, :L_b]
-    return one
-
-
 @pytest.mark.parametrize("shape,lengths,append", [
     ("llama8b_32k", (6000, 3001, 1777), False),
     ("llama8b_32k", (2900, 6004, 4097), True),
@@ -582,7 +570,7 @@ def test_ragged_decode_step(shape, lengths, append):
                           c.rank, c.basis_groups)
     theta = oracle_cfg(c)["rope_theta"]
     for b, L_b in enumerate(lengths):
-        one = _slice_state(st, b, L_b)
+        one = slice_state(st, b, L_b)
         if append:
             # the new rows went to row L_b - 1 of this sequence only: equal to the
             # oracle's projection up to one bf16 rounding step ...

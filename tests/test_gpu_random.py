@@ -22,7 +22,8 @@ import torch
 import paper_2608_00528_amd as s4r
 import workloads as W
 from oracle import decode
-from gpu_util import cfg_from_workload, check_selection, dev, oracle_cfg, rel_err_rows, to_gpu_state, unpad_latent
+from gpu_util import (cfg_from_workload, check_selection, dev, draw_random_workload, oracle_cfg, rel_err_rows,
+                      to_gpu_state, unpad_latent)
 
 pytestmark = pytest.mark.gpu
 
@@ -30,42 +31,9 @@ OUT_TOL = {"bf16": 2e-2, "fp32": 1e-4}
 N_CASES = 40
 
 
-def draw_config(case):
-    """One configuration within the fused attention kernel's (G, rank) set:
-    G in {1, 2, 4, 7, 8}, rank stride / 32 in 1..6 or 8 (7 for bf16 only)."""
-    rng = np.random.default_rng(1000 + case)
-    dtype = "fp32" if rng.random() < 0.25 else "bf16"
-    head_dim = 64 if rng.random() < 0.3 else 128
-    G = int(rng.choice([1, 2, 4, 7, 8]))
-    hkv = int(rng.choice([1, 2, 4, 8] if G <= 4 else [1, 2, 4]))
-    nb = 2 if (hkv >= 2 and rng.random() < 0.3) else 1
-    dg = hkv * head_dim // nb
-    blocks = [b for b in (1, 2, 3, 4, 5, 6, 7, 8) if (b != 7 or dtype == "bf16") and 32 * b * nb <= 256
-              and 32 * (b - 1) + 1 <= dg]
-    b = int(rng.choice(blocks))
-    rank = int(rng.integers(32 * (b - 1) + 1, min(32 * b, dg) + 1))
-    batch = int(rng.integers(1, 4))
-    L = int(rng.integers(300, 5000))
-    n_sink = int(rng.choice([0, 2, 4]))
-    window = int(rng.choice([0, 8, 32, 64]))
-    q_window = int(rng.choice([1, 1, 2, 3, 4]))
-    while G * q_window > 128:
-        q_window -= 1
-    topk = int(rng.integers(1, max(2, (L - window) // 3)))
-    wl = W.CONFIGS["llama8b_32k"].scaled(
-        name=f"random{case}", batch=batch, n_q_heads=G * hkv, n_kv_heads=hkv, head_dim=head_dim,
-        N=L + n_sink, n_sink=n_sink, rank=rank, basis_groups=nb, window=window, topk=topk, dtype=dtype,
-        r_true=max(4, (rank * nb * 3) // 4), q_window=q_window, pool_kernel=int(rng.choice([1, 3, 5, 7])),
-        pool_mode=str(rng.choice(["max", "avg"])), group_agg=str(rng.choice(["mean", "max"])), n_needles=4,
-        outlier_channels=0, recipe="latent")
-    cap = ((L + 15) // 16) * 16 + 16 * int(rng.integers(0, 3))
-    append = bool(rng.random() < 0.35)
-    return wl, cap, append
-
-
 @pytest.mark.parametrize("case", range(N_CASES))
 def test_random_configuration(case):
-    wl, cap, append = draw_config(case)
+    wl, cap, append = draw_random_workload(case)
     L = wl.L
     print(f"[random {case}] {wl.describe()} rank/group {wl.rank} nb {wl.basis_groups} W_q {wl.q_window} "
           f"kappa {wl.pool_kernel} {wl.pool_mode}/{wl.group_agg} cap {cap} append {append}", flush=True)
