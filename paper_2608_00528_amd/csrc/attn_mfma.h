@@ -10,10 +10,12 @@
 //
 //   1. the split's index list goes to LDS; the tiles are gathered in pairs
 //      into two LDS buffers (even pairs in one, odd pairs in the other) with
-//      16-byte global->LDS loads (lane l of a wave load lands at byte 16 l of
+//      16-byte buffer->LDS loads (lane l of a wave load lands at byte 16 l of
 //      the destination, so one wave load writes one 16-token x 32-column block;
 //      lane l fetches quarter (l % 4) ^ ((l / 8) % 4) of token l / 4's row, an
-//      XOR swizzle that keeps the operand reads free of bank conflicts).
+//      XOR swizzle that keeps the operand reads free of bank conflicts).  One
+//      32-bit lane offset per tile serves all of a tile's blocks, whose 1 KiB
+//      steps go in the scalar offset: no 64-bit address arithmetic per block.
 //      Pairs 0 and 1 are requested up front; pair
 //      p + 2 as soon as every wave has read pair p, so the gathers overlap
 //      the arithmetic of pair p + 1;
@@ -77,25 +79,24 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // one wave's gather of one 16-token tile into slot u of a pair buffer: its RBH
-// 1 KiB blocks of C^K and RBV of C^V as 16-byte global->LDS loads (lane l: token
-// l / 4, quarter (l % 4) ^ ((l / 8) % 4) of the 32 columns, stored at byte 16 l;
-// a token past the list reads row 0, never used).  T is the tile's number within the workgroup.  The LDS
-// destinations are named directly (plain LDS pointers for the builtin).
+// 1 KiB blocks of C^K and RBV of C^V as 16-byte buffer->LDS loads through the
+// resources rsk / rsv (lane l: token l / 4, quarter (l % 4) ^ ((l / 8) % 4) of
+// the 32 columns, stored at byte 16 l; a token past the list reads row 0,
+// never used).  T is the tile's number within the workgroup.  The LDS
+// destinations are named directly (LDS pointers for the builtin).
 #define S4R_GATHER_TILE(GK, GV, U, T)                                                       \
   do {                                                                                       \
     const int32_t x_ = tok_at((T) * 16 + (lane >> 2));                                       \
     const uint32_t tok_ = x_ < 0 ? 0u : (uint32_t)x_;                                        \
-    const int64_t in_ = (tok_ & 15) * 32 + (((lane & 3) ^ ((lane >> 3) & 3)) * 8);          \
-    const int64_t offk_ = (int64_t)(tok_ >> 4) * 16 * R + in_;                               \
-    const int64_t offv_ = (int64_t)(tok_ >> 4) * 16 * Rv + in_;                              \
-    _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb) {                                     \
-      uint16_t* dk_ = &GK[U][kb][0];                                                         \
-      __builtin_amdgcn_global_load_lds(ckb + offk_ + kb * 512, dk_, 16, 0, 0);               \
-    }                                                                                        \
-    _Pragma("unroll") for (int kb = 0; kb < RBV; ++kb) {                                     \
-      uint16_t* dv_ = &GV[U][kb][0];                                                         \
-      __builtin_amdgcn_global_load_lds(cvb + offv_ + kb * 512, dv_, 16, 0, 0);               \
-    }                                                                                        \
+    const uint32_t in_ = ((tok_ & 15) * 32 + (((lane & 3) ^ ((lane >> 3) & 3)) * 8)) * 2;   \
+    const uint32_t offk_ = (tok_ >> 4) * (32u * R) + in_;                                    \
+    const uint32_t offv_ = (tok_ >> 4) * (32u * Rv) + in_;                                   \
+    _Pragma("unroll") for (int kb = 0; kb < RBH; ++kb)                                       \
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(                                              \
+          rsk, (__attribute__((address_space(3))) void*)&GK[U][kb][0], 16, offk_, kb * 1024, 0, 0); \
+    _Pragma("unroll") for (int kb = 0; kb < RBV; ++kb)                                       \
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(                                              \
+          rsv, (__attribute__((address_space(3))) void*)&GV[U][kb][0], 16, offv_, kb * 1024, 0, 0); \
   } while (0)
 
 // IDENT: every token of the sequence in order (full reconstruction,
@@ -206,6 +207,11 @@ __global__ __launch_bounds__(NW * 64, (attn_tiles_waves_per_simd<RBH, RBV, NMH>(
   lds_barrier();                                   // sidx visible
   const uint16_t* ckb = coef_k + (int64_t)b * cap * R + (int64_t)kb0 * 512;
   const uint16_t* cvb = coef_v + (int64_t)b * cap * Rv + (int64_t)kbv0 * 512;
+  // buffer resources over the sequence's caches (byte offsets below cap * R * 2
+  // <= 2^32 by the capacity limit; no range check): one 32-bit lane offset per
+  // tile row serves every 32-column block, whose 1 KiB steps go in the scalar offset
+  const __amdgpu_buffer_rsrc_t rsk = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(ckb), (short)0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsv = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(cvb), (short)0, -1, 0x00020000);
   // tile t is gathered by wave t % NW; pairs 0 and 1 now (every wave issues
   // the same number of loads), pair p + 2 once pair p has been read
 #pragma unroll
