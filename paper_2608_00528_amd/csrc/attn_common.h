@@ -30,7 +30,7 @@ __device__ __forceinline__ void rope_cs_fixed(int64_t pos, uint64_t F, float& c,
   // 32-bit multiplies and an add
   const uint32_t p = (uint32_t)pos, flo = (uint32_t)F, fhi = (uint32_t)(F >> 32);
   const uint32_t hi = (uint32_t)(((uint64_t)p * flo) >> 32) + p * fhi;
-  const float x = (float)(hi >> 8) * 5.9604644775390625e-08f;   // top 24 bits, 2^-24 revolutions
+  const float x = (float)hi * 2.3283064365386963e-10f;          // 2^-32 revolutions, rounded to 24 bits
   c = __builtin_amdgcn_cosf(x);
   s = __builtin_amdgcn_sinf(x);
 }
