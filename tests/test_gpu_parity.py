@@ -258,8 +258,9 @@ def test_fused_equals_composition(case):
     torch.cuda.synchronize()
     assert torch.equal(idx_f, idx_c)
     # the composition reconstructs K^ / V^ in fp32; the fused bf16 kernel
-    # rounds K~ and V^ once to bf16 (the output bound for bf16 storage), the
-    # fp32 path runs the same arithmetic as the composition
+    # carries K~ as two bf16 parts and rounds V^ and the weights P once to
+    # bf16 (the output bound for bf16 storage), the fp32 path runs the same
+    # arithmetic as the composition
     err = rel_err_rows(out_f.cpu().numpy(), out_c.cpu().numpy())
     print(f"[fused vs composition] {case}: {err:.2e}", flush=True)
     assert err < (OUT_TOL["bf16"] if wl.dtype == "bf16" else 1e-4)
