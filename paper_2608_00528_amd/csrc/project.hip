@@ -22,6 +22,10 @@ namespace s4r {
 // ---------------------------------------------------------------------------
 constexpr int kPCols = 8;                     // latent columns per query workgroup (4 or 8)
 constexpr int kQVec = 4;                      // query vectors per pass
+// the step kernel's query workgroups: 16 columns, two vectors per pass, so
+// its query and new-row workgroups (R / 16 + 2 R / 32 per sequence) fit one
+// round of the chip at three waves per SIMD for a 32-sequence batch
+constexpr int kSPCols = 16, kSQVec = 2;
 
 // 8 consecutive basis elements, kept in their storage format until used
 struct Raw8bf16 {
@@ -65,6 +69,31 @@ struct Raw4f32 {
     return c == 0 ? a.x : c == 1 ? a.y : c == 2 ? a.z : a.w;
   }
 };
+// 16 consecutive basis elements (the step projection's 16-column workgroups)
+struct Raw16bf16 {
+  Raw8bf16 a, b;
+  __device__ __forceinline__ void load(const uint16_t* p) {
+    a.load(p);
+    b.load(p + 8);
+  }
+  __device__ __forceinline__ void opaque() {
+    a.opaque();
+    b.opaque();
+  }
+  __device__ __forceinline__ float operator[](int c) const { return c < 8 ? a[c] : b[c - 8]; }
+};
+struct Raw16f32 {
+  Raw8f32 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a.load(p);
+    b.load(p + 8);
+  }
+  __device__ __forceinline__ void opaque() {
+    a.opaque();
+    b.opaque();
+  }
+  __device__ __forceinline__ float operator[](int c) const { return c < 8 ? a[c] : b[c - 8]; }
+};
 template <typename T, int N>
 struct RawN;
 template <>
@@ -74,6 +103,14 @@ struct RawN<uint16_t, 8> {
 template <>
 struct RawN<float, 8> {
   using type = Raw8f32;
+};
+template <>
+struct RawN<uint16_t, 16> {
+  using type = Raw16bf16;
+};
+template <>
+struct RawN<float, 16> {
+  using type = Raw16f32;
 };
 template <>
 struct RawN<uint16_t, 4> {
@@ -162,7 +199,7 @@ __device__ __forceinline__ void qimg_pack4(float4 x, uint2 (&pk)[3]) {
 // window's older rows from qwin_prev when given.  The image's other rows are
 // never read.
 // ---------------------------------------------------------------------------
-template <typename T, int NCH>
+template <typename T, int NCH, int PC = kPCols, int QV = kQVec>
 __device__ __forceinline__ void project_query_body(const T* __restrict__ q, const T* __restrict__ bases_k,
                                                    const float* __restrict__ qwin_prev, uint16_t* __restrict__ qimg,
                                                    float* __restrict__ qcoef, float* __restrict__ qcoef_out,
@@ -172,33 +209,39 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int Dp = hkv * dh, Dg = Dp / nb;
   const int ldh = __builtin_ctz(dh);              // head_dim is a power of two
-  const int c0 = cblk * kPCols;                   // first latent column of the block
+  const int c0 = cblk * PC;                   // first latent column of the block
   const int grp = c0 / rank;                      // its basis group
-  // the window's older query rows (oldest first): unit t is latent columns
-  // c0 + 4 (t % U) .. + 3 of older row j = t / U (U = kPCols / 4 units per
-  // row), i.e. group j / (W_q - 1), window row j % (W_q - 1) (G (W_q - 1)
-  // <= 127 rows, so one unit per thread).  Requested first, written last.
-  constexpr int U = kPCols / 4;
+  // the window's older query rows (oldest first): unit u = t + 256 k is
+  // latent columns c0 + 4 (u % U) .. + 3 of older row j = u / U (U = PC / 4
+  // units per row), i.e. group j / (W_q - 1), window row j % (W_q - 1)
+  // (G (W_q - 1) <= 127 rows: NOU units per thread).  Requested first, written last.
+  constexpr int U = PC / 4, NOU = (127 * U + 255) / 256;
   const bool old_rows = qimg && qwin_prev && Wq > 1;
   const int n_old = old_rows ? G * (Wq - 1) : 0;
-  const int jo = min(t / U, max(n_old - 1, 0));
-  const int go = n_old ? jo / (Wq - 1) : 0, wo = n_old ? jo - go * (Wq - 1) : 0;
-  const int oc = c0 + 4 * (t % U);
-  float4 oldv = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (old_rows) oldv = *reinterpret_cast<const float4*>(qwin_prev + (((int64_t)b * G + go) * (Wq - 1) + wo) * R + oc);
+  float4 oldv[NOU];
+#pragma unroll
+  for (int k = 0; k < NOU; ++k) {
+    const int u = t + 256 * k, jo = u / U;
+    oldv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (jo < n_old) {
+      const int go = jo / (Wq - 1), wo = jo - go * (Wq - 1);
+      oldv[k] = *reinterpret_cast<const float4*>(qwin_prev + (((int64_t)b * G + go) * (Wq - 1) + wo) * R + c0 +
+                                                 4 * (u % U));
+    }
+  }
 
   // basis rows t + 256 i of the block's columns (rows past the group's end:
   // a re-read of its last row, met by x = 0)
   const T* bases = bases_k + (bases_shared ? 0 : (int64_t)b * Dp * rank) + (int64_t)grp * Dg * rank + (c0 - grp * rank);
-  typename RawN<T, kPCols>::type bw[NCH];
+  typename RawN<T, PC>::type bw[NCH];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) bw[i].load(bases + (int64_t)min(t + 256 * i, Dg - 1) * rank);
   // the group's query elements of those rows, for vectors v0 .. v0 + 3 (the
   // last vector repeated past G)
-  float x[kQVec][NCH];
+  float x[QV][NCH];
   auto load_x = [&](int v0) {
 #pragma unroll
-    for (int v = 0; v < kQVec; ++v)
+    for (int v = 0; v < QV; ++v)
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
         const int d = grp * Dg + min(t + 256 * i, Dg - 1);   // feature index in Dp
@@ -207,37 +250,37 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   };
   load_x(0);
   // the step's selection histograms start from zero (the relevance and
-  // classify kernels add to them later in the step): the sequence's R / 8
+  // classify kernels add to them later in the step): the sequence's R / PC
   // workgroups clear a slice each
   {
-    const int nblk = R / kPCols, per = (kHistStride / 4 + nblk - 1) / nblk;
+    const int nblk = R / PC, per = (kHistStride / 4 + nblk - 1) / nblk;
     uint4* hz = reinterpret_cast<uint4*>(hist + (int64_t)b * kHistStride);
     const int i1 = min((cblk + 1) * per, kHistStride / 4);
     for (int i = cblk * per + t; i < i1; i += blockDim.x) hz[i] = make_uint4(0u, 0u, 0u, 0u);
   }
 
   __shared__ double red[4][32];
-  for (int v0 = 0; v0 < G; v0 += kQVec) {
+  for (int v0 = 0; v0 < G; v0 += QV) {
     if (v0 > 0) load_x(v0);
-    double acc[kQVec * kPCols];                   // [vector][column]
+    double acc[QV * PC];                   // [vector][column]
 #pragma unroll
-    for (int j = 0; j < kQVec * kPCols; ++j) acc[j] = 0.0;
+    for (int j = 0; j < QV * PC; ++j) acc[j] = 0.0;
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const bool in = t + 256 * i < Dg;
-      typename RawN<T, kPCols>::type bi = bw[i];   // converted here, in every pass
+      typename RawN<T, PC>::type bi = bw[i];   // converted here, in every pass
       bi.opaque();
 #pragma unroll
-      for (int c = 0; c < kPCols; ++c) {
+      for (int c = 0; c < PC; ++c) {
         const double bc = (double)bi[c];
 #pragma unroll
-        for (int v = 0; v < kQVec; ++v) acc[v * kPCols + c] = fma(in ? (double)x[v][i] : 0.0, bc, acc[v * kPCols + c]);
+        for (int v = 0; v < QV; ++v) acc[v * PC + c] = fma(in ? (double)x[v][i] : 0.0, bc, acc[v * PC + c]);
       }
     }
-    reduce_wave<kQVec * kPCols>(acc, red, wave, lane);
+    reduce_wave<QV * PC>(acc, red, wave, lane);
     __syncthreads();
-    if (t < kQVec * kPCols && v0 + t / kPCols < G) {
-      const int g = v0 + t / kPCols, col = c0 + t % kPCols;
+    if (t < QV * PC && v0 + t / PC < G) {
+      const int g = v0 + t / PC, col = c0 + t % PC;
       const double xq = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
       qcoef[((int64_t)b * G + g) * R + col] = (float)xq;
       if (qcoef_out) qcoef_out[((int64_t)b * G + g) * R + col] = (float)xq;
@@ -251,12 +294,17 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
     }
     __syncthreads();                              // red is reused by the next pass
   }
-  if (old_rows && t / U < n_old) {
-    uint2 pk[3];
-    qimg_pack4(oldv, pk);
-    uint16_t* p = qimg_at(qimg, b, ncb, nmb, R, go * Wq + wo, oc);
 #pragma unroll
-    for (int part = 0; part < 3; ++part) *reinterpret_cast<uint2*>(p + part * R) = pk[part];
+  for (int k = 0; k < NOU; ++k) {
+    const int u = t + 256 * k, jo = u / U;
+    if (jo < n_old) {
+      const int go = jo / (Wq - 1), wo = jo - go * (Wq - 1);
+      uint2 pk[3];
+      qimg_pack4(oldv[k], pk);
+      uint16_t* p = qimg_at(qimg, b, ncb, nmb, R, go * Wq + wo, c0 + 4 * (u % U));
+#pragma unroll
+      for (int part = 0; part < 3; ++part) *reinterpret_cast<uint2*>(p + part * R) = pk[part];
+    }
   }
 }
 
@@ -341,11 +389,11 @@ __global__ __launch_bounds__(256) void k_project_rows(const T* __restrict__ base
 }
 
 // both projections of a step that appends a token, in one launch: per
-// sequence R / 8 query-coefficient workgroups and max(R, R_V) / 32 new-row
+// sequence R / 16 query-coefficient workgroups and max(R, R_V) / 32 new-row
 // workgroups per side.  They touch disjoint memory, and one launch saves a
 // dispatch and a first-read latency.  Every workgroup of sequence b runs on
 // XCD b mod 8 (workgroup i is dispatched to XCD i mod 8): the query and key
-// workgroups read different columns of the same basis rows (16 and 64 bytes
+// workgroups read different columns of the same basis rows (32 and 64 bytes
 // of each bf16 row), so a row's cache lines come from HBM once into that
 // XCD's L2 instead of once per XCD.
 template <typename T, int NCH>
@@ -358,15 +406,15 @@ __global__ __launch_bounds__(256) void k_project_step(const T* __restrict__ q, c
                                                       int hkv, int dh, int G, int Wq, int nb, int rank, int R,
                                                       int rank_v, int Rv, int bases_shared, int64_t cap, int B,
                                                       int ncb, int nmb, Lens lens) {
-  const int ncq = R / kPCols;
+  const int ncq = R / kSPCols;
   const int ncr = max(R, Rv) / kRCols;             // row blocks per (sequence, side)
   const int per_seq = ncq + 2 * ncr;
   const int xcd = blockIdx.x & 7, k = blockIdx.x >> 3;
   const int b = xcd + 8 * (k / per_seq), id = k % per_seq;
   if (b >= B) return;
   if (id < ncq) {
-    project_query_body<T, NCH>(q, bases_k, qwin_prev, qimg, qcoef, nullptr, hist, hq, hkv, dh, G, Wq, nb, rank, R,
-                               bases_shared, ncb, nmb, id, b);
+    project_query_body<T, NCH, kSPCols, kSQVec>(q, bases_k, qwin_prev, qimg, qcoef, nullptr, hist, hq, hkv, dh, G,
+                                                Wq, nb, rank, R, bases_shared, ncb, nmb, id, b);
   } else {
     const int cblk = (id - ncq) % ncr, which = (id - ncq) / ncr;
     if (cblk * kRCols >= (which ? Rv : R)) return;
@@ -497,7 +545,7 @@ template <typename T, int NCH>
 static void launch_step_t(const Problem& P, const Workspace& ws, const void* q, const void* bases_k,
                           const void* bases_v, const void* k_new, const void* v_new, void* coef_k, void* coef_v,
                           const float* qwin_prev, int64_t row, hipStream_t st) {
-  const int per_seq = P.R / kPCols + 2 * (std::max(P.R, P.Rv) / kRCols);
+  const int per_seq = P.R / kSPCols + 2 * (std::max(P.R, P.Rv) / kRCols);
   const dim3 grid(8 * ((P.B + 7) / 8) * per_seq);  // sequence b on XCD b mod 8
   hipLaunchKernelGGL((k_project_step<T, NCH>), grid, dim3(256), 0, st, (const T*)q, (const T*)bases_k,
                      (const T*)bases_v, (const T*)k_new, (const T*)v_new, (T*)coef_k, (T*)coef_v, qwin_prev, ws.qimg,
