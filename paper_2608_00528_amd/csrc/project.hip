@@ -189,9 +189,10 @@ __device__ __forceinline__ void qimg_pack4(float4 x, uint2 (&pk)[3]) {
 }
 
 // ---------------------------------------------------------------------------
-// query coefficients: grid (R / 8, B).  A workgroup forms, for its 8 latent
-// columns and every query group g, c^Q[g] = q_g B^K over all rows of the
-// basis group (kQVec groups per pass), and writes it (1) rounded to fp32 into
+// query coefficients: grid (R / PC, B).  A workgroup forms, for its PC latent
+// columns (8 in k_project_query, 16 in the step kernel) and every query
+// group g, c^Q[g] = q_g B^K over all rows of the basis group (QV groups per
+// pass), and writes it (1) rounded to fp32 into
 // qcoef [B][G][R] (and the caller's qcoef_out), (2) as the hi / mid / lo bf16
 // parts the scoring kernel's MFMA A operand holds, into the operand image
 // qimg [B][column blocks][NMB][16][R] (query column gi = g W_q + i in block
@@ -209,7 +210,7 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int Dp = hkv * dh, Dg = Dp / nb;
   const int ldh = __builtin_ctz(dh);              // head_dim is a power of two
-  const int c0 = cblk * PC;                   // first latent column of the block
+  const int c0 = cblk * PC;                       // first latent column of the block
   const int grp = c0 / rank;                      // its basis group
   // the window's older query rows (oldest first): unit u = t + 256 k is
   // latent columns c0 + 4 (u % U) .. + 3 of older row j = u / U (U = PC / 4
@@ -262,13 +263,13 @@ __device__ __forceinline__ void project_query_body(const T* __restrict__ q, cons
   __shared__ double red[4][32];
   for (int v0 = 0; v0 < G; v0 += QV) {
     if (v0 > 0) load_x(v0);
-    double acc[QV * PC];                   // [vector][column]
+    double acc[QV * PC];                          // [vector][column]
 #pragma unroll
     for (int j = 0; j < QV * PC; ++j) acc[j] = 0.0;
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const bool in = t + 256 * i < Dg;
-      typename RawN<T, PC>::type bi = bw[i];   // converted here, in every pass
+      typename RawN<T, PC>::type bi = bw[i];       // converted here, in every pass
       bi.opaque();
 #pragma unroll
       for (int c = 0; c < PC; ++c) {
